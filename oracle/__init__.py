@@ -1,0 +1,180 @@
+"""CPU oracle for the semantic draft source (Oilbird, arXiv 2608.03839).
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, by ``__graft_entry__.smoke()``
+and by the CPU-baseline leg of ``bench.py``; never by the product package.
+It shares no code with the HIP path: the arithmetic lives in ``oracle.c``
+(plain C, double precision, each routine citing the paper passage it follows);
+this module only builds that file with gcc and marshals numpy arrays.
+
+bf16 values travel as ``numpy.uint16`` bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.environ.get("OILBIRD_ORACLE_LIB") or os.path.join(_HERE, "liboilbird_oracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c with gcc (-O2, strict IEEE double, OpenMP loops)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC",
+               "-shared", "-std=c11", "-Wall", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, i64, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+        lib.orc_bf16_round.restype = ctypes.c_uint16
+        lib.orc_bf16_round.argtypes = [ctypes.c_double]
+        lib.orc_bf16_round_array.argtypes = [P, i64, P]
+        lib.orc_normalize_rows.argtypes = [P, ctypes.c_int, i64, i32, P]
+        lib.orc_scores.argtypes = [P, i64, i32, P, i32, P]
+        lib.orc_topk.argtypes = [P, i64, i32, P, P, i32, P, P]
+        lib.orc_gather.argtypes = [P, P, i64, P, P, i32, i32, f32, i32, P, P, i32, P, P]
+        lib.orc_tree_merge.argtypes = [i32, P, P, P, i32, i32, i32, P, P, i32, i32, i32, i32,
+                                       P, P, P, P]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _check(rc, name):
+    if rc != 0:
+        raise ValueError(f"oracle {name} rejected its arguments (rc={rc})")
+
+
+# ---------------------------------------------------------------- bf16 helpers
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> float64 (a bf16 is a float32 with 16 zero low bits)."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32).astype(np.float64)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bf16 (nearest, ties to even) -> uint16 bits."""
+    x = _c(x, np.float64)
+    out = np.empty(x.shape, dtype=np.uint16)
+    _load().orc_bf16_round_array(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+# ---------------------------------------------------------------- the method
+def normalize_rows(raw: np.ndarray) -> np.ndarray:
+    """Eq. 1 store format: each row divided by its L2 norm (float64), rounded to bf16.
+
+    ``raw`` is float32 (any float array is cast) or uint16 bf16 bits, shape (n, d).
+    """
+    raw = np.asarray(raw)
+    if raw.dtype == np.uint16:
+        dt = 1
+    else:
+        raw, dt = _c(raw, np.float32), 0
+    raw = np.ascontiguousarray(raw)
+    n, d = raw.shape
+    out = np.empty((n, d), dtype=np.uint16)
+    _check(_load().orc_normalize_rows(_ptr(raw), dt, n, d, _ptr(out)), "normalize_rows")
+    return out
+
+
+def scores(keys: np.ndarray, q: np.ndarray) -> np.ndarray:
+    """Exact float64 dot of every stored bf16 key with every bf16 query: (B, n)."""
+    keys, q = _c(keys, np.uint16), _c(q, np.uint16)
+    n, d = keys.shape
+    B = q.shape[0]
+    assert q.shape[1] == d
+    s = np.empty((B, n), dtype=np.float64)
+    _check(_load().orc_scores(_ptr(keys), n, d, _ptr(q), B, _ptr(s)), "scores")
+    return s
+
+
+def topk(s: np.ndarray, k: int, prompt=None, exclude=None):
+    """Eq. 2 arg top-k by (score desc, index asc), self-exclusion optional."""
+    s = _c(s, np.float64)
+    B, n = s.shape
+    pr = None if prompt is None else _c(prompt, np.int32)
+    ex = None if exclude is None else _c(exclude, np.int32)
+    ts = np.empty((B, k), dtype=np.float64)
+    ti = np.empty((B, k), dtype=np.int32)
+    _check(_load().orc_topk(_ptr(s), n, B, _ptr(pr), _ptr(ex), k, _ptr(ts), _ptr(ti)), "topk")
+    return ts, ti
+
+
+def query_topk(keys, raw_queries, k, prompt=None, exclude=None):
+    """Query prep + score + top-k, the oracle's view of one retrieval call."""
+    q = normalize_rows(raw_queries)
+    return topk(scores(keys, q), k, prompt, exclude)
+
+
+def paper_rule(theta=0.8):
+    """D(s) of Eq. 3: 48 tokens if s >= 0.90, 8 if s >= 0.82, else 0."""
+    return dict(theta=theta, band_min=[0.90, 0.82], band_depth=[48, 8])
+
+
+def fixed_rule(L, theta=0.8):
+    """Fixed-length span (the batching-probe variant): L tokens whenever fired."""
+    return dict(theta=theta, band_min=[-np.inf], band_depth=[L])
+
+
+def gather(tokens, traces, n_valid, idx, top_scores, rule, L):
+    """Eq. 3 continuations: (chain_tokens (B,k,L) int32 with -1 pad, chain_len (B,k))."""
+    idx = _c(idx, np.int32)
+    sc = _c(top_scores, np.float32)
+    B, k = idx.shape
+    tok, tr = _c(tokens, np.int32), _c(traces, np.int32)
+    bm = _c(rule["band_min"], np.float32)
+    bd = _c(rule["band_depth"], np.int32)
+    ct = np.empty((B, k, L), dtype=np.int32)
+    cl = np.empty((B, k), dtype=np.int32)
+    _check(_load().orc_gather(_ptr(tok), _ptr(tr), int(n_valid), _ptr(idx), _ptr(sc), B, k,
+                              float(rule["theta"]), len(bm), _ptr(bm), _ptr(bd), L,
+                              _ptr(ct), _ptr(cl)), "gather")
+    return ct, cl
+
+
+def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget,
+               max_nodes):
+    """Eq. 4 root-first merge -> (node_token, node_parent, node_source, n_nodes).
+
+    ``lex_tokens`` is (B, n_lex, L_lex) (n_lex may be 0); ``sem_tokens`` is (B, k, L).
+    """
+    anchor = _c(anchor, np.int32)
+    B = anchor.shape[0]
+    lex_tokens = _c(lex_tokens, np.int32)
+    lex_len = _c(lex_len, np.int32)
+    sem_tokens = _c(sem_tokens, np.int32)
+    sem_len = _c(sem_len, np.int32)
+    n_lex, L_lex = lex_tokens.shape[1], lex_tokens.shape[2]
+    k, L = sem_tokens.shape[1], sem_tokens.shape[2]
+    nt = np.empty((B, max_nodes), dtype=np.int32)
+    npar = np.empty((B, max_nodes), dtype=np.int32)
+    ns = np.empty((B, max_nodes), dtype=np.int8)
+    nn = np.empty((B,), dtype=np.int32)
+    _check(_load().orc_tree_merge(B, _ptr(anchor), _ptr(lex_tokens), _ptr(lex_len), n_lex,
+                                  max(L_lex, 1), lex_budget, _ptr(sem_tokens), _ptr(sem_len), k,
+                                  max(L, 1), sem_budget, max_nodes, _ptr(nt), _ptr(npar),
+                                  _ptr(ns), _ptr(nn)), "tree_merge")
+    return nt, npar, ns, nn

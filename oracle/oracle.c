@@ -1,0 +1,371 @@
+/*
+ * CPU ORACLE for the semantic draft source of Oilbird (arXiv 2608.03839).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or call
+ * this file; only the tests, the smoke check and the CPU-baseline leg of the
+ * benchmark do.  It shares no code, header, table or helper with the HIP
+ * library: every routine below is written from the paper's definitions, in
+ * plain C, in double precision, with no blocking, fusion or reordering beyond
+ * what each definition states.  It is deliberately slow.
+ *
+ * Paper passages followed (section / equation / algorithm of the paper):
+ *   - Store (Sec. 4 (i), Eq. 1): one record (x_i, h_i) per committed position,
+ *     h_i kept L2-normalised in half precision.  Read here as bf16, the
+ *     precision the models run in (Sec. 5 setup).  Normalisation: h / ||h||,
+ *     evaluated in double, rounded once to bf16 (round to nearest, ties to even).
+ *   - Similarity (Algorithm 1, "retrieve" step; Sec. 4 (ii)): s_i = cos(h_t, h_i)
+ *     over every stored position.  With unit stored keys and a unit query the
+ *     cosine is the dot product of the stored operands; that dot is taken here
+ *     exactly in double (bf16 x bf16 products are exact in double).
+ *   - Retrieval (Eq. 2): E_t = arg top-k of s over the whole pool, fired only
+ *     when the best score reaches theta (a gate on the maximum, not a filter).
+ *     Positions whose stored prompt equals the one being served are skipped
+ *     (Sec. 4 (i)).  Equal scores are ordered by lower position first.
+ *   - Continuation (Eq. 3 and the chain step of Algorithm 1): gamma_i =
+ *     x_{i+2 .. i+1+D(s_i)}, read out of the trace that holds i, with
+ *     D(s) = 48 if s >= 0.90, 8 if s >= 0.82, else 0 (or a fixed span length,
+ *     the variant the batching probe uses, Sec. 5 / Fig. 5); chains shorter
+ *     than two tokens are dropped.
+ *   - Merge (Sec. 4 (iii), Eq. 4; BuildLexical and MergeFromRoot in
+ *     Algorithm 1): every chain re-walks the tree from the root; a token
+ *     already present as a child is walked for free, a new one buys a node
+ *     while the phase's budget lasts.  Lexical drafts are merged first under
+ *     the lexical allocation, retrieved chains after them under the fixed
+ *     retrieval reservation B_ret.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_EINVAL (-1)
+
+/* ------------------------------------------------------------------------ */
+/* bf16 <-> double.                                                          */
+/* A bf16 value is an IEEE binary32 value whose low 16 bits are zero.        */
+/* ------------------------------------------------------------------------ */
+
+double orc_bf16_to_double(uint16_t b)
+{
+    uint32_t bits = ((uint32_t)b) << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+/* Round a finite double to the nearest bf16 value, ties to the candidate with
+ * an even last significand bit.  Written from the definition: bf16 keeps 8
+ * significant bits, so near x (x = m * 2^e, 0.5 <= |m| < 1) the representable
+ * values are the integer multiples of 2^(e-8); below the smallest normal
+ * (2^-126) the spacing stays at 2^-133.  The two neighbours of x on that grid
+ * are compared directly. */
+uint16_t orc_bf16_round(double x)
+{
+    if (x != x)
+        return 0x7FC0; /* NaN */
+    if (x == 0.0)
+        return signbit(x) ? 0x8000 : 0x0000;
+    int e;
+    (void)frexp(x, &e);
+    if (e - 8 < -133)
+        e = -133 + 8;
+    double ulp = ldexp(1.0, e - 8);
+    double q = x / ulp;             /* exact: division by a power of two */
+    double lo = floor(q), hi = lo + 1.0;
+    double pick;
+    if (q - lo < hi - q)
+        pick = lo;
+    else if (hi - q < q - lo)
+        pick = hi;
+    else
+        pick = (fmod(fabs(lo), 2.0) == 0.0) ? lo : hi; /* tie: even multiple */
+    double v = pick * ulp;
+    if (fabs(v) > 3.3895313892515355e38) /* beyond the largest finite bf16 */
+        return (v > 0) ? 0x7F80 : 0xFF80;
+    float f = (float)v; /* exactly representable: 8 significant bits */
+    uint32_t bits;
+    memcpy(&bits, &f, sizeof bits);
+    return (uint16_t)(bits >> 16);
+}
+
+void orc_bf16_round_array(const double *x, int64_t n, uint16_t *out)
+{
+    for (int64_t i = 0; i < n; i++)
+        out[i] = orc_bf16_round(x[i]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Store: normalise each row to unit L2 norm and keep it in bf16 (Eq. 1).     */
+/* raw_dtype 0: float32 rows, 1: bf16 rows.  A zero row stays zero.          */
+/* ------------------------------------------------------------------------ */
+
+static double raw_elem(const void *raw, int raw_dtype, int64_t at)
+{
+    if (raw_dtype == 0)
+        return (double)((const float *)raw)[at];
+    return orc_bf16_to_double(((const uint16_t *)raw)[at]);
+}
+
+int orc_normalize_rows(const void *raw, int raw_dtype, int64_t n, int32_t d, uint16_t *out)
+{
+    if (!raw || !out || n < 0 || d < 1 || (raw_dtype != 0 && raw_dtype != 1))
+        return ORC_EINVAL;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < n; r++) {
+        double ss = 0.0;
+        for (int32_t j = 0; j < d; j++) {
+            double v = raw_elem(raw, raw_dtype, r * (int64_t)d + j);
+            ss += v * v;
+        }
+        double norm = sqrt(ss);
+        for (int32_t j = 0; j < d; j++) {
+            double v = raw_elem(raw, raw_dtype, r * (int64_t)d + j);
+            out[r * (int64_t)d + j] = orc_bf16_round(norm > 0.0 ? v / norm : 0.0);
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Similarity: s[b][i] = sum_j q[b][j] * k[i][j] for every stored position    */
+/* (Algorithm 1 retrieve step).  Exact products, summed in index order.       */
+/* ------------------------------------------------------------------------ */
+
+int orc_scores(const uint16_t *keys, int64_t n, int32_t d, const uint16_t *q, int32_t B, double *s)
+{
+    if ((!keys && n > 0) || !q || !s || n < 0 || d < 1 || B < 1)
+        return ORC_EINVAL;
+    for (int32_t b = 0; b < B; b++) {
+#pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < n; i++) {
+            double acc = 0.0;
+            for (int32_t j = 0; j < d; j++)
+                acc += orc_bf16_to_double(q[(int64_t)b * d + j]) *
+                       orc_bf16_to_double(keys[i * (int64_t)d + j]);
+            s[(int64_t)b * n + i] = acc;
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Top-k (Eq. 2): sort every admissible position by (score desc, index asc)   */
+/* and keep the first k.  Positions whose prompt id equals the query's are    */
+/* skipped (Sec. 4 (i)); an exclude value < 0 skips nothing.  Missing ranks   */
+/* are padded with score -inf and index -1.                                   */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    double s;
+    int64_t i;
+} orc_cand;
+
+static int cand_cmp(const void *pa, const void *pb)
+{
+    const orc_cand *a = (const orc_cand *)pa, *b = (const orc_cand *)pb;
+    if (a->s > b->s)
+        return -1;
+    if (a->s < b->s)
+        return 1;
+    return (a->i < b->i) ? -1 : (a->i > b->i);
+}
+
+int orc_topk(const double *s, int64_t n, int32_t B, const int32_t *prompt, const int32_t *exclude,
+             int32_t k, double *top_s, int32_t *top_i)
+{
+    if ((!s && n > 0) || !top_s || !top_i || n < 0 || B < 1 || k < 1)
+        return ORC_EINVAL;
+    orc_cand *c = (orc_cand *)malloc(sizeof(orc_cand) * (size_t)(n > 0 ? n : 1));
+    if (!c)
+        return ORC_EINVAL;
+    for (int32_t b = 0; b < B; b++) {
+        int64_t m = 0;
+        for (int64_t i = 0; i < n; i++) {
+            if (prompt && exclude && exclude[b] >= 0 && prompt[i] == exclude[b])
+                continue;
+            c[m].s = s[(int64_t)b * n + i];
+            c[m].i = i;
+            m++;
+        }
+        qsort(c, (size_t)m, sizeof(orc_cand), cand_cmp);
+        for (int32_t r = 0; r < k; r++) {
+            top_s[(int64_t)b * k + r] = (r < m) ? c[r].s : -INFINITY;
+            top_i[(int64_t)b * k + r] = (r < m) ? (int32_t)c[r].i : -1;
+        }
+    }
+    free(c);
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Gate, depth and continuation (Eq. 2 gate, Eq. 3, Algorithm 1 chain step).  */
+/*                                                                            */
+/* The query fires when the best retrieved score reaches theta.  For each     */
+/* retrieved i (rank order), the copy depth is the depth of the first band    */
+/* whose lower edge the score reaches (inclusive), else 0, capped at L.  The  */
+/* chain is x_{i+2}, ..., x_{i+1+depth}, stopping early at the end of the     */
+/* pool or where the trace id changes.  A chain of fewer than two tokens is   */
+/* dropped (length 0).  Scores arrive in float32 and are compared in float32. */
+/* ------------------------------------------------------------------------ */
+
+int orc_gather(const int32_t *tokens, const int32_t *traces, int64_t n_valid, const int32_t *idx,
+               const float *scores, int32_t B, int32_t k, float theta, int32_t n_bands,
+               const float *band_min, const int32_t *band_depth, int32_t L, int32_t *chain_tokens,
+               int32_t *chain_len)
+{
+    if (!idx || !scores || !chain_tokens || !chain_len || B < 1 || k < 1 || L < 1 || n_bands < 0 ||
+        (n_bands > 0 && (!band_min || !band_depth)) || n_valid < 0)
+        return ORC_EINVAL;
+    for (int32_t b = 0; b < B; b++) {
+        int fire = 0;
+        float best = -INFINITY;
+        for (int32_t r = 0; r < k; r++) {
+            int32_t i = idx[(int64_t)b * k + r];
+            if (i >= 0 && scores[(int64_t)b * k + r] > best)
+                best = scores[(int64_t)b * k + r];
+        }
+        if (best >= theta)
+            fire = 1;
+        for (int32_t r = 0; r < k; r++) {
+            int64_t o = ((int64_t)b * k + r);
+            int32_t *out = chain_tokens + o * L;
+            for (int32_t m = 0; m < L; m++)
+                out[m] = -1;
+            chain_len[o] = 0;
+            int32_t i = idx[o];
+            if (!fire || i < 0 || i >= n_valid)
+                continue;
+            float sc = scores[o];
+            int32_t depth = 0;
+            for (int32_t j = 0; j < n_bands; j++) {
+                if (sc >= band_min[j]) {
+                    depth = band_depth[j];
+                    break;
+                }
+            }
+            if (depth > L)
+                depth = L;
+            int32_t got = 0;
+            for (int32_t m = 1; m <= depth; m++) {
+                int64_t p = (int64_t)i + 1 + m; /* x_{i+2} first */
+                if (p >= n_valid || traces[p] != traces[i])
+                    break;
+                out[got++] = tokens[p];
+            }
+            if (got < 2) {
+                for (int32_t m = 0; m < L; m++)
+                    out[m] = -1;
+                got = 0;
+            }
+            chain_len[o] = got;
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Root-first merge (Sec. 4 (iii), Eq. 4; BuildLexical, MergeFromRoot).       */
+/*                                                                            */
+/* A pointer trie.  The root carries the anchor (the last committed token)    */
+/* and is not charged to any budget.  Phase 1 inserts the lexical drafts in   */
+/* the order given under lex_budget; phase 2 inserts the retrieved chains in  */
+/* rank order under sem_budget (a fixed reservation: lexical leftovers do not */
+/* roll over).  Inserting a chain walks from the root: a child carrying the   */
+/* next token is walked for free; otherwise a node is bought if the phase's   */
+/* budget remains, else the rest of that chain is dropped.  Nodes are         */
+/* numbered in creation order; unused slots are padded with -1.               */
+/* ------------------------------------------------------------------------ */
+
+typedef struct orc_node {
+    int32_t token, id;
+    int8_t source;
+    struct orc_node *parent, *first_child, *next_sibling;
+} orc_node;
+
+static orc_node *find_child(orc_node *cur, int32_t token)
+{
+    for (orc_node *c = cur->first_child; c; c = c->next_sibling)
+        if (c->token == token)
+            return c;
+    return NULL;
+}
+
+static void insert_chain(orc_node **nodes, int32_t *count, int32_t max_nodes, int32_t *spent,
+                         int32_t budget, int8_t source, const int32_t *chain, int32_t len)
+{
+    orc_node *cur = nodes[0];
+    for (int32_t m = 0; m < len; m++) {
+        orc_node *next = find_child(cur, chain[m]);
+        if (!next) {
+            if (*spent >= budget || *count >= max_nodes)
+                return;
+            next = (orc_node *)calloc(1, sizeof(orc_node));
+            next->token = chain[m];
+            next->id = *count;
+            next->source = source;
+            next->parent = cur;
+            /* append at the end of the sibling list: children in creation order */
+            if (!cur->first_child) {
+                cur->first_child = next;
+            } else {
+                orc_node *t = cur->first_child;
+                while (t->next_sibling)
+                    t = t->next_sibling;
+                t->next_sibling = next;
+            }
+            nodes[(*count)++] = next;
+            (*spent)++;
+        }
+        cur = next;
+    }
+}
+
+int orc_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens, const int32_t *lex_len,
+                   int32_t n_lex, int32_t L_lex, int32_t lex_budget, const int32_t *sem_tokens,
+                   const int32_t *sem_len, int32_t k, int32_t L, int32_t sem_budget, int32_t max_nodes,
+                   int32_t *node_token, int32_t *node_parent, int8_t *node_source, int32_t *n_nodes)
+{
+    if (B < 1 || !anchor || n_lex < 0 || k < 0 || lex_budget < 0 || sem_budget < 0 ||
+        max_nodes < 1 + lex_budget + sem_budget || !node_token || !node_parent || !node_source ||
+        !n_nodes || (n_lex > 0 && (!lex_tokens || !lex_len || L_lex < 1)) ||
+        (k > 0 && (!sem_tokens || !sem_len || L < 1)))
+        return ORC_EINVAL;
+    orc_node **nodes = (orc_node **)calloc((size_t)max_nodes, sizeof(orc_node *));
+    for (int32_t b = 0; b < B; b++) {
+        int32_t count = 0, spent = 0;
+        orc_node *root = (orc_node *)calloc(1, sizeof(orc_node));
+        root->token = anchor[b];
+        root->id = 0;
+        root->source = 0;
+        nodes[count++] = root;
+        for (int32_t c = 0; c < n_lex; c++) {
+            int64_t o = (int64_t)b * n_lex + c;
+            int32_t len = lex_len[o] < L_lex ? lex_len[o] : L_lex;
+            insert_chain(nodes, &count, max_nodes, &spent, lex_budget, 1, lex_tokens + o * L_lex, len);
+        }
+        spent = 0;
+        for (int32_t c = 0; c < k; c++) {
+            int64_t o = (int64_t)b * k + c;
+            int32_t len = sem_len[o] < L ? sem_len[o] : L;
+            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 2, sem_tokens + o * L, len);
+        }
+        for (int32_t j = 0; j < max_nodes; j++) {
+            int64_t o = (int64_t)b * max_nodes + j;
+            if (j < count) {
+                node_token[o] = nodes[j]->token;
+                node_parent[o] = nodes[j]->parent ? nodes[j]->parent->id : -1;
+                node_source[o] = nodes[j]->source;
+            } else {
+                node_token[o] = -1;
+                node_parent[o] = -1;
+                node_source[o] = -1;
+            }
+        }
+        n_nodes[b] = count;
+        for (int32_t j = 0; j < count; j++)
+            free(nodes[j]);
+    }
+    free(nodes);
+    return ORC_OK;
+}

@@ -1,0 +1,46 @@
+"""The pins must catch plausible mistakes: each mutant below plants one in a
+copy of the oracle's C source (on the CPU, in a temporary directory), and the
+pin suite, pointed at the mutant library, must fail."""
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "oracle.c")
+
+MUTANTS = {
+    "copy starts one after the neighbour": ("int64_t p = (int64_t)i + 1 + m;", "int64_t p = (int64_t)i + m;"),
+    "trace boundary ignored": ("if (p >= n_valid || traces[p] != traces[i])", "if (p >= n_valid)"),
+    "band edge exclusive": ("if (sc >= band_min[j]) {", "if (sc > band_min[j]) {"),
+    "theta exclusive": ("if (best >= theta)", "if (best > theta)"),
+    "short chains kept": ("if (got < 2) {", "if (got < 1) {"),
+    "ties broken by higher index": ("return (a->i < b->i) ? -1 : (a->i > b->i);", "return (a->i > b->i) ? -1 : (a->i < b->i);"),
+    "lexical budget rolls over": ("        spent = 0;\n        for (int32_t c = 0; c < k; c++) {", "        spent = spent - lex_budget;\n        for (int32_t c = 0; c < k; c++) {"),
+    "root charged to the budget": ("        int32_t count = 0, spent = 0;", "        int32_t count = 0, spent = 1;"),
+    "no prefix walk (root-attached)": ("        orc_node *next = find_child(cur, chain[m]);", "        orc_node *next = m < 0 ? find_child(cur, chain[m]) : NULL;"),
+    "norm without square root": ("double norm = sqrt(ss);", "double norm = ss;"),
+    "rounding ties away from zero": ("pick = (fmod(fabs(lo), 2.0) == 0.0) ? lo : hi;", "pick = hi;"),
+    "score drops the last dim": ("for (int32_t j = 0; j < d; j++)\n                acc +=", "for (int32_t j = 0; j < d - 1; j++)\n                acc +="),
+    "exclusion ignored": ("if (prompt && exclude && exclude[b] >= 0 && prompt[i] == exclude[b])", "if (0)"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name!r} not found exactly once"
+    with tempfile.TemporaryDirectory() as td:
+        c = os.path.join(td, "mut.c")
+        so = os.path.join(td, "libmut.so")
+        open(c, "w").write(src.replace(old, new))
+        subprocess.run(["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC",
+                        "-shared", "-std=c11", "-o", so, c, "-lm"], check=True)
+        env = dict(os.environ, OILBIRD_ORACLE_LIB=so)
+        r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
+                            os.path.join(ROOT, "tests", "test_oracle.py")],
+                           env=env, cwd=ROOT, capture_output=True, text=True, timeout=300)
+        assert r.returncode != 0, f"pins did not catch mutant {name!r}"
