@@ -1,0 +1,200 @@
+/*
+ * oilbird.h -- C ABI of the semantic draft source hot path (Oilbird,
+ * arXiv 2608.03839), for AMD Instinct MI355X (gfx950).
+ *
+ * The path: a store of committed positions keyed by the verifier's hidden
+ * state (Sec. 4 (i), Eq. 1); a batch of query states scored against every
+ * stored key by cosine similarity and the exact top-k positions selected
+ * (Algorithm 1 retrieve step, Eq. 2); the continuation that follows each hit
+ * read out of its trace (Eq. 3); and a root-first merge of those chains,
+ * beside lexical drafts, into a draft tree under a node budget (Sec. 4 (iii),
+ * Eq. 4).
+ *
+ * Conventions shared by every call:
+ *   - Buffers are DEVICE pointers owned by the caller unless marked (host).
+ *     The library allocates no device memory; the only thing it owns is the
+ *     small host-side pool handle.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Every call validates its arguments on the host, enqueues its kernels on
+ *     `stream` and returns without synchronising.  Outputs are valid once the
+ *     stream has reached that point.  Calls on one pool must be ordered by the
+ *     caller (one stream, or explicit events); a pool handle is not
+ *     thread-safe.
+ *   - On a bad argument a call returns a negative status and enqueues
+ *     nothing.  A failed launch returns OIL_E_HIP.  A device fault surfaces at
+ *     the caller's next synchronisation.
+ *   - bf16 values are stored as 16-bit patterns (the upper half of an IEEE
+ *     binary32); the dtype codes below name the raw input formats accepted.
+ */
+#ifndef OILBIRD_H
+#define OILBIRD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct oil_pool oil_pool;
+
+enum {
+    OIL_OK = 0,
+    OIL_E_INVALID = -1,     /* bad argument: null pointer, size out of range, misalignment */
+    OIL_E_CAPACITY = -2,    /* an append would exceed the pool's capacity */
+    OIL_E_UNSUPPORTED = -3, /* a valid request this build does not serve (e.g. k > 64) */
+    OIL_E_HIP = -4,         /* the HIP runtime reported an error while enqueuing */
+    OIL_E_WORKSPACE = -5    /* workspace too small or misaligned */
+};
+
+enum { OIL_F32 = 0, OIL_BF16 = 1 };
+
+/* Largest k, query batch and tree size served. */
+#define OIL_MAX_K 64
+#define OIL_MAX_B 64
+#define OIL_MAX_NODES 256
+#define OIL_MAX_BANDS 4
+
+/* Padded key width, in bf16 elements: `dim` rounded up to a multiple of 64.
+ * The padding columns are kept zero by the library, so they never change a
+ * dot product. */
+int32_t oil_key_stride(int32_t dim);
+
+/* Bytes the caller must provide for `capacity` keys of width `dim`:
+ * oil_key_stride(dim) * (capacity rounded up to 32) * 2.
+ *
+ * Key buffer layout (bf16 elements).  Rows are grouped in blocks of 32 and
+ * the padded columns in windows of 64; each (row block, window) pair is one
+ * contiguous 4 KiB tile in MFMA operand order, and tiles are stored window
+ * by window: all row blocks of window 0, then of window 1, and so on.  While
+ * the scan's wavefronts walk their row blocks window by window, the chip
+ * reads one contiguous region at a time, and every 16-byte per-lane load
+ * covers 1 KiB contiguous.  With R = capacity rounded up to 32, divided by
+ * 32, row i and column j live at
+ *     ((j / 64) * R + i / 32) * 2048 + (s * 64 + lane) * 8 + (j % 8),
+ *     s = (j % 32) / 8,  lane = i % 32 + 32 * ((j % 64) / 32).
+ */
+size_t oil_pool_key_bytes(int32_t dim, int64_t capacity);
+
+/* Create a pool over caller-owned storage (Sec. 4 (i), Eq. 1: one record
+ * (x_i, h_i) per committed position).
+ *   dim        key width d_model, >= 1.
+ *   capacity   rows the buffers hold, 1 .. 2^31 - 1.
+ *   key_buf    oil_pool_key_bytes(dim, capacity) bytes, 256-byte aligned, in
+ *              the tiled layout above (written only by oil_pool_append).
+ *   token_buf  capacity int32: x_i, the token committed at position i.
+ *   trace_buf  capacity int32: the trace (request) holding position i; a
+ *              continuation never crosses a change of trace id.
+ *   prompt_buf capacity int32 or NULL: prompt id of the request that produced
+ *              position i, >= 0; needed only for self-exclusion at query time.
+ *   out        (host) receives the handle.  The pool starts empty. */
+int32_t oil_pool_create(int32_t dim, int64_t capacity, void *key_buf, int32_t *token_buf,
+                        int32_t *trace_buf, int32_t *prompt_buf, oil_pool **out);
+
+/* Release the host handle (the caller's buffers are untouched). */
+int32_t oil_pool_destroy(oil_pool *pool);
+
+/* (host) Number of stored positions, counted in enqueue order. */
+int32_t oil_pool_size(const oil_pool *pool, int64_t *n_valid);
+
+/* Append n positions at [n_valid, n_valid + n) (Sec. 4 (i), Eq. 1): each raw
+ * key row is divided by its L2 norm (evaluated in double precision) and
+ * rounded to bf16, nearest-even; a zero row is stored as zeros.
+ *   keys       n x dim raw rows, row-major, dense (stride dim), dtype
+ *              OIL_F32 or OIL_BF16, 16-byte aligned.
+ *   tokens, trace_ids  n int32 each.
+ *   prompt_ids n int32 (>= 0), required iff the pool has a prompt buffer.
+ *   n          0 .. capacity - n_valid (n = 0 is a no-op); beyond that the
+ *              call returns OIL_E_CAPACITY and stores nothing.
+ * The handle's count advances at enqueue time; later calls on the same
+ * stream see the new rows. */
+int32_t oil_pool_append(oil_pool *pool, const void *keys, int32_t key_dtype, const int32_t *tokens,
+                        const int32_t *trace_ids, const int32_t *prompt_ids, int64_t n,
+                        void *stream);
+
+/* Workspace bytes oil_pool_query_topk needs for B queries and k neighbours
+ * (sized from the pool's capacity, so it stays valid as the pool grows). */
+size_t oil_query_workspace_bytes(const oil_pool *pool, int32_t B, int32_t k);
+
+/* Retrieval (Algorithm 1 retrieve step, Eq. 2): normalise each query row as
+ * keys are normalised, score it against every stored key (dot product of the
+ * unit bf16 operands, fp32 accumulation) and return the k best positions in
+ * the total order (score descending, position ascending).
+ *   queries    B x dim raw rows, dense, OIL_F32 or OIL_BF16, 16-byte aligned.
+ *   B          1 .. OIL_MAX_B.   k  1 .. OIL_MAX_K.
+ *   exclude_prompt  B int32 or NULL: query b never returns a position whose
+ *              prompt id equals exclude_prompt[b] (Sec. 4 (i): a request does
+ *              not draft from a copy of itself); a negative value excludes
+ *              nothing.  Requires a pool created with a prompt buffer.
+ *   workspace  >= oil_query_workspace_bytes(pool, B, k) bytes, 256-byte aligned.
+ *   scores     B x k float32, descending per row; -inf where no position.
+ *   idx        B x k int32 positions; -1 where no position (pool smaller
+ *              than k, or every remaining position excluded).
+ * The firing gate (best score >= theta) is applied by the gather call. */
+int32_t oil_pool_query_topk(const oil_pool *pool, const void *queries, int32_t q_dtype, int32_t B,
+                            int32_t k, const int32_t *exclude_prompt, void *workspace,
+                            size_t workspace_bytes, float *scores, int32_t *idx, void *stream);
+
+/* Copy-depth rule (Eq. 3).  A query fires when its best score is >= theta
+ * (Eq. 2).  A fired entry with score s copies band_depth[j] tokens for the
+ * first band j (in order) with s >= band_min[j], else 0, capped at L.
+ * The paper's rule: {0.8f, 2, {0.90f, 0.82f}, {48, 8}}.
+ * The fixed-span variant of the batching probe: {theta, 1, {-INFINITY}, {L}}. */
+typedef struct {
+    float theta;
+    int32_t n_bands; /* 0 .. OIL_MAX_BANDS */
+    float band_min[OIL_MAX_BANDS];
+    int32_t band_depth[OIL_MAX_BANDS];
+} oil_depth_rule;
+
+/* Continuations (Eq. 3, Algorithm 1 chain step): for every (query b, rank r)
+ * with idx i = idx[b*k + r] >= 0 of a fired query, the chain
+ * x_{i+2}, ..., x_{i+1+depth}, stopping early at the end of the pool or where
+ * the trace id changes; chains shorter than two tokens are dropped.
+ *   idx, scores  B x k as returned by oil_pool_query_topk (any order; the
+ *              gate uses the maximum over entries with idx >= 0).
+ *   rule       (host) depth rule.   L  1 .. 64: chain width.
+ *   chain_tokens  B x k x L int32, -1 padded.   chain_len  B x k int32. */
+int32_t oil_gather_continuations(const oil_pool *pool, const int32_t *idx, const float *scores,
+                                 int32_t B, int32_t k, const oil_depth_rule *rule, int32_t L,
+                                 int32_t *chain_tokens, int32_t *chain_len, void *stream);
+
+/* Root-first merge (Sec. 4 (iii), Eq. 4; BuildLexical then MergeFromRoot in
+ * Algorithm 1).  Per query: node 0 is the root (token anchor[b], parent -1,
+ * source 0, charged to no budget).  The n_lex lexical drafts are inserted in
+ * order under lex_budget, then the k retrieved chains in rank order under
+ * sem_budget (a fixed reservation; unused lexical budget does not roll over).
+ * Inserting a chain walks from the root: a child carrying the next token is
+ * walked for free, otherwise a node is bought while the phase's budget lasts,
+ * else the rest of that chain is dropped.
+ *   lex_tokens B x n_lex x L_lex int32, lex_len B x n_lex (n_lex may be 0,
+ *              then both may be NULL).   sem_tokens B x k x L, sem_len B x k.
+ *   max_nodes  1 + lex_budget + sem_budget .. OIL_MAX_NODES.
+ *   node_token, node_parent  B x max_nodes int32; node_source B x max_nodes
+ *              int8 (0 root, 1 lexical, 2 retrieved); nodes in creation
+ *              order (parents precede children), slots past n_nodes[b] = -1.
+ *   n_nodes    B int32. */
+int32_t oil_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens,
+                       const int32_t *lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
+                       const int32_t *sem_tokens, const int32_t *sem_len, int32_t k, int32_t L,
+                       int32_t sem_budget, int32_t max_nodes, int32_t *node_token,
+                       int32_t *node_parent, int8_t *node_source, int32_t *n_nodes, void *stream);
+
+/* Benchmark instrumentation (host; not thread-safe).  While enabled, each
+ * oil_pool_query_topk call records a HIP event pair around its pool-scan
+ * kernel on the call's stream, for up to max_launches calls (1 .. 65536).
+ * oil_scan_timer_stop waits for those events, returns how many launches were
+ * timed and their summed duration in milliseconds, and disables timing.
+ * Events are created by start and destroyed by stop; no device memory is
+ * allocated. */
+int32_t oil_scan_timer_start(int32_t max_launches);
+int32_t oil_scan_timer_stop(int32_t *n_launches, double *total_ms);
+
+/* (host) Static description of a status code. */
+const char *oil_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OILBIRD_H */

@@ -41,6 +41,8 @@ def _load():
         lib = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
         i32, i64, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+        lib.orc_max_threads.restype = ctypes.c_int
+        lib.orc_max_threads.argtypes = []
         lib.orc_bf16_round.restype = ctypes.c_uint16
         lib.orc_bf16_round.argtypes = [ctypes.c_double]
         lib.orc_bf16_round_array.argtypes = [P, i64, P]
@@ -65,6 +67,11 @@ def _c(a, dtype):
 def _check(rc, name):
     if rc != 0:
         raise ValueError(f"oracle {name} rejected its arguments (rc={rc})")
+
+
+def max_threads() -> int:
+    """Threads the oracle's OpenMP loops use."""
+    return int(_load().orc_max_threads())
 
 
 # ---------------------------------------------------------------- bf16 helpers

@@ -34,6 +34,9 @@
  *     retrieval reservation B_ret.
  */
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -45,6 +48,16 @@
 /* bf16 <-> double.                                                          */
 /* A bf16 value is an IEEE binary32 value whose low 16 bits are zero.        */
 /* ------------------------------------------------------------------------ */
+
+/* Threads the OpenMP loops below may use (1 without OpenMP). */
+int orc_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
 
 double orc_bf16_to_double(uint16_t b)
 {

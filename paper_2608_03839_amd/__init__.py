@@ -1,0 +1,292 @@
+"""Oilbird semantic draft source on AMD Instinct MI355X (gfx950).
+
+Thin Python binding over the C ABI declared in ``include/oilbird.h``
+(``liboilbird.so``, built by ``python -m paper_2608_03839_amd.build``).  Every
+step of the retrieval path runs in the library's HIP kernels; this module only
+marshals torch tensors (device memory) and the current torch stream into the
+C calls.  There is no fallback: if the library is missing, importing the
+binding's entry points raises.
+
+Entry points carry the names of the C calls without their ``oil_`` prefix:
+``pool_create``, ``pool_append``, ``pool_size``, ``query_workspace_bytes``,
+``pool_query_topk``, ``gather_continuations``, ``tree_merge``; ``Pool`` bundles
+a pool's buffers and handle.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboilbird.so")
+
+OIL_F32, OIL_BF16 = 0, 1
+MAX_K, MAX_B, MAX_NODES, MAX_BANDS = 64, 64, 256, 4
+
+_lib = None
+
+
+class OilError(RuntimeError):
+    def __init__(self, call, status):
+        self.status = status
+        msg = lib().oil_status_string(status).decode()
+        super().__init__(f"{call} failed: {msg} (status {status})")
+
+
+class DepthRule(ctypes.Structure):
+    """Copy-depth rule of Eq. 3 (see oil_depth_rule)."""
+    _fields_ = [("theta", ctypes.c_float), ("n_bands", ctypes.c_int32),
+                ("band_min", ctypes.c_float * MAX_BANDS), ("band_depth", ctypes.c_int32 * MAX_BANDS)]
+
+    @classmethod
+    def make(cls, theta, band_min, band_depth):
+        r = cls()
+        r.theta = float(theta)
+        r.n_bands = len(band_min)
+        if len(band_min) != len(band_depth) or len(band_min) > MAX_BANDS:
+            raise ValueError("band_min and band_depth must have equal length <= 4")
+        for j, (m, dd) in enumerate(zip(band_min, band_depth)):
+            r.band_min[j] = float(m)
+            r.band_depth[j] = int(dd)
+        return r
+
+    @classmethod
+    def paper(cls, theta=0.8):
+        """D(s) = 48 if s >= 0.90, 8 if s >= 0.82, else 0 (Eq. 3)."""
+        return cls.make(theta, [0.90, 0.82], [48, 8])
+
+    @classmethod
+    def fixed(cls, L, theta=0.8):
+        """A fixed span of L tokens for every entry of a fired query."""
+        return cls.make(theta, [-math.inf], [L])
+
+
+def lib():
+    """Load liboilbird.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2608_03839_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        sig = {
+            "oil_key_stride": (i32, [i32]),
+            "oil_pool_key_bytes": (sz, [i32, i64]),
+            "oil_pool_create": (i32, [i32, i64, P, P, P, P, ctypes.POINTER(P)]),
+            "oil_pool_destroy": (i32, [P]),
+            "oil_pool_size": (i32, [P, ctypes.POINTER(i64)]),
+            "oil_pool_append": (i32, [P, P, i32, P, P, P, i64, P]),
+            "oil_query_workspace_bytes": (sz, [P, i32, i32]),
+            "oil_pool_query_topk": (i32, [P, P, i32, i32, i32, P, P, sz, P, P, P]),
+            "oil_gather_continuations": (i32, [P, P, P, i32, i32, ctypes.POINTER(DepthRule), i32,
+                                               P, P, P]),
+            "oil_tree_merge": (i32, [i32, P, P, P, i32, i32, i32, P, P, i32, i32, i32, i32, P, P,
+                                     P, P, P]),
+            "oil_status_string": (ctypes.c_char_p, [i32]),
+            "oil_scan_timer_start": (i32, [i32]),
+            "oil_scan_timer_stop": (i32, [ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+# ---------------------------------------------------------------- marshalling
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("device tensor expected")
+    if not t.is_contiguous():
+        raise ValueError("contiguous tensor expected")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return OIL_F32
+    if t.dtype == torch.bfloat16:
+        return OIL_BF16
+    raise ValueError(f"rows must be float32 or bfloat16, got {t.dtype}")
+
+
+def _check(call, status):
+    if status != 0:
+        raise OilError(call, status)
+
+
+def _i32(t, name):
+    if t.dtype != torch.int32:
+        raise ValueError(f"{name} must be int32")
+    return t
+
+
+# ---------------------------------------------------------------- C calls
+def key_stride(dim: int) -> int:
+    return lib().oil_key_stride(dim)
+
+
+def pool_key_bytes(dim: int, capacity: int) -> int:
+    return lib().oil_pool_key_bytes(dim, capacity)
+
+
+def pool_create(dim, capacity, key_buf, token_buf, trace_buf, prompt_buf=None):
+    h = ctypes.c_void_p()
+    _check("oil_pool_create", lib().oil_pool_create(dim, capacity, _ptr(key_buf), _ptr(token_buf),
+                                                    _ptr(trace_buf), _ptr(prompt_buf),
+                                                    ctypes.byref(h)))
+    return h
+
+
+def pool_destroy(handle):
+    _check("oil_pool_destroy", lib().oil_pool_destroy(handle))
+
+
+def pool_size(handle) -> int:
+    n = ctypes.c_int64()
+    _check("oil_pool_size", lib().oil_pool_size(handle, ctypes.byref(n)))
+    return n.value
+
+
+def pool_append(handle, keys, tokens, trace_ids, prompt_ids=None, stream=None):
+    n = keys.shape[0] if keys.dim() == 2 else 0
+    _check("oil_pool_append", lib().oil_pool_append(
+        handle, _ptr(keys), _dtype_code(keys), _ptr(_i32(tokens, "tokens")),
+        _ptr(_i32(trace_ids, "trace_ids")),
+        _ptr(None if prompt_ids is None else _i32(prompt_ids, "prompt_ids")), n, _stream(stream)))
+
+
+def query_workspace_bytes(handle, B, k) -> int:
+    return lib().oil_query_workspace_bytes(handle, B, k)
+
+
+def pool_query_topk(handle, queries, k, workspace, scores, idx, exclude_prompt=None, stream=None):
+    B = queries.shape[0]
+    _check("oil_pool_query_topk", lib().oil_pool_query_topk(
+        handle, _ptr(queries), _dtype_code(queries), B, k,
+        _ptr(None if exclude_prompt is None else _i32(exclude_prompt, "exclude_prompt")),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(scores),
+        _ptr(_i32(idx, "idx")), _stream(stream)))
+
+
+def gather_continuations(handle, idx, scores, rule: DepthRule, L, chain_tokens, chain_len,
+                         stream=None):
+    B, k = idx.shape
+    _check("oil_gather_continuations", lib().oil_gather_continuations(
+        handle, _ptr(_i32(idx, "idx")), _ptr(scores), B, k, ctypes.byref(rule), L,
+        _ptr(chain_tokens), _ptr(chain_len), _stream(stream)))
+
+
+def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget,
+               max_nodes, node_token, node_parent, node_source, n_nodes, stream=None):
+    """Root-first merge.  ``lex_tokens`` (B, n_lex, L_lex) or None; ``sem_tokens`` (B, k, L)."""
+    B = anchor.shape[0]
+    if lex_tokens is None or lex_tokens.shape[1] == 0:
+        n_lex, L_lex, lt, ll = 0, 1, None, None
+    else:
+        n_lex, L_lex, lt, ll = lex_tokens.shape[1], lex_tokens.shape[2], lex_tokens, lex_len
+    k, L = sem_tokens.shape[1], sem_tokens.shape[2]
+    _check("oil_tree_merge", lib().oil_tree_merge(
+        B, _ptr(_i32(anchor, "anchor")), _ptr(lt), _ptr(ll), n_lex, L_lex, lex_budget,
+        _ptr(sem_tokens), _ptr(sem_len), k, L, sem_budget, max_nodes, _ptr(node_token),
+        _ptr(node_parent), _ptr(node_source), _ptr(n_nodes), _stream(stream)))
+
+
+def scan_timer_start(max_launches: int):
+    _check("oil_scan_timer_start", lib().oil_scan_timer_start(max_launches))
+
+
+def scan_timer_stop():
+    """-> (number of timed scan launches, summed milliseconds)."""
+    n, ms = ctypes.c_int32(), ctypes.c_double()
+    _check("oil_scan_timer_stop", lib().oil_scan_timer_stop(ctypes.byref(n), ctypes.byref(ms)))
+    return n.value, ms.value
+
+
+# ---------------------------------------------------------------- convenience
+class Pool:
+    """A pool and the device buffers it lives in (torch tensors, caller-owned)."""
+
+    def __init__(self, dim: int, capacity: int, device="cuda", with_prompts: bool = True):
+        self.dim, self.capacity = dim, capacity
+        self.device = torch.device(device)
+        self.stride = key_stride(dim)
+        # tiled bf16 storage (see oil_pool_key_bytes); torch's caching allocator
+        # aligns blocks to >= 512 bytes
+        nbytes = pool_key_bytes(dim, capacity)
+        self.keys = torch.empty((nbytes // 2,), dtype=torch.bfloat16, device=self.device)
+        self.tokens = torch.empty((capacity,), dtype=torch.int32, device=self.device)
+        self.traces = torch.empty((capacity,), dtype=torch.int32, device=self.device)
+        self.prompts = (torch.empty((capacity,), dtype=torch.int32, device=self.device)
+                        if with_prompts else None)
+        self.handle = pool_create(dim, capacity, self.keys, self.tokens, self.traces, self.prompts)
+        self._ws = {}
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and _lib is not None:
+            _lib.oil_pool_destroy(h)
+            self.handle = None
+
+    def __len__(self):
+        return pool_size(self.handle)
+
+    def append(self, keys, tokens, trace_ids, prompt_ids=None, stream=None):
+        pool_append(self.handle, keys, tokens, trace_ids, prompt_ids, stream)
+
+    def workspace(self, B, k):
+        key = (B, k)
+        if key not in self._ws:
+            nb = query_workspace_bytes(self.handle, B, k)
+            if nb == 0:
+                raise ValueError(f"unsupported query batch/k: B={B} k={k}")
+            self._ws[key] = torch.empty((nb,), dtype=torch.uint8, device=self.device)
+        return self._ws[key]
+
+    def query_topk(self, queries, k, exclude_prompt=None, stream=None, out=None):
+        B = queries.shape[0]
+        if out is None:
+            scores = torch.empty((B, k), dtype=torch.float32, device=self.device)
+            idx = torch.empty((B, k), dtype=torch.int32, device=self.device)
+        else:
+            scores, idx = out
+        pool_query_topk(self.handle, queries, k, self.workspace(B, k), scores, idx,
+                        exclude_prompt, stream)
+        return scores, idx
+
+    def gather(self, idx, scores, rule: DepthRule, L, stream=None, out=None):
+        B, k = idx.shape
+        if out is None:
+            ct = torch.empty((B, k, L), dtype=torch.int32, device=self.device)
+            cl = torch.empty((B, k), dtype=torch.int32, device=self.device)
+        else:
+            ct, cl = out
+        gather_continuations(self.handle, idx, scores, rule, L, ct, cl, stream)
+        return ct, cl
+
+
+def merge_trees(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget,
+                max_nodes, stream=None, out=None):
+    """Allocate outputs and run tree_merge; returns (node_token, node_parent, node_source, n_nodes)."""
+    B = anchor.shape[0]
+    dev = anchor.device
+    if out is None:
+        nt = torch.empty((B, max_nodes), dtype=torch.int32, device=dev)
+        npar = torch.empty((B, max_nodes), dtype=torch.int32, device=dev)
+        ns = torch.empty((B, max_nodes), dtype=torch.int8, device=dev)
+        nn = torch.empty((B,), dtype=torch.int32, device=dev)
+    else:
+        nt, npar, ns, nn = out
+    tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget, max_nodes,
+               nt, npar, ns, nn, stream)
+    return nt, npar, ns, nn

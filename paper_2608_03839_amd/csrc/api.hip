@@ -1,0 +1,298 @@
+// C ABI of the retrieval path: argument checks, workspace carving and kernel
+// launches.  Declarations and the contract of every entry point are in
+// include/oilbird.h.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "../../include/oilbird.h"
+#include "common.hpp"
+#include "internal.hpp"
+
+static_assert(OIL_MAX_K == OIL_TOPK_MAX, "top-k capacity");
+static_assert(OIL_MAX_NODES == OIL_NODES_MAX, "tree capacity");
+static_assert(OIL_MAX_BANDS == OIL_BANDS_MAX, "band table");
+
+struct oil_pool {
+    int32_t dim, ld;
+    int64_t capacity, n_valid;
+    int64_t rs, ws;  // tile strides of the key buffer (elements)
+    uint16_t* keys;
+    int32_t *tokens, *traces, *prompts;
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int32_t hip_status(hipError_t e) { return e == hipSuccess ? OIL_OK : OIL_E_HIP; }
+
+struct QueryWorkspace {
+    size_t q_off, s_off, ca_off, cb_off, total;
+    int64_t s_ld;
+};
+
+QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
+{
+    QueryWorkspace w;
+    const int tiles = oil::scan_query_tiles(B);
+    const size_t q_bytes = (size_t)tiles * 32 * (size_t)p->ld * sizeof(uint16_t);
+    w.s_ld = (int64_t)round_up((size_t)p->capacity, 64);
+    const size_t s_bytes = (size_t)B * (size_t)w.s_ld * sizeof(float);
+    const size_t c_bytes = oil::topk_cand_bytes(B, k, p->capacity);
+    w.q_off = 0;
+    w.s_off = round_up(w.q_off + q_bytes, kAlign);
+    w.ca_off = round_up(w.s_off + s_bytes, kAlign);
+    w.cb_off = round_up(w.ca_off + c_bytes, kAlign);
+    w.total = round_up(w.cb_off + c_bytes, kAlign);
+    return w;
+}
+
+// Scan-kernel timing for the benchmark (see oil_scan_timer_start).
+struct ScanTimer {
+    hipEvent_t* ev = nullptr;
+    int32_t cap = 0, used = 0;
+};
+ScanTimer g_timer;
+
+void timer_mark(hipStream_t st, int which)
+{
+    if (g_timer.ev && g_timer.used < g_timer.cap)
+        (void)hipEventRecord(g_timer.ev[2 * g_timer.used + which], st);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t oil_scan_timer_start(int32_t max_launches)
+{
+    if (max_launches < 1 || max_launches > 65536 || g_timer.ev)
+        return OIL_E_INVALID;
+    g_timer.ev = (hipEvent_t*)calloc(2 * (size_t)max_launches, sizeof(hipEvent_t));
+    if (!g_timer.ev)
+        return OIL_E_INVALID;
+    for (int32_t i = 0; i < 2 * max_launches; i++) {
+        if (hipEventCreate(&g_timer.ev[i]) != hipSuccess) {
+            for (int32_t j = 0; j < i; j++)
+                (void)hipEventDestroy(g_timer.ev[j]);
+            free(g_timer.ev);
+            g_timer.ev = nullptr;
+            return OIL_E_HIP;
+        }
+    }
+    g_timer.cap = max_launches;
+    g_timer.used = 0;
+    return OIL_OK;
+}
+
+int32_t oil_scan_timer_stop(int32_t* n_launches, double* total_ms)
+{
+    if (!n_launches || !total_ms || !g_timer.ev)
+        return OIL_E_INVALID;
+    int32_t st = OIL_OK;
+    double total = 0.0;
+    for (int32_t i = 0; i < g_timer.used; i++) {
+        float ms = 0.f;
+        if (hipEventSynchronize(g_timer.ev[2 * i + 1]) != hipSuccess ||
+            hipEventElapsedTime(&ms, g_timer.ev[2 * i], g_timer.ev[2 * i + 1]) != hipSuccess)
+            st = OIL_E_HIP;
+        total += ms;
+    }
+    for (int32_t i = 0; i < 2 * g_timer.cap; i++)
+        (void)hipEventDestroy(g_timer.ev[i]);
+    free(g_timer.ev);
+    *n_launches = g_timer.used;
+    *total_ms = total;
+    g_timer = ScanTimer();
+    return st;
+}
+
+int32_t oil_key_stride(int32_t dim)
+{
+    if (dim < 1)
+        return 0;
+    return (int32_t)round_up((size_t)dim, 64);
+}
+
+size_t oil_pool_key_bytes(int32_t dim, int64_t capacity)
+{
+    if (dim < 1 || capacity < 1)
+        return 0;
+    return (size_t)oil_key_stride(dim) * round_up((size_t)capacity, oil::kRowBlock) * sizeof(uint16_t);
+}
+
+int32_t oil_pool_create(int32_t dim, int64_t capacity, void* key_buf, int32_t* token_buf,
+                        int32_t* trace_buf, int32_t* prompt_buf, oil_pool** out)
+{
+    if (!out)
+        return OIL_E_INVALID;
+    *out = nullptr;
+    if (dim < 1 || dim > (1 << 20) || capacity < 1 || capacity > INT32_MAX || !key_buf ||
+        !token_buf || !trace_buf || !aligned(key_buf, kAlign))
+        return OIL_E_INVALID;
+    oil_pool* p = (oil_pool*)calloc(1, sizeof(oil_pool));
+    if (!p)
+        return OIL_E_INVALID;
+    p->dim = dim;
+    p->ld = oil_key_stride(dim);
+    p->capacity = capacity;
+    p->n_valid = 0;
+    // window-major tiles: tile (row block, window) at (window * row_blocks + row block) * 2048
+    p->rs = 2048;
+    p->ws = 2048 * (int64_t)round_up((size_t)capacity, oil::kRowBlock) / oil::kRowBlock;
+    p->keys = (uint16_t*)key_buf;
+    p->tokens = token_buf;
+    p->traces = trace_buf;
+    p->prompts = prompt_buf;
+    *out = p;
+    return OIL_OK;
+}
+
+int32_t oil_pool_destroy(oil_pool* pool)
+{
+    if (!pool)
+        return OIL_E_INVALID;
+    free(pool);
+    return OIL_OK;
+}
+
+int32_t oil_pool_size(const oil_pool* pool, int64_t* n_valid)
+{
+    if (!pool || !n_valid)
+        return OIL_E_INVALID;
+    *n_valid = pool->n_valid;
+    return OIL_OK;
+}
+
+int32_t oil_pool_append(oil_pool* pool, const void* keys, int32_t key_dtype, const int32_t* tokens,
+                        const int32_t* trace_ids, const int32_t* prompt_ids, int64_t n, void* stream)
+{
+    if (!pool || n < 0 || (key_dtype != OIL_F32 && key_dtype != OIL_BF16))
+        return OIL_E_INVALID;
+    if (n == 0)
+        return OIL_OK;
+    if (!keys || !tokens || !trace_ids || !aligned(keys, 16))
+        return OIL_E_INVALID;
+    if ((pool->prompts != nullptr) != (prompt_ids != nullptr))
+        return OIL_E_INVALID;
+    if (n > pool->capacity - pool->n_valid)
+        return OIL_E_CAPACITY;
+    hipError_t e = oil::launch_normalize_rows(
+        keys, key_dtype, pool->dim, n, n, pool->keys, pool->n_valid, pool->ld, oil::kLayoutTiled,
+        pool->rs, pool->ws,
+        tokens, trace_ids, prompt_ids, pool->tokens, pool->traces, pool->prompts, (hipStream_t)stream);
+    if (e != hipSuccess)
+        return OIL_E_HIP;
+    pool->n_valid += n;
+    return OIL_OK;
+}
+
+size_t oil_query_workspace_bytes(const oil_pool* pool, int32_t B, int32_t k)
+{
+    if (!pool || B < 1 || B > OIL_MAX_B || k < 1 || k > OIL_MAX_K)
+        return 0;
+    return carve(pool, B, k).total;
+}
+
+int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q_dtype, int32_t B,
+                            int32_t k, const int32_t* exclude_prompt, void* workspace,
+                            size_t workspace_bytes, float* scores, int32_t* idx, void* stream)
+{
+    if (!pool || !queries || !scores || !idx || B < 1 || k < 1 ||
+        (q_dtype != OIL_F32 && q_dtype != OIL_BF16) || !aligned(queries, 16))
+        return OIL_E_INVALID;
+    if (B > OIL_MAX_B || k > OIL_MAX_K)
+        return OIL_E_UNSUPPORTED;
+    if (exclude_prompt && !pool->prompts)
+        return OIL_E_INVALID;
+    const QueryWorkspace w = carve(pool, B, k);
+    if (!workspace || workspace_bytes < w.total || !aligned(workspace, kAlign))
+        return OIL_E_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    uint16_t* qbuf = (uint16_t*)(ws + w.q_off);
+    float* S = (float*)(ws + w.s_off);
+    uint64_t* ca = (uint64_t*)(ws + w.ca_off);
+    uint64_t* cb = (uint64_t*)(ws + w.cb_off);
+    const int64_t n_valid = pool->n_valid;
+
+    const bool mfma = oil::scan_uses_mfma(B, pool->ld);
+    const int tiles = oil::scan_query_tiles(B);
+    hipError_t e = oil::launch_normalize_rows(
+        queries, q_dtype, pool->dim, B, mfma ? (int64_t)tiles * 32 : B, qbuf, 0, pool->ld,
+        mfma ? oil::kLayoutTiled : oil::kLayoutRows, 2048, 2048 * (int64_t)tiles, nullptr, nullptr,
+        nullptr, nullptr, nullptr, nullptr, st);
+    if (e == hipSuccess) {
+        timer_mark(st, 0);
+        e = oil::launch_scan(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, pool->prompts,
+                             exclude_prompt, S, w.s_ld, st);
+        timer_mark(st, 1);
+        if (g_timer.ev && g_timer.used < g_timer.cap)
+            g_timer.used++;
+    }
+    if (e == hipSuccess)
+        e = oil::launch_topk(S, w.s_ld, n_valid, B, k, ca, cb, scores, idx, st);
+    return hip_status(e);
+}
+
+int32_t oil_gather_continuations(const oil_pool* pool, const int32_t* idx, const float* scores,
+                                 int32_t B, int32_t k, const oil_depth_rule* rule, int32_t L,
+                                 int32_t* chain_tokens, int32_t* chain_len, void* stream)
+{
+    if (!pool || !idx || !scores || !rule || !chain_tokens || !chain_len || B < 1 || k < 1 || L < 1)
+        return OIL_E_INVALID;
+    if (k > OIL_MAX_K || L > 64 || rule->n_bands < 0 || rule->n_bands > OIL_MAX_BANDS)
+        return OIL_E_UNSUPPORTED;
+    oil::DepthRule r;
+    r.theta = rule->theta;
+    r.n_bands = rule->n_bands;
+    for (int j = 0; j < OIL_MAX_BANDS; j++) {
+        r.band_min[j] = rule->band_min[j];
+        r.band_depth[j] = rule->band_depth[j];
+    }
+    return hip_status(oil::launch_gather(pool->tokens, pool->traces, pool->n_valid, idx, scores, B, k,
+                                         r, L, chain_tokens, chain_len, (hipStream_t)stream));
+}
+
+int32_t oil_tree_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
+                       const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
+                       const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                       int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
+                       int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, void* stream)
+{
+    if (B < 1 || !anchor || !node_token || !node_parent || !node_source || !n_nodes || n_lex < 0 ||
+        k < 0 || lex_budget < 0 || sem_budget < 0)
+        return OIL_E_INVALID;
+    if (n_lex > 0 && (!lex_tokens || !lex_len || L_lex < 1))
+        return OIL_E_INVALID;
+    if (k > 0 && (!sem_tokens || !sem_len || L < 1))
+        return OIL_E_INVALID;
+    if ((int64_t)lex_budget + sem_budget + 1 > max_nodes)
+        return OIL_E_INVALID;
+    if (max_nodes > OIL_MAX_NODES || L_lex > 64 || L > 64)
+        return OIL_E_UNSUPPORTED;
+    return hip_status(oil::launch_merge(B, anchor, lex_tokens, lex_len, n_lex, L_lex < 1 ? 1 : L_lex,
+                                        lex_budget, sem_tokens, sem_len, k, L < 1 ? 1 : L, sem_budget,
+                                        max_nodes, node_token, node_parent, node_source, n_nodes,
+                                        (hipStream_t)stream));
+}
+
+const char* oil_status_string(int32_t status)
+{
+    switch (status) {
+    case OIL_OK: return "ok";
+    case OIL_E_INVALID: return "invalid argument";
+    case OIL_E_CAPACITY: return "pool capacity exceeded";
+    case OIL_E_UNSUPPORTED: return "unsupported size";
+    case OIL_E_HIP: return "HIP runtime error";
+    case OIL_E_WORKSPACE: return "workspace too small or misaligned";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

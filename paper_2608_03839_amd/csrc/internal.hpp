@@ -1,0 +1,58 @@
+// Launchers shared between the kernel files and the C ABI (internal only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#define OIL_TOPK_MAX 64
+#define OIL_NODES_MAX 256
+#define OIL_BANDS_MAX 4
+
+namespace oil {
+
+struct DepthRule {
+    float theta;
+    int32_t n_bands;
+    float band_min[OIL_BANDS_MAX];
+    int32_t band_depth[OIL_BANDS_MAX];
+};
+
+// Destination layouts of normalised rows (see store.hip).
+enum { kLayoutRows = 0, kLayoutTiled = 1 };
+
+// Key pool geometry: rows in blocks of 32, columns padded to 64.
+constexpr int kRowBlock = 32;
+constexpr int kWindow = 64;
+
+hipError_t launch_normalize_rows(const void* raw, int dtype, int32_t d, int64_t n_rows_in,
+                                 int64_t n_rows_out, uint16_t* out, int64_t row_offset, int32_t ld,
+                                 int layout, int64_t rs, int64_t ws, const int32_t* tok_in,
+                                 const int32_t* trace_in, const int32_t* prompt_in, int32_t* tok_out,
+                                 int32_t* trace_out, int32_t* prompt_out, hipStream_t stream);
+
+int scan_uses_mfma(int32_t B, int32_t ld);
+int scan_query_tiles(int32_t B);
+hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+                       const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
+                       float* S, int64_t s_ld, hipStream_t stream);
+
+int64_t topk_chunks(int64_t n);
+size_t topk_cand_bytes(int32_t B, int32_t k, int64_t capacity);
+hipError_t launch_topk(const float* S, int64_t s_ld, int64_t n_valid, int32_t B, int32_t k,
+                       uint64_t* cand_a, uint64_t* cand_b, float* out_s, int32_t* out_i,
+                       hipStream_t stream);
+
+hipError_t launch_gather(const int32_t* tokens, const int32_t* traces, int64_t n_valid,
+                         const int32_t* idx, const float* scores, int32_t B, int32_t k,
+                         const DepthRule& rule, int32_t L, int32_t* chain_tokens, int32_t* chain_len,
+                         hipStream_t stream);
+
+hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
+                        const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
+                        const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                        int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
+                        int32_t* node_parent, int8_t* node_source, int32_t* n_nodes,
+                        hipStream_t stream);
+
+}  // namespace oil

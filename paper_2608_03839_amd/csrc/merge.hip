@@ -1,0 +1,118 @@
+// Root-first merge of draft chains into one tree per query (Sec. 4 (iii),
+// Eq. 4; BuildLexical then MergeFromRoot in Algorithm 1).
+//
+// One wave per tree.  The tree lives in registers: node slot j belongs to
+// lane j % 64, register j / 64 (up to 256 slots).  Each token of a chain is
+// one wave-wide step: every lane tests its slots for "child of the current
+// node carrying this token" and a ballot names the match (siblings never
+// repeat a token, so there is at most one).  A match is walked for free;
+// otherwise the next slot is bought if the phase's budget remains, else the
+// rest of the chain is dropped.  Lexical drafts go first under their
+// allocation, retrieved chains after them under the fixed reservation.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace oil {
+
+constexpr int kSlotsPerLane = OIL_NODES_MAX / 64;
+
+__device__ __forceinline__ void insert_chain(int32_t (&ntok)[kSlotsPerLane], int32_t (&npar)[kSlotsPerLane],
+                                             int32_t (&nsrc)[kSlotsPerLane], int& count, int& spent,
+                                             int budget, int src, const int32_t* __restrict__ chain,
+                                             int len)
+{
+    const int lane = threadIdx.x;
+    const int32_t mine = lane < len ? chain[lane] : -1;
+    int cur = 0;
+    for (int m = 0; m < len; m++) {
+        const int32_t t = __builtin_amdgcn_readlane(mine, m);
+        int found = -1;
+#pragma unroll
+        for (int q = 0; q < kSlotsPerLane; q++) {
+            const int slot = q * 64 + lane;
+            const bool hit = slot < count && npar[q] == cur && ntok[q] == t;
+            const uint64_t msk = __ballot(hit);
+            if (msk && found < 0)
+                found = q * 64 + __ffsll((unsigned long long)msk) - 1;
+        }
+        if (found >= 0) {
+            cur = found;
+            continue;
+        }
+        if (spent >= budget)
+            return;
+        const int j = count++;
+        spent++;
+#pragma unroll
+        for (int q = 0; q < kSlotsPerLane; q++) {
+            if (q * 64 + lane == j) {
+                ntok[q] = t;
+                npar[q] = cur;
+                nsrc[q] = src;
+            }
+        }
+        cur = j;
+    }
+}
+
+__global__ __launch_bounds__(64) void merge_kernel(
+    const int32_t* __restrict__ anchor, const int32_t* __restrict__ lex_tokens,
+    const int32_t* __restrict__ lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
+    const int32_t* __restrict__ sem_tokens, const int32_t* __restrict__ sem_len, int32_t k, int32_t L,
+    int32_t sem_budget, int32_t max_nodes, int32_t* __restrict__ node_token,
+    int32_t* __restrict__ node_parent, int8_t* __restrict__ node_source, int32_t* __restrict__ n_nodes)
+{
+    const int b = blockIdx.x, lane = threadIdx.x;
+    int32_t ntok[kSlotsPerLane], npar[kSlotsPerLane], nsrc[kSlotsPerLane];
+#pragma unroll
+    for (int q = 0; q < kSlotsPerLane; q++) {
+        ntok[q] = -1;
+        npar[q] = -1;
+        nsrc[q] = -1;
+    }
+    if (lane == 0) {
+        ntok[0] = anchor[b];
+        nsrc[0] = 0;
+    }
+    int count = 1;
+    int spent = 0;
+    for (int c = 0; c < n_lex; c++) {
+        const int64_t o = (int64_t)b * n_lex + c;
+        int len = lex_len[o];
+        len = len < L_lex ? len : L_lex;
+        insert_chain(ntok, npar, nsrc, count, spent, lex_budget, 1, lex_tokens + o * L_lex, len);
+    }
+    spent = 0;
+    for (int c = 0; c < k; c++) {
+        const int64_t o = (int64_t)b * k + c;
+        int len = sem_len[o];
+        len = len < L ? len : L;
+        insert_chain(ntok, npar, nsrc, count, spent, sem_budget, 2, sem_tokens + o * L, len);
+    }
+#pragma unroll
+    for (int q = 0; q < kSlotsPerLane; q++) {
+        const int slot = q * 64 + lane;
+        if (slot < max_nodes) {
+            const int64_t o = (int64_t)b * max_nodes + slot;
+            node_token[o] = ntok[q];
+            node_parent[o] = npar[q];
+            node_source[o] = (int8_t)nsrc[q];
+        }
+    }
+    if (lane == 0)
+        n_nodes[b] = count;
+}
+
+hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
+                        const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
+                        const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                        int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
+                        int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, hipStream_t stream)
+{
+    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(64), 0, stream, anchor, lex_tokens, lex_len, n_lex,
+                       L_lex, lex_budget, sem_tokens, sem_len, k, L, sem_budget, max_nodes, node_token,
+                       node_parent, node_source, n_nodes);
+    return hipGetLastError();
+}
+
+}  // namespace oil

@@ -1,0 +1,286 @@
+// Pool scan: s[b][i] = q_b . k_i for every stored position i < n_valid
+// (Algorithm 1 retrieve step; with unit operands this is cos(h_t, h_i)).
+// bf16 operands, fp32 accumulation.  The key pool is read exactly once per
+// call; scores go to a B x s_ld fp32 workspace for the top-k passes.
+//
+// The pool is stored as 4 KiB tiles (32 rows x 64 columns) in MFMA operand
+// order, window-major (see store.hip): every 16-byte-per-lane load reads
+// 1 KiB contiguous, and while the waves walk their row blocks window by
+// window the chip reads one contiguous region at a time, the access pattern
+// of a plain copy.
+//
+// Two kernels, chosen by the query batch:
+//  * scan_gemv (B <= 4): a matrix-vector product on the vector ALU
+//    (v_dot2 bf16 -> fp32).  Lane l accumulates row l % 32 of the tile over
+//    half of each window's columns; one xor-32 exchange completes the row.
+//    Queries sit in LDS, read as broadcasts.
+//  * scan_mfma (4 < B <= 64): the batch makes the scan a dense contraction;
+//    v_mfma_f32_32x32x16_bf16 multiplies a 32-key tile by a 32-query tile
+//    fragment per instruction, the fragments pre-swizzled by query prep.
+//
+// Both run a software pipeline: a ring of PF + 1 register stages, window
+// w + PF requested before window w is consumed.  Loads are unconditional
+// (window index clamped; the repeats at the end hit in cache) so the compiler
+// counts outstanding loads exactly.
+//
+// Tile (row block rb, window w) starts at element rb * rs + w * ws, so the
+// kernels serve both tile orders (row-block-major and window-major).
+//
+// A key's accumulation order never depends on where the key sits, so
+// identical keys score identically.  Positions whose prompt id equals the
+// query's exclusion id get the "no position" bit pattern.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace oil {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// acc + sum of the 8 products a[e] * b[e] (four v_dot2 bf16 -> fp32 steps, in order).
+__device__ __forceinline__ float dot8_bf16(const bf16x8 a, const bf16x8 b, float acc)
+{
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1),
+                                          __builtin_shufflevector(b, b, 0, 1), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3),
+                                          __builtin_shufflevector(b, b, 2, 3), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 4, 5),
+                                          __builtin_shufflevector(b, b, 4, 5), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 6, 7),
+                                          __builtin_shufflevector(b, b, 6, 7), acc, false);
+    return acc;
+}
+
+__device__ __forceinline__ float masked_score(float s, int64_t row, int32_t ex,
+                                              const int32_t* __restrict__ prompt)
+{
+    if (ex >= 0 && prompt[row] == ex)
+        return __uint_as_float(kNoScoreBits);
+    return s;
+}
+
+// ----------------------------------------------------------------- GEMV (B <= 4)
+template <int NB, int PF>
+__global__ __launch_bounds__(256) void scan_gemv_kernel(
+    const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+    const uint16_t* __restrict__ q, const int32_t* __restrict__ prompt,
+    const int32_t* __restrict__ exclude, float* __restrict__ S, int64_t s_ld)
+{
+    constexpr int NS = PF + 1;
+    extern __shared__ __align__(16) uint16_t q_lds[];  // NB x ld, row-major
+    for (int64_t j = threadIdx.x * 8; j < (int64_t)NB * ld; j += 256 * 8)
+        *(bf16x8*)(q_lds + j) = *(const bf16x8*)(q + j);
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63;
+    const int h = lane >> 5, r = lane & 31;
+    const int64_t rb = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (rb * kRowBlock >= n_valid)
+        return;
+    const int nwin = ld / kWindow;
+    const bf16x8* tile = (const bf16x8*)(keys + rb * rs) + lane;
+    const int64_t ws8 = ws / 8;
+
+    float acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; b++)
+        acc[b] = 0.f;
+    bf16x8 a[NS][4];
+#pragma unroll
+    for (int p = 0; p < PF; p++) {
+        const int w = p < nwin ? p : nwin - 1;
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+            a[p][s] = __builtin_nontemporal_load(tile + w * ws8 + s * 64);
+    }
+    const int nloop = (nwin + NS - 1) / NS * NS;
+    for (int w0 = 0; w0 < nloop; w0 += NS) {
+#pragma unroll
+        for (int u = 0; u < NS; u++) {
+            const int wl = w0 + u + PF < nwin ? w0 + u + PF : nwin - 1;
+#pragma unroll
+            for (int s = 0; s < 4; s++)
+                a[(u + PF) % NS][s] = __builtin_nontemporal_load(tile + wl * ws8 + s * 64);
+            if (w0 + u < nwin) {
+                const int col = (w0 + u) * kWindow + 32 * h;
+#pragma unroll
+                for (int s = 0; s < 4; s++)
+#pragma unroll
+                    for (int b = 0; b < NB; b++)
+                        acc[b] = dot8_bf16(a[u][s], *(const bf16x8*)(q_lds + b * ld + col + 8 * s),
+                                           acc[b]);
+            }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < NB; b++)
+        acc[b] += __shfl_xor(acc[b], 32, kWave);
+    const int64_t row = rb * kRowBlock + r;
+    if (h != 0 || row >= n_valid)
+        return;
+#pragma unroll
+    for (int b = 0; b < NB; b++) {
+        const int32_t ex = exclude ? exclude[b] : -1;
+        S[b * s_ld + row] = masked_score(acc[b], row, ex, prompt);
+    }
+}
+
+// ----------------------------------------------------------------- MFMA (4 < B <= 64)
+template <int MT, int NT>
+__device__ __forceinline__ void load_window(bf16x8 (&a)[MT][4], bf16x8 (&b)[NT][4],
+                                            const bf16x8* const (&tile)[MT], int64_t ws8,
+                                            const bf16x8* __restrict__ qf, int w)
+{
+#pragma unroll
+    for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+            a[mt][s] = __builtin_nontemporal_load(tile[mt] + w * ws8 + s * 64);
+#pragma unroll
+    for (int nt = 0; nt < NT; nt++)
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+            b[nt][s] = qf[(((int64_t)w * NT + nt) * 4 + s) * 64];
+}
+
+template <int MT, int NT, int PF>
+__global__ __launch_bounds__(256) void scan_mfma_kernel(
+    const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+    const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
+    const int32_t* __restrict__ exclude, float* __restrict__ S, int64_t s_ld)
+{
+    constexpr int NS = PF + 1;
+    const int lane = threadIdx.x & 63;
+    const int h = lane >> 5, r = lane & 31;
+    const int64_t rb0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * MT;
+    if (rb0 * kRowBlock >= n_valid)
+        return;
+    const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
+    const int nwin = ld / kWindow;
+    const int64_t ws8 = ws / 8;
+
+    const bf16x8* tile[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; mt++) {
+        const int64_t rb = rb0 + mt < n_rb ? rb0 + mt : n_rb - 1;  // clamp: stays inside the pool
+        tile[mt] = (const bf16x8*)(keys + rb * rs) + lane;
+    }
+    const bf16x8* qf = qfrag + lane;
+
+    floatx16 acc[MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+        for (int nt = 0; nt < NT; nt++)
+            acc[mt][nt] = floatx16{};
+
+    bf16x8 a[NS][MT][4], b[NS][NT][4];
+#pragma unroll
+    for (int p = 0; p < PF; p++)
+        load_window<MT, NT>(a[p], b[p], tile, ws8, qf, p < nwin ? p : nwin - 1);
+    const int nloop = (nwin + NS - 1) / NS * NS;
+    for (int w0 = 0; w0 < nloop; w0 += NS) {
+#pragma unroll
+        for (int u = 0; u < NS; u++) {
+            const int wl = w0 + u + PF < nwin ? w0 + u + PF : nwin - 1;
+            load_window<MT, NT>(a[(u + PF) % NS], b[(u + PF) % NS], tile, ws8, qf, wl);
+            if (w0 + u < nwin) {
+#pragma unroll
+                for (int s = 0; s < 4; s++)
+#pragma unroll
+                    for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+                        for (int nt = 0; nt < NT; nt++)
+                            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                a[u][mt][s], b[u][nt][s], acc[mt][nt], 0, 0, 0);
+            }
+        }
+    }
+
+    // Accumulator layout of a 32x32 MFMA tile: lane l, element 4 i + j holds
+    // row 8 i + 4 (l / 32) + j (a key) and column l % 32 (a query).
+#pragma unroll
+    for (int nt = 0; nt < NT; nt++) {
+        const int qb = nt * 32 + r;
+        if (qb >= B)
+            continue;
+        const int32_t ex = exclude ? exclude[qb] : -1;
+        float* srow = S + (int64_t)qb * s_ld;
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++) {
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int64_t row = (rb0 + mt) * kRowBlock + i * 8 + h * 4;
+                floatx4 v;
+                v[0] = acc[mt][nt][4 * i + 0];
+                v[1] = acc[mt][nt][4 * i + 1];
+                v[2] = acc[mt][nt][4 * i + 2];
+                v[3] = acc[mt][nt][4 * i + 3];
+                if (ex >= 0) {
+#pragma unroll
+                    for (int j = 0; j < 4; j++)
+                        if (row + j < n_valid)
+                            v[j] = masked_score(v[j], row + j, ex, prompt);
+                }
+                if (row + 3 < n_valid) {
+                    *(floatx4*)(srow + row) = v;
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; j++)
+                        if (row + j < n_valid)
+                            srow[row + j] = v[j];
+                }
+            }
+        }
+    }
+}
+
+// ----------------------------------------------------------------- launchers
+// The GEMV keeps all queries of the call in LDS (at most 64 KiB).
+int scan_uses_mfma(int32_t B, int32_t ld) { return B > 4 || (int64_t)B * ld * 2 > 65536; }
+
+int scan_query_tiles(int32_t B) { return (B + 31) / 32; }
+
+template <int NB>
+static void launch_gemv(dim3 g, size_t lds, hipStream_t st, const uint16_t* keys, int32_t ld,
+                        int64_t rs, int64_t ws, int64_t n_valid, const uint16_t* q,
+                        const int32_t* prompt, const int32_t* exclude, float* S, int64_t s_ld)
+{
+    hipLaunchKernelGGL((scan_gemv_kernel<NB, 3>), g, dim3(256), lds, st, keys, ld, rs, ws, n_valid, q,
+                       prompt, exclude, S, s_ld);
+}
+
+hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+                       const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
+                       float* S, int64_t s_ld, hipStream_t stream)
+{
+    if (n_valid <= 0)
+        return hipSuccess;
+    const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
+    if (!scan_uses_mfma(B, ld)) {
+        const dim3 g((unsigned)((n_rb + 3) / 4));
+        const size_t lds = (size_t)B * ld * sizeof(uint16_t);
+        const uint16_t* q = (const uint16_t*)qbuf;
+        switch (B) {
+        case 1: launch_gemv<1>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld); break;
+        case 2: launch_gemv<2>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld); break;
+        case 3: launch_gemv<3>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld); break;
+        default: launch_gemv<4>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld); break;
+        }
+        return hipGetLastError();
+    }
+    const bf16x8* qf = (const bf16x8*)qbuf;
+    if (scan_query_tiles(B) == 1) {
+        constexpr int MT = 4, PF = 1;
+        const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
+        hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF>), g, dim3(256), 0, stream, keys, ld, rs, ws,
+                           n_valid, qf, B, prompt, exclude, S, s_ld);
+    } else {
+        constexpr int MT = 4, PF = 1;
+        const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
+        hipLaunchKernelGGL((scan_mfma_kernel<MT, 2, PF>), g, dim3(256), 0, stream, keys, ld, rs, ws,
+                           n_valid, qf, B, prompt, exclude, S, s_ld);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace oil

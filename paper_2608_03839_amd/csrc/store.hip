@@ -1,0 +1,105 @@
+// Store and query preparation: unit-normalise raw hidden-state rows and
+// round them to bf16 (Sec. 4 (i), Eq. 1: keys are kept L2-normalised in half
+// precision; queries get the same treatment so that the dot product of the
+// two operands is their cosine, Algorithm 1 retrieve step).
+//
+// One 256-thread block per row.  The squared norm is accumulated in double
+// with a fixed reduction tree, so identical raw rows always produce
+// identical stored bits wherever they sit in the pool.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace oil {
+
+__device__ __forceinline__ double load_raw(const void* raw, int dtype, int64_t at)
+{
+    if (dtype == 0)
+        return (double)((const float*)raw)[at];
+    return (double)bf16_bits_to_float(((const uint16_t*)raw)[at]);
+}
+
+// Block-wide sum of one double per thread, fixed order (wave xor-tree, then
+// the four wave totals in wave order).
+__device__ __forceinline__ double block_sum_256(double v, double* red)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        v += __shfl_xor(v, o, kWave);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0)
+        red[wave] = v;
+    __syncthreads();
+    const double t = ((red[0] + red[1]) + red[2]) + red[3];
+    __syncthreads();
+    return t;
+}
+
+// Destination layouts of a normalised row (offsets in bf16 elements; row i,
+// column j; ld = width rounded up to 64):
+//   kLayoutRows: i * ld + j (queries of the GEMV scan).
+//   kLayoutTiled: rows in blocks of 32, columns in windows of 64; each
+//     (row block, window) pair is a 4 KiB tile in MFMA operand order, tile
+//     (i / 32, j / 64) starting at (i / 32) * rs + (j / 64) * ws:
+//       (i / 32) * rs + (j / 64) * ws + (s * 64 + lane) * 8 + e,
+//     s = (j % 32) / 8, e = j % 8, lane = i % 32 + 32 * ((j % 64) / 32).
+//     One 16-byte load per lane of a tile sub-step s reads 1 KiB contiguous.
+//     The key pool uses it, and so do the MFMA scan's query fragments
+//     (rs = 2048, ws = 2048 * query tiles).
+__device__ __forceinline__ int64_t layout_offset(int layout, int64_t i, int32_t j, int32_t ld,
+                                                 int64_t rs, int64_t ws)
+{
+    if (layout == kLayoutRows)
+        return i * (int64_t)ld + j;
+    const int s = (j >> 3) & 3, e = j & 7;
+    const int lane = (int)(i & 31) + 32 * ((j >> 5) & 1);
+    return (i >> 5) * rs + (int64_t)(j >> 6) * ws + (s * 64 + lane) * 8 + e;
+}
+
+__global__ __launch_bounds__(256) void normalize_rows_kernel(
+    const void* __restrict__ raw, int dtype, int32_t d, int64_t n_rows_in, uint16_t* __restrict__ out,
+    int64_t row_offset, int32_t ld, int layout, int64_t rs, int64_t ws, const int32_t* __restrict__ tok_in,
+    const int32_t* __restrict__ trace_in, const int32_t* __restrict__ prompt_in,
+    int32_t* __restrict__ tok_out, int32_t* __restrict__ trace_out, int32_t* __restrict__ prompt_out)
+{
+    __shared__ double red[4];
+    const int64_t r = blockIdx.x;  // row within this call
+    const bool live = r < n_rows_in;
+    double ss = 0.0;
+    if (live) {
+        for (int32_t j = threadIdx.x; j < d; j += 256) {
+            const double v = load_raw(raw, dtype, r * (int64_t)d + j);
+            ss += v * v;
+        }
+    }
+    const double norm = sqrt(block_sum_256(ss, red));
+    const int64_t dst_row = row_offset + r;
+    for (int32_t j = threadIdx.x; j < ld; j += 256) {
+        uint16_t b = 0;
+        if (live && j < d && norm > 0.0)
+            b = double_to_bf16_rne(load_raw(raw, dtype, r * (int64_t)d + j) / norm);
+        const int64_t at = layout_offset(layout, dst_row, j, ld, rs, ws);
+        out[at] = b;
+    }
+    if (threadIdx.x == 0 && live && tok_out) {
+        tok_out[dst_row] = tok_in[r];
+        trace_out[dst_row] = trace_in[r];
+        if (prompt_out)
+            prompt_out[dst_row] = prompt_in[r];
+    }
+}
+
+hipError_t launch_normalize_rows(const void* raw, int dtype, int32_t d, int64_t n_rows_in,
+                                 int64_t n_rows_out, uint16_t* out, int64_t row_offset, int32_t ld,
+                                 int layout, int64_t rs, int64_t ws, const int32_t* tok_in,
+                                 const int32_t* trace_in, const int32_t* prompt_in, int32_t* tok_out,
+                                 int32_t* trace_out, int32_t* prompt_out, hipStream_t stream)
+{
+    if (n_rows_out <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(normalize_rows_kernel, dim3((unsigned)n_rows_out), dim3(256), 0, stream, raw,
+                       dtype, d, n_rows_in, out, row_offset, ld, layout, rs, ws, tok_in, trace_in,
+                       prompt_in, tok_out, trace_out, prompt_out);
+    return hipGetLastError();
+}
+
+}  // namespace oil

@@ -1,0 +1,95 @@
+"""Comparison rules between the HIP path and the CPU oracle.
+
+Scores: |s_gpu - s_oracle| <= TOL (fp32 accumulation against the exact dot of
+unit bf16 operands; cosines are O(1), so the relative tolerance of 2e-3 is an
+absolute one).
+
+Top-k index sets (o = oracle scores of every eligible position, o_k the k-th
+best, o_k1 the (k+1)-th):
+  T1  every position with o > o_k + TOL is returned;
+  T2  every returned position has o >= o_k - TOL;
+  T3  if o_k - o_k1 >= TOL the sets are equal; if moreover every adjacent gap
+      inside the oracle's top-k is >= TOL the order is equal too.
+Padding (-1) appears exactly when fewer than k positions are eligible.
+Gather and merge are integer procedures: bit-exact on identical inputs.
+"""
+import numpy as np
+
+import oracle
+
+TOL = 2e-3
+
+
+def untile_keys(buf_bits, n, dim, capacity):
+    """Rows [0, n) of a tiled key buffer (numpy uint16), as an (n, dim) array.
+
+    Layout: 4 KiB tiles of 32 rows x 64 columns ordered (sub-step s,
+    lane = row % 32 + 32 * half, element e), stored window-major: tile
+    (row block rb, window w) at (w * R + rb) * 2048, R = ceil(capacity / 32)."""
+    ld = (dim + 63) // 64 * 64
+    R = (capacity + 31) // 32
+    t = np.asarray(buf_bits)[: R * 32 * ld].reshape(ld // 64, R, 4, 2, 32, 8)
+    rows = t.transpose(1, 4, 0, 3, 2, 5).reshape(R * 32, ld)
+    return np.ascontiguousarray(rows[:n, :dim])
+
+
+def oracle_rows(keys_bits, raw_q, prompt=None, exclude=None):
+    """Oracle scores of every position (excluded -> -inf) for each raw query."""
+    q = oracle.normalize_rows(raw_q)
+    s = oracle.scores(keys_bits, q)
+    if prompt is not None and exclude is not None:
+        for b, e in enumerate(exclude):
+            if e >= 0:
+                s[b, prompt == e] = -np.inf
+    return s
+
+
+def check_topk(gpu_s, gpu_i, orc_full, k, tol=TOL):
+    """Apply T1-T3 and the score tolerance; returns per-query flags
+    (unambiguous set, unambiguous order)."""
+    B = gpu_i.shape[0]
+    flags = []
+    for b in range(B):
+        o = orc_full[b]
+        elig = np.flatnonzero(np.isfinite(o))
+        order = elig[np.lexsort((elig, -o[elig]))]
+        n_el = len(order)
+        gi = gpu_i[b]
+        gs = gpu_s[b]
+        valid = gi >= 0
+        nv = int(valid.sum())
+        assert nv == min(k, n_el), f"query {b}: {nv} returned, {min(k, n_el)} eligible"
+        assert np.all(valid[:nv]) and not np.any(valid[nv:]), f"query {b}: padding not at the end"
+        assert np.all(np.isneginf(gs[nv:]))
+        got = gi[:nv].astype(np.int64)
+        assert len(set(got.tolist())) == nv, f"query {b}: duplicate positions"
+        assert np.all(np.isfinite(o[got])), f"query {b}: returned an excluded position"
+        # scores: tolerance against the oracle, descending, ties by position
+        assert np.all(np.abs(gs[:nv] - o[got]) <= tol), \
+            f"query {b}: score error {np.max(np.abs(gs[:nv] - o[got]))}"
+        assert np.all(np.diff(gs[:nv]) <= 0), f"query {b}: scores not descending"
+        eq = np.flatnonzero(np.diff(gs[:nv]) == 0)
+        assert np.all(got[eq] < got[eq + 1]), f"query {b}: equal scores not in position order"
+        if nv == 0:
+            flags.append((True, True))
+            continue
+        ok_ = o[order[nv - 1]]
+        ok1 = o[order[nv]] if n_el > nv else -np.inf
+        top = order[:nv]
+        must = order[o[order] > ok_ + tol]
+        assert set(must.tolist()) <= set(got.tolist()), f"query {b}: T1 violated"
+        assert np.all(o[got] >= ok_ - tol), f"query {b}: T2 violated"
+        set_unamb = (ok_ - ok1) >= tol
+        order_unamb = set_unamb and bool(np.all(-np.diff(o[top]) >= tol))
+        if set_unamb:
+            assert set(got.tolist()) == set(top.tolist()), f"query {b}: T3 set violated"
+        if order_unamb:
+            assert got.tolist() == top.tolist(), f"query {b}: T3 order violated"
+        flags.append((set_unamb, order_unamb))
+    return flags
+
+
+def away_from_edges(scores32, edges, tol=TOL):
+    """True when no finite score lies within tol of a threshold (theta, band edges)."""
+    s = scores32[np.isfinite(scores32)]
+    return all(np.all(np.abs(s - e) >= tol) for e in edges if np.isfinite(e))

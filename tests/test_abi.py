@@ -1,0 +1,110 @@
+"""C ABI contract checks that need no GPU: the library loads, exports every
+entry point include/oilbird.h declares, and rejects bad arguments on the host
+before enqueuing anything (these calls never reach a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "oilbird.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(oil_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2608_03839_amd as oil
+    return oil.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared()
+    assert len(names) >= 11
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_stride_and_sizes(L):
+    assert L.oil_key_stride(1) == 64
+    assert L.oil_key_stride(64) == 64
+    assert L.oil_key_stride(100) == 128
+    assert L.oil_key_stride(4096) == 4096
+    assert L.oil_key_stride(0) == 0
+    assert L.oil_pool_key_bytes(4096, 10) == 4096 * 10 * 2
+    assert L.oil_pool_key_bytes(0, 10) == 0
+
+
+class _FakeBufs:
+    """Host memory standing in for device pointers: the calls below only
+    validate and record them, never dereference them."""
+
+    def __init__(self, n=4096):
+        self.raw = ctypes.create_string_buffer(n + 512)
+        base = ctypes.addressof(self.raw)
+        self.aligned = ctypes.c_void_p((base + 255) // 256 * 256)
+        self.misaligned = ctypes.c_void_p((base + 255) // 256 * 256 + 8)
+
+
+def test_create_validates(L):
+    import paper_2608_03839_amd as oil
+    f = _FakeBufs()
+    h = ctypes.c_void_p()
+    P = f.aligned
+    assert L.oil_pool_create(0, 10, P, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_pool_create(16, 0, P, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_pool_create(16, 10, None, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_pool_create(16, 10, f.misaligned, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_pool_create(16, 2**31, P, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_pool_create(16, 10, P, P, P, None, ctypes.byref(h)) == 0
+    n = ctypes.c_int64(-5)
+    assert L.oil_pool_size(h, ctypes.byref(n)) == 0 and n.value == 0
+    # capacity: appending 11 rows into 10 is refused before any launch
+    assert L.oil_pool_append(h, P, 0, P, P, None, 11, None) == -2
+    # prompt ids given to a pool without a prompt buffer
+    assert L.oil_pool_append(h, P, 0, P, P, P, 1, None) == -1
+    assert L.oil_pool_append(h, P, 7, P, P, None, 1, None) == -1     # bad dtype
+    assert L.oil_pool_append(h, f.misaligned, 0, P, P, None, 1, None) == -1
+    assert L.oil_pool_append(h, P, 0, P, P, None, 0, None) == 0      # n = 0 is a no-op
+    assert L.oil_pool_size(h, ctypes.byref(n)) == 0 and n.value == 0
+    # query: sizes and workspace
+    assert L.oil_query_workspace_bytes(h, 0, 8) == 0
+    assert L.oil_query_workspace_bytes(h, 1, 65) == 0
+    assert L.oil_query_workspace_bytes(h, 65, 8) == 0
+    ws = L.oil_query_workspace_bytes(h, 4, 8)
+    assert ws > 0 and ws % 256 == 0
+    assert L.oil_pool_query_topk(h, P, 0, 4, 65, None, P, ws, P, P, None) == -3
+    assert L.oil_pool_query_topk(h, P, 0, 65, 8, None, P, ws, P, P, None) == -3
+    assert L.oil_pool_query_topk(h, P, 0, 0, 8, None, P, ws, P, P, None) == -1
+    assert L.oil_pool_query_topk(h, P, 0, 4, 8, None, P, ws - 1, P, P, None) == -5
+    assert L.oil_pool_query_topk(h, P, 0, 4, 8, None, f.misaligned, ws, P, P, None) == -5
+    assert L.oil_pool_query_topk(h, P, 0, 4, 8, P, P, ws, P, P, None) == -1  # no prompt buffer
+    rule = oil.DepthRule.paper()
+    assert L.oil_gather_continuations(h, P, P, 1, 8, ctypes.byref(rule), 0, P, P, None) == -1
+    assert L.oil_gather_continuations(h, P, P, 1, 65, ctypes.byref(rule), 8, P, P, None) == -3
+    bad = oil.DepthRule.paper()
+    bad.n_bands = 5
+    assert L.oil_gather_continuations(h, P, P, 1, 8, ctypes.byref(bad), 8, P, P, None) == -3
+    assert L.oil_pool_destroy(h) == 0
+    assert L.oil_pool_destroy(None) == -1
+
+
+def test_merge_validates(L):
+    f = _FakeBufs()
+    P = f.aligned
+    # budgets that do not fit max_nodes
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, 10, 10, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, -1, P, P, 4, 4, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 1, 4, 4, P, P, 4, 4, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, 300, 301, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(0, P, None, None, 0, 1, 0, P, P, 4, 4, 10, 64, P, P, P, P, None) == -1
+
+
+def test_status_strings(L):
+    for s in (0, -1, -2, -3, -4, -5, 99):
+        assert isinstance(L.oil_status_string(s), bytes)

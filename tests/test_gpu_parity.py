@@ -1,0 +1,390 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Every input is seeded and synthetic (workloads/), handed identically to both
+sides.  Rules (tests/_parity.py): scores within 2e-3 of the oracle's exact
+dot; top-k sets/orders by T1-T3; stored keys, gathered chains and merged trees
+bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests._parity import TOL, away_from_edges, check_topk, oracle_rows, untile_keys
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def oil():
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_2608_03839_amd as m
+    m.lib()
+    return m
+
+
+def _bits(t):
+    """bf16 tensor -> numpy uint16 bit patterns."""
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def _raw_np(t):
+    t = t.detach().cpu()
+    return _bits(t) if t.dtype == torch.bfloat16 else t.float().numpy()
+
+
+def _fill(oil, wp, n=None, with_prompts=True, capacity=None, chunk=65536):
+    """A GPU pool holding rows [0, n) of synthetic pool `wp`; returns (pool, raw rows)."""
+    n = wp.spec.n if n is None else n
+    pool = oil.Pool(wp.spec.d, capacity or n, with_prompts=with_prompts)
+    raws = []
+    for s in range(0, n, chunk):
+        m = min(chunk, n - s)
+        raw = wp.raw_rows(s, m)
+        raws.append(raw.cpu())
+        pool.append(raw.cuda(), wp.tokens[s:s + m].cuda(), wp.traces[s:s + m].cuda(),
+                    wp.prompts[s:s + m].cuda() if with_prompts else None)
+    return pool, torch.cat(raws) if raws else torch.empty(0)
+
+
+def _stored(pool, n):
+    return untile_keys(_bits(pool.keys), n, pool.dim, pool.capacity)
+
+
+# ---------------------------------------------------------------- store (Eq. 1)
+@pytest.mark.parametrize("d,dtype", [(512, "f32"), (100, "f32"), (4096, "bf16"), (1, "f32")])
+def test_store_matches_oracle(oil, d, dtype):
+    n = 777
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=1000, seed=11, key_dtype=dtype))
+    raw = wp.raw_rows(0, n)
+    raw[5] = 0                                          # a zero row is stored as zeros
+    pool = oil.Pool(d, n)
+    pool.append(raw.cuda(), wp.tokens.cuda(), wp.traces.cuda(), wp.prompts.cuda())
+    torch.cuda.synchronize()
+    got = _stored(pool, n)
+    ref = oracle.normalize_rows(_raw_np(raw))
+    diff = np.abs(got.astype(np.int32) - ref.astype(np.int32))
+    assert diff.max() <= 1 and (diff > 0).mean() <= 1e-6
+    assert np.all(got[5] == 0)
+    if pool.stride > d:                                 # padding columns stay zero
+        padded = untile_keys(_bits(pool.keys), n, pool.stride, pool.capacity)
+        assert np.all(padded[:, d:] == 0)
+    assert torch.equal(pool.tokens[:n].cpu(), wp.tokens)
+    assert torch.equal(pool.traces[:n].cpu(), wp.traces)
+    assert torch.equal(pool.prompts[:n].cpu(), wp.prompts)
+
+
+# ---------------------------------------------------------------- retrieval (Eq. 2)
+def _query_case(oil, n, d, B, k, seed, dtype="f32", p_random=0.25, clusters=0):
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=5000, seed=seed, n_clusters=clusters,
+                                           key_dtype=dtype))
+    pool, raw = _fill(oil, wp)
+    q, src = workloads.queries(wp, workloads.QuerySpec(B=B, p_random=p_random, seed=seed + 1))
+    s, i = pool.query_topk(q.cuda(), k)
+    torch.cuda.synchronize()
+    keys = _stored(pool, n)
+    o = oracle_rows(keys, _raw_np(q))
+    flags = check_topk(s.cpu().numpy(), i.cpu().numpy(), o, k)
+    if clusters == 0 and n > k:
+        # a noisy copy of a stored key (cos ~ 0.999) has that key as its unique best
+        top1 = i[:, 0].cpu().numpy()
+        for b in range(B):
+            if src[b] >= 0:
+                assert top1[b] == src[b]
+    return wp, pool, q, s, i, flags
+
+
+@pytest.mark.parametrize("B", [1, 2, 3, 4, 5, 16, 32, 33, 64])
+def test_topk_over_query_batches(oil, B):
+    """GEMV (B <= 4) and MFMA (one and two 32-query tiles), ragged pool of 5000."""
+    _query_case(oil, 5000, 512, B, 16, seed=20 + B)
+
+
+@pytest.mark.parametrize("k", [1, 7, 32, 64])
+@pytest.mark.parametrize("n", [1, 63, 4096, 4097, 12345])
+def test_topk_k_and_ragged_pools(oil, k, n):
+    _query_case(oil, n, 128, 6, k, seed=n + k)
+    _query_case(oil, n, 128, 2, k, seed=n + k + 1)
+
+
+@pytest.mark.parametrize("d", [64, 100, 1000, 5120])
+def test_topk_widths(oil, d):
+    _query_case(oil, 3000, d, 8, 16, seed=d, dtype="bf16", clusters=16)
+    _query_case(oil, 3000, d, 1, 16, seed=d + 1, dtype="bf16", clusters=16)
+
+
+def test_topk_many_merge_levels(oil):
+    """A pool of 600k rows at k = 64 needs two merge passes of candidate lists."""
+    _query_case(oil, 600_000, 64, 3, 64, seed=5)
+    _query_case(oil, 600_000, 64, 40, 64, seed=6)
+
+
+def test_empty_pool_returns_padding(oil):
+    pool = oil.Pool(64, 100)
+    for B in (1, 9):
+        s, i = pool.query_topk(torch.randn(B, 64, device="cuda"), 8)
+        torch.cuda.synchronize()
+        assert torch.all(i == -1) and torch.all(torch.isneginf(s))
+
+
+@pytest.mark.parametrize("B", [1, 8, 40])
+def test_planted_duplicates_rank_first(oil, B):
+    """A query equal to a stored key scores ||k||^2 and ranks first; its exact
+    copies follow in position order with bit-identical scores, wherever they
+    sit inside a tile (Cauchy-Schwarz; total order of Eq. 2 ties)."""
+    n, d = 9000, 256
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=100, seed=77, key_dtype="f32"))
+    raw = wp.raw_rows(0, n)
+    rng = np.random.default_rng(0)
+    srcs = rng.choice(n, B, replace=False)
+    for b, p in enumerate(srcs):
+        for c in rng.choice(n, 2, replace=False):     # two extra copies at random positions
+            raw[c] = raw[p]
+    pool = oil.Pool(d, n)
+    pool.append(raw.cuda(), wp.tokens.cuda(), wp.traces.cuda(), wp.prompts.cuda())
+    q = raw[srcs].clone()
+    s, i = pool.query_topk(q.cuda(), 5)
+    torch.cuda.synchronize()
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    raw_np = raw.numpy()
+    for b in range(B):
+        copies = np.flatnonzero((raw_np == raw_np[srcs[b]]).all(1))
+        m = min(len(copies), 5)
+        assert len(copies) >= 3
+        assert i[b, :m].tolist() == sorted(copies.tolist())[:m]
+        assert np.all(s[b, :m] == s[b, 0])
+        assert abs(s[b, 0] - 1.0) <= 2.0 ** -8 + 1e-6
+        assert m == 5 or s[b, m] < s[b, 0]
+
+
+def test_self_exclusion(oil):
+    n, d, B = 4800, 256, 6
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=50, seed=3, n_clusters=4,
+                                           key_dtype="bf16"))
+    pool, raw = _fill(oil, wp)
+    q, src = workloads.queries(wp, workloads.QuerySpec(B=B, p_random=0.0, seed=9))
+    ex = wp.prompts[src.long()].clone()
+    ex[1] = -1                                        # this query excludes nothing
+    for Bq in (B, 3):                                 # MFMA and GEMV paths
+        s, i = pool.query_topk(q[:Bq].cuda(), 32, exclude_prompt=ex[:Bq].cuda())
+        torch.cuda.synchronize()
+        o = oracle_rows(_stored(pool, n), _raw_np(q[:Bq]), wp.prompts.numpy(), ex[:Bq].numpy())
+        check_topk(s.cpu().numpy(), i.cpu().numpy(), o, 32)
+        got = i.cpu().numpy()
+        for b in range(Bq):
+            if ex[b] >= 0:
+                assert not np.any(wp.prompts.numpy()[got[b][got[b] >= 0]] == ex[b].item())
+
+
+def test_exclusion_can_empty_the_pool(oil):
+    pool = oil.Pool(64, 10)
+    raw = torch.randn(10, 64)
+    pool.append(raw.cuda(), torch.arange(10, dtype=torch.int32).cuda(),
+                torch.zeros(10, dtype=torch.int32).cuda(), torch.full((10,), 4, dtype=torch.int32).cuda())
+    s, i = pool.query_topk(raw[:2].cuda(), 3, exclude_prompt=torch.tensor([4, 5], dtype=torch.int32).cuda())
+    torch.cuda.synchronize()
+    assert torch.all(i[0] == -1)
+    assert sorted(i[1].tolist()) == sorted(set(i[1].tolist())) and torch.all(i[1] >= 0)
+
+
+def test_repeat_is_bit_identical(oil):
+    wp, pool, q, s, i, _ = _query_case(oil, 20000, 512, 12, 32, seed=4, clusters=8, dtype="bf16")
+    s2, i2 = pool.query_topk(q.cuda(), 32)
+    torch.cuda.synchronize()
+    assert torch.equal(s, s2) and torch.equal(i, i2)
+
+
+# ---------------------------------------------------------------- gather (Eq. 3)
+def _rule_pair(oil, kind, L, theta=0.8):
+    if kind == "paper":
+        return oil.DepthRule.paper(theta), oracle.paper_rule(theta)
+    return oil.DepthRule.fixed(L, theta), oracle.fixed_rule(L, theta)
+
+
+@pytest.mark.parametrize("kind,L", [("paper", 8), ("paper", 64), ("fixed", 16), ("fixed", 1)])
+def test_gather_bit_exact(oil, kind, L):
+    n = 3000
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=64, vocab=999, seed=8, key_dtype="f32"))
+    pool, _ = _fill(oil, wp)
+    rng = np.random.default_rng(1)
+    B, k = 40, 16
+    idx = rng.integers(-1, n, (B, k)).astype(np.int32)
+    idx[:, 0] = rng.integers(n - 5, n, B)              # hits near the end of the pool
+    sc = rng.choice(np.float32([0.95, 0.9, np.nextafter(np.float32(0.9), 0), 0.85, 0.82,
+                                0.81, 0.8, 0.5, -0.2]), (B, k)).astype(np.float32)
+    r_gpu, r_orc = _rule_pair(oil, kind, L)
+    ct, cl = pool.gather(torch.from_numpy(idx).cuda(), torch.from_numpy(sc).cuda(), r_gpu, L)
+    torch.cuda.synchronize()
+    ect, ecl = oracle.gather(wp.tokens.numpy(), wp.traces.numpy(), n, idx, sc, r_orc, L)
+    assert np.array_equal(cl.cpu().numpy(), ecl)
+    assert np.array_equal(ct.cpu().numpy(), ect)
+
+
+# ---------------------------------------------------------------- merge (Eq. 4)
+def _chains(rng, B, c, L, vocab):
+    base = rng.integers(0, vocab, (B, 1, L))
+    t = np.where(rng.random((B, c, L)) < 0.7, base, rng.integers(0, vocab, (B, c, L)))
+    ln = rng.integers(0, L + 1, (B, c))
+    t = np.where(np.arange(L)[None, None, :] < ln[..., None], t, -1)
+    return t.astype(np.int32), ln.astype(np.int32)
+
+
+@pytest.mark.parametrize("n_lex,lb,sb,mx", [(0, 0, 32, 33), (4, 48, 16, 65), (3, 10, 200, 256),
+                                            (4, 0, 0, 1), (2, 100, 100, 230)])
+def test_merge_bit_exact(oil, n_lex, lb, sb, mx):
+    rng = np.random.default_rng(lb * 7 + sb)
+    B, k, L, L_lex = 70, 32, 12, 12
+    lt, ll = _chains(rng, B, n_lex, L_lex, 5)
+    st, sl = _chains(rng, B, k, L, 5)
+    anchor = rng.integers(0, 1000, B).astype(np.int32)
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    nt, npar, ns, nn = oil.merge_trees(cu(anchor), cu(lt) if n_lex else None,
+                                       cu(ll) if n_lex else None, lb, cu(st), cu(sl), sb, mx)
+    torch.cuda.synchronize()
+    ent, enp, ens, enn = oracle.tree_merge(anchor, lt if n_lex else np.zeros((B, 0, 1), np.int32),
+                                           ll if n_lex else np.zeros((B, 0), np.int32), lb, st, sl,
+                                           sb, mx)
+    assert np.array_equal(nn.cpu().numpy(), enn)
+    assert np.array_equal(nt.cpu().numpy(), ent)
+    assert np.array_equal(npar.cpu().numpy(), enp)
+    assert np.array_equal(ns.cpu().numpy(), ens)
+
+
+def test_merge_golden(oil):
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "merge_eq4.json")))
+    for c in g["cases"]:
+        lex = c["lex"]
+        n_lex = len(lex)
+        L_lex = max([len(x) for x in lex] + [1])
+        lt = np.full((1, max(n_lex, 1), L_lex), -1, np.int32)
+        ll = np.zeros((1, max(n_lex, 1)), np.int32)
+        for j, x in enumerate(lex):
+            lt[0, j, :len(x)] = x
+            ll[0, j] = len(x)
+        L = max(len(x) for x in c["sem"])
+        st = np.full((1, len(c["sem"]), L), -1, np.int32)
+        sl = np.zeros((1, len(c["sem"])), np.int32)
+        for j, x in enumerate(c["sem"]):
+            st[0, j, :len(x)] = x
+            sl[0, j] = len(x)
+        cu = lambda a: torch.from_numpy(a).cuda()
+        nt, npar, ns, nn = oil.merge_trees(cu(np.array([c["anchor"]], np.int32)),
+                                           cu(lt) if n_lex else None, cu(ll) if n_lex else None,
+                                           c["lex_budget"], cu(st), cu(sl), c["sem_budget"],
+                                           c["max_nodes"])
+        torch.cuda.synchronize()
+        n = c["n_nodes"]
+        assert nn.item() == n, c["why"]
+        assert nt[0, :n].tolist() == c["node_token"]
+        assert npar[0, :n].tolist() == c["node_parent"]
+        assert ns[0, :n].tolist() == c["node_source"]
+
+
+# ---------------------------------------------------------------- end to end
+def _end_to_end(oil, cfg, n=None, device_gen="cpu"):
+    ps, qs = cfg["pool"], cfg["query"]
+    wp = workloads.Pool(ps, device=device_gen)
+    n = ps.n if n is None else n
+    pool, raw = _fill(oil, wp, n)
+    q, src = workloads.queries(wp, qs, n_valid=n)
+    k, L = cfg["k"], cfg["L"]
+    rule_g, rule_o = _rule_pair(oil, "fixed", L)
+    s, i = pool.query_topk(q.cuda(), k)
+    ct, cl = pool.gather(i, s, rule_g, L)
+    anchor = workloads.anchors(wp, src)
+    mx = 1 + cfg["lex_budget"] + cfg["sem_budget"]
+    tree = oil.merge_trees(anchor.cuda(), None, None, 0, ct, cl, cfg["sem_budget"], mx)
+    torch.cuda.synchronize()
+    keys = _stored(pool, n)
+    o = oracle_rows(keys, _raw_np(q))
+    gs, gi = s.cpu().numpy(), i.cpu().numpy()
+    flags = check_topk(gs, gi, o, k)
+    # oracle's own top-k, gather and merge
+    os_, oi = oracle.topk(o, k)
+    os32 = os_.astype(np.float32)
+    ect, ecl = oracle.gather(wp.tokens.numpy()[:n], wp.traces.numpy()[:n], n, oi, os32, rule_o, L)
+    etree = oracle.tree_merge(anchor.numpy(), np.zeros((qs.B, 0, 1), np.int32),
+                              np.zeros((qs.B, 0), np.int32), 0, ect, ecl, cfg["sem_budget"], mx)
+    # (1) the GPU gather and merge on the oracle's top-k are bit-exact
+    ct2, cl2 = pool.gather(torch.from_numpy(oi).cuda(), torch.from_numpy(os32).cuda(), rule_g, L)
+    tree2 = oil.merge_trees(anchor.cuda(), None, None, 0, ct2, cl2, cfg["sem_budget"], mx)
+    torch.cuda.synchronize()
+    assert np.array_equal(cl2.cpu().numpy(), ecl) and np.array_equal(ct2.cpu().numpy(), ect)
+    for a, e in zip(tree2, etree):
+        assert np.array_equal(a.cpu().numpy(), e)
+    # (2) end to end wherever the retrieval is unambiguous and away from theta:
+    #     the same chains when the top-k set is unambiguous, the same arrays
+    #     (chain order, tree) when the order is too
+    n_checked = 0
+    gcl, gct = cl.cpu().numpy(), ct.cpu().numpy()
+    for b in range(qs.B):
+        if flags[b][0] and away_from_edges(os32[b], [rule_o["theta"]]):
+            got = sorted(tuple(gct[b, r, :gcl[b, r]]) for r in range(k))
+            want = sorted(tuple(ect[b, r, :ecl[b, r]]) for r in range(k))
+            assert got == want
+        if flags[b][1] and away_from_edges(os32[b], [rule_o["theta"]]):
+            n_checked += 1
+            assert np.array_equal(cl.cpu().numpy()[b], ecl[b])
+            assert np.array_equal(ct.cpu().numpy()[b], ect[b])
+            for a, e in zip(tree, etree):
+                assert np.array_equal(a.cpu().numpy()[b], e[b])
+    return flags, n_checked, ecl
+
+
+def test_tiny_end_to_end(oil):
+    # the query fires and its true neighbour copies a full span; ranks 8 and 9
+    # of this iid pool sit 3e-5 apart, so the set itself is compared by T1-T3 only
+    flags, n_checked, ecl = _end_to_end(oil, workloads.TINY)
+    assert ecl[0, 0] == 8
+
+
+def test_tiny_paper_rule(oil):
+    """The paper's depth bands on the tiny pool: only the true neighbour (s ~ 0.999) copies."""
+    cfg = workloads.TINY
+    wp = workloads.Pool(cfg["pool"])
+    pool, raw = _fill(oil, wp)
+    q, src = workloads.queries(wp, workloads.QuerySpec(B=4, seed=5))
+    s, i = pool.query_topk(q.cuda(), 8)
+    ct, cl = pool.gather(i, s, oil.DepthRule.paper(), 64)
+    torch.cuda.synchronize()
+    ect, ecl = oracle.gather(wp.tokens.numpy(), wp.traces.numpy(), wp.spec.n, i.cpu().numpy(),
+                             s.cpu().numpy(), oracle.paper_rule(), 64)
+    assert np.array_equal(cl.cpu().numpy(), ecl) and np.array_equal(ct.cpu().numpy(), ect)
+    assert np.all(ecl[:, 1:] == 0)
+
+
+def test_decode_64k_end_to_end(oil):
+    """One single-stream decode step: N = 65,536, d = 4,096 bf16, k = 16, L = 16."""
+    flags, n_checked, _ = _end_to_end(oil, workloads.DECODE_64K)
+    assert len(flags) == 1
+
+
+def test_streaming_appends(oil):
+    """Ragged appends of 1-8 rows interleaved with queries; every query sees
+    exactly the rows appended before it on the stream."""
+    ps = workloads.PoolSpec(n=3000, d=320, vocab=3000, seed=12, n_clusters=8)
+    wp = workloads.Pool(ps)
+    pool = oil.Pool(ps.d, ps.n)
+    raw = wp.raw_rows(0, ps.n)
+    sizes = workloads.append_sizes(3, 400)
+    at = 0
+    pool.append(raw[:2000].cuda(), wp.tokens[:2000].cuda(), wp.traces[:2000].cuda(),
+                wp.prompts[:2000].cuda())
+    at = 2000
+    for step, m in enumerate(sizes.tolist()):
+        m = min(m, ps.n - at)
+        if m == 0:
+            break
+        pool.append(raw[at:at + m].cuda(), wp.tokens[at:at + m].cuda(), wp.traces[at:at + m].cuda(),
+                    wp.prompts[at:at + m].cuda())
+        at += m
+        if step % 40 == 0:
+            q, _ = workloads.queries(wp, workloads.QuerySpec(B=5, seed=step), n_valid=at)
+            s, i = pool.query_topk(q.cuda(), 16)
+            torch.cuda.synchronize()
+            assert len(pool) == at
+            o = oracle_rows(_stored(pool, at), _raw_np(q))
+            check_topk(s.cpu().numpy(), i.cpu().numpy(), o, 16)
