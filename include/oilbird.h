@@ -167,8 +167,9 @@ int32_t oil_gather_continuations(const oil_pool *pool, const int32_t *idx, const
  * Inserting a chain walks from the root: a child carrying the next token is
  * walked for free, otherwise a node is bought while the phase's budget lasts,
  * else the rest of that chain is dropped.
- *   lex_tokens B x n_lex x L_lex int32, lex_len B x n_lex (n_lex may be 0,
- *              then both may be NULL).   sem_tokens B x k x L, sem_len B x k.
+ *   lex_tokens B x n_lex x L_lex int32, lex_len B x n_lex (n_lex 0 .. 64;
+ *              with 0 both may be NULL).   sem_tokens B x k x L, sem_len B x k
+ *              (k 0 .. 64).   L_lex, L 1 .. 64 (ignored when their count is 0).
  *   max_nodes  1 + lex_budget + sem_budget .. OIL_MAX_NODES.
  *   node_token, node_parent  B x max_nodes int32; node_source B x max_nodes
  *              int8 (0 root, 1 lexical, 2 retrieved); nodes in creation

@@ -32,8 +32,8 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 int32_t hip_status(hipError_t e) { return e == hipSuccess ? OIL_OK : OIL_E_HIP; }
 
 struct QueryWorkspace {
-    size_t q_off, s_off, ca_off, cb_off, total;
-    int64_t s_ld;
+    size_t q_off, s_off, g_off, ca_off, cb_off, total;
+    int64_t s_ld, g_ld;
 };
 
 QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
@@ -43,10 +43,13 @@ QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
     const size_t q_bytes = (size_t)tiles * 32 * (size_t)p->ld * sizeof(uint16_t);
     w.s_ld = (int64_t)round_up((size_t)p->capacity, 64);
     const size_t s_bytes = (size_t)B * (size_t)w.s_ld * sizeof(float);
+    w.g_ld = oil::topk_block_ld(p->capacity);
+    const size_t g_bytes = (size_t)B * (size_t)w.g_ld * sizeof(uint64_t);
     const size_t c_bytes = oil::topk_cand_bytes(B, k, p->capacity);
     w.q_off = 0;
     w.s_off = round_up(w.q_off + q_bytes, kAlign);
-    w.ca_off = round_up(w.s_off + s_bytes, kAlign);
+    w.g_off = round_up(w.s_off + s_bytes, kAlign);
+    w.ca_off = round_up(w.g_off + g_bytes, kAlign);
     w.cb_off = round_up(w.ca_off + c_bytes, kAlign);
     w.total = round_up(w.cb_off + c_bytes, kAlign);
     return w;
@@ -217,6 +220,7 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
     char* ws = (char*)workspace;
     uint16_t* qbuf = (uint16_t*)(ws + w.q_off);
     float* S = (float*)(ws + w.s_off);
+    uint64_t* G = (uint64_t*)(ws + w.g_off);
     uint64_t* ca = (uint64_t*)(ws + w.ca_off);
     uint64_t* cb = (uint64_t*)(ws + w.cb_off);
     const int64_t n_valid = pool->n_valid;
@@ -230,13 +234,13 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
     if (e == hipSuccess) {
         timer_mark(st, 0);
         e = oil::launch_scan(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, pool->prompts,
-                             exclude_prompt, S, w.s_ld, st);
+                             exclude_prompt, S, w.s_ld, G, w.g_ld, st);
         timer_mark(st, 1);
         if (g_timer.ev && g_timer.used < g_timer.cap)
             g_timer.used++;
     }
     if (e == hipSuccess)
-        e = oil::launch_topk(S, w.s_ld, n_valid, B, k, ca, cb, scores, idx, st);
+        e = oil::launch_topk(S, w.s_ld, G, w.g_ld, n_valid, B, k, ca, cb, scores, idx, st);
     return hip_status(e);
 }
 
@@ -268,18 +272,21 @@ int32_t oil_tree_merge(int32_t B, const int32_t* anchor, const int32_t* lex_toke
     if (B < 1 || !anchor || !node_token || !node_parent || !node_source || !n_nodes || n_lex < 0 ||
         k < 0 || lex_budget < 0 || sem_budget < 0)
         return OIL_E_INVALID;
+    if (n_lex == 0)
+        L_lex = 1;  // unused
+    if (k == 0)
+        L = 1;      // unused
     if (n_lex > 0 && (!lex_tokens || !lex_len || L_lex < 1))
         return OIL_E_INVALID;
     if (k > 0 && (!sem_tokens || !sem_len || L < 1))
         return OIL_E_INVALID;
     if ((int64_t)lex_budget + sem_budget + 1 > max_nodes)
         return OIL_E_INVALID;
-    if (max_nodes > OIL_MAX_NODES || L_lex > 64 || L > 64)
+    if (max_nodes > OIL_MAX_NODES || L_lex > 64 || L > 64 || n_lex > 64 || k > 64)
         return OIL_E_UNSUPPORTED;
-    return hip_status(oil::launch_merge(B, anchor, lex_tokens, lex_len, n_lex, L_lex < 1 ? 1 : L_lex,
-                                        lex_budget, sem_tokens, sem_len, k, L < 1 ? 1 : L, sem_budget,
-                                        max_nodes, node_token, node_parent, node_source, n_nodes,
-                                        (hipStream_t)stream));
+    return hip_status(oil::launch_merge(B, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget,
+                                        sem_tokens, sem_len, k, L, sem_budget, max_nodes, node_token,
+                                        node_parent, node_source, n_nodes, (hipStream_t)stream));
 }
 
 const char* oil_status_string(int32_t status)

@@ -35,13 +35,14 @@ int scan_uses_mfma(int32_t B, int32_t ld);
 int scan_query_tiles(int32_t B);
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
-                       float* S, int64_t s_ld, hipStream_t stream);
+                       float* S, int64_t s_ld, uint64_t* G, int64_t g_ld, hipStream_t stream);
 
 int64_t topk_chunks(int64_t n);
+int64_t topk_block_ld(int64_t capacity);
 size_t topk_cand_bytes(int32_t B, int32_t k, int64_t capacity);
-hipError_t launch_topk(const float* S, int64_t s_ld, int64_t n_valid, int32_t B, int32_t k,
-                       uint64_t* cand_a, uint64_t* cand_b, float* out_s, int32_t* out_i,
-                       hipStream_t stream);
+hipError_t launch_topk(const float* S, int64_t s_ld, const uint64_t* G, int64_t g_ld, int64_t n_valid,
+                       int32_t B, int32_t k, uint64_t* cand_a, uint64_t* cand_b, float* out_s,
+                       int32_t* out_i, hipStream_t stream);
 
 hipError_t launch_gather(const int32_t* tokens, const int32_t* traces, int64_t n_valid,
                          const int32_t* idx, const float* scores, int32_t B, int32_t k,

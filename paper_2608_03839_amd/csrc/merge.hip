@@ -1,7 +1,8 @@
 // Root-first merge of draft chains into one tree per query (Sec. 4 (iii),
 // Eq. 4; BuildLexical then MergeFromRoot in Algorithm 1).
 //
-// One wave per tree.  The tree lives in registers: node slot j belongs to
+// One wave per tree.  The tree's input chains are first copied into LDS with
+// coalesced loads; the tree itself lives in registers: node slot j belongs to
 // lane j % 64, register j / 64 (up to 256 slots).  Each token of a chain is
 // one wave-wide step: every lane tests its slots for "child of the current
 // node carrying this token" and a ballot names the match (siblings never
@@ -18,8 +19,7 @@ constexpr int kSlotsPerLane = OIL_NODES_MAX / 64;
 
 __device__ __forceinline__ void insert_chain(int32_t (&ntok)[kSlotsPerLane], int32_t (&npar)[kSlotsPerLane],
                                              int32_t (&nsrc)[kSlotsPerLane], int& count, int& spent,
-                                             int budget, int src, const int32_t* __restrict__ chain,
-                                             int len)
+                                             int budget, int src, const int32_t* chain, int len)
 {
     const int lane = threadIdx.x;
     const int32_t mine = lane < len ? chain[lane] : -1;
@@ -29,11 +29,15 @@ __device__ __forceinline__ void insert_chain(int32_t (&ntok)[kSlotsPerLane], int
         int found = -1;
 #pragma unroll
         for (int q = 0; q < kSlotsPerLane; q++) {
+            if (q * 64 >= count)
+                break;
             const int slot = q * 64 + lane;
             const bool hit = slot < count && npar[q] == cur && ntok[q] == t;
             const uint64_t msk = __ballot(hit);
-            if (msk && found < 0)
+            if (msk) {
                 found = q * 64 + __ffsll((unsigned long long)msk) - 1;
+                break;
+            }
         }
         if (found >= 0) {
             cur = found;
@@ -62,7 +66,27 @@ __global__ __launch_bounds__(64) void merge_kernel(
     int32_t sem_budget, int32_t max_nodes, int32_t* __restrict__ node_token,
     int32_t* __restrict__ node_parent, int8_t* __restrict__ node_source, int32_t* __restrict__ n_nodes)
 {
+    // LDS: lexical chains, retrieved chains, then the two length arrays
+    extern __shared__ int32_t sm[];
+    int32_t* lex_s = sm;
+    int32_t* sem_s = lex_s + n_lex * L_lex;
+    int32_t* llen_s = sem_s + k * L;
+    int32_t* slen_s = llen_s + n_lex;
     const int b = blockIdx.x, lane = threadIdx.x;
+    {
+        const int32_t* lt = lex_tokens + (int64_t)b * n_lex * L_lex;
+        for (int i = lane; i < n_lex * L_lex; i += 64)
+            lex_s[i] = lt[i];
+        const int32_t* st = sem_tokens + (int64_t)b * k * L;
+        for (int i = lane; i < k * L; i += 64)
+            sem_s[i] = st[i];
+        for (int i = lane; i < n_lex; i += 64)
+            llen_s[i] = lex_len[(int64_t)b * n_lex + i];
+        for (int i = lane; i < k; i += 64)
+            slen_s[i] = sem_len[(int64_t)b * k + i];
+    }
+    __syncthreads();
+
     int32_t ntok[kSlotsPerLane], npar[kSlotsPerLane], nsrc[kSlotsPerLane];
 #pragma unroll
     for (int q = 0; q < kSlotsPerLane; q++) {
@@ -77,17 +101,15 @@ __global__ __launch_bounds__(64) void merge_kernel(
     int count = 1;
     int spent = 0;
     for (int c = 0; c < n_lex; c++) {
-        const int64_t o = (int64_t)b * n_lex + c;
-        int len = lex_len[o];
+        int len = llen_s[c];
         len = len < L_lex ? len : L_lex;
-        insert_chain(ntok, npar, nsrc, count, spent, lex_budget, 1, lex_tokens + o * L_lex, len);
+        insert_chain(ntok, npar, nsrc, count, spent, lex_budget, 1, lex_s + c * L_lex, len);
     }
     spent = 0;
     for (int c = 0; c < k; c++) {
-        const int64_t o = (int64_t)b * k + c;
-        int len = sem_len[o];
+        int len = slen_s[c];
         len = len < L ? len : L;
-        insert_chain(ntok, npar, nsrc, count, spent, sem_budget, 2, sem_tokens + o * L, len);
+        insert_chain(ntok, npar, nsrc, count, spent, sem_budget, 2, sem_s + c * L, len);
     }
 #pragma unroll
     for (int q = 0; q < kSlotsPerLane; q++) {
@@ -103,13 +125,19 @@ __global__ __launch_bounds__(64) void merge_kernel(
         n_nodes[b] = count;
 }
 
+size_t merge_lds_bytes(int32_t n_lex, int32_t L_lex, int32_t k, int32_t L)
+{
+    return ((size_t)n_lex * L_lex + (size_t)k * L + n_lex + k) * sizeof(int32_t);
+}
+
 hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
                         const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
                         const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
                         int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                         int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, hipStream_t stream)
 {
-    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(64), 0, stream, anchor, lex_tokens, lex_len, n_lex,
+    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(64), merge_lds_bytes(n_lex, L_lex, k, L), stream,
+                       anchor, lex_tokens, lex_len, n_lex,
                        L_lex, lex_budget, sem_tokens, sem_len, k, L, sem_budget, max_nodes, node_token,
                        node_parent, node_source, n_nodes);
     return hipGetLastError();

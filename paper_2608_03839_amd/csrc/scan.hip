@@ -63,7 +63,8 @@ template <int NB, int PF>
 __global__ __launch_bounds__(256) void scan_gemv_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const uint16_t* __restrict__ q, const int32_t* __restrict__ prompt,
-    const int32_t* __restrict__ exclude, float* __restrict__ S, int64_t s_ld)
+    const int32_t* __restrict__ exclude, float* __restrict__ S, int64_t s_ld,
+    uint64_t* __restrict__ G, int64_t g_ld)
 {
     constexpr int NS = PF + 1;
     extern __shared__ __align__(16) uint16_t q_lds[];  // NB x ld, row-major
@@ -111,16 +112,26 @@ __global__ __launch_bounds__(256) void scan_gemv_kernel(
             }
         }
     }
-#pragma unroll
-    for (int b = 0; b < NB; b++)
-        acc[b] += __shfl_xor(acc[b], 32, kWave);
+    // Lanes r and r + 32 now both hold row r's full score.  Each query also
+    // gets the best (score, position) key of this row block (top-k first
+    // picks row blocks by that key, then looks inside them).
     const int64_t row = rb * kRowBlock + r;
-    if (h != 0 || row >= n_valid)
-        return;
 #pragma unroll
     for (int b = 0; b < NB; b++) {
+        const float full = acc[b] + __shfl_xor(acc[b], 32, kWave);
         const int32_t ex = exclude ? exclude[b] : -1;
-        S[b * s_ld + row] = masked_score(acc[b], row, ex, prompt);
+        const bool have = row < n_valid;
+        const float v = have ? masked_score(full, row, ex, prompt) : 0.f;
+        if (have && h == 0)
+            S[b * s_ld + row] = v;
+        uint64_t best = have ? rank_key(v, (uint32_t)row) : 0ull;
+#pragma unroll
+        for (int o = 16; o >= 1; o >>= 1) {
+            const uint64_t other = __shfl_xor(best, o, kWave);
+            best = other > best ? other : best;
+        }
+        if (lane == 0)
+            G[b * g_ld + rb] = best;
     }
 }
 
@@ -146,7 +157,8 @@ template <int MT, int NT, int PF>
 __global__ __launch_bounds__(256) void scan_mfma_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
-    const int32_t* __restrict__ exclude, float* __restrict__ S, int64_t s_ld)
+    const int32_t* __restrict__ exclude, float* __restrict__ S, int64_t s_ld,
+    uint64_t* __restrict__ G, int64_t g_ld)
 {
     constexpr int NS = PF + 1;
     const int lane = threadIdx.x & 63;
@@ -197,30 +209,35 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     }
 
     // Accumulator layout of a 32x32 MFMA tile: lane l, element 4 i + j holds
-    // row 8 i + 4 (l / 32) + j (a key) and column l % 32 (a query).
+    // row 8 i + 4 (l / 32) + j (a key) and column l % 32 (a query).  Besides
+    // the scores, each (query, row block) gets its best (score, position) key:
+    // top-k first picks row blocks by that key, then looks inside them.
 #pragma unroll
     for (int nt = 0; nt < NT; nt++) {
         const int qb = nt * 32 + r;
-        if (qb >= B)
-            continue;
-        const int32_t ex = exclude ? exclude[qb] : -1;
-        float* srow = S + (int64_t)qb * s_ld;
+        const bool qlive = qb < B;
+        const int32_t ex = (exclude && qlive) ? exclude[qb] : -1;
+        float* srow = S + (int64_t)(qlive ? qb : 0) * s_ld;
 #pragma unroll
         for (int mt = 0; mt < MT; mt++) {
+            const int64_t rb = rb0 + mt;
+            uint64_t best = 0;
 #pragma unroll
             for (int i = 0; i < 4; i++) {
-                const int64_t row = (rb0 + mt) * kRowBlock + i * 8 + h * 4;
+                const int64_t row = rb * kRowBlock + i * 8 + h * 4;
                 floatx4 v;
-                v[0] = acc[mt][nt][4 * i + 0];
-                v[1] = acc[mt][nt][4 * i + 1];
-                v[2] = acc[mt][nt][4 * i + 2];
-                v[3] = acc[mt][nt][4 * i + 3];
-                if (ex >= 0) {
 #pragma unroll
-                    for (int j = 0; j < 4; j++)
-                        if (row + j < n_valid)
-                            v[j] = masked_score(v[j], row + j, ex, prompt);
+                for (int j = 0; j < 4; j++) {
+                    v[j] = acc[mt][nt][4 * i + j];
+                    if (ex >= 0 && row + j < n_valid)
+                        v[j] = masked_score(v[j], row + j, ex, prompt);
+                    if (row + j < n_valid) {
+                        const uint64_t key = rank_key(v[j], (uint32_t)(row + j));
+                        best = key > best ? key : best;
+                    }
                 }
+                if (!qlive)
+                    continue;
                 if (row + 3 < n_valid) {
                     *(floatx4*)(srow + row) = v;
                 } else {
@@ -230,6 +247,10 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
                             srow[row + j] = v[j];
                 }
             }
+            const uint64_t other = __shfl_xor(best, 32, kWave);
+            best = other > best ? other : best;
+            if (qlive && h == 0 && rb * kRowBlock < n_valid)
+                G[qb * g_ld + rb] = best;
         }
     }
 }
@@ -243,15 +264,16 @@ int scan_query_tiles(int32_t B) { return (B + 31) / 32; }
 template <int NB>
 static void launch_gemv(dim3 g, size_t lds, hipStream_t st, const uint16_t* keys, int32_t ld,
                         int64_t rs, int64_t ws, int64_t n_valid, const uint16_t* q,
-                        const int32_t* prompt, const int32_t* exclude, float* S, int64_t s_ld)
+                        const int32_t* prompt, const int32_t* exclude, float* S, int64_t s_ld,
+                        uint64_t* G, int64_t g_ld)
 {
     hipLaunchKernelGGL((scan_gemv_kernel<NB, 3>), g, dim3(256), lds, st, keys, ld, rs, ws, n_valid, q,
-                       prompt, exclude, S, s_ld);
+                       prompt, exclude, S, s_ld, G, g_ld);
 }
 
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
-                       float* S, int64_t s_ld, hipStream_t stream)
+                       float* S, int64_t s_ld, uint64_t* G, int64_t g_ld, hipStream_t stream)
 {
     if (n_valid <= 0)
         return hipSuccess;
@@ -261,10 +283,10 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
         const size_t lds = (size_t)B * ld * sizeof(uint16_t);
         const uint16_t* q = (const uint16_t*)qbuf;
         switch (B) {
-        case 1: launch_gemv<1>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld); break;
-        case 2: launch_gemv<2>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld); break;
-        case 3: launch_gemv<3>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld); break;
-        default: launch_gemv<4>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld); break;
+        case 1: launch_gemv<1>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld, G, g_ld); break;
+        case 2: launch_gemv<2>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld, G, g_ld); break;
+        case 3: launch_gemv<3>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld, G, g_ld); break;
+        default: launch_gemv<4>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld, G, g_ld); break;
         }
         return hipGetLastError();
     }
@@ -273,12 +295,12 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
         constexpr int MT = 4, PF = 1;
         const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
         hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF>), g, dim3(256), 0, stream, keys, ld, rs, ws,
-                           n_valid, qf, B, prompt, exclude, S, s_ld);
+                           n_valid, qf, B, prompt, exclude, S, s_ld, G, g_ld);
     } else {
         constexpr int MT = 4, PF = 1;
         const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
         hipLaunchKernelGGL((scan_mfma_kernel<MT, 2, PF>), g, dim3(256), 0, stream, keys, ld, rs, ws,
-                           n_valid, qf, B, prompt, exclude, S, s_ld);
+                           n_valid, qf, B, prompt, exclude, S, s_ld, G, g_ld);
     }
     return hipGetLastError();
 }

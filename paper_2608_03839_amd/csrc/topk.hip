@@ -1,27 +1,32 @@
 // Exact top-k (Eq. 2) over the scan's scores, in the total order
 // (score descending, position ascending).
 //
-// Every (score, position) pair becomes one 64-bit key whose unsigned order is
+// Every (score, position) pair is one 64-bit key whose unsigned order is
 // that total order (score code in the high word, complemented position in the
 // low word; 0 = "no position").  Keys are distinct, so "the k largest keys"
 // is exact and independent of evaluation order.
 //
-// Pass 1: one 256-thread block per (query, 4096-score chunk) selects the k
-// largest keys of its chunk by an 8-bit-digit radix select over the 64-bit
-// keys (LDS histogram, wave-aggregated increments, early exit once the
-// boundary digit holds exactly the keys still needed).
-// Pass 2..: the same block routine merges groups of candidate lists until one
-// list per query remains; that last pass ranks its k keys and writes them in
-// order.  The union of per-chunk top-k sets contains the global top-k, so the
-// result is exact.
+// The scan leaves, besides every score, the largest key of each 32-row block
+// ("block key").  The k largest keys of the pool lie inside the k row blocks
+// with the largest block keys: if a top-k key's block were not among them,
+// those k blocks would hold k keys above it.  So:
+//   1. select the k largest block keys per query (chunks of 4096 block keys
+//      per workgroup, then merges of the candidate lists, until one list of k
+//      remains);
+//   2. read the 32 scores of each selected block (k * 32 keys) and select the
+//      k largest, ranked and written in order.
+// Selection inside a workgroup is a radix select over 8-bit digits of the
+// 64-bit keys (LDS histogram with wave-aggregated increments; it stops as
+// soon as the boundary digit holds exactly the keys still needed).
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace oil {
 
 constexpr int kSelThreads = 256;
-constexpr int kSelVpt = 16;                         // keys per thread
-constexpr int kSelSpan = kSelThreads * kSelVpt;     // 4096 keys per block
+constexpr int kSelVpt = 16;                         // keys per thread, list selection
+constexpr int kSelSpan = kSelThreads * kSelVpt;     // 4096 keys per workgroup
+constexpr int kFinalVpt = OIL_TOPK_MAX * kRowBlock / kSelThreads;  // 8: k blocks x 32 rows
 
 struct SelShared {
     int hist[256];
@@ -30,9 +35,11 @@ struct SelShared {
     uint64_t sel[OIL_TOPK_MAX];
 };
 
-// Block-wide: select the k (<= OIL_TOPK_MAX) largest of the block's
-// kSelSpan keys (zeros included as padding) into sh.sel[0..k), unordered.
-__device__ void block_select(const uint64_t (&v)[kSelVpt], int k, SelShared& sh)
+// Block-wide: select the k (<= OIL_TOPK_MAX) largest of the block's keys
+// (zeros included as padding; there are always at least k keys) into
+// sh.sel[0..k), unordered.
+template <int VPT>
+__device__ void block_select(const uint64_t (&v)[VPT], int k, SelShared& sh)
 {
     const int tid = threadIdx.x, lane = tid & 63;
     uint64_t prefix = 0;
@@ -46,7 +53,7 @@ __device__ void block_select(const uint64_t (&v)[kSelVpt], int k, SelShared& sh)
         sh.hist[tid] = 0;
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < kSelVpt; j++) {
+        for (int j = 0; j < VPT; j++) {
             const bool act = (shift == 56) || ((v[j] >> (shift + 8)) == prefix);
             const uint32_t dig = (uint32_t)(v[j] >> shift) & 255u;
             const uint64_t m = __ballot(act);
@@ -96,8 +103,8 @@ __device__ void block_select(const uint64_t (&v)[kSelVpt], int k, SelShared& sh)
             break;
     }
 #pragma unroll
-    for (int j = 0; j < kSelVpt; j++) {
-        const uint64_t hi = (shift == 64) ? 0 : (v[j] >> shift);
+    for (int j = 0; j < VPT; j++) {
+        const uint64_t hi = v[j] >> shift;
         bool take = hi > prefix;
         if (!take && hi == prefix)
             take = atomicAdd(&sh.eq_ctr, 1) < need;
@@ -107,57 +114,31 @@ __device__ void block_select(const uint64_t (&v)[kSelVpt], int k, SelShared& sh)
     __syncthreads();
 }
 
-// Rank the k selected keys (descending; equal keys, i.e. padding, in slot
-// order) and write them as scores / positions.
-__device__ void block_emit_sorted(SelShared& sh, int k, float* __restrict__ out_s,
-                                  int32_t* __restrict__ out_i)
-{
-    const int t = threadIdx.x;
-    if (t < k) {
-        const uint64_t me = sh.sel[t];
-        int rank = 0;
-        for (int j = 0; j < k; j++) {
-            const uint64_t o = sh.sel[j];
-            rank += (o > me) || (o == me && j < t);
-        }
-        if (me == 0) {
-            out_s[rank] = -INFINITY;
-            out_i[rank] = -1;
-        } else {
-            out_s[rank] = code_score((uint32_t)(me >> 32));
-            out_i[rank] = (int32_t)key_pos(me);
-        }
-    }
-}
-
-// Pass 1: scores -> per-chunk candidates (or the final sorted list when the
-// pool fits one chunk).
-__global__ __launch_bounds__(kSelThreads) void topk_chunk_kernel(
-    const float* __restrict__ S, int64_t s_ld, int64_t n_valid, int k, uint64_t* __restrict__ cand,
-    int n_chunks, float* __restrict__ out_s, int32_t* __restrict__ out_i)
+// Step 1, first level: block keys -> k candidates per 4096-key chunk.
+__global__ __launch_bounds__(kSelThreads) void topk_blocks_kernel(
+    const uint64_t* __restrict__ G, int64_t g_ld, int64_t n_rb, int k, uint64_t* __restrict__ cand,
+    int n_chunks)
 {
     __shared__ SelShared sh;
     const int b = blockIdx.y, c = blockIdx.x;
     const int64_t base = (int64_t)c * kSelSpan;
-    const float* row = S + (int64_t)b * s_ld;
+    const uint64_t* row = G + (int64_t)b * g_ld;
     uint64_t v[kSelVpt];
 #pragma unroll
     for (int j = 0; j < kSelVpt; j++) {
-        const int64_t pos = base + j * kSelThreads + threadIdx.x;
-        v[j] = pos < n_valid ? rank_key(row[pos], (uint32_t)pos) : 0ull;
+        const int64_t at = base + j * kSelThreads + threadIdx.x;
+        v[j] = at < n_rb ? row[at] : 0ull;
     }
     block_select(v, k, sh);
-    if (n_chunks == 1) {
-        block_emit_sorted(sh, k, out_s + (int64_t)b * k, out_i + (int64_t)b * k);
-    } else if (threadIdx.x < k) {
+    if (threadIdx.x < k)
         cand[((int64_t)b * n_chunks + c) * k + threadIdx.x] = sh.sel[threadIdx.x];
-    }
 }
 
-// Pass 2..: merge groups of `group` candidate lists (group * k <= kSelSpan).
+// Step 1, further levels: merge groups of `group` candidate lists
+// (group * k <= 4096 keys per workgroup).
 __global__ __launch_bounds__(kSelThreads) void topk_merge_kernel(
     const uint64_t* __restrict__ cand_in, int n_lists, int k, int group, uint64_t* __restrict__ cand_out,
-    int n_out, float* __restrict__ out_s, int32_t* __restrict__ out_i)
+    int n_out)
 {
     __shared__ SelShared sh;
     const int b = blockIdx.y, g = blockIdx.x;
@@ -171,41 +152,97 @@ __global__ __launch_bounds__(kSelThreads) void topk_merge_kernel(
         v[j] = at < n_keys ? in[at] : 0ull;
     }
     block_select(v, k, sh);
-    if (n_out == 1) {
-        block_emit_sorted(sh, k, out_s + (int64_t)b * k, out_i + (int64_t)b * k);
-    } else if (threadIdx.x < k) {
+    if (threadIdx.x < k)
         cand_out[((int64_t)b * n_out + g) * k + threadIdx.x] = sh.sel[threadIdx.x];
+}
+
+// Step 2: the 32 scores of each of the k selected row blocks -> the k best
+// positions, ranked (descending; equal keys, i.e. padding, in slot order).
+__global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
+    const uint64_t* __restrict__ blocks, int k, const float* __restrict__ S, int64_t s_ld,
+    int64_t n_valid, float* __restrict__ out_s, int32_t* __restrict__ out_i)
+{
+    __shared__ SelShared sh;
+    __shared__ int64_t first_row[OIL_TOPK_MAX];
+    const int b = blockIdx.x, t = threadIdx.x;
+    if (t < k) {
+        const uint64_t bk = blocks[(int64_t)b * k + t];
+        first_row[t] = bk ? (int64_t)(key_pos(bk) / kRowBlock) * kRowBlock : -1;
+    }
+    __syncthreads();
+    const float* srow = S + (int64_t)b * s_ld;
+    uint64_t v[kFinalVpt];
+#pragma unroll
+    for (int j = 0; j < kFinalVpt; j++) {
+        const int slot = j * kSelThreads + t;
+        const int g = slot / kRowBlock;
+        v[j] = 0ull;
+        if (g < k && first_row[g] >= 0) {
+            const int64_t row = first_row[g] + slot % kRowBlock;
+            if (row < n_valid)
+                v[j] = rank_key(srow[row], (uint32_t)row);
+        }
+    }
+    block_select(v, k, sh);
+    if (t < k) {
+        const uint64_t me = sh.sel[t];
+        int rank = 0;
+        for (int j = 0; j < k; j++) {
+            const uint64_t o = sh.sel[j];
+            rank += (o > me) || (o == me && j < t);
+        }
+        float* os = out_s + (int64_t)b * k;
+        int32_t* oi = out_i + (int64_t)b * k;
+        if (me == 0) {
+            os[rank] = -INFINITY;
+            oi[rank] = -1;
+        } else {
+            os[rank] = code_score((uint32_t)(me >> 32));
+            oi[rank] = (int32_t)key_pos(me);
+        }
     }
 }
 
 int64_t topk_chunks(int64_t n) { return n <= 0 ? 1 : (n + kSelSpan - 1) / kSelSpan; }
 
-size_t topk_cand_bytes(int32_t B, int32_t k, int64_t capacity)
+int64_t topk_block_ld(int64_t capacity)
 {
-    return (size_t)B * (size_t)topk_chunks(capacity) * (size_t)k * sizeof(uint64_t);
+    const int64_t n_rb = (capacity + kRowBlock - 1) / kRowBlock;
+    return (n_rb + 63) / 64 * 64;
 }
 
-hipError_t launch_topk(const float* S, int64_t s_ld, int64_t n_valid, int32_t B, int32_t k,
-                       uint64_t* cand_a, uint64_t* cand_b, float* out_s, int32_t* out_i,
-                       hipStream_t stream)
+size_t topk_cand_bytes(int32_t B, int32_t k, int64_t capacity)
 {
-    int n_lists = (int)topk_chunks(n_valid);
-    hipLaunchKernelGGL(topk_chunk_kernel, dim3(n_lists, B), dim3(kSelThreads), 0, stream, S, s_ld,
-                       n_valid, k, cand_a, n_lists, out_s, out_i);
+    const int64_t n_rb = (capacity + kRowBlock - 1) / kRowBlock;
+    return (size_t)B * (size_t)topk_chunks(n_rb) * (size_t)k * sizeof(uint64_t);
+}
+
+hipError_t launch_topk(const float* S, int64_t s_ld, const uint64_t* G, int64_t g_ld, int64_t n_valid,
+                       int32_t B, int32_t k, uint64_t* cand_a, uint64_t* cand_b, float* out_s,
+                       int32_t* out_i, hipStream_t stream)
+{
+    const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
+    int n_lists = (int)topk_chunks(n_rb);
+    hipLaunchKernelGGL(topk_blocks_kernel, dim3(n_lists, B), dim3(kSelThreads), 0, stream, G, g_ld,
+                       n_rb, k, cand_a, n_lists);
     hipError_t e = hipGetLastError();
     const int group = kSelSpan / k;
     uint64_t *src = cand_a, *dst = cand_b;
     while (e == hipSuccess && n_lists > 1) {
         const int n_out = (n_lists + group - 1) / group;
         hipLaunchKernelGGL(topk_merge_kernel, dim3(n_out, B), dim3(kSelThreads), 0, stream, src,
-                           n_lists, k, group, dst, n_out, out_s, out_i);
+                           n_lists, k, group, dst, n_out);
         e = hipGetLastError();
         n_lists = n_out;
         uint64_t* t = src;
         src = dst;
         dst = t;
     }
-    return e;
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(topk_final_kernel, dim3(B), dim3(kSelThreads), 0, stream, src, k, S, s_ld,
+                       n_valid, out_s, out_i);
+    return hipGetLastError();
 }
 
 }  // namespace oil

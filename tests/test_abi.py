@@ -36,7 +36,8 @@ def test_stride_and_sizes(L):
     assert L.oil_key_stride(100) == 128
     assert L.oil_key_stride(4096) == 4096
     assert L.oil_key_stride(0) == 0
-    assert L.oil_pool_key_bytes(4096, 10) == 4096 * 10 * 2
+    assert L.oil_pool_key_bytes(4096, 10) == 4096 * 32 * 2      # rows round up to 32
+    assert L.oil_pool_key_bytes(100, 33) == 128 * 64 * 2
     assert L.oil_pool_key_bytes(0, 10) == 0
 
 
@@ -103,6 +104,9 @@ def test_merge_validates(L):
     assert L.oil_tree_merge(1, P, None, None, 1, 4, 4, P, P, 4, 4, 10, 64, P, P, P, P, None) == -1
     assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, 300, 301, P, P, P, P, None) == -3
     assert L.oil_tree_merge(0, P, None, None, 0, 1, 0, P, P, 4, 4, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, P, P, 65, 4, 4, P, P, 4, 4, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 65, 4, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 65, 10, 64, P, P, P, P, None) == -3
 
 
 def test_status_strings(L):
