@@ -1,0 +1,201 @@
+"""GPU parity at the full workload sizes, in the launch configurations the
+benchmark times.
+
+The pool is generated on the GPU in 64K-row chunks; each chunk is appended to
+the GPU pool and copied to the host, where the oracle normalises it and scores
+it against the sampled queries (rows are independent, so scoring chunk by
+chunk is the oracle's own definition applied row by row).  Sampled queries get
+the full T1-T3 check against exact oracle scores of every position; every
+query's returned positions are re-scored one by one by the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests._parity import TOL, away_from_edges, check_topk, untile_keys
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def oil():
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_2608_03839_amd as m
+    m.lib()
+    return m
+
+
+def _bits(t):
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+class StreamedOracle:
+    """Exact oracle scores of a growing pool for a fixed set of raw queries."""
+
+    def __init__(self, raw_q_bits, n_max):
+        self.q = oracle.normalize_rows(raw_q_bits)
+        self.s = np.full((self.q.shape[0], n_max), -np.inf)
+        self.n = 0
+
+    def add(self, keys):
+        """Append already oracle-normalised rows."""
+        m = keys.shape[0]
+        self.s[:, self.n:self.n + m] = oracle.scores(keys, self.q)
+        self.n += m
+
+
+def _fill(pool, wp, start, stop, dev, orc=None, chunk=65536):
+    for s0 in range(start, stop, chunk):
+        m = min(chunk, stop - s0)
+        raw = wp.raw_rows(s0, m)
+        pool.append(raw, wp.tokens[s0:s0 + m].to(dev), wp.traces[s0:s0 + m].to(dev),
+                    wp.prompts[s0:s0 + m].to(dev))
+        if orc:
+            keys = oracle.normalize_rows(_bits(raw))
+            for o in orc:
+                o.add(keys)
+
+
+def _rescore_returned(wp, gs, gi, raw_q_bits, tol=TOL):
+    """Every returned (query, position): the oracle's own score of that one key."""
+    qn = oracle.normalize_rows(raw_q_bits)
+    for b in range(gi.shape[0]):
+        ok = gi[b] >= 0
+        rows = gi[b][ok].astype(np.int64)
+        raw = torch.cat([wp.raw_rows(int(r), 1).cpu() for r in rows]) if rows.size else None
+        if raw is None:
+            continue
+        keys = oracle.normalize_rows(_bits(raw))
+        s = oracle.scores(keys, qn[b:b + 1])[0]
+        assert np.all(np.abs(gs[b][ok] - s) <= tol)
+
+
+def test_batched_1m_full_size(oil):
+    """N = 1,048,576, d = 4,096 bf16, B = 32, k = 32 (the benchmark's launch)."""
+    cfg = workloads.BATCHED_1M
+    ps, qs, k, L = cfg["pool"], cfg["query"], cfg["k"], cfg["L"]
+    dev = torch.device("cuda")
+    wp = workloads.Pool(ps, device=dev)
+    q, src = workloads.queries(wp, qs)
+    sample = [0, 1, 2, 3, 4, 5, 6, 7]
+    orc = StreamedOracle(_bits(q[sample]), ps.n)
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    _fill(pool, wp, 0, ps.n, dev, [orc])
+    s, i = pool.query_topk(q, k)
+    torch.cuda.synchronize()
+    gs, gi = s.cpu().numpy(), i.cpu().numpy()
+    flags = check_topk(gs[sample], gi[sample], orc.s, k)
+    _rescore_returned(wp, gs, gi, _bits(q))
+    # gather and merge on the oracle's own top-k are bit-exact
+    os_, oi = oracle.topk(orc.s, k)
+    os32 = os_.astype(np.float32)
+    rule_g, rule_o = oil.DepthRule.fixed(L), oracle.fixed_rule(L)
+    ct, cl = pool.gather(torch.from_numpy(oi).to(dev), torch.from_numpy(os32).to(dev), rule_g, L)
+    anchor = workloads.anchors(wp, src[sample])
+    mx = 1 + cfg["sem_budget"]
+    tree = oil.merge_trees(anchor.to(dev), None, None, 0, ct, cl, cfg["sem_budget"], mx)
+    torch.cuda.synchronize()
+    tok, tr = wp.tokens.numpy(), wp.traces.numpy()
+    ect, ecl = oracle.gather(tok, tr, ps.n, oi, os32, rule_o, L)
+    assert np.array_equal(ct.cpu().numpy(), ect) and np.array_equal(cl.cpu().numpy(), ecl)
+    etree = oracle.tree_merge(anchor.numpy(), np.zeros((len(sample), 0, 1), np.int32),
+                              np.zeros((len(sample), 0), np.int32), 0, ect, ecl,
+                              cfg["sem_budget"], mx)
+    for a, e in zip(tree, etree):
+        assert np.array_equal(a.cpu().numpy(), e)
+    # end to end where the retrieval is unambiguous and away from theta
+    gct, gcl = pool.gather(i, s, rule_g, L)
+    torch.cuda.synchronize()
+    gct, gcl = gct.cpu().numpy(), gcl.cpu().numpy()
+    for j, b in enumerate(sample):
+        if flags[j][1] and away_from_edges(os32[j], [0.8]):
+            assert np.array_equal(gcl[b], ecl[j]) and np.array_equal(gct[b], ect[j])
+
+
+def test_stream_5120_checkpoints(oil):
+    """d = 5,120 bf16 pool growing from 262,144 to 2,097,152 positions; at each
+    checkpoint a few streaming steps (append 1-8 positions + 16 queries); the
+    last step's sampled queries are checked against the oracle over exactly the
+    positions appended before them."""
+    cfg = workloads.STREAM_5120
+    ps, qs, k = cfg["pool"], cfg["query"], cfg["k"]
+    dev = torch.device("cuda")
+    checkpoints = [262144, 524288, 1048576, 2097152 - 64]
+    steps = 4
+    sizes = workloads.append_sizes(41, steps * len(checkpoints)).view(len(checkpoints), steps)
+    n_final = [c + int(sizes[j].sum()) for j, c in enumerate(checkpoints)]
+    wp = workloads.Pool(ps, device=dev)
+    queries, orcs = [], []
+    for j, c in enumerate(checkpoints):
+        q, _ = workloads.queries(wp, workloads.QuerySpec(B=qs.B, noise=qs.noise,
+                                                         p_random=qs.p_random, seed=qs.seed + j),
+                                 n_valid=c)
+        queries.append(q)
+        orcs.append(StreamedOracle(_bits(q[:2]), n_final[j]))
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    at = 0
+    for j, c in enumerate(checkpoints):
+        live = [o for jj, o in enumerate(orcs) if jj >= j]
+        _fill(pool, wp, at, c, dev, live)
+        at = c
+        for t in range(steps):
+            m = int(sizes[j, t])
+            _fill(pool, wp, at, at + m, dev, live)
+            at += m
+            s, i = pool.query_topk(queries[j], k)
+        torch.cuda.synchronize()
+        assert len(pool) == n_final[j] == at
+        o = orcs[j]
+        assert o.n == at
+        check_topk(s.cpu().numpy()[:2], i.cpu().numpy()[:2], o.s, k)
+
+
+def test_full_step_8192(oil):
+    """N = 524,288, d = 8,192 bf16, B = 64, k = 32 chains of 12 merged with
+    4 exact-suffix lexical drafts per query under 48 + 16 nodes."""
+    cfg = workloads.FULL_STEP_8192
+    ps, qs, k, L = cfg["pool"], cfg["query"], cfg["k"], cfg["L"]
+    n_lex, L_lex, lb, sb = cfg["n_lex"], cfg["L_lex"], cfg["lex_budget"], cfg["sem_budget"]
+    dev = torch.device("cuda")
+    wp = workloads.Pool(ps, device=dev)
+    q, src = workloads.queries(wp, qs)
+    sample = list(range(8))
+    orc = StreamedOracle(_bits(q[sample]), ps.n)
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    _fill(pool, wp, 0, ps.n, dev, [orc])
+    lt, ll = workloads.lexical_drafts(wp, src, ps.n, n_lex, L_lex)
+    anchor = workloads.anchors(wp, src)
+    rule_g, rule_o = oil.DepthRule.fixed(L), oracle.fixed_rule(L)
+    mx = 1 + lb + sb
+    s, i = pool.query_topk(q, k)
+    ct, cl = pool.gather(i, s, rule_g, L)
+    tree = oil.merge_trees(anchor.to(dev), lt.to(dev), ll.to(dev), lb, ct, cl, sb, mx)
+    torch.cuda.synchronize()
+    gs, gi = s.cpu().numpy(), i.cpu().numpy()
+    flags = check_topk(gs[sample], gi[sample], orc.s, k)
+    _rescore_returned(wp, gs, gi, _bits(q))
+    tok, tr = wp.tokens.numpy(), wp.traces.numpy()
+    nn = tree[3].cpu().numpy()
+    assert np.all(nn <= mx) and nn.max() > 1 + sb     # lexical drafts used their nodes
+    # the oracle's retrieval for the sampled queries, then gather and merge on
+    # both sides from those same inputs: bit-exact
+    os_, oi = oracle.topk(orc.s, k)
+    os32 = os_.astype(np.float32)
+    oct_, ocl = oracle.gather(tok, tr, ps.n, oi, os32, rule_o, L)
+    otree = oracle.tree_merge(anchor.numpy()[sample], lt.numpy()[sample], ll.numpy()[sample], lb,
+                              oct_, ocl, sb, mx)
+    ct2, cl2 = pool.gather(torch.from_numpy(oi).to(dev), torch.from_numpy(os32).to(dev), rule_g, L)
+    tree2 = oil.merge_trees(anchor[sample].to(dev), lt[sample].to(dev), ll[sample].to(dev), lb,
+                            ct2, cl2, sb, mx)
+    torch.cuda.synchronize()
+    assert np.array_equal(ct2.cpu().numpy(), oct_) and np.array_equal(cl2.cpu().numpy(), ocl)
+    for a, e in zip(tree2, otree):
+        assert np.array_equal(a.cpu().numpy(), e)
+    # end to end for unambiguous sampled queries
+    for j, b in enumerate(sample):
+        if flags[j][1] and away_from_edges(os32[j], [0.8]):
+            assert np.array_equal(cl.cpu().numpy()[b], ocl[j])
+            for a, e in zip(tree, otree):
+                assert np.array_equal(a.cpu().numpy()[b], e[j])

@@ -342,18 +342,30 @@ def test_tiny_end_to_end(oil):
 
 
 def test_tiny_paper_rule(oil):
-    """The paper's depth bands on the tiny pool: only the true neighbour (s ~ 0.999) copies."""
+    """The paper's depth bands on the tiny pool: only the true neighbour
+    (s ~ 0.999) copies, 48 tokens capped at the end of its 48-token trace."""
     cfg = workloads.TINY
     wp = workloads.Pool(cfg["pool"])
     pool, raw = _fill(oil, wp)
     q, src = workloads.queries(wp, workloads.QuerySpec(B=4, seed=5))
+    o = oracle_rows(oracle.normalize_rows(raw.numpy()), q.numpy())
+    os_, oi = oracle.topk(o, 8)
+    os32 = os_.astype(np.float32)
+    ect, ecl = oracle.gather(wp.tokens.numpy(), wp.traces.numpy(), wp.spec.n, oi, os32,
+                             oracle.paper_rule(), 64)
+    ct, cl = pool.gather(torch.from_numpy(oi).cuda(), torch.from_numpy(os32).cuda(),
+                         oil.DepthRule.paper(), 64)
     s, i = pool.query_topk(q.cuda(), 8)
-    ct, cl = pool.gather(i, s, oil.DepthRule.paper(), 64)
+    ct_e2e, cl_e2e = pool.gather(i, s, oil.DepthRule.paper(), 64)
     torch.cuda.synchronize()
-    ect, ecl = oracle.gather(wp.tokens.numpy(), wp.traces.numpy(), wp.spec.n, i.cpu().numpy(),
-                             s.cpu().numpy(), oracle.paper_rule(), 64)
     assert np.array_equal(cl.cpu().numpy(), ecl) and np.array_equal(ct.cpu().numpy(), ect)
-    assert np.all(ecl[:, 1:] == 0)
+    # rank 1 is the source (s ~ 0.999 >= 0.90: depth 48), clipped at the end of
+    # its 48-token trace: 46 - (position in trace) tokens, dropped below 2
+    assert oi[:, 0].tolist() == src.tolist()
+    want = [(46 - p % 48) if (46 - p % 48) >= 2 else 0 for p in src.tolist()]
+    assert ecl[:, 0].tolist() == want and np.all(ecl[:, 1:] == 0)
+    # end to end: rank 1 is unambiguous (0.999 against ~0.15) and the others copy nothing
+    assert np.array_equal(cl_e2e.cpu().numpy(), ecl) and np.array_equal(ct_e2e.cpu().numpy(), ect)
 
 
 def test_decode_64k_end_to_end(oil):

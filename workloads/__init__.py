@@ -185,10 +185,107 @@ def append_sizes(seed: int, steps: int, lo: int = 1, hi: int = 8) -> torch.Tenso
 
 
 def anchors(pool: Pool, src: torch.Tensor) -> torch.Tensor:
-    """Root token per query: the stored token at the query's source position (random token else)."""
+    """Root token per query (a random token for random queries).
+
+    The query state lags the drafted position by one token (paper Sec. 4 (ii)),
+    so a query built from the key at position i0 stands for a request whose
+    last committed token is the one at i0 + 1 (inside i0's instance)."""
     g = _gen(pool.spec.seed + 31, "cpu")
     rnd = torch.randint(0, pool.spec.vocab, (src.numel(),), generator=g, dtype=torch.int32)
     out = rnd.clone()
-    ok = src >= 0
-    out[ok] = pool.tokens[src[ok].long()]
+    n = pool.spec.n
+    for b in range(src.numel()):
+        i0 = int(src[b])
+        if i0 >= 0:
+            a = i0 + 1 if (i0 + 1 < n and int(pool.traces[i0 + 1]) == int(pool.traces[i0])) else i0
+            out[b] = pool.tokens[a]
     return out
+
+
+def lexical_drafts(pool: Pool, src: torch.Tensor, n_valid: int, n_lex: int = 4, L_lex: int = 12,
+                   max_suffix: int = 16, seed: int = 0):
+    """Exact-suffix drafts to merge beside the retrieved chains (tree inputs).
+
+    The request behind query b is a fresh instance of the source position's
+    call: its context is the up-to-16 tokens of the source instance ending at
+    the anchor (i0 + 1), with that instance's minted positions re-drawn.  The
+    drafts follow the recipe of the paper's exact-match drafter (Sec. 3): take
+    the longest context suffix (<= 16 tokens) that recurs in the pool, back off
+    to shorter suffixes (down to 2) until n_lex distinct continuations are
+    found, rank them by frequency then earliest position, and copy L_lex tokens
+    after each match, clipped at the end of its trace.  Matches inside the
+    request's own source instance are skipped.  Random queries (src < 0) get
+    no drafts.  Returns (tokens (B, n_lex, L_lex) int32 -1 padded, lens (B, n_lex)).
+    """
+    import numpy as np
+    tok = pool.tokens[:n_valid].numpy()
+    tr = pool.traces[:n_valid].numpy()
+    B = src.numel()
+    out = np.full((B, n_lex, L_lex), -1, dtype=np.int32)
+    lens = np.zeros((B, n_lex), dtype=np.int32)
+    rng = np.random.default_rng(seed)
+    for b in range(B):
+        i0 = int(src[b])
+        if i0 < 0 or i0 + 1 >= n_valid:
+            continue
+        inst = int(tr[i0])
+        a = i0 + 1 if tr[i0 + 1] == inst else i0
+        start = max(a - max_suffix + 1, int(np.searchsorted(tr, inst, side="left")))
+        ctx = tok[start:a + 1].copy()
+        # re-mint the source instance's minted values: positions where this
+        # instance departs from another instance of its cluster
+        if pool.inst_cluster is not None:
+            c = int(pool.inst_cluster[inst])
+            twins = np.flatnonzero(pool.inst_cluster.numpy()[: (n_valid // TEMPLATE_LEN)] == c)
+            twins = twins[twins != inst]
+            if twins.size:
+                other = int(twins[0]) * TEMPLATE_LEN
+                off = start - inst * TEMPLATE_LEN
+                ref = tok[other + off: other + off + len(ctx)]
+                if len(ref) == len(ctx):
+                    diff = ref != ctx
+                    ctx[diff] = rng.integers(0, pool.spec.vocab, int(diff.sum()))
+        m_max = len(ctx)
+        if m_max < 2:
+            continue
+        # candidate end positions p with tok[p-1], tok[p] equal to the last two context tokens
+        cand = np.flatnonzero((tok[1:] == ctx[-1]) & (tok[:-1] == ctx[-2])) + 1
+        cand = cand[tr[cand] != inst]
+        if cand.size == 0:
+            continue
+        mlen = np.full(cand.size, 2)
+        alive = np.ones(cand.size, dtype=bool)
+        for m in range(3, m_max + 1):
+            pos = cand - (m - 1)
+            ok = alive & (pos >= 0)
+            ok[ok] = tok[pos[ok]] == ctx[-m]
+            mlen[ok] = m
+            alive = ok
+        picked, seen = [], set()
+        for m in range(int(mlen.max()), 1, -1):
+            hits = cand[mlen >= m]
+            conts = {}
+            for p in hits.tolist():
+                e = p + 1
+                seq = []
+                while e < n_valid and len(seq) < L_lex and tr[e] == tr[p]:
+                    seq.append(int(tok[e]))
+                    e += 1
+                if len(seq) == 0:
+                    continue
+                key = tuple(seq)
+                cnt, first = conts.get(key, (0, p))
+                conts[key] = (cnt + 1, min(first, p))
+            ranked = sorted(conts.items(), key=lambda kv: (-kv[1][0], kv[1][1]))
+            for key, _ in ranked:
+                if key not in seen:
+                    seen.add(key)
+                    picked.append(key)
+                if len(picked) == n_lex:
+                    break
+            if len(picked) == n_lex:
+                break
+        for j, seq in enumerate(picked):
+            out[b, j, :len(seq)] = seq
+            lens[b, j] = len(seq)
+    return torch.from_numpy(out), torch.from_numpy(lens)
