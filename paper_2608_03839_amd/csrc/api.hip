@@ -32,8 +32,8 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 int32_t hip_status(hipError_t e) { return e == hipSuccess ? OIL_OK : OIL_E_HIP; }
 
 struct QueryWorkspace {
-    size_t q_off, s_off, g_off, ca_off, cb_off, total;
-    int64_t s_ld, g_ld;
+    size_t q_off, sc_off, g_off, ca_off, cb_off, total;
+    int64_t g_ld;
 };
 
 QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
@@ -41,14 +41,13 @@ QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
     QueryWorkspace w;
     const int tiles = oil::scan_query_tiles(B);
     const size_t q_bytes = (size_t)tiles * 32 * (size_t)p->ld * sizeof(uint16_t);
-    w.s_ld = (int64_t)round_up((size_t)p->capacity, 64);
-    const size_t s_bytes = (size_t)B * (size_t)w.s_ld * sizeof(float);
+    const size_t sc_bytes = (size_t)B * (size_t)k * oil::kRowBlock * sizeof(float);
     w.g_ld = oil::topk_block_ld(p->capacity);
     const size_t g_bytes = (size_t)B * (size_t)w.g_ld * sizeof(uint64_t);
     const size_t c_bytes = oil::topk_cand_bytes(B, k, p->capacity);
     w.q_off = 0;
-    w.s_off = round_up(w.q_off + q_bytes, kAlign);
-    w.g_off = round_up(w.s_off + s_bytes, kAlign);
+    w.sc_off = round_up(w.q_off + q_bytes, kAlign);
+    w.g_off = round_up(w.sc_off + sc_bytes, kAlign);
     w.ca_off = round_up(w.g_off + g_bytes, kAlign);
     w.cb_off = round_up(w.ca_off + c_bytes, kAlign);
     w.total = round_up(w.cb_off + c_bytes, kAlign);
@@ -219,7 +218,7 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
     hipStream_t st = (hipStream_t)stream;
     char* ws = (char*)workspace;
     uint16_t* qbuf = (uint16_t*)(ws + w.q_off);
-    float* S = (float*)(ws + w.s_off);
+    float* SC = (float*)(ws + w.sc_off);
     uint64_t* G = (uint64_t*)(ws + w.g_off);
     uint64_t* ca = (uint64_t*)(ws + w.ca_off);
     uint64_t* cb = (uint64_t*)(ws + w.cb_off);
@@ -234,13 +233,19 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
     if (e == hipSuccess) {
         timer_mark(st, 0);
         e = oil::launch_scan(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, pool->prompts,
-                             exclude_prompt, S, w.s_ld, G, w.g_ld, st);
+                             exclude_prompt, G, w.g_ld, st);
         timer_mark(st, 1);
         if (g_timer.ev && g_timer.used < g_timer.cap)
             g_timer.used++;
     }
+    const uint64_t* chosen = nullptr;
     if (e == hipSuccess)
-        e = oil::launch_topk(S, w.s_ld, G, w.g_ld, n_valid, B, k, ca, cb, scores, idx, st);
+        e = oil::launch_topk_blocks(G, w.g_ld, n_valid, B, k, ca, cb, &chosen, st);
+    if (e == hipSuccess)
+        e = oil::launch_rescore(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, chosen, k,
+                                pool->prompts, exclude_prompt, SC, st);
+    if (e == hipSuccess)
+        e = oil::launch_topk_final(chosen, B, k, SC, n_valid, scores, idx, st);
     return hip_status(e);
 }
 

@@ -35,14 +35,20 @@ int scan_uses_mfma(int32_t B, int32_t ld);
 int scan_query_tiles(int32_t B);
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
-                       float* S, int64_t s_ld, uint64_t* G, int64_t g_ld, hipStream_t stream);
+                       uint64_t* G, int64_t g_ld, hipStream_t stream);
+hipError_t launch_rescore(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+                          const void* qbuf, int32_t B, const uint64_t* blocks, int32_t k,
+                          const int32_t* prompt, const int32_t* exclude, float* SC,
+                          hipStream_t stream);
 
 int64_t topk_chunks(int64_t n);
 int64_t topk_block_ld(int64_t capacity);
 size_t topk_cand_bytes(int32_t B, int32_t k, int64_t capacity);
-hipError_t launch_topk(const float* S, int64_t s_ld, const uint64_t* G, int64_t g_ld, int64_t n_valid,
-                       int32_t B, int32_t k, uint64_t* cand_a, uint64_t* cand_b, float* out_s,
-                       int32_t* out_i, hipStream_t stream);
+hipError_t launch_topk_blocks(const uint64_t* G, int64_t g_ld, int64_t n_valid, int32_t B, int32_t k,
+                              uint64_t* cand_a, uint64_t* cand_b, const uint64_t** chosen,
+                              hipStream_t stream);
+hipError_t launch_topk_final(const uint64_t* chosen, int32_t B, int32_t k, const float* SC,
+                             int64_t n_valid, float* out_s, int32_t* out_i, hipStream_t stream);
 
 hipError_t launch_gather(const int32_t* tokens, const int32_t* traces, int64_t n_valid,
                          const int32_t* idx, const float* scores, int32_t B, int32_t k,

@@ -1,7 +1,12 @@
 // Pool scan: s[b][i] = q_b . k_i for every stored position i < n_valid
 // (Algorithm 1 retrieve step; with unit operands this is cos(h_t, h_i)).
 // bf16 operands, fp32 accumulation.  The key pool is read exactly once per
-// call; scores go to a B x s_ld fp32 workspace for the top-k passes.
+// call.  The scan keeps, per (query, 32-row block), only the block's best
+// (score, position) key; the top-k passes pick the k best blocks per query
+// and the rescore kernels below recompute those blocks' 32 scores with the
+// scan's own instruction sequence (bit-identical values).  Writing every
+// score (B x N x 4 bytes) interleaves a large store stream with the key reads
+// and costs far more than its bytes; re-reading k blocks per query does not.
 //
 // The pool is stored as 4 KiB tiles (32 rows x 64 columns) in MFMA operand
 // order, window-major (see store.hip): every 16-byte-per-lane load reads
@@ -63,8 +68,7 @@ template <int NB, int PF>
 __global__ __launch_bounds__(256) void scan_gemv_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const uint16_t* __restrict__ q, const int32_t* __restrict__ prompt,
-    const int32_t* __restrict__ exclude, float* __restrict__ S, int64_t s_ld,
-    uint64_t* __restrict__ G, int64_t g_ld)
+    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld)
 {
     constexpr int NS = PF + 1;
     extern __shared__ __align__(16) uint16_t q_lds[];  // NB x ld, row-major
@@ -112,9 +116,8 @@ __global__ __launch_bounds__(256) void scan_gemv_kernel(
             }
         }
     }
-    // Lanes r and r + 32 now both hold row r's full score.  Each query also
-    // gets the best (score, position) key of this row block (top-k first
-    // picks row blocks by that key, then looks inside them).
+    // Lanes r and r + 32 now both hold row r's full score; each query keeps
+    // the best (score, position) key of this row block.
     const int64_t row = rb * kRowBlock + r;
 #pragma unroll
     for (int b = 0; b < NB; b++) {
@@ -122,8 +125,6 @@ __global__ __launch_bounds__(256) void scan_gemv_kernel(
         const int32_t ex = exclude ? exclude[b] : -1;
         const bool have = row < n_valid;
         const float v = have ? masked_score(full, row, ex, prompt) : 0.f;
-        if (have && h == 0)
-            S[b * s_ld + row] = v;
         uint64_t best = have ? rank_key(v, (uint32_t)row) : 0ull;
 #pragma unroll
         for (int o = 16; o >= 1; o >>= 1) {
@@ -157,8 +158,7 @@ template <int MT, int NT, int PF>
 __global__ __launch_bounds__(256) void scan_mfma_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
-    const int32_t* __restrict__ exclude, float* __restrict__ S, int64_t s_ld,
-    uint64_t* __restrict__ G, int64_t g_ld)
+    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld)
 {
     constexpr int NS = PF + 1;
     const int lane = threadIdx.x & 63;
@@ -209,15 +209,13 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     }
 
     // Accumulator layout of a 32x32 MFMA tile: lane l, element 4 i + j holds
-    // row 8 i + 4 (l / 32) + j (a key) and column l % 32 (a query).  Besides
-    // the scores, each (query, row block) gets its best (score, position) key:
-    // top-k first picks row blocks by that key, then looks inside them.
+    // row 8 i + 4 (l / 32) + j (a key) and column l % 32 (a query).  Each
+    // (query, row block) keeps its best (score, position) key.
 #pragma unroll
     for (int nt = 0; nt < NT; nt++) {
         const int qb = nt * 32 + r;
         const bool qlive = qb < B;
         const int32_t ex = (exclude && qlive) ? exclude[qb] : -1;
-        float* srow = S + (int64_t)(qlive ? qb : 0) * s_ld;
 #pragma unroll
         for (int mt = 0; mt < MT; mt++) {
             const int64_t rb = rb0 + mt;
@@ -225,26 +223,15 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 const int64_t row = rb * kRowBlock + i * 8 + h * 4;
-                floatx4 v;
 #pragma unroll
                 for (int j = 0; j < 4; j++) {
-                    v[j] = acc[mt][nt][4 * i + j];
-                    if (ex >= 0 && row + j < n_valid)
-                        v[j] = masked_score(v[j], row + j, ex, prompt);
                     if (row + j < n_valid) {
-                        const uint64_t key = rank_key(v[j], (uint32_t)(row + j));
+                        float v = acc[mt][nt][4 * i + j];
+                        if (ex >= 0)
+                            v = masked_score(v, row + j, ex, prompt);
+                        const uint64_t key = rank_key(v, (uint32_t)(row + j));
                         best = key > best ? key : best;
                     }
-                }
-                if (!qlive)
-                    continue;
-                if (row + 3 < n_valid) {
-                    *(floatx4*)(srow + row) = v;
-                } else {
-#pragma unroll
-                    for (int j = 0; j < 4; j++)
-                        if (row + j < n_valid)
-                            srow[row + j] = v[j];
                 }
             }
             const uint64_t other = __shfl_xor(best, 32, kWave);
@@ -253,6 +240,141 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
                 G[qb * g_ld + rb] = best;
         }
     }
+}
+
+// ----------------------------------------------------------------- rescore the chosen blocks
+// One wave per (chosen block slot, query).  The block comes from its best key
+// (0: no block, the slot's scores are "no position").  Scores land in
+// SC[(query * k + slot) * 32 + row in block].
+
+// MFMA path: the same v_mfma_f32_32x32x16_bf16 sequence as the scan (windows
+// in order, sub-steps in order, starting from zero) on the block's tile and
+// the query's 32-query fragment tile, so element (row, query) is bit-identical
+// to the scan's; the wave keeps the query's column.
+template <int PF>
+__global__ __launch_bounds__(64) void rescore_mfma_kernel(
+    const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+    const bf16x8* __restrict__ qfrag, int n_qtiles, const uint64_t* __restrict__ blocks, int k,
+    const int32_t* __restrict__ prompt, const int32_t* __restrict__ exclude, float* __restrict__ SC)
+{
+    constexpr int NS = PF + 1;
+    const int slot = blockIdx.x, qb = blockIdx.y, lane = threadIdx.x;
+    const int h = lane >> 5, r = lane & 31;
+    float* out = SC + ((int64_t)qb * k + slot) * kRowBlock;
+    const uint64_t bk = blocks[(int64_t)qb * k + slot];
+    if (bk == 0) {
+        if (lane < kRowBlock)
+            out[lane] = __uint_as_float(kNoScoreBits);
+        return;
+    }
+    const int64_t rb = key_pos(bk) / kRowBlock;
+    const int t = qb >> 5, n = qb & 31;
+    const int nwin = ld / kWindow;
+    const int64_t ws8 = ws / 8;
+    const bf16x8* tile = (const bf16x8*)(keys + rb * rs) + lane;
+    const bf16x8* qf = qfrag + lane;
+    floatx16 acc = floatx16{};
+    bf16x8 a[NS][4], b[NS][4];
+    auto load = [&](int stage, int w) {
+#pragma unroll
+        for (int s = 0; s < 4; s++) {
+            a[stage][s] = __builtin_nontemporal_load(tile + w * ws8 + s * 64);
+            b[stage][s] = qf[(((int64_t)w * n_qtiles + t) * 4 + s) * 64];
+        }
+    };
+#pragma unroll
+    for (int p = 0; p < PF; p++)
+        load(p, p < nwin ? p : nwin - 1);
+    const int nloop = (nwin + NS - 1) / NS * NS;
+    for (int w0 = 0; w0 < nloop; w0 += NS) {
+#pragma unroll
+        for (int u = 0; u < NS; u++) {
+            const int wl = w0 + u + PF < nwin ? w0 + u + PF : nwin - 1;
+            load((u + PF) % NS, wl);
+            if (w0 + u < nwin) {
+#pragma unroll
+                for (int s = 0; s < 4; s++)
+                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[u][s], b[u][s], acc, 0, 0, 0);
+            }
+        }
+    }
+    if (r != n)
+        return;
+    const int32_t ex = exclude ? exclude[qb] : -1;
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const int rr = i * 8 + h * 4 + j;
+            const int64_t row = rb * kRowBlock + rr;
+            float v = acc[4 * i + j];
+            if (row >= n_valid)
+                v = __uint_as_float(kNoScoreBits);
+            else if (ex >= 0)
+                v = masked_score(v, row, ex, prompt);
+            out[rr] = v;
+        }
+}
+
+// GEMV path: the scan's per-query order (windows, then sub-steps, v_dot2 in
+// element order, then the xor-32 exchange), query read from global memory.
+template <int PF>
+__global__ __launch_bounds__(64) void rescore_gemv_kernel(
+    const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+    const uint16_t* __restrict__ q, const uint64_t* __restrict__ blocks, int k,
+    const int32_t* __restrict__ prompt, const int32_t* __restrict__ exclude, float* __restrict__ SC)
+{
+    constexpr int NS = PF + 1;
+    const int slot = blockIdx.x, qb = blockIdx.y, lane = threadIdx.x;
+    const int h = lane >> 5, r = lane & 31;
+    float* out = SC + ((int64_t)qb * k + slot) * kRowBlock;
+    const uint64_t bk = blocks[(int64_t)qb * k + slot];
+    if (bk == 0) {
+        if (lane < kRowBlock)
+            out[lane] = __uint_as_float(kNoScoreBits);
+        return;
+    }
+    const int64_t rb = key_pos(bk) / kRowBlock;
+    const int nwin = ld / kWindow;
+    const int64_t ws8 = ws / 8;
+    const bf16x8* tile = (const bf16x8*)(keys + rb * rs) + lane;
+    const uint16_t* qrow = q + (int64_t)qb * ld;
+    float acc = 0.f;
+    bf16x8 a[NS][4];
+#pragma unroll
+    for (int p = 0; p < PF; p++) {
+        const int w = p < nwin ? p : nwin - 1;
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+            a[p][s] = __builtin_nontemporal_load(tile + w * ws8 + s * 64);
+    }
+    const int nloop = (nwin + NS - 1) / NS * NS;
+    for (int w0 = 0; w0 < nloop; w0 += NS) {
+#pragma unroll
+        for (int u = 0; u < NS; u++) {
+            const int wl = w0 + u + PF < nwin ? w0 + u + PF : nwin - 1;
+#pragma unroll
+            for (int s = 0; s < 4; s++)
+                a[(u + PF) % NS][s] = __builtin_nontemporal_load(tile + wl * ws8 + s * 64);
+            if (w0 + u < nwin) {
+                const int col = (w0 + u) * kWindow + 32 * h;
+#pragma unroll
+                for (int s = 0; s < 4; s++)
+                    acc = dot8_bf16(a[u][s], *(const bf16x8*)(qrow + col + 8 * s), acc);
+            }
+        }
+    }
+    const float full = acc + __shfl_xor(acc, 32, kWave);
+    if (h != 0)
+        return;
+    const int64_t row = rb * kRowBlock + r;
+    const int32_t ex = exclude ? exclude[qb] : -1;
+    float v = full;
+    if (row >= n_valid)
+        v = __uint_as_float(kNoScoreBits);
+    else if (ex >= 0)
+        v = masked_score(v, row, ex, prompt);
+    out[r] = v;
 }
 
 // ----------------------------------------------------------------- launchers
@@ -264,16 +386,15 @@ int scan_query_tiles(int32_t B) { return (B + 31) / 32; }
 template <int NB>
 static void launch_gemv(dim3 g, size_t lds, hipStream_t st, const uint16_t* keys, int32_t ld,
                         int64_t rs, int64_t ws, int64_t n_valid, const uint16_t* q,
-                        const int32_t* prompt, const int32_t* exclude, float* S, int64_t s_ld,
-                        uint64_t* G, int64_t g_ld)
+                        const int32_t* prompt, const int32_t* exclude, uint64_t* G, int64_t g_ld)
 {
     hipLaunchKernelGGL((scan_gemv_kernel<NB, 3>), g, dim3(256), lds, st, keys, ld, rs, ws, n_valid, q,
-                       prompt, exclude, S, s_ld, G, g_ld);
+                       prompt, exclude, G, g_ld);
 }
 
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
-                       float* S, int64_t s_ld, uint64_t* G, int64_t g_ld, hipStream_t stream)
+                       uint64_t* G, int64_t g_ld, hipStream_t stream)
 {
     if (n_valid <= 0)
         return hipSuccess;
@@ -283,25 +404,36 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
         const size_t lds = (size_t)B * ld * sizeof(uint16_t);
         const uint16_t* q = (const uint16_t*)qbuf;
         switch (B) {
-        case 1: launch_gemv<1>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld, G, g_ld); break;
-        case 2: launch_gemv<2>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld, G, g_ld); break;
-        case 3: launch_gemv<3>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld, G, g_ld); break;
-        default: launch_gemv<4>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, S, s_ld, G, g_ld); break;
+        case 1: launch_gemv<1>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
+        case 2: launch_gemv<2>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
+        case 3: launch_gemv<3>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
+        default: launch_gemv<4>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
         }
         return hipGetLastError();
     }
     const bf16x8* qf = (const bf16x8*)qbuf;
-    if (scan_query_tiles(B) == 1) {
-        constexpr int MT = 4, PF = 1;
-        const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
+    constexpr int MT = 4, PF = 1;
+    const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
+    if (scan_query_tiles(B) == 1)
         hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF>), g, dim3(256), 0, stream, keys, ld, rs, ws,
-                           n_valid, qf, B, prompt, exclude, S, s_ld, G, g_ld);
-    } else {
-        constexpr int MT = 4, PF = 1;
-        const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
+                           n_valid, qf, B, prompt, exclude, G, g_ld);
+    else
         hipLaunchKernelGGL((scan_mfma_kernel<MT, 2, PF>), g, dim3(256), 0, stream, keys, ld, rs, ws,
-                           n_valid, qf, B, prompt, exclude, S, s_ld, G, g_ld);
-    }
+                           n_valid, qf, B, prompt, exclude, G, g_ld);
+    return hipGetLastError();
+}
+
+hipError_t launch_rescore(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+                          const void* qbuf, int32_t B, const uint64_t* blocks, int32_t k,
+                          const int32_t* prompt, const int32_t* exclude, float* SC, hipStream_t stream)
+{
+    const dim3 g((unsigned)k, (unsigned)B);
+    if (!scan_uses_mfma(B, ld))
+        hipLaunchKernelGGL((rescore_gemv_kernel<3>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
+                           (const uint16_t*)qbuf, blocks, k, prompt, exclude, SC);
+    else
+        hipLaunchKernelGGL((rescore_mfma_kernel<3>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
+                           (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC);
     return hipGetLastError();
 }
 

@@ -6,15 +6,16 @@
 // low word; 0 = "no position").  Keys are distinct, so "the k largest keys"
 // is exact and independent of evaluation order.
 //
-// The scan leaves, besides every score, the largest key of each 32-row block
-// ("block key").  The k largest keys of the pool lie inside the k row blocks
-// with the largest block keys: if a top-k key's block were not among them,
-// those k blocks would hold k keys above it.  So:
+// The scan leaves the largest key of each 32-row block ("block key").  The k
+// largest keys of the pool lie inside the k row blocks with the largest
+// block keys: if a top-k key's block were not among them, those k blocks
+// would hold k keys above it.  So:
 //   1. select the k largest block keys per query (chunks of 4096 block keys
 //      per workgroup, then merges of the candidate lists, until one list of k
 //      remains);
-//   2. read the 32 scores of each selected block (k * 32 keys) and select the
-//      k largest, ranked and written in order.
+//   2. the rescore kernels (scan.hip) recompute the 32 scores of each chosen
+//      block, bit-identical to the scan's;
+//   3. select the k largest of those k * 32 keys, ranked and written in order.
 // Selection inside a workgroup is a radix select over 8-bit digits of the
 // 64-bit keys (LDS histogram with wave-aggregated increments; it stops as
 // soon as the boundary digit holds exactly the keys still needed).
@@ -156,11 +157,11 @@ __global__ __launch_bounds__(kSelThreads) void topk_merge_kernel(
         cand_out[((int64_t)b * n_out + g) * k + threadIdx.x] = sh.sel[threadIdx.x];
 }
 
-// Step 2: the 32 scores of each of the k selected row blocks -> the k best
-// positions, ranked (descending; equal keys, i.e. padding, in slot order).
+// Step 3: the 32 rescored scores of each of the k chosen row blocks -> the k
+// best positions, ranked (descending; equal keys, i.e. padding, in slot order).
 __global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
-    const uint64_t* __restrict__ blocks, int k, const float* __restrict__ S, int64_t s_ld,
-    int64_t n_valid, float* __restrict__ out_s, int32_t* __restrict__ out_i)
+    const uint64_t* __restrict__ blocks, int k, const float* __restrict__ SC, int64_t n_valid,
+    float* __restrict__ out_s, int32_t* __restrict__ out_i)
 {
     __shared__ SelShared sh;
     __shared__ int64_t first_row[OIL_TOPK_MAX];
@@ -170,7 +171,7 @@ __global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
         first_row[t] = bk ? (int64_t)(key_pos(bk) / kRowBlock) * kRowBlock : -1;
     }
     __syncthreads();
-    const float* srow = S + (int64_t)b * s_ld;
+    const float* sc = SC + (int64_t)b * k * kRowBlock;
     uint64_t v[kFinalVpt];
 #pragma unroll
     for (int j = 0; j < kFinalVpt; j++) {
@@ -180,7 +181,7 @@ __global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
         if (g < k && first_row[g] >= 0) {
             const int64_t row = first_row[g] + slot % kRowBlock;
             if (row < n_valid)
-                v[j] = rank_key(srow[row], (uint32_t)row);
+                v[j] = rank_key(sc[slot], (uint32_t)row);
         }
     }
     block_select(v, k, sh);
@@ -217,9 +218,9 @@ size_t topk_cand_bytes(int32_t B, int32_t k, int64_t capacity)
     return (size_t)B * (size_t)topk_chunks(n_rb) * (size_t)k * sizeof(uint64_t);
 }
 
-hipError_t launch_topk(const float* S, int64_t s_ld, const uint64_t* G, int64_t g_ld, int64_t n_valid,
-                       int32_t B, int32_t k, uint64_t* cand_a, uint64_t* cand_b, float* out_s,
-                       int32_t* out_i, hipStream_t stream)
+hipError_t launch_topk_blocks(const uint64_t* G, int64_t g_ld, int64_t n_valid, int32_t B, int32_t k,
+                              uint64_t* cand_a, uint64_t* cand_b, const uint64_t** chosen,
+                              hipStream_t stream)
 {
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
     int n_lists = (int)topk_chunks(n_rb);
@@ -238,9 +239,14 @@ hipError_t launch_topk(const float* S, int64_t s_ld, const uint64_t* G, int64_t 
         src = dst;
         dst = t;
     }
-    if (e != hipSuccess)
-        return e;
-    hipLaunchKernelGGL(topk_final_kernel, dim3(B), dim3(kSelThreads), 0, stream, src, k, S, s_ld,
+    *chosen = src;
+    return e;
+}
+
+hipError_t launch_topk_final(const uint64_t* chosen, int32_t B, int32_t k, const float* SC,
+                             int64_t n_valid, float* out_s, int32_t* out_i, hipStream_t stream)
+{
+    hipLaunchKernelGGL(topk_final_kernel, dim3(B), dim3(kSelThreads), 0, stream, chosen, k, SC,
                        n_valid, out_s, out_i);
     return hipGetLastError();
 }
