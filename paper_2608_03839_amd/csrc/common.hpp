@@ -59,7 +59,7 @@ __device__ __forceinline__ uint16_t double_to_bf16_rne(double x)
 // position" (outside the pool, or excluded) and maps to it.
 __device__ __forceinline__ uint32_t score_code(float s)
 {
-    const uint32_t b = __float_as_uint(s);
+    const uint32_t b = __float_as_uint(s) == 0x80000000u ? 0u : __float_as_uint(s);  // -0 ranks as +0
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 

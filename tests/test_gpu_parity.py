@@ -158,6 +158,50 @@ def test_planted_duplicates_rank_first(oil, B):
         assert m == 5 or s[b, m] < s[b, 0]
 
 
+@pytest.mark.parametrize("B", [1, 8])
+def test_zero_query_ranks_by_position(oil, B):
+    """A zero query row normalises to zero, every score is exactly 0, and the
+    total order of Eq. 2 ties then returns positions 0..k-1 (closed form)."""
+    wp = workloads.Pool(workloads.PoolSpec(n=3000, d=192, vocab=100, seed=9, key_dtype="f32"))
+    pool, _ = _fill(oil, wp)
+    q = torch.zeros((B, 192), dtype=torch.float32)
+    s, i = pool.query_topk(q.cuda(), 16)
+    torch.cuda.synchronize()
+    assert i.cpu().numpy().tolist() == [list(range(16))] * B
+    assert torch.all(s == 0)
+
+
+def test_maximum_sizes(oil):
+    """B = 64, k = 64, L = 64, 64 lexical drafts of 64 tokens, 256-node trees."""
+    n, d, B, k, L = 9000, 256, 64, 64, 64
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=60, seed=21, n_clusters=4,
+                                           key_dtype="bf16"))
+    pool, raw = _fill(oil, wp)
+    q, src = workloads.queries(wp, workloads.QuerySpec(B=B, p_random=0.1, seed=22))
+    s, i = pool.query_topk(q.cuda(), k)
+    torch.cuda.synchronize()
+    o = oracle_rows(_stored(pool, n), _raw_np(q))
+    check_topk(s.cpu().numpy(), i.cpu().numpy(), o, k)
+    os_, oi = oracle.topk(o, k)
+    os32 = os_.astype(np.float32)
+    ect, ecl = oracle.gather(wp.tokens.numpy(), wp.traces.numpy(), n, oi, os32,
+                             oracle.fixed_rule(L, theta=0.5), L)
+    ct, cl = pool.gather(torch.from_numpy(oi).cuda(), torch.from_numpy(os32).cuda(),
+                         oil.DepthRule.fixed(L, theta=0.5), L)
+    torch.cuda.synchronize()
+    assert np.array_equal(ct.cpu().numpy(), ect) and np.array_equal(cl.cpu().numpy(), ecl)
+    rng = np.random.default_rng(3)
+    lt, ll = _chains(rng, B, 64, 64, 6)
+    anchor = rng.integers(0, 100, B).astype(np.int32)
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    tree = oil.merge_trees(cu(anchor), cu(lt), cu(ll), 120, cu(ect), cu(ecl), 135, 256)
+    torch.cuda.synchronize()
+    etree = oracle.tree_merge(anchor, lt, ll, 120, ect, ecl, 135, 256)
+    for a, e in zip(tree, etree):
+        assert np.array_equal(a.cpu().numpy(), e)
+    assert etree[3].max() > 200                         # the large trees really fill
+
+
 def test_self_exclusion(oil):
     n, d, B = 4800, 256, 6
     wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=50, seed=3, n_clusters=4,
