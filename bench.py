@@ -67,6 +67,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=int, default=262144)
     ap.add_argument("--cpu-sample-queries", type=int, default=4)
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the step benchmark: retrieval calls on the same pool for "
+                         "B in 1..512, one JSON line with the scan's GB/s and MFMA TFLOP/s per B")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (3 launches), the reference "
                          "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
@@ -102,6 +105,9 @@ def main():
     B, N, d = qs.B, ps.n, ps.d
     K, W = args.steps, args.warmup
     steps = K + W
+
+    if args.sweep:
+        return sweep(args, oil, workloads, dev, cfg)
 
     # ---------------------------------------------------------------- inputs
     t0 = time.time()
@@ -227,6 +233,49 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def sweep(args, oil, workloads, dev, cfg):
+    """Scan throughput across query batches on the 1M x 4096 pool."""
+    import torch
+    ps, qs, k = cfg["pool"], cfg["query"], cfg["k"]
+    N, d = ps.n, ps.d
+    wp = workloads.Pool(ps, device=dev)
+    pool = oil.Pool(d, N, device=dev)
+    for s0 in range(0, N, 65536):
+        pool.append(wp.raw_rows(s0, 65536), wp.tokens[s0:s0 + 65536].to(dev),
+                    wp.traces[s0:s0 + 65536].to(dev), wp.prompts[s0:s0 + 65536].to(dev))
+    rows = []
+    K, W = max(args.steps // 10, 5), 2
+    for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
+        q, _ = workloads.queries(wp, workloads.QuerySpec(B=B, noise=qs.noise, p_random=qs.p_random,
+                                                         seed=qs.seed + 1000 + B))
+        q = q.contiguous()
+        out = (torch.empty((B, k), dtype=torch.float32, device=dev),
+               torch.empty((B, k), dtype=torch.int32, device=dev))
+        for _ in range(W):
+            pool.query_topk(q, k, out=out)
+        torch.cuda.synchronize()
+        oil.scan_timer_start(K)
+        t0 = time.perf_counter()
+        for _ in range(K):
+            pool.query_topk(q, k, out=out)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        n_t, ms = oil.scan_timer_stop()
+        scan_s = ms / n_t / 1e3
+        gbs = (N * d * 2 + B * d * 2) / scan_s / 1e9
+        tflops = 2.0 * B * N * d / scan_s / 1e12
+        rows.append({"B": B, "scan_ms": round(scan_s * 1e3, 4), "scan_GBps": round(gbs, 1),
+                     "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "scan_TFLOPs": round(tflops, 1),
+                     "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "query_topk_ms": round(1e3 * el / K, 4), "queries_per_s": round(B * K / el, 1)})
+        log(f"B={B}: scan {scan_s * 1e3:.3f} ms, {gbs:.0f} GB/s, {tflops:.0f} TFLOP/s")
+    print(json.dumps({"sweep": rows, "pool_rows": N, "dim": d, "k": k,
+                      "kernels": "B<=4 scan_gemv, B<=64 scan_mfma, B>64 scan_mfma_wide"}), flush=True)
 
 
 if __name__ == "__main__":

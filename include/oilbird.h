@@ -51,7 +51,7 @@ enum { OIL_F32 = 0, OIL_BF16 = 1 };
 
 /* Largest k, query batch and tree size served. */
 #define OIL_MAX_K 64
-#define OIL_MAX_B 64
+#define OIL_MAX_B 512
 #define OIL_MAX_NODES 256
 #define OIL_MAX_BANDS 4
 

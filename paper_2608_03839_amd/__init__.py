@@ -24,7 +24,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboilbird.so")
 
 OIL_F32, OIL_BF16 = 0, 1
-MAX_K, MAX_B, MAX_NODES, MAX_BANDS = 64, 64, 256, 4
+MAX_K, MAX_B, MAX_NODES, MAX_BANDS = 64, 512, 256, 4
 
 _lib = None
 

@@ -22,6 +22,8 @@
 //  * scan_mfma (4 < B <= 64): the batch makes the scan a dense contraction;
 //    v_mfma_f32_32x32x16_bf16 multiplies a 32-key tile by a 32-query tile
 //    fragment per instruction, the fragments pre-swizzled by query prep.
+//  * scan_mfma_wide (64 < B <= 512): the same instruction, keys shared by all
+//    query tiles through LDS (the contraction turns MFMA-bound near B ~ 300).
 //
 // Both run a software pipeline: a ring of PF + 1 register stages, window
 // w + PF requested before window w is consumed.  Loads are unconditional
@@ -242,6 +244,154 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     }
 }
 
+// ----------------------------------------------------------------- MFMA, wide batches (64 < B <= 512)
+// Past ~300 queries the contraction is MFMA-bound, so keys must be fetched
+// once and reused by every query tile.  A block owns MT row blocks; its four
+// waves split the query tiles (NTW tiles each).  Each 64-column window of the
+// block's keys (MT tiles of 4 KiB) is copied into LDS once with gfx950's
+// 16-byte global->LDS loads (the four waves share the copies), double
+// buffered with one barrier per window; every wave reads its A operands from
+// LDS (lane l's 16 bytes sit at 16 l: conflict-free) and its own query
+// fragments from L2.  Per (row block, query tile) the MFMA sequence is the
+// same as in scan_mfma_kernel (windows in order, sub-steps in order).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_at_most()
+{
+    // s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14;
+    // expcnt and lgkmcnt at their maxima (no wait on them).
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <int MT, int NTW>
+__global__ __launch_bounds__(256) void scan_mfma_wide_kernel(
+    const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+    const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
+    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld)
+{
+    __shared__ bf16x8 ring[2][MT][4][64];  // two windows of the block's MT key tiles
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int h = lane >> 5, r = lane & 31;
+    const int64_t rb0 = (int64_t)blockIdx.x * MT;
+    const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
+    const int nwin = ld / kWindow;
+    const int n_qt = (B + 31) / 32;
+    const int64_t ws8 = ws / 8;
+
+    // this wave's share of the block's key copies: (mt, s) pairs with (4 mt + s) % 4 == wave
+    const bf16x8* src[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; mt++) {
+        const int64_t rb = rb0 + mt < n_rb ? rb0 + mt : n_rb - 1;  // clamp: stays inside the pool
+        src[mt] = (const bf16x8*)(keys + rb * rs) + wave * 64 + lane;
+    }
+    auto copy_keys = [&](int buf, int w) {
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++)
+            __builtin_amdgcn_global_load_lds(
+                (const void __attribute__((address_space(1)))*)(src[mt] + w * ws8),
+                (void __attribute__((address_space(3)))*)&ring[buf][mt][wave][0], 16, 0, 0);
+    };
+    const bf16x8* qf = qfrag + lane;
+    int qt[NTW];
+#pragma unroll
+    for (int nt = 0; nt < NTW; nt++) {
+        const int t = wave * NTW + nt;
+        qt[nt] = t < n_qt ? t : n_qt - 1;  // clamp: idle tiles recompute a live one, never stored
+    }
+    auto load_q = [&](bf16x8 (&b)[NTW][4], int w) {
+#pragma unroll
+        for (int nt = 0; nt < NTW; nt++)
+#pragma unroll
+            for (int s = 0; s < 4; s++)
+                b[nt][s] = qf[(((int64_t)w * n_qt + qt[nt]) * 4 + s) * 64];
+    };
+
+    floatx16 acc[MT][NTW];
+#pragma unroll
+    for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+        for (int nt = 0; nt < NTW; nt++)
+            acc[mt][nt] = floatx16{};
+
+    // Two-stage ping-pong: stage 0 holds even windows (ring[0], b0), stage 1
+    // odd ones (ring[1], b1).  Each stage reads its keys out of LDS, starts
+    // the next window's copies into the other buffers (window index clamped:
+    // the extra copy past the end is harmless), multiplies, then waits for
+    // its copies and meets the other waves at the barrier.
+    auto mma = [&](const bf16x8 (&a)[MT][4], const bf16x8 (&b)[NTW][4]) {
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+#pragma unroll
+            for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+                for (int nt = 0; nt < NTW; nt++)
+                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt][s], b[nt][s], acc[mt][nt],
+                                                                          0, 0, 0);
+    };
+    auto read_keys = [&](bf16x8 (&a)[MT][4], int buf) {
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+            for (int s = 0; s < 4; s++)
+                a[mt][s] = ring[buf][mt][s][lane];
+    };
+    bf16x8 b0[NTW][4], b1[NTW][4], a[MT][4];
+    copy_keys(0, 0);
+    load_q(b0, 0);
+    wait_vmcnt_at_most<0>();
+    __syncthreads();
+    const int nloop = (nwin + 1) / 2 * 2;
+    for (int w0 = 0; w0 < nloop; w0 += 2) {
+        const int w1 = w0 + 1 < nwin ? w0 + 1 : nwin - 1;
+        const int w2 = w0 + 2 < nwin ? w0 + 2 : nwin - 1;
+        read_keys(a, 0);
+        copy_keys(1, w1);
+        load_q(b1, w1);
+        mma(a, b0);
+        wait_vmcnt_at_most<0>();
+        __syncthreads();
+        read_keys(a, 1);
+        copy_keys(0, w2);
+        load_q(b0, w2);
+        if (w0 + 1 < nwin)
+            mma(a, b1);
+        wait_vmcnt_at_most<0>();
+        __syncthreads();
+    }
+
+    // block keys, as in scan_mfma_kernel
+#pragma unroll
+    for (int nt = 0; nt < NTW; nt++) {
+        const int qb = (wave * NTW + nt) * 32 + r;
+        const bool qlive = qb < B;
+        const int32_t ex = (exclude && qlive) ? exclude[qb] : -1;
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++) {
+            const int64_t rb = rb0 + mt;
+            uint64_t best = 0;
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int64_t row = rb * kRowBlock + i * 8 + h * 4;
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    if (row + j < n_valid) {
+                        float v = acc[mt][nt][4 * i + j];
+                        if (ex >= 0)
+                            v = masked_score(v, row + j, ex, prompt);
+                        const uint64_t key = rank_key(v, (uint32_t)(row + j));
+                        best = key > best ? key : best;
+                    }
+                }
+            }
+            const uint64_t other = __shfl_xor(best, 32, kWave);
+            best = other > best ? other : best;
+            if (qlive && h == 0 && rb * kRowBlock < n_valid)
+                G[qb * g_ld + rb] = best;
+        }
+    }
+}
+
 // ----------------------------------------------------------------- rescore the chosen blocks
 // One wave per (chosen block slot, query).  The block comes from its best key
 // (0: no block, the slot's scores are "no position").  Scores land in
@@ -412,6 +562,21 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
         return hipGetLastError();
     }
     const bf16x8* qf = (const bf16x8*)qbuf;
+    if (B > 64) {
+        constexpr int MTW = 4;
+        const dim3 gw((unsigned)((n_rb + MTW - 1) / MTW));
+        const int ntw = (scan_query_tiles(B) + 3) / 4;
+        if (ntw == 1)
+            hipLaunchKernelGGL((scan_mfma_wide_kernel<MTW, 1>), gw, dim3(256), 0, stream, keys, ld, rs, ws,
+                               n_valid, qf, B, prompt, exclude, G, g_ld);
+        else if (ntw == 2)
+            hipLaunchKernelGGL((scan_mfma_wide_kernel<MTW, 2>), gw, dim3(256), 0, stream, keys, ld, rs, ws,
+                               n_valid, qf, B, prompt, exclude, G, g_ld);
+        else  // 4 query tiles per wave: 2 row blocks keep the accumulators in registers
+            hipLaunchKernelGGL((scan_mfma_wide_kernel<2, 4>), dim3((unsigned)((n_rb + 1) / 2)), dim3(256), 0,
+                               stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
+        return hipGetLastError();
+    }
     constexpr int MT = 4, PF = 1;
     const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
     if (scan_query_tiles(B) == 1)

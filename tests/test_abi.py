@@ -76,11 +76,12 @@ def test_create_validates(L):
     # query: sizes and workspace
     assert L.oil_query_workspace_bytes(h, 0, 8) == 0
     assert L.oil_query_workspace_bytes(h, 1, 65) == 0
-    assert L.oil_query_workspace_bytes(h, 65, 8) == 0
+    assert L.oil_query_workspace_bytes(h, 513, 8) == 0
+    assert L.oil_query_workspace_bytes(h, 512, 64) > 0
     ws = L.oil_query_workspace_bytes(h, 4, 8)
     assert ws > 0 and ws % 256 == 0
     assert L.oil_pool_query_topk(h, P, 0, 4, 65, None, P, ws, P, P, None) == -3
-    assert L.oil_pool_query_topk(h, P, 0, 65, 8, None, P, ws, P, P, None) == -3
+    assert L.oil_pool_query_topk(h, P, 0, 513, 8, None, P, ws, P, P, None) == -3
     assert L.oil_pool_query_topk(h, P, 0, 0, 8, None, P, ws, P, P, None) == -1
     assert L.oil_pool_query_topk(h, P, 0, 4, 8, None, P, ws - 1, P, P, None) == -5
     assert L.oil_pool_query_topk(h, P, 0, 4, 8, None, f.misaligned, ws, P, P, None) == -5

@@ -101,6 +101,25 @@ def test_topk_over_query_batches(oil, B):
     _query_case(oil, 5000, 512, B, 16, seed=20 + B)
 
 
+@pytest.mark.parametrize("B", [65, 96, 128, 200, 256, 512])
+def test_topk_wide_batches(oil, B):
+    """Wide batches share every key window through LDS across query tiles."""
+    _query_case(oil, 5000, 512, B, 16, seed=40 + B)
+
+
+def test_wide_batch_ragged_width_and_exclusion(oil):
+    n, d, B = 4100, 200, 130
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=50, seed=31, n_clusters=8,
+                                           key_dtype="bf16"))
+    pool, raw = _fill(oil, wp)
+    q, src = workloads.queries(wp, workloads.QuerySpec(B=B, p_random=0.2, seed=32))
+    ex = torch.where(src >= 0, wp.prompts[src.clamp(min=0).long()], torch.full_like(src, -1))
+    s, i = pool.query_topk(q.cuda(), 32, exclude_prompt=ex.cuda())
+    torch.cuda.synchronize()
+    o = oracle_rows(_stored(pool, n), _raw_np(q), wp.prompts.numpy(), ex.numpy())
+    check_topk(s.cpu().numpy(), i.cpu().numpy(), o, 32)
+
+
 @pytest.mark.parametrize("k", [1, 7, 32, 64])
 @pytest.mark.parametrize("n", [1, 63, 4096, 4097, 12345])
 def test_topk_k_and_ragged_pools(oil, k, n):
