@@ -181,6 +181,30 @@ int32_t oil_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_toke
                        int32_t sem_budget, int32_t max_nodes, int32_t *node_token,
                        int32_t *node_parent, int8_t *node_source, int32_t *n_nodes, void *stream);
 
+/* Attention mask of merged trees (Sec. 4 (iii): a node attends to itself and
+ * its ancestors and to nothing else; Sec. 4 (iv): one forward verifies the
+ * whole tree under that mask).
+ *   node_parent, n_nodes  as written by oil_tree_merge (B x max_nodes, B).
+ *   max_nodes  1 .. OIL_MAX_NODES.
+ *   mask       B x max_nodes x ceil(max_nodes / 32) uint32: row i has bit j
+ *              (word j / 32, bit j % 32) set iff j == i or j is an ancestor
+ *              of i; rows i >= n_nodes[b] are zero.
+ * Parent ids outside [0, max_nodes) end a walk; walks are bounded. */
+int32_t oil_tree_mask(int32_t B, int32_t max_nodes, const int32_t *node_parent, const int32_t *n_nodes,
+                      uint32_t *mask, void *stream);
+
+/* Greedy acceptance of a verified tree (Sec. 4 (iv); VerifyMaskedGreedy in
+ * Algorithm 1).  target[b * max_nodes + i] is the token the verifier
+ * predicts after node i's root path.  From the root, move to the child whose
+ * token equals the prediction at the current node, until no child does.
+ *   accept_len    B int32: accepted draft nodes (the root is not counted).
+ *   accept_nodes  B x max_nodes int32: their ids in path order, -1 padded.
+ *   bonus         B int32: the prediction at the last accepted node (at the
+ *                 root when nothing was accepted), committed with the path. */
+int32_t oil_accept_walk(int32_t B, int32_t max_nodes, const int32_t *node_token,
+                        const int32_t *node_parent, const int32_t *n_nodes, const int32_t *target,
+                        int32_t *accept_len, int32_t *accept_nodes, int32_t *bonus, void *stream);
+
 /* Benchmark instrumentation (host; not thread-safe).  While enabled, each
  * oil_pool_query_topk call records a HIP event pair around its pool-scan
  * kernel on the call's stream, for up to max_launches calls (1 .. 65536).

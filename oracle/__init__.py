@@ -52,6 +52,8 @@ def _load():
         lib.orc_gather.argtypes = [P, P, i64, P, P, i32, i32, f32, i32, P, P, i32, P, P]
         lib.orc_tree_merge.argtypes = [i32, P, P, P, i32, i32, i32, P, P, i32, i32, i32, i32,
                                        P, P, P, P]
+        lib.orc_tree_mask.argtypes = [i32, i32, P, P, P]
+        lib.orc_accept_walk.argtypes = [i32, i32, P, P, P, P, P, P, P]
         _lib = lib
     return _lib
 
@@ -185,3 +187,28 @@ def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem
                                   max(L, 1), sem_budget, max_nodes, _ptr(nt), _ptr(npar),
                                   _ptr(ns), _ptr(nn)), "tree_merge")
     return nt, npar, ns, nn
+
+
+def tree_mask(node_parent, n_nodes):
+    """Ancestor mask (Sec. 4 (iii)-(iv)): (B, max_nodes, ceil(max_nodes/32)) uint32 bit rows."""
+    npar = _c(node_parent, np.int32)
+    nn = _c(n_nodes, np.int32)
+    B, mx = npar.shape
+    out = np.empty((B, mx, (mx + 31) // 32), dtype=np.uint32)
+    _check(_load().orc_tree_mask(B, mx, _ptr(npar), _ptr(nn), _ptr(out)), "tree_mask")
+    return out
+
+
+def accept_walk(node_token, node_parent, n_nodes, target):
+    """Greedy verification walk (Sec. 4 (iv)) -> (accept_len (B,), accept_nodes (B, max_nodes), bonus (B,))."""
+    nt = _c(node_token, np.int32)
+    npar = _c(node_parent, np.int32)
+    nn = _c(n_nodes, np.int32)
+    tg = _c(target, np.int32)
+    B, mx = nt.shape
+    al = np.empty((B,), np.int32)
+    an = np.empty((B, mx), np.int32)
+    bo = np.empty((B,), np.int32)
+    _check(_load().orc_accept_walk(B, mx, _ptr(nt), _ptr(npar), _ptr(nn), _ptr(tg), _ptr(al),
+                                   _ptr(an), _ptr(bo)), "accept_walk")
+    return al, an, bo

@@ -382,3 +382,76 @@ int orc_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens, 
     free(nodes);
     return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Tree attention mask (Sec. 4 (iii): a node attends to itself and its        */
+/* ancestors and to nothing else; Sec. 4 (iv): one forward verifies the whole  */
+/* tree under that mask).  mask[b][i] is a bit row over nodes j: bit j set iff */
+/* j == i or j is an ancestor of i.  Rows of unused slots (i >= n_nodes) are   */
+/* zero.  words = ceil(max_nodes / 32); bit j lives in word j / 32, bit j % 32. */
+/* ------------------------------------------------------------------------ */
+
+int orc_tree_mask(int32_t B, int32_t max_nodes, const int32_t *node_parent, const int32_t *n_nodes,
+                  uint32_t *mask)
+{
+    if (B < 1 || max_nodes < 1 || !node_parent || !n_nodes || !mask)
+        return ORC_EINVAL;
+    int32_t words = (max_nodes + 31) / 32;
+    for (int32_t b = 0; b < B; b++) {
+        for (int32_t i = 0; i < max_nodes; i++) {
+            uint32_t *row = mask + ((int64_t)b * max_nodes + i) * words;
+            for (int32_t w = 0; w < words; w++)
+                row[w] = 0;
+            if (i >= n_nodes[b])
+                continue;
+            /* walk the parent pointers up to the root */
+            int32_t j = i, guard = 0;
+            while (j >= 0 && guard++ <= max_nodes) {
+                row[j / 32] |= 1u << (j % 32);
+                j = node_parent[(int64_t)b * max_nodes + j];
+            }
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Greedy verification walk (Sec. 4 (iv), VerifyMaskedGreedy in Algorithm 1). */
+/* target[b][i] is the token the verifier predicts after node i's root path.  */
+/* From the root, repeatedly move to the child whose token equals the         */
+/* prediction at the current node; stop when no child does.  The accepted     */
+/* path (node ids, root excluded) is committed together with the bonus token, */
+/* the prediction at the last accepted node (at the root when nothing was     */
+/* accepted).                                                                 */
+/* ------------------------------------------------------------------------ */
+
+int orc_accept_walk(int32_t B, int32_t max_nodes, const int32_t *node_token, const int32_t *node_parent,
+                    const int32_t *n_nodes, const int32_t *target, int32_t *accept_len,
+                    int32_t *accept_nodes, int32_t *bonus)
+{
+    if (B < 1 || max_nodes < 1 || !node_token || !node_parent || !n_nodes || !target || !accept_len ||
+        !accept_nodes || !bonus)
+        return ORC_EINVAL;
+    for (int32_t b = 0; b < B; b++) {
+        const int64_t o = (int64_t)b * max_nodes;
+        for (int32_t j = 0; j < max_nodes; j++)
+            accept_nodes[o + j] = -1;
+        int32_t cur = 0, len = 0;
+        for (;;) {
+            int32_t want = target[o + cur], next = -1;
+            for (int32_t c = 1; c < n_nodes[b]; c++) {
+                if (node_parent[o + c] == cur && node_token[o + c] == want) {
+                    next = c;
+                    break;
+                }
+            }
+            if (next < 0)
+                break;
+            accept_nodes[o + len++] = next;
+            cur = next;
+        }
+        accept_len[b] = len;
+        bonus[b] = target[o + cur];
+    }
+    return ORC_OK;
+}

@@ -86,6 +86,8 @@ def lib():
             "oil_tree_merge": (i32, [i32, P, P, P, i32, i32, i32, P, P, i32, i32, i32, i32, P, P,
                                      P, P, P]),
             "oil_status_string": (ctypes.c_char_p, [i32]),
+            "oil_tree_mask": (i32, [i32, i32, P, P, P, P]),
+            "oil_accept_walk": (i32, [i32, i32, P, P, P, P, P, P, P, P]),
             "oil_scan_timer_start": (i32, [i32]),
             "oil_scan_timer_stop": (i32, [ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]),
         }
@@ -200,6 +202,33 @@ def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem
         B, _ptr(_i32(anchor, "anchor")), _ptr(lt), _ptr(ll), n_lex, L_lex, lex_budget,
         _ptr(sem_tokens), _ptr(sem_len), k, L, sem_budget, max_nodes, _ptr(node_token),
         _ptr(node_parent), _ptr(node_source), _ptr(n_nodes), _stream(stream)))
+
+
+def tree_mask(node_parent, n_nodes, mask=None, stream=None):
+    """Ancestor mask of merged trees: (B, max_nodes, ceil(max_nodes/32)) int32 bit rows."""
+    B, mx = node_parent.shape
+    if mask is None:
+        mask = torch.empty((B, mx, (mx + 31) // 32), dtype=torch.int32, device=node_parent.device)
+    _check("oil_tree_mask", lib().oil_tree_mask(B, mx, _ptr(_i32(node_parent, "node_parent")),
+                                                _ptr(_i32(n_nodes, "n_nodes")), _ptr(mask),
+                                                _stream(stream)))
+    return mask
+
+
+def accept_walk(node_token, node_parent, n_nodes, target, out=None, stream=None):
+    """Greedy acceptance: (accept_len (B,), accept_nodes (B, max_nodes), bonus (B,))."""
+    B, mx = node_token.shape
+    dev = node_token.device
+    if out is None:
+        out = (torch.empty((B,), dtype=torch.int32, device=dev),
+               torch.empty((B, mx), dtype=torch.int32, device=dev),
+               torch.empty((B,), dtype=torch.int32, device=dev))
+    al, an, bo = out
+    _check("oil_accept_walk", lib().oil_accept_walk(
+        B, mx, _ptr(_i32(node_token, "node_token")), _ptr(_i32(node_parent, "node_parent")),
+        _ptr(_i32(n_nodes, "n_nodes")), _ptr(_i32(target, "target")), _ptr(al), _ptr(an), _ptr(bo),
+        _stream(stream)))
+    return al, an, bo
 
 
 def scan_timer_start(max_launches: int):

@@ -294,6 +294,29 @@ int32_t oil_tree_merge(int32_t B, const int32_t* anchor, const int32_t* lex_toke
                                         node_parent, node_source, n_nodes, (hipStream_t)stream));
 }
 
+int32_t oil_tree_mask(int32_t B, int32_t max_nodes, const int32_t* node_parent, const int32_t* n_nodes,
+                      uint32_t* mask, void* stream)
+{
+    if (B < 1 || max_nodes < 1 || !node_parent || !n_nodes || !mask)
+        return OIL_E_INVALID;
+    if (max_nodes > OIL_MAX_NODES)
+        return OIL_E_UNSUPPORTED;
+    return hip_status(oil::launch_tree_mask(B, max_nodes, node_parent, n_nodes, mask, (hipStream_t)stream));
+}
+
+int32_t oil_accept_walk(int32_t B, int32_t max_nodes, const int32_t* node_token, const int32_t* node_parent,
+                        const int32_t* n_nodes, const int32_t* target, int32_t* accept_len,
+                        int32_t* accept_nodes, int32_t* bonus, void* stream)
+{
+    if (B < 1 || max_nodes < 1 || !node_token || !node_parent || !n_nodes || !target || !accept_len ||
+        !accept_nodes || !bonus)
+        return OIL_E_INVALID;
+    if (max_nodes > OIL_MAX_NODES)
+        return OIL_E_UNSUPPORTED;
+    return hip_status(oil::launch_accept_walk(B, max_nodes, node_token, node_parent, n_nodes, target,
+                                              accept_len, accept_nodes, bonus, (hipStream_t)stream));
+}
+
 const char* oil_status_string(int32_t status)
 {
     switch (status) {

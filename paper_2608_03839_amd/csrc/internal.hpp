@@ -62,4 +62,11 @@ hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tok
                         int32_t* node_parent, int8_t* node_source, int32_t* n_nodes,
                         hipStream_t stream);
 
+hipError_t launch_tree_mask(int32_t B, int32_t max_nodes, const int32_t* node_parent,
+                            const int32_t* n_nodes, uint32_t* mask, hipStream_t stream);
+hipError_t launch_accept_walk(int32_t B, int32_t max_nodes, const int32_t* node_token,
+                              const int32_t* node_parent, const int32_t* n_nodes, const int32_t* target,
+                              int32_t* accept_len, int32_t* accept_nodes, int32_t* bonus,
+                              hipStream_t stream);
+
 }  // namespace oil

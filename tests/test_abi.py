@@ -110,6 +110,17 @@ def test_merge_validates(L):
     assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 65, 10, 64, P, P, P, P, None) == -3
 
 
+def test_verify_validates(L):
+    f = _FakeBufs()
+    P = f.aligned
+    assert L.oil_tree_mask(0, 8, P, P, P, None) == -1
+    assert L.oil_tree_mask(1, 0, P, P, P, None) == -1
+    assert L.oil_tree_mask(1, 257, P, P, P, None) == -3
+    assert L.oil_tree_mask(1, 8, None, P, P, None) == -1
+    assert L.oil_accept_walk(1, 8, P, P, P, P, P, P, None, None) == -1
+    assert L.oil_accept_walk(1, 300, P, P, P, P, P, P, P, None) == -3
+
+
 def test_status_strings(L):
     for s in (0, -1, -2, -3, -4, -5, 99):
         assert isinstance(L.oil_status_string(s), bytes)

@@ -25,6 +25,8 @@ MUTANTS = {
     "rounding ties away from zero": ("pick = (fmod(fabs(lo), 2.0) == 0.0) ? lo : hi;", "pick = hi;"),
     "score drops the last dim": ("for (int32_t j = 0; j < d; j++)\n                acc +=", "for (int32_t j = 0; j < d - 1; j++)\n                acc +="),
     "exclusion ignored": ("if (prompt && exclude && exclude[b] >= 0 && prompt[i] == exclude[b])", "if (0)"),
+    "mask misses the node itself": ("            int32_t j = i, guard = 0;", "            int32_t j = node_parent[(int64_t)b * max_nodes + i], guard = 0;"),
+    "bonus always from the root": ("        bonus[b] = target[o + cur];", "        bonus[b] = target[o];"),
 }
 
 
@@ -41,6 +43,7 @@ def test_pins_catch_mutant(name):
                         "-shared", "-std=c11", "-o", so, c, "-lm"], check=True)
         env = dict(os.environ, OILBIRD_ORACLE_LIB=so)
         r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
-                            os.path.join(ROOT, "tests", "test_oracle.py")],
+                            os.path.join(ROOT, "tests", "test_oracle.py"),
+                            os.path.join(ROOT, "tests", "test_oracle_verify.py")],
                            env=env, cwd=ROOT, capture_output=True, text=True, timeout=300)
         assert r.returncode != 0, f"pins did not catch mutant {name!r}"
