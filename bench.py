@@ -181,6 +181,29 @@ def main():
     fired = float((out_s[:, 0] >= 0.8).float().mean())
     log(f"{K} steps in {elapsed * 1e3:.1f} ms; scan timed {n_timed}x, {scan_ms_total / n_timed:.4f} ms avg")
 
+    # the calls after the merge (tree mask for the verifying forward, greedy
+    # accept-walk on synthetic verifier predictions), timed separately so the
+    # step above stays the retrieval hot path
+    extras = {}
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    target = torch.randint(0, 128256, tree[0].shape, generator=g, device=dev, dtype=torch.int32)
+    target[:, 0] = tree[0][:, 1]                      # the first draft token is always accepted
+    mask_out = oil.tree_mask(tree[1], tree[3])
+    walk_out = oil.accept_walk(tree[0], tree[1], tree[3], target)
+    for name, fn in (("tree_mask_us", lambda: oil.tree_mask(tree[1], tree[3], mask=mask_out)),
+                     ("accept_walk_us", lambda: oil.accept_walk(tree[0], tree[1], tree[3], target,
+                                                                out=walk_out))):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        extras[name] = round(1e3 * e0.elapsed_time(e1) / K, 2)
+    extras["mean_tree_nodes"] = round(float(tree[3].float().mean()), 2)
+    extras["mean_accepted"] = round(float(walk_out[0].float().mean()), 2)
+
     # roofline of the dominant kernel (pool scan): algorithmic bytes = keys read once
     mean_n = (n_before + n_after) / 2.0
     bytes_alg = mean_n * d * 2 + B * d * 2
@@ -231,6 +254,7 @@ def main():
                    "parallelism": "single GPU", "fired_fraction": round(fired, 3)},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "extras": extras,
     }
     print(json.dumps(line), flush=True)
 
