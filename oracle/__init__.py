@@ -53,6 +53,7 @@ def _load():
         lib.orc_tree_merge.argtypes = [i32, P, P, P, i32, i32, i32, P, P, i32, i32, i32, i32,
                                        P, P, P, P]
         lib.orc_tree_mask.argtypes = [i32, i32, P, P, P]
+        lib.orc_lexical_drafts.argtypes = [P, P, P, i64, P, P, i32, i32, P, i32, i32, i32, i64, P, P]
         lib.orc_accept_walk.argtypes = [i32, i32, P, P, P, P, P, P, P]
         _lib = lib
     return _lib
@@ -212,3 +213,23 @@ def accept_walk(node_token, node_parent, n_nodes, target):
     _check(_load().orc_accept_walk(B, mx, _ptr(nt), _ptr(npar), _ptr(nn), _ptr(tg), _ptr(al),
                                    _ptr(an), _ptr(bo)), "accept_walk")
     return al, an, bo
+
+
+def lexical_drafts(tokens, traces, prompts, n_valid, ctx, ctx_len, n_lex, L_lex, exclude_prompt=None,
+                   min_match=2, max_cand=1 << 62):
+    """Exact-suffix drafts: (tokens (B, n_lex, L_lex) -1 padded, lengths (B, n_lex)).
+
+    ``ctx`` is (B, C) right-aligned (most recent token last); the last
+    ``ctx_len[b]`` entries of row b are the request's context."""
+    tok, tr, pr = _c(tokens, np.int32), _c(traces, np.int32), _c(prompts, np.int32)
+    ctx = _c(ctx, np.int32)
+    cl = _c(ctx_len, np.int32)
+    B, C = ctx.shape
+    ex = None if exclude_prompt is None else _c(exclude_prompt, np.int32)
+    ot = np.empty((B, n_lex, L_lex), np.int32)
+    ol = np.empty((B, n_lex), np.int32)
+    _check(_load().orc_lexical_drafts(_ptr(tok), _ptr(tr), _ptr(pr), int(n_valid), _ptr(ctx), _ptr(cl),
+                                      C, B, _ptr(ex), n_lex, L_lex, min_match, int(max_cand), _ptr(ot),
+                                      _ptr(ol)),
+           "lexical_drafts")
+    return ot, ol

@@ -455,3 +455,190 @@ int orc_accept_walk(int32_t B, int32_t max_nodes, const int32_t *node_token, con
     }
     return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Exact-suffix lexical drafts: the lexical key of Sec. 2 over the token pool */
+/* (longest recurring suffix of the context, back-off to shorter suffixes,    */
+/* propose what followed the matches), with the exact-match drafter's knobs   */
+/* of Sec. 3 (suffixes up to the context length, back off until n_lex         */
+/* distinct candidates are held, two-token minimum key).  For request b,      */
+/* whose cl most recent committed tokens are ctx (most recent last):          */
+/*  1. a stored position p matches to length m(p), the largest m <= cl with   */
+/*     x[p-j] = ctx[cl-1-j] for every j < m, all of p-m+1 .. p in p's trace;   */
+/*  2. p is a candidate when m(p) >= min_match, its prompt is not the one     */
+/*     being served (the self-exclusion of Sec. 4 (i)) and x[p+1] exists in   */
+/*     p's trace; its continuation is x[p+1 .. p+L_lex], clipped at the end of */
+/*     the trace and of the pool;                                              */
+/*  3. candidate capacity (a bound of the index, not of the paper): with      */
+/*     n(m) the number of candidates matching to length >= m and m* the       */
+/*     longest match, back-off visits m = m*, m*-1, ... while n(m) <= max_cand;*/
+/*     if already n(m*) > max_cand only level m* is visited, over its max_cand */
+/*     earliest candidates;                                                   */
+/*  4. at each visited level m, the distinct continuations of the (kept)      */
+/*     candidates with m(p) >= m that are not yet held are ranked by how many  */
+/*     of those candidates give them (more first), then by their earliest     */
+/*     position, and taken in that order until n_lex are held.              */
+/* Output: n_lex slots per request in pick order; unused slots -1 / length 0. */
+/* Parity pins: brute force, a library special case, relations (exclusion,    */
+/* back-off, capacity) and a hand-worked fixture.                              */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t p;     /* earliest position of the group at the current level */
+    int64_t count; /* candidates of the group at the current level */
+    int64_t group; /* representative candidate (first in position order) */
+} orc_level_entry;
+
+static int32_t cont_len(const int32_t *traces, int64_t n_valid, int64_t p, int32_t L)
+{
+    int32_t len = 0;
+    while (len < L && p + 1 + len < n_valid && traces[p + 1 + len] == traces[p])
+        len++;
+    return len;
+}
+
+static int same_cont(const int32_t *tokens, const int32_t *traces, int64_t n_valid, int64_t p, int64_t q,
+                     int32_t L)
+{
+    int32_t a = cont_len(traces, n_valid, p, L), b = cont_len(traces, n_valid, q, L);
+    if (a != b)
+        return 0;
+    for (int32_t j = 1; j <= a; j++)
+        if (tokens[p + j] != tokens[q + j])
+            return 0;
+    return 1;
+}
+
+static int level_cmp(const void *pa, const void *pb)
+{
+    const orc_level_entry *a = (const orc_level_entry *)pa, *b = (const orc_level_entry *)pb;
+    if (a->count != b->count)
+        return a->count > b->count ? -1 : 1;
+    return (a->p < b->p) ? -1 : (a->p > b->p);
+}
+
+int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32_t *prompts, int64_t n_valid,
+                       const int32_t *ctx, const int32_t *ctx_len, int32_t C, int32_t B,
+                       const int32_t *exclude_prompt, int32_t n_lex, int32_t L_lex, int32_t min_match,
+                       int64_t max_cand, int32_t *out_tokens, int32_t *out_len)
+{
+    if (!tokens || !traces || !prompts || !ctx || !ctx_len || !out_tokens || !out_len || n_valid < 0 ||
+        C < 1 || B < 1 || n_lex < 1 || L_lex < 1 || min_match < 1 || max_cand < 1)
+        return ORC_EINVAL;
+    size_t cap = (size_t)(n_valid > 0 ? n_valid : 1);
+    int64_t *cand = (int64_t *)malloc(sizeof(int64_t) * cap);
+    int32_t *mlen = (int32_t *)malloc(sizeof(int32_t) * cap);
+    int64_t *group = (int64_t *)malloc(sizeof(int64_t) * cap);
+    orc_level_entry *lev = (orc_level_entry *)malloc(sizeof(orc_level_entry) * cap);
+    int64_t *picked = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_lex);
+    int64_t *n_at = (int64_t *)calloc((size_t)C + 2, sizeof(int64_t));
+    if (!cand || !mlen || !group || !lev || !picked || !n_at) {
+        free(cand), free(mlen), free(group), free(lev), free(picked), free(n_at);
+        return ORC_EINVAL;
+    }
+    for (int32_t b = 0; b < B; b++) {
+        int32_t *ot = out_tokens + (int64_t)b * n_lex * L_lex;
+        int32_t *ol = out_len + (int64_t)b * n_lex;
+        for (int32_t j = 0; j < n_lex * L_lex; j++)
+            ot[j] = -1;
+        for (int32_t j = 0; j < n_lex; j++)
+            ol[j] = 0;
+        int32_t cl = ctx_len[b] < C ? ctx_len[b] : C;
+        if (cl < min_match)
+            continue;
+        const int32_t *cx = ctx + (int64_t)b * C + (C - cl); /* the cl most recent tokens */
+        int32_t ex = exclude_prompt ? exclude_prompt[b] : -1;
+        /* 1-2: candidates, in position order, and their match lengths */
+        int64_t nc = 0;
+        int32_t mtop = 0;
+        for (int32_t m = 0; m <= C + 1; m++)
+            n_at[m] = 0;
+        for (int64_t p = 0; p < n_valid; p++) {
+            int32_t m = 0;
+            while (m < cl && p - m >= 0 && traces[p - m] == traces[p] && tokens[p - m] == cx[cl - 1 - m])
+                m++;
+            if (m < min_match || (ex >= 0 && prompts[p] == ex) || cont_len(traces, n_valid, p, 1) == 0)
+                continue;
+            cand[nc] = p;
+            mlen[nc] = m;
+            nc++;
+            n_at[m]++;
+            if (m > mtop)
+                mtop = m;
+        }
+        if (nc == 0)
+            continue;
+        /* 3: visited levels [m_lo, mtop]; n(m) accumulated from the top */
+        int32_t m_lo = mtop;
+        int64_t n_ge = n_at[mtop];
+        for (int32_t m = mtop - 1; m >= min_match; m--) {
+            if (n_ge + n_at[m] > max_cand)
+                break;
+            n_ge += n_at[m];
+            m_lo = m;
+        }
+        {
+            int64_t w = 0, kept_top = 0;
+            for (int64_t i = 0; i < nc; i++) {
+                if (mlen[i] < m_lo)
+                    continue;
+                if (n_at[mtop] > max_cand && ++kept_top > max_cand)
+                    continue; /* only the earliest max_cand of the longest level */
+                cand[w] = cand[i];
+                mlen[w] = mlen[i];
+                w++;
+            }
+            nc = w;
+        }
+        /* 4: groups of identical continuations; each candidate names the first
+           candidate (in position order) with the same continuation */
+        for (int64_t i = 0; i < nc; i++) {
+            group[i] = i;
+            for (int64_t j = 0; j < i; j++) {
+                if (group[j] == j && same_cont(tokens, traces, n_valid, cand[i], cand[j], L_lex)) {
+                    group[i] = j;
+                    break;
+                }
+            }
+        }
+        int32_t n_picked = 0;
+        for (int32_t m = mtop; m >= m_lo && n_picked < n_lex; m--) {
+            int64_t ne = 0;
+            for (int64_t g = 0; g < nc; g++) {
+                if (group[g] != g)
+                    continue;
+                int already = 0;
+                for (int32_t t = 0; t < n_picked; t++)
+                    if (picked[t] == g)
+                        already = 1;
+                if (already)
+                    continue;
+                int64_t cnt = 0, first = -1;
+                for (int64_t i = 0; i < nc; i++) {
+                    if (group[i] == g && mlen[i] >= m) {
+                        cnt++;
+                        if (first < 0)
+                            first = cand[i];
+                    }
+                }
+                if (cnt == 0)
+                    continue;
+                lev[ne].p = first;
+                lev[ne].count = cnt;
+                lev[ne].group = g;
+                ne++;
+            }
+            qsort(lev, (size_t)ne, sizeof(orc_level_entry), level_cmp);
+            for (int64_t e = 0; e < ne && n_picked < n_lex; e++) {
+                int64_t p = lev[e].p;
+                int32_t len = cont_len(traces, n_valid, p, L_lex);
+                for (int32_t j = 0; j < len; j++)
+                    ot[(int64_t)n_picked * L_lex + j] = tokens[p + 1 + j];
+                ol[n_picked] = len;
+                picked[n_picked++] = lev[e].group;
+            }
+        }
+    }
+    free(cand), free(mlen), free(group), free(lev), free(picked), free(n_at);
+    return ORC_OK;
+}

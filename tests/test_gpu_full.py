@@ -165,7 +165,10 @@ def test_full_step_8192(oil):
     orc = StreamedOracle(_bits(q[sample]), ps.n)
     pool = oil.Pool(ps.d, ps.n, device=dev)
     _fill(pool, wp, 0, ps.n, dev, [orc])
-    lt, ll = workloads.lexical_drafts(wp, src, ps.n, n_lex, L_lex)
+    ctx, ctx_len, excl = workloads.lexical_contexts(wp, src, ps.n)
+    lt, ll = (torch.from_numpy(a) for a in oracle.lexical_drafts(
+        wp.tokens.numpy(), wp.traces.numpy(), wp.prompts.numpy(), ps.n, ctx.numpy(), ctx_len.numpy(),
+        n_lex, L_lex, excl.numpy()))
     anchor = workloads.anchors(wp, src)
     rule_g, rule_o = oil.DepthRule.fixed(L), oracle.fixed_rule(L)
     mx = 1 + lb + sb

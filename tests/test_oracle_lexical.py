@@ -1,0 +1,225 @@
+"""Pins of the oracle's exact-suffix lexical source (CPU only).
+
+Each test fixes the oracle against something other than itself: a
+hand-worked fixture, a brute-force enumeration written from the definition
+by a different route (sets of occurrences per suffix length, dictionaries of
+continuations), a special case that reduces to numpy window matching plus
+``collections.Counter``, and relations any correct implementation obeys
+(excluding a prompt equals deleting its trace; back-off stops once the
+longest level is full; the candidate capacity acts as a raised minimum key).
+"""
+import collections
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "lexical_sec3.json")
+
+
+def _run(pool, ctx_rows, n_lex, L_lex, C=None, exclude=None, min_match=2, max_cand=1 << 62):
+    tok, tr, pr = pool
+    C = C or max(1, max(len(c) for c in ctx_rows))
+    B = len(ctx_rows)
+    ctx = np.full((B, C), -1, np.int32)
+    cl = np.zeros(B, np.int32)
+    for b, c in enumerate(ctx_rows):
+        if len(c):
+            ctx[b, C - len(c):] = c
+        cl[b] = len(c)
+    ex = None if exclude is None else np.asarray(exclude, np.int32)
+    ot, ol = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, ex, min_match, max_cand)
+    return [[[int(t) for t in ot[b, j, :ol[b, j]]] for j in range(n_lex) if ol[b, j] > 0] for b in range(B)]
+
+
+def test_golden_sec3():
+    g = json.load(open(GOLDEN))
+    pool = tuple(np.asarray(g["pool"][k], np.int32) for k in ("tokens", "traces", "prompts"))
+    for case in g["cases"]:
+        got = _run(pool, [case["ctx"]], case["n_lex"], case["L_lex"], exclude=[case["exclude_prompt"]],
+                   min_match=case["min_match"], max_cand=case["max_cand"])[0]
+        assert got == case["expect"], case["name"]
+
+
+def brute_force(tok, tr, pr, ctx, n_lex, L_lex, ex, min_match, max_cand):
+    """The definition enumerated: per suffix length, the set of its occurrences."""
+    tok, tr, pr = list(tok), list(tr), list(pr)
+    n = len(tok)
+    cl = len(ctx)
+    if cl < min_match:
+        return []
+
+    def cont(p):
+        out = []
+        q = p + 1
+        while q < n and tr[q] == tr[p] and len(out) < L_lex:
+            out.append(tok[q])
+            q += 1
+        return tuple(out)
+
+    occ = {}
+    for m in range(min_match, cl + 1):
+        suf = list(ctx[cl - m:])
+        occ[m] = set()
+        for start in range(0, n - m + 1):
+            p = start + m - 1
+            if tok[start:p + 1] == suf and len(set(tr[start:p + 1])) == 1 and pr[p] != ex and cont(p):
+                occ[m].add(p)
+    levels = [m for m in range(cl, min_match - 1, -1) if occ[m]]
+    if not levels:
+        return []
+    top = levels[0]
+    if len(occ[top]) > max_cand:
+        keep = set(sorted(occ[top])[:max_cand])
+        visit = [(top, keep)]
+    else:
+        visit = [(m, occ[m]) for m in levels if len(occ[m]) <= max_cand]
+        # n(m) is monotone, so the admissible levels are a prefix of `levels`
+        visit = [(m, s) for (m, s) in visit if all(len(occ[mm]) <= max_cand for mm in range(m, top + 1))]
+    picked = []
+    for m, s in visit:
+        stats = {}
+        for p in sorted(s):
+            c = cont(p)
+            cnt, first = stats.get(c, (0, p))
+            stats[c] = (cnt + 1, min(first, p))
+        for c, _ in sorted(stats.items(), key=lambda kv: (-kv[1][0], kv[1][1])):
+            if len(picked) == n_lex:
+                break
+            if c not in picked:
+                picked.append(c)
+        if len(picked) == n_lex:
+            break
+    return [list(c) for c in picked]
+
+
+def _random_pool(rng, n, vocab, mean_trace):
+    lens = []
+    while sum(lens) < n:
+        lens.append(int(rng.integers(1, 2 * mean_trace)))
+    tr = np.repeat(np.arange(len(lens)), lens)[:n].astype(np.int32)
+    tok = rng.integers(0, vocab, n).astype(np.int32)
+    pr = (tr // 2).astype(np.int32)          # two traces share each prompt
+    return tok, tr, pr
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_brute_force_tiny(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(20, 160))
+    vocab = int(rng.integers(2, 5))
+    tok, tr, pr = _random_pool(rng, n, vocab, int(rng.integers(3, 12)))
+    for _ in range(6):
+        cl = int(rng.integers(0, 8))
+        # half the contexts are copied out of the pool, so long matches happen
+        if rng.random() < 0.5 and n > cl:
+            s0 = int(rng.integers(0, n - cl + 1))
+            ctx = tok[s0:s0 + cl].tolist()
+        else:
+            ctx = rng.integers(0, vocab, cl).tolist()
+        n_lex = int(rng.integers(1, 6))
+        L_lex = int(rng.integers(1, 5))
+        mm = int(rng.integers(1, 4))
+        cap = int(rng.choice([1, 2, 3, 5, 1 << 40]))
+        ex = int(rng.integers(-1, int(pr.max()) + 1))
+        want = brute_force(tok, tr, pr, ctx, n_lex, L_lex, ex, mm, cap)
+        got = _run((tok, tr, pr), [ctx], n_lex, L_lex, C=8, exclude=[ex], min_match=mm, max_cand=cap)[0]
+        assert got == want, (seed, ctx, n_lex, L_lex, mm, cap, ex)
+
+
+def test_full_context_next_tokens_match_counter():
+    """No back-off (min_match = context length), one token of continuation,
+    one trace: the picks are the tokens that follow the context's occurrences,
+    most frequent first, ties by first occurrence -- numpy's window view finds
+    the occurrences and Counter.most_common ranks them (it orders equal counts
+    by first insertion)."""
+    rng = np.random.default_rng(7)
+    tok = rng.integers(0, 3, 4000).astype(np.int32)
+    tr = np.zeros_like(tok)
+    pr = np.zeros_like(tok)
+    for cl in (2, 3, 4, 5):
+        ctx = tok[100:100 + cl]
+        win = np.lib.stride_tricks.sliding_window_view(tok, cl)
+        ends = np.flatnonzero((win == ctx).all(axis=1)) + cl - 1
+        ends = ends[ends + 1 < len(tok)]
+        ranked = [t for t, _ in collections.Counter(tok[ends + 1].tolist()).most_common()]
+        got = _run((tok, tr, pr), [ctx.tolist()], 3, 1, min_match=cl)[0]
+        assert got == [[t] for t in ranked[:3]]
+
+
+def test_exclusion_equals_removing_the_trace():
+    rng = np.random.default_rng(3)
+    tok, tr, pr = _random_pool(rng, 3000, 3, 20)
+    tr = np.arange(len(np.unique(tr)), dtype=np.int32)[np.searchsorted(np.unique(tr), tr)]
+    pr = tr.copy()                              # one prompt per trace here
+    for trial in range(10):
+        ex = int(rng.integers(0, int(pr.max()) + 1))
+        s0 = int(np.flatnonzero(pr == ex)[0])
+        ctx = tok[s0:s0 + 6].tolist()
+        keep = pr != ex
+        got = _run((tok, tr, pr), [ctx], 4, 5, exclude=[ex])[0]
+        want = _run((tok[keep], tr[keep], pr[keep]), [ctx], 4, 5)[0]
+        assert got == want
+
+
+def test_backoff_stops_once_full():
+    """When the longest matching suffix already yields n_lex distinct
+    continuations, shorter suffixes change nothing."""
+    rng = np.random.default_rng(11)
+    tok, tr, pr = _random_pool(rng, 6000, 2, 40)
+    hits = 0
+    for trial in range(40):
+        s0 = int(rng.integers(0, 5990))
+        ctx = tok[s0:s0 + 4].tolist()
+        full = _run((tok, tr, pr), [ctx], 3, 3, min_match=4)[0]
+        if len(full) == 3:
+            hits += 1
+            assert _run((tok, tr, pr), [ctx], 3, 3, min_match=1)[0] == full
+    assert hits > 5
+
+
+def test_capacity_is_a_raised_minimum_key():
+    """If the longest level fits the capacity, a capacity c gives the same
+    drafts as no capacity with the minimum key raised to the shortest suffix
+    whose candidates still fit."""
+    rng = np.random.default_rng(5)
+    tok, tr, pr = _random_pool(rng, 5000, 3, 30)
+    checked = 0
+    for trial in range(30):
+        s0 = int(rng.integers(0, 4990))
+        ctx = tok[s0:s0 + 6].tolist()
+        for cap in (4, 20, 100):
+            # number of candidates at level >= m, from the brute force's occurrence sets
+            occ = [len(_occurrences(tok, tr, ctx, m)) for m in range(1, 7)]
+            fits = [m for m in range(1, 7) if occ[m - 1] <= cap and occ[m - 1] > 0]
+            if not fits or max(m for m in range(1, 7) if occ[m - 1] > 0) not in fits:
+                continue
+            m_lo = min(fits)
+            got = _run((tok, tr, pr), [ctx], 4, 3, min_match=1, max_cand=cap)[0]
+            want = _run((tok, tr, pr), [ctx], 4, 3, min_match=m_lo)[0]
+            assert got == want
+            checked += 1
+    assert checked > 10
+
+
+def _occurrences(tok, tr, ctx, m):
+    """Positions ending an in-trace occurrence of the context's last m tokens
+    that have a continuation."""
+    suf = np.asarray(ctx[len(ctx) - m:], np.int32)
+    win = np.lib.stride_tricks.sliding_window_view(tok, m)
+    twin = np.lib.stride_tricks.sliding_window_view(tr, m)
+    ok = (win == suf).all(axis=1) & (twin == twin[:, :1]).all(axis=1)
+    ends = np.flatnonzero(ok) + m - 1
+    return [int(p) for p in ends if p + 1 < len(tok) and tr[p + 1] == tr[p]]
+
+
+def test_empty_inputs():
+    tok = np.zeros(0, np.int32)
+    assert _run((tok, tok, tok), [[1, 2, 3]], 2, 2) == [[]]
+    pool = (np.arange(10, dtype=np.int32), np.zeros(10, np.int32), np.zeros(10, np.int32))
+    assert _run(pool, [[]], 2, 2, C=4) == [[]]
+    assert _run(pool, [[3]], 2, 2, C=4) == [[]]            # shorter than the minimum key
+    assert _run(pool, [[2, 3]], 2, 2, C=4) == [[[4, 5]]]

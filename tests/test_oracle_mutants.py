@@ -27,6 +27,14 @@ MUTANTS = {
     "exclusion ignored": ("if (prompt && exclude && exclude[b] >= 0 && prompt[i] == exclude[b])", "if (0)"),
     "mask misses the node itself": ("            int32_t j = i, guard = 0;", "            int32_t j = node_parent[(int64_t)b * max_nodes + i], guard = 0;"),
     "bonus always from the root": ("        bonus[b] = target[o + cur];", "        bonus[b] = target[o];"),
+    "suffix match crosses traces": ("p - m >= 0 && traces[p - m] == traces[p] && tokens[p - m]", "p - m >= 0 && tokens[p - m]"),
+    "draft starts at the match": ("ot[(int64_t)n_picked * L_lex + j] = tokens[p + 1 + j];", "ot[(int64_t)n_picked * L_lex + j] = tokens[p + j];"),
+    "rarest continuation first": ("return a->count > b->count ? -1 : 1;", "return a->count < b->count ? -1 : 1;"),
+    "lexical ties by latest position": ("return (a->p < b->p) ? -1 : (a->p > b->p);", "return (a->p > b->p) ? -1 : (a->p < b->p);"),
+    "lexical self-exclusion ignored": ("(ex >= 0 && prompts[p] == ex)", "(0)"),
+    "draft not clipped at trace end": ("p + 1 + len < n_valid && traces[p + 1 + len] == traces[p]", "p + 1 + len < n_valid"),
+    "capacity ignored": ("if (n_ge + n_at[m] > max_cand)", "if (0)"),
+    "held draft proposed again": ("if (picked[t] == g)", "if (picked[t] == -7)"),
 }
 
 
@@ -44,6 +52,7 @@ def test_pins_catch_mutant(name):
         env = dict(os.environ, OILBIRD_ORACLE_LIB=so)
         r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
                             os.path.join(ROOT, "tests", "test_oracle.py"),
-                            os.path.join(ROOT, "tests", "test_oracle_verify.py")],
+                            os.path.join(ROOT, "tests", "test_oracle_verify.py"),
+                            os.path.join(ROOT, "tests", "test_oracle_lexical.py")],
                            env=env, cwd=ROOT, capture_output=True, text=True, timeout=300)
         assert r.returncode != 0, f"pins did not catch mutant {name!r}"

@@ -202,90 +202,48 @@ def anchors(pool: Pool, src: torch.Tensor) -> torch.Tensor:
     return out
 
 
-def lexical_drafts(pool: Pool, src: torch.Tensor, n_valid: int, n_lex: int = 4, L_lex: int = 12,
-                   max_suffix: int = 16, seed: int = 0):
-    """Exact-suffix drafts to merge beside the retrieved chains (tree inputs).
+def lexical_contexts(pool: Pool, src: torch.Tensor, n_valid: int, C: int = 16, seed: int = 0):
+    """Committed-token contexts for the lexical source, one request per query.
 
     The request behind query b is a fresh instance of the source position's
-    call: its context is the up-to-16 tokens of the source instance ending at
-    the anchor (i0 + 1), with that instance's minted positions re-drawn.  The
-    drafts follow the recipe of the paper's exact-match drafter (Sec. 3): take
-    the longest context suffix (<= 16 tokens) that recurs in the pool, back off
-    to shorter suffixes (down to 2) until n_lex distinct continuations are
-    found, rank them by frequency then earliest position, and copy L_lex tokens
-    after each match, clipped at the end of its trace.  Matches inside the
-    request's own source instance are skipped.  Random queries (src < 0) get
-    no drafts.  Returns (tokens (B, n_lex, L_lex) int32 -1 padded, lens (B, n_lex)).
-    """
+    call: its context is the up-to-C tokens of the source instance ending at
+    the anchor (i0 + 1), with that instance's minted values re-drawn (the
+    positions where it departs from another instance of its cluster), so the
+    exact suffix dies at those tokens as it does in the paper's traffic
+    (Sec. 1, Sec. 3).  The request's own source instance is excluded by prompt.
+    Random queries (src < 0) get an empty context.
+
+    Returns (ctx (B, C) int32 right-aligned, most recent token last, -1 on the
+    left; ctx_len (B,) int32; exclude_prompt (B,) int32, -1 for none)."""
     import numpy as np
     tok = pool.tokens[:n_valid].numpy()
     tr = pool.traces[:n_valid].numpy()
+    pr = pool.prompts[:n_valid].numpy()
     B = src.numel()
-    out = np.full((B, n_lex, L_lex), -1, dtype=np.int32)
-    lens = np.zeros((B, n_lex), dtype=np.int32)
+    ctx = np.full((B, C), -1, dtype=np.int32)
+    ctx_len = np.zeros((B,), dtype=np.int32)
+    excl = np.full((B,), -1, dtype=np.int32)
     rng = np.random.default_rng(seed)
     for b in range(B):
         i0 = int(src[b])
-        if i0 < 0 or i0 + 1 >= n_valid:
+        if i0 < 0 or i0 >= n_valid:
             continue
         inst = int(tr[i0])
-        a = i0 + 1 if tr[i0 + 1] == inst else i0
-        start = max(a - max_suffix + 1, int(np.searchsorted(tr, inst, side="left")))
-        ctx = tok[start:a + 1].copy()
-        # re-mint the source instance's minted values: positions where this
-        # instance departs from another instance of its cluster
+        a = i0 + 1 if (i0 + 1 < n_valid and tr[i0 + 1] == inst) else i0
+        start = max(a - C + 1, int(np.searchsorted(tr, inst, side="left")))
+        c = tok[start:a + 1].copy()
         if pool.inst_cluster is not None:
-            c = int(pool.inst_cluster[inst])
-            twins = np.flatnonzero(pool.inst_cluster.numpy()[: (n_valid // TEMPLATE_LEN)] == c)
+            cl = int(pool.inst_cluster[inst])
+            twins = np.flatnonzero(pool.inst_cluster.numpy()[: (n_valid // TEMPLATE_LEN)] == cl)
             twins = twins[twins != inst]
             if twins.size:
                 other = int(twins[0]) * TEMPLATE_LEN
                 off = start - inst * TEMPLATE_LEN
-                ref = tok[other + off: other + off + len(ctx)]
-                if len(ref) == len(ctx):
-                    diff = ref != ctx
-                    ctx[diff] = rng.integers(0, pool.spec.vocab, int(diff.sum()))
-        m_max = len(ctx)
-        if m_max < 2:
-            continue
-        # candidate end positions p with tok[p-1], tok[p] equal to the last two context tokens
-        cand = np.flatnonzero((tok[1:] == ctx[-1]) & (tok[:-1] == ctx[-2])) + 1
-        cand = cand[tr[cand] != inst]
-        if cand.size == 0:
-            continue
-        mlen = np.full(cand.size, 2)
-        alive = np.ones(cand.size, dtype=bool)
-        for m in range(3, m_max + 1):
-            pos = cand - (m - 1)
-            ok = alive & (pos >= 0)
-            ok[ok] = tok[pos[ok]] == ctx[-m]
-            mlen[ok] = m
-            alive = ok
-        picked, seen = [], set()
-        for m in range(int(mlen.max()), 1, -1):
-            hits = cand[mlen >= m]
-            conts = {}
-            for p in hits.tolist():
-                e = p + 1
-                seq = []
-                while e < n_valid and len(seq) < L_lex and tr[e] == tr[p]:
-                    seq.append(int(tok[e]))
-                    e += 1
-                if len(seq) == 0:
-                    continue
-                key = tuple(seq)
-                cnt, first = conts.get(key, (0, p))
-                conts[key] = (cnt + 1, min(first, p))
-            ranked = sorted(conts.items(), key=lambda kv: (-kv[1][0], kv[1][1]))
-            for key, _ in ranked:
-                if key not in seen:
-                    seen.add(key)
-                    picked.append(key)
-                if len(picked) == n_lex:
-                    break
-            if len(picked) == n_lex:
-                break
-        for j, seq in enumerate(picked):
-            out[b, j, :len(seq)] = seq
-            lens[b, j] = len(seq)
-    return torch.from_numpy(out), torch.from_numpy(lens)
+                ref = tok[other + off: other + off + len(c)]
+                if len(ref) == len(c):
+                    diff = ref != c
+                    c[diff] = rng.integers(0, pool.spec.vocab, int(diff.sum()))
+        ctx[b, C - len(c):] = c
+        ctx_len[b] = len(c)
+        excl[b] = int(pr[i0])
+    return torch.from_numpy(ctx), torch.from_numpy(ctx_len), torch.from_numpy(excl)
