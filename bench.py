@@ -141,6 +141,7 @@ def main():
                                    n_valid=N)
         Qs.append(q.contiguous())
         anchors.append(workloads.anchors(wp, src).to(dev))
+    last_src = src
     rule = oil.DepthRule.fixed(L)
     mx = 1 + sem_budget
     out_s = torch.empty((B, k), dtype=torch.float32, device=dev)
@@ -201,6 +202,18 @@ def main():
         e1.record()
         torch.cuda.synchronize()
         extras[name] = round(1e3 * e0.elapsed_time(e1) / K, 2)
+    # the exact-suffix lexical source on the same pool's tokens, for the last
+    # step's requests (16-token contexts, 4 drafts of up to 12 tokens)
+    lctx, lcl, lex_ex = (t.to(dev) for t in workloads.lexical_contexts(wp, last_src, len(pool)))
+    lex_out = pool.lexical(lctx, lcl, 4, 12, lex_ex)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(K):
+        pool.lexical(lctx, lcl, 4, 12, lex_ex, out=lex_out)
+    e1.record()
+    torch.cuda.synchronize()
+    extras["lexical_us"] = round(1e3 * e0.elapsed_time(e1) / K, 2)
+    extras["mean_lexical_drafts"] = round(float((lex_out[1] > 0).float().sum(1).mean()), 2)
     extras["mean_tree_nodes"] = round(float(tree[3].float().mean()), 2)
     extras["mean_accepted"] = round(float(walk_out[0].float().mean()), 2)
 

@@ -55,6 +55,13 @@ enum { OIL_F32 = 0, OIL_BF16 = 1 };
 #define OIL_MAX_NODES 256
 #define OIL_MAX_BANDS 4
 
+/* Limits of the exact-suffix lexical source: context tokens, drafts per
+ * request, tokens per draft, and the candidate capacity per request. */
+#define OIL_LEX_MAX_CTX 32
+#define OIL_LEX_MAX_N 16
+#define OIL_LEX_MAX_LEN 64
+#define OIL_LEX_MAX_CAND 4096
+
 /* Padded key width, in bf16 elements: `dim` rounded up to a multiple of 64.
  * The padding columns are kept zero by the library, so they never change a
  * dot product. */
@@ -158,6 +165,45 @@ typedef struct {
 int32_t oil_gather_continuations(const oil_pool *pool, const int32_t *idx, const float *scores,
                                  int32_t B, int32_t k, const oil_depth_rule *rule, int32_t L,
                                  int32_t *chain_tokens, int32_t *chain_len, void *stream);
+
+/* Workspace bytes oil_lexical_drafts needs for B requests with candidate
+ * capacity max_cand (sized from the pool's capacity). */
+size_t oil_lexical_workspace_bytes(const oil_pool *pool, int32_t B, int32_t max_cand);
+
+/* Exact-suffix lexical drafts over the pool's tokens: the lexical key of
+ * Sec. 2 (the longest suffix of the context that recurs verbatim, backing off
+ * to shorter suffixes, proposing what followed the matches), with the
+ * exact-match drafter's knobs of Sec. 3 (suffixes up to the context length,
+ * back off until n_lex distinct candidates are held, minimum key length).
+ * These are the lexical drafts oil_tree_merge takes.  For request b with
+ * context c = the last cl = min(ctx_len[b], C) tokens of row b:
+ *   1. position p matches to length m(p): the largest m <= cl with
+ *      x[p-j] = c[cl-1-j] for all j < m, positions p-m+1 .. p in one trace;
+ *   2. p is a candidate when m(p) >= min_match, its prompt id differs from
+ *      exclude_prompt[b] (Sec. 4 (i)) and x[p+1] exists in p's trace; its
+ *      draft is x[p+1 .. p+L_lex], clipped at the end of its trace and pool;
+ *   3. with n(m) the number of candidates matching to length >= m and m* the
+ *      longest match, back-off visits m = m*, m*-1, ... while
+ *      n(m) <= max_cand; if n(m*) > max_cand only m* is visited, over its
+ *      max_cand earliest candidates (a bound of this index, not the paper's);
+ *   4. at each visited level the distinct drafts of the candidates matching
+ *      to >= that length that are not yet held are ranked by how many of those
+ *      candidates give them (more first), then by earliest position, and
+ *      taken in that order until n_lex are held.
+ *   ctx        B x C int32, right-aligned (the most recent token last).
+ *   ctx_len    B int32 (negative counts as 0).   C  1 .. OIL_LEX_MAX_CTX.
+ *   exclude_prompt  B int32 or NULL; negative excludes nothing.  Requires a
+ *              pool created with a prompt buffer when not NULL.
+ *   B 1 .. OIL_MAX_B.  n_lex 1 .. OIL_LEX_MAX_N.  L_lex 1 .. OIL_LEX_MAX_LEN.
+ *   min_match  1 .. OIL_LEX_MAX_CTX.   max_cand  1 .. OIL_LEX_MAX_CAND.
+ *   workspace  >= oil_lexical_workspace_bytes(pool, B, max_cand), 256-byte aligned.
+ *   lex_tokens B x n_lex x L_lex int32 in pick order, -1 padded;
+ *   lex_len    B x n_lex int32, 0 for unused slots. */
+int32_t oil_lexical_drafts(const oil_pool *pool, const int32_t *ctx, const int32_t *ctx_len, int32_t C,
+                           int32_t B, const int32_t *exclude_prompt, int32_t n_lex, int32_t L_lex,
+                           int32_t min_match, int32_t max_cand, void *workspace,
+                           size_t workspace_bytes, int32_t *lex_tokens, int32_t *lex_len,
+                           void *stream);
 
 /* Root-first merge (Sec. 4 (iii), Eq. 4; BuildLexical then MergeFromRoot in
  * Algorithm 1).  Per query: node 0 is the root (token anchor[b], parent -1,

@@ -603,30 +603,31 @@ int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32
         }
         int32_t n_picked = 0;
         for (int32_t m = mtop; m >= m_lo && n_picked < n_lex; m--) {
+            /* per group: candidates matching to >= m, and the earliest of them */
+            for (int64_t g = 0; g < nc; g++) {
+                lev[g].count = 0;
+                lev[g].p = -1;
+                lev[g].group = g;
+            }
+            for (int64_t i = 0; i < nc; i++) {
+                if (mlen[i] < m)
+                    continue;
+                orc_level_entry *e = &lev[group[i]];
+                e->count++;
+                if (e->p < 0)
+                    e->p = cand[i]; /* candidates are in position order */
+            }
+            /* keep the groups present at this level and not yet held */
             int64_t ne = 0;
             for (int64_t g = 0; g < nc; g++) {
-                if (group[g] != g)
+                if (lev[g].count == 0)
                     continue;
                 int already = 0;
                 for (int32_t t = 0; t < n_picked; t++)
                     if (picked[t] == g)
                         already = 1;
-                if (already)
-                    continue;
-                int64_t cnt = 0, first = -1;
-                for (int64_t i = 0; i < nc; i++) {
-                    if (group[i] == g && mlen[i] >= m) {
-                        cnt++;
-                        if (first < 0)
-                            first = cand[i];
-                    }
-                }
-                if (cnt == 0)
-                    continue;
-                lev[ne].p = first;
-                lev[ne].count = cnt;
-                lev[ne].group = g;
-                ne++;
+                if (!already)
+                    lev[ne++] = lev[g];
             }
             qsort(lev, (size_t)ne, sizeof(orc_level_entry), level_cmp);
             for (int64_t e = 0; e < ne && n_picked < n_lex; e++) {

@@ -25,6 +25,7 @@ LIB_PATH = os.path.join(_HERE, "liboilbird.so")
 
 OIL_F32, OIL_BF16 = 0, 1
 MAX_K, MAX_B, MAX_NODES, MAX_BANDS = 64, 512, 256, 4
+LEX_MAX_CTX, LEX_MAX_N, LEX_MAX_LEN, LEX_MAX_CAND = 32, 16, 64, 4096
 
 _lib = None
 
@@ -87,6 +88,8 @@ def lib():
                                      P, P, P]),
             "oil_status_string": (ctypes.c_char_p, [i32]),
             "oil_tree_mask": (i32, [i32, i32, P, P, P, P]),
+            "oil_lexical_workspace_bytes": (sz, [P, i32, i32]),
+            "oil_lexical_drafts": (i32, [P, P, P, i32, i32, P, i32, i32, i32, i32, P, sz, P, P, P]),
             "oil_accept_walk": (i32, [i32, i32, P, P, P, P, P, P, P, P]),
             "oil_scan_timer_start": (i32, [i32]),
             "oil_scan_timer_stop": (i32, [ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]),
@@ -179,6 +182,20 @@ def pool_query_topk(handle, queries, k, workspace, scores, idx, exclude_prompt=N
         _ptr(None if exclude_prompt is None else _i32(exclude_prompt, "exclude_prompt")),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(scores),
         _ptr(_i32(idx, "idx")), _stream(stream)))
+
+
+def lexical_workspace_bytes(handle, B, max_cand) -> int:
+    return lib().oil_lexical_workspace_bytes(handle, B, max_cand)
+
+
+def lexical_drafts(handle, ctx, ctx_len, n_lex, L_lex, workspace, lex_tokens, lex_len,
+                   exclude_prompt=None, min_match=2, max_cand=LEX_MAX_CAND, stream=None):
+    B, C = ctx.shape
+    _check("oil_lexical_drafts", lib().oil_lexical_drafts(
+        handle, _ptr(_i32(ctx, "ctx")), _ptr(_i32(ctx_len, "ctx_len")), C, B,
+        _ptr(None if exclude_prompt is None else _i32(exclude_prompt, "exclude_prompt")), n_lex,
+        L_lex, min_match, max_cand, _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _ptr(_i32(lex_tokens, "lex_tokens")), _ptr(_i32(lex_len, "lex_len")), _stream(stream)))
 
 
 def gather_continuations(handle, idx, scores, rule: DepthRule, L, chain_tokens, chain_len,
@@ -292,6 +309,26 @@ class Pool:
         pool_query_topk(self.handle, queries, k, self.workspace(B, k), scores, idx,
                         exclude_prompt, stream)
         return scores, idx
+
+    def lexical(self, ctx, ctx_len, n_lex, L_lex, exclude_prompt=None, min_match=2,
+                max_cand=None, stream=None, out=None):
+        """Exact-suffix lexical drafts: (tokens (B, n_lex, L_lex), lengths (B, n_lex))."""
+        B = ctx.shape[0]
+        max_cand = LEX_MAX_CAND if max_cand is None else max_cand
+        key = ("lex", B, max_cand)
+        if key not in self._ws:
+            nb = lexical_workspace_bytes(self.handle, B, max_cand)
+            if nb == 0:
+                raise ValueError(f"unsupported lexical batch/capacity: B={B} max_cand={max_cand}")
+            self._ws[key] = torch.empty((nb,), dtype=torch.uint8, device=self.device)
+        if out is None:
+            lt = torch.empty((B, n_lex, L_lex), dtype=torch.int32, device=self.device)
+            ll = torch.empty((B, n_lex), dtype=torch.int32, device=self.device)
+        else:
+            lt, ll = out
+        lexical_drafts(self.handle, ctx, ctx_len, n_lex, L_lex, self._ws[key], lt, ll,
+                       exclude_prompt, min_match, max_cand, stream)
+        return lt, ll
 
     def gather(self, idx, scores, rule: DepthRule, L, stream=None, out=None):
         B, k = idx.shape

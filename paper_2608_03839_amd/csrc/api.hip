@@ -12,6 +12,9 @@
 static_assert(OIL_MAX_K == OIL_TOPK_MAX, "top-k capacity");
 static_assert(OIL_MAX_NODES == OIL_NODES_MAX, "tree capacity");
 static_assert(OIL_MAX_BANDS == OIL_BANDS_MAX, "band table");
+static_assert(OIL_LEX_MAX_CTX == OIL_LEX_CTX_MAX && OIL_LEX_MAX_N == OIL_LEX_N_MAX &&
+                  OIL_LEX_MAX_LEN == OIL_LEX_LEN_MAX && OIL_LEX_MAX_CAND == OIL_LEX_CAND_MAX,
+              "lexical limits");
 
 struct oil_pool {
     int32_t dim, ld;
@@ -266,6 +269,35 @@ int32_t oil_gather_continuations(const oil_pool* pool, const int32_t* idx, const
     }
     return hip_status(oil::launch_gather(pool->tokens, pool->traces, pool->n_valid, idx, scores, B, k,
                                          r, L, chain_tokens, chain_len, (hipStream_t)stream));
+}
+
+size_t oil_lexical_workspace_bytes(const oil_pool* pool, int32_t B, int32_t max_cand)
+{
+    if (!pool || B < 1 || B > OIL_MAX_B || max_cand < 1 || max_cand > OIL_LEX_MAX_CAND)
+        return 0;
+    return oil::lexical_workspace_bytes(pool->capacity, B, max_cand);
+}
+
+int32_t oil_lexical_drafts(const oil_pool* pool, const int32_t* ctx, const int32_t* ctx_len, int32_t C,
+                           int32_t B, const int32_t* exclude_prompt, int32_t n_lex, int32_t L_lex,
+                           int32_t min_match, int32_t max_cand, void* workspace,
+                           size_t workspace_bytes, int32_t* lex_tokens, int32_t* lex_len, void* stream)
+{
+    if (!pool || !ctx || !ctx_len || !lex_tokens || !lex_len || C < 1 || B < 1 || n_lex < 1 ||
+        L_lex < 1 || min_match < 1 || max_cand < 1)
+        return OIL_E_INVALID;
+    if (exclude_prompt && !pool->prompts)
+        return OIL_E_INVALID;
+    if (C > OIL_LEX_MAX_CTX || B > OIL_MAX_B || n_lex > OIL_LEX_MAX_N || L_lex > OIL_LEX_MAX_LEN ||
+        min_match > OIL_LEX_MAX_CTX || max_cand > OIL_LEX_MAX_CAND)
+        return OIL_E_UNSUPPORTED;
+    if (!workspace || workspace_bytes < oil::lexical_workspace_bytes(pool->capacity, B, max_cand) ||
+        !aligned(workspace, kAlign))
+        return OIL_E_WORKSPACE;
+    return hip_status(oil::launch_lexical(pool->tokens, pool->traces, pool->prompts, pool->n_valid, ctx,
+                                          ctx_len, C, B, exclude_prompt, n_lex, L_lex, min_match,
+                                          max_cand, workspace, pool->capacity, lex_tokens, lex_len,
+                                          (hipStream_t)stream));
 }
 
 int32_t oil_tree_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,

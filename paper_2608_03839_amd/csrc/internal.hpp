@@ -8,6 +8,10 @@
 #define OIL_TOPK_MAX 64
 #define OIL_NODES_MAX 256
 #define OIL_BANDS_MAX 4
+#define OIL_LEX_CTX_MAX 32
+#define OIL_LEX_N_MAX 16
+#define OIL_LEX_LEN_MAX 64
+#define OIL_LEX_CAND_MAX 4096
 
 namespace oil {
 
@@ -64,6 +68,12 @@ hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tok
 
 hipError_t launch_tree_mask(int32_t B, int32_t max_nodes, const int32_t* node_parent,
                             const int32_t* n_nodes, uint32_t* mask, hipStream_t stream);
+size_t lexical_workspace_bytes(int64_t capacity, int32_t B, int32_t max_cand);
+hipError_t launch_lexical(const int32_t* tokens, const int32_t* traces, const int32_t* prompts,
+                          int64_t n_valid, const int32_t* ctx, const int32_t* ctx_len, int32_t C,
+                          int32_t B, const int32_t* exclude, int32_t n_lex, int32_t L_lex,
+                          int32_t min_match, int32_t max_cand, void* workspace, int64_t capacity,
+                          int32_t* lex_tokens, int32_t* lex_len, hipStream_t stream);
 hipError_t launch_accept_walk(int32_t B, int32_t max_nodes, const int32_t* node_token,
                               const int32_t* node_parent, const int32_t* n_nodes, const int32_t* target,
                               int32_t* accept_len, int32_t* accept_nodes, int32_t* bonus,

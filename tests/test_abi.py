@@ -124,3 +124,45 @@ def test_verify_validates(L):
 def test_status_strings(L):
     for s in (0, -1, -2, -3, -4, -5, 99):
         assert isinstance(L.oil_status_string(s), bytes)
+
+
+def test_lexical_validates(L):
+    f = _FakeBufs()
+    h = ctypes.c_void_p()
+    P = f.aligned
+    assert L.oil_pool_create(16, 10000, P, P, P, None, ctypes.byref(h)) == 0
+    assert L.oil_lexical_workspace_bytes(h, 0, 64) == 0
+    assert L.oil_lexical_workspace_bytes(h, 513, 64) == 0
+    assert L.oil_lexical_workspace_bytes(h, 4, 0) == 0
+    assert L.oil_lexical_workspace_bytes(h, 4, 4097) == 0
+    ws = L.oil_lexical_workspace_bytes(h, 4, 64)
+    assert ws > 0 and ws % 256 == 0
+    assert L.oil_lexical_workspace_bytes(h, 4, 4096) > ws
+    # (pool, ctx, ctx_len, C, B, exclude, n_lex, L_lex, min_match, max_cand, ws, ws_bytes, tok, len, stream)
+    ok = (h, P, P, 16, 4, None, 4, 12, 2, 64, P, ws, P, P, None)
+
+    def call(**kw):
+        names = ["pool", "ctx", "ctx_len", "C", "B", "exclude", "n_lex", "L_lex", "min_match",
+                 "max_cand", "ws", "ws_bytes", "tok", "len", "stream"]
+        a = dict(zip(names, ok))
+        a.update(kw)
+        return L.oil_lexical_drafts(*[a[n] for n in names])
+
+    assert call(ctx=None) == -1
+    assert call(C=0) == -1
+    assert call(B=0) == -1
+    assert call(n_lex=0) == -1
+    assert call(L_lex=0) == -1
+    assert call(min_match=0) == -1
+    assert call(max_cand=0) == -1
+    assert call(exclude=P) == -1                 # pool without a prompt buffer
+    assert call(C=33) == -3
+    assert call(B=513) == -3
+    assert call(n_lex=17) == -3
+    assert call(L_lex=65) == -3
+    assert call(min_match=33) == -3
+    assert call(max_cand=4097) == -3
+    assert call(ws_bytes=ws - 1) == -5
+    assert call(ws=f.misaligned) == -5
+    assert call(ws=None) == -5
+    assert L.oil_pool_destroy(h) == 0

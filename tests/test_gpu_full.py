@@ -154,7 +154,8 @@ def test_stream_5120_checkpoints(oil):
 
 def test_full_step_8192(oil):
     """N = 524,288, d = 8,192 bf16, B = 64, k = 32 chains of 12 merged with
-    4 exact-suffix lexical drafts per query under 48 + 16 nodes."""
+    4 exact-suffix lexical drafts per query (GPU lexical source) under 48 + 16
+    nodes: the whole draft step on the device."""
     cfg = workloads.FULL_STEP_8192
     ps, qs, k, L = cfg["pool"], cfg["query"], cfg["k"], cfg["L"]
     n_lex, L_lex, lb, sb = cfg["n_lex"], cfg["L_lex"], cfg["lex_budget"], cfg["sem_budget"]
@@ -165,10 +166,14 @@ def test_full_step_8192(oil):
     orc = StreamedOracle(_bits(q[sample]), ps.n)
     pool = oil.Pool(ps.d, ps.n, device=dev)
     _fill(pool, wp, 0, ps.n, dev, [orc])
+    # the lexical drafts come from the GPU lexical source and must equal the oracle's
     ctx, ctx_len, excl = workloads.lexical_contexts(wp, src, ps.n)
-    lt, ll = (torch.from_numpy(a) for a in oracle.lexical_drafts(
-        wp.tokens.numpy(), wp.traces.numpy(), wp.prompts.numpy(), ps.n, ctx.numpy(), ctx_len.numpy(),
-        n_lex, L_lex, excl.numpy()))
+    glt, gll = pool.lexical(ctx.to(dev), ctx_len.to(dev), n_lex, L_lex, excl.to(dev))
+    elt, ell = oracle.lexical_drafts(wp.tokens.numpy(), wp.traces.numpy(), wp.prompts.numpy(), ps.n,
+                                     ctx.numpy(), ctx_len.numpy(), n_lex, L_lex, excl.numpy())
+    torch.cuda.synchronize()
+    assert np.array_equal(gll.cpu().numpy(), ell) and np.array_equal(glt.cpu().numpy(), elt)
+    lt, ll = glt.cpu(), gll.cpu()
     anchor = workloads.anchors(wp, src)
     rule_g, rule_o = oil.DepthRule.fixed(L), oracle.fixed_rule(L)
     mx = 1 + lb + sb
