@@ -35,8 +35,10 @@ constexpr int kLexPerThread = 16;
 constexpr int kLexChunk = kLexThreads * kLexPerThread;  // positions per workgroup
 constexpr int kLexGroup = 64;                           // requests per workgroup
 constexpr int kLexLevels = OIL_LEX_CTX_MAX + 1;         // match lengths 0 .. 32
+constexpr int kLexHistLd = 36;                          // histogram row stride (16-byte rows)
 constexpr int kLexTable = 256;                          // last-token table slots (>= 4 x kLexGroup)
 constexpr int kLexWords = kLexChunk / 32;               // bitmap words per request
+constexpr int kLexList = 2048;                          // kept candidates a chunk records in LDS
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelPer = OIL_LEX_CAND_MAX / kSelThreads;
@@ -69,18 +71,29 @@ __device__ void lex_stage(LexScanShared& s, const int32_t* __restrict__ ctx,
                           const int32_t* __restrict__ exclude, int32_t min_match)
 {
     const int t = threadIdx.x;
-    for (int e = t; e < kLexGroup * OIL_LEX_CTX_MAX; e += kLexThreads) {
-        const int g = e / OIL_LEX_CTX_MAX, j = e % OIL_LEX_CTX_MAX;
-        s.rc[g][j] = (g < G && j < C) ? ctx[(int64_t)(g0 + g) * C + (C - 1 - j)] : -1;
+    // every load first, then every LDS store: one memory latency in all
+    constexpr int kIters = kLexGroup * OIL_LEX_CTX_MAX / kLexThreads;
+    int32_t v[kIters];
+#pragma unroll
+    for (int r = 0; r < kIters; r++) {
+        const int e = t + r * kLexThreads, g = e / OIL_LEX_CTX_MAX, j = e % OIL_LEX_CTX_MAX;
+        const bool in = g < G && j < C;
+        const int32_t x = ctx[in ? (int64_t)(g0 + g) * C + (C - 1 - j) : 0];  // clamped, unconditional
+        v[r] = in ? x : -1;
+    }
+    const int tq = t < G ? t : 0;
+    int c = ctx_len[g0 + tq], x = exclude ? exclude[g0 + tq] : -1;
+    if (t >= G) {
+        c = 0;
+        x = -1;
+    }
+#pragma unroll
+    for (int r = 0; r < kIters; r++) {
+        const int e = t + r * kLexThreads;
+        s.rc[e / OIL_LEX_CTX_MAX][e % OIL_LEX_CTX_MAX] = v[r];
     }
     if (t < kLexGroup) {
-        int c = 0, x = -1;
-        if (t < G) {
-            c = ctx_len[g0 + t];
-            c = c < 0 ? 0 : (c > C ? C : c);
-            x = exclude ? exclude[g0 + t] : -1;
-        }
-        s.cl[t] = c;
+        s.cl[t] = c < 0 ? 0 : (c > C ? C : c);
         s.ex[t] = x;
     }
     for (int e = t; e < kLexTable; e += kLexThreads) {
@@ -119,21 +132,43 @@ __device__ inline uint64_t lex_lookup(const LexScanShared& s, int32_t v)
 }
 
 // Match length of position p for request g (its last token already equal),
-// or 0 when p is not a candidate (short match, excluded prompt, no continuation).
+// or 0 when p is not a candidate (short match, excluded prompt, no
+// continuation).  The walk back loads 16 positions at a time with independent
+// loads, so a long match costs one memory latency per 16 tokens.
 __device__ inline int lex_candidate(const LexScanShared& s, int g, int64_t p, int64_t n_valid,
                                     const int32_t* __restrict__ tokens, const int32_t* __restrict__ traces,
                                     const int32_t* __restrict__ prompts, int32_t min_match)
 {
+    // Every load below is unconditional at a clamped (always valid) address
+    // and its validity is applied afterwards, so the compiler issues them
+    // back to back instead of waiting on each one.
     const int cl = s.cl[g];
     const int32_t trp = traces[p];
+    const int32_t tr_next = traces[p + 1 < n_valid ? p + 1 : p];
+    const int32_t pr = prompts ? prompts[p] : -1;
     int m = 1;
-    while (m < cl && p - m >= 0 && tokens[p - m] == s.rc[g][m] && traces[p - m] == trp)
-        m++;
-    if (m < min_match)
+    for (int m0 = 1; m0 < cl; m0 += 16) {
+        int32_t tk[16], tr[16];
+#pragma unroll
+        for (int u = 0; u < 16; u++) {
+            const int64_t q = p - m0 - u;
+            const int64_t qc = q >= 0 ? q : 0;
+            tk[u] = tokens[qc];
+            tr[u] = traces[qc];
+        }
+#pragma unroll
+        for (int u = 0; u < 16; u++) {
+            const bool in = m0 + u < cl && p - m0 - u >= 0;
+            const int at = min(m0 + u, OIL_LEX_CTX_MAX - 1);
+            if (in && m == m0 + u && tr[u] == trp && tk[u] == s.rc[g][at])
+                m++;
+        }
+        if (m < m0 + 16)
+            break;
+    }
+    if (m < min_match || p + 1 >= n_valid || tr_next != trp)
         return 0;
-    if (p + 1 >= n_valid || traces[p + 1] != trp)
-        return 0;
-    if (s.ex[g] >= 0 && prompts[p] == s.ex[g])
+    if (s.ex[g] >= 0 && pr == s.ex[g])
         return 0;
     return m;
 }
@@ -149,14 +184,29 @@ __global__ __launch_bounds__(kLexThreads) void lex_hist_kernel(
     const int t = threadIdx.x, c = blockIdx.x;
     const int g0 = blockIdx.y * kLexGroup;
     const int G = min(kLexGroup, B - g0);
+    const int64_t base = (int64_t)c * kLexChunk;
+    int32_t tk[kLexPerThread];
+#pragma unroll
+    for (int j = 0; j < kLexPerThread; j++) {
+        const int64_t p = base + j * kLexThreads + t;
+        tk[j] = p < n_valid ? tokens[p] : 0;
+    }
     for (int e = t; e < kLexGroup * kLexLevels; e += kLexThreads)
         (&hist[0][0])[e] = 0;
     lex_stage(s, ctx, ctx_len, C, g0, G, exclude, min_match);
-    const int64_t base = (int64_t)c * kLexChunk;
+    // probe every prefetched token; walk only the (rare) hits, in a loop kept
+    // rolled so the walk is emitted once
+    uint32_t hits = 0u;
+#pragma unroll
     for (int j = 0; j < kLexPerThread; j++) {
         const int64_t p = base + j * kLexThreads + t;
-        if (p >= n_valid)
-            break;
+        if (p < n_valid && lex_lookup(s, tk[j]))
+            hits |= 1u << j;
+    }
+    while (hits) {
+        const int j = __ffs(hits) - 1;
+        hits &= hits - 1;
+        const int64_t p = base + j * kLexThreads + t;
         uint64_t mk = lex_lookup(s, tokens[p]);
         while (mk) {
             const int g = __ffsll((unsigned long long)mk) - 1;
@@ -167,14 +217,37 @@ __global__ __launch_bounds__(kLexThreads) void lex_hist_kernel(
         }
     }
     __syncthreads();
+    // chunk-major: H[b][c][m], one contiguous run of levels per request
     for (int e = t; e < G * kLexLevels; e += kLexThreads) {
         const int g = e / kLexLevels, m = e % kLexLevels;
-        H[((int64_t)(g0 + g) * n_chunks + c) * kLexLevels + m] = hist[g][m];
+        H[((int64_t)(g0 + g) * n_chunks + c) * kLexHistLd + m] = hist[g][m];
     }
 }
 
-// plan[b] = {m*, shortest visited level, kept candidates, 0}; off[b][c] = the
-// list index of chunk c's first kept candidate.
+// Chunk c's histogram row, levels below `from` (and chunks past the end) as 0:
+// nine unconditional 16-byte loads at a clamped row.
+__device__ inline void lex_hist_row(const int32_t* __restrict__ Hb, int c, int n_chunks, int from,
+                                    int32_t (&v)[kLexLevels])
+{
+    const int cc = c < n_chunks ? c : n_chunks - 1;
+    const int4* row = (const int4*)(Hb + (int64_t)cc * kLexHistLd);
+    int4 x[kLexHistLd / 4];
+#pragma unroll
+    for (int k = 0; k < kLexHistLd / 4; k++)
+        x[k] = row[k];
+#pragma unroll
+    for (int k = 0; k < kLexHistLd / 4; k++) {
+        const int32_t e[4] = {x[k].x, x[k].y, x[k].z, x[k].w};
+#pragma unroll
+        for (int u = 0; u < 4; u++)
+            if (4 * k + u < kLexLevels)
+                v[4 * k + u] = (c < n_chunks && 4 * k + u >= from) ? e[u] : 0;
+    }
+}
+
+// plan[b] = {m*, shortest visited level, kept candidates, mask of visited
+// levels holding candidates (bit m - 1)}; off[b][c] = the list index of chunk
+// c's first kept candidate, off[b][n_chunks] = the number kept.
 __global__ __launch_bounds__(kLexThreads) void lex_plan_kernel(const int32_t* __restrict__ H,
                                                                int32_t n_chunks, int32_t min_match,
                                                                int32_t max_cand, int32_t* __restrict__ off,
@@ -187,12 +260,17 @@ __global__ __launch_bounds__(kLexThreads) void lex_plan_kernel(const int32_t* __
     if (t < kLexLevels)
         n_at[t] = 0;
     __syncthreads();
-    const int32_t* Hb = H + (int64_t)b * n_chunks * kLexLevels;
-    const int64_t n_e = (int64_t)n_chunks * kLexLevels;
-    for (int64_t e = t; e < n_e; e += kLexThreads) {
-        const int32_t v = Hb[e];
-        if (v)
-            atomicAdd(&n_at[e % kLexLevels], v);
+    const int32_t* Hb = H + (int64_t)b * n_chunks * kLexHistLd;
+    // level totals: most entries are zero, so each thread adds its nonzero
+    // ones straight into LDS (no wave reductions)
+    int32_t v[kLexLevels];
+    for (int c0 = 0; c0 < n_chunks; c0 += kLexThreads) {
+        const int c = c0 + t;
+        lex_hist_row(Hb, c, n_chunks, min_match, v);
+#pragma unroll
+        for (int m = 0; m < kLexLevels; m++)
+            if (v[m])
+                atomicAdd(&n_at[m], v[m]);
     }
     __syncthreads();
     int32_t top = 0;
@@ -219,13 +297,17 @@ __global__ __launch_bounds__(kLexThreads) void lex_plan_kernel(const int32_t* __
     }
     __syncthreads();
     const int32_t lo = s_lo;
+    int32_t* ob = off + (int64_t)b * (n_chunks + 1);
     int64_t carry = 0;
     for (int c0 = 0; c0 < n_chunks; c0 += kLexThreads) {
         const int c = c0 + t;
+        if (n_chunks > kLexThreads) {  // the registers hold the last tile only
+            lex_hist_row(Hb, c, n_chunks, lo, v);
+        }
         int32_t cnt = 0;
-        if (c < n_chunks)
-            for (int m = lo; m < kLexLevels; m++)
-                cnt += Hb[(int64_t)c * kLexLevels + m];
+#pragma unroll
+        for (int m = 0; m < kLexLevels; m++)
+            cnt += m >= lo ? v[m] : 0;
         int32_t incl = cnt;
 #pragma unroll
         for (int o = 1; o < kWave; o <<= 1) {
@@ -237,23 +319,30 @@ __global__ __launch_bounds__(kLexThreads) void lex_plan_kernel(const int32_t* __
             wsum[w] = incl;
         __syncthreads();
         int64_t before = carry, total = carry;
-        for (int v = 0; v < kLexThreads / kWave; v++) {
-            if (v < w)
-                before += wsum[v];
-            total += wsum[v];
+        for (int q = 0; q < kLexThreads / kWave; q++) {
+            if (q < w)
+                before += wsum[q];
+            total += wsum[q];
         }
         if (c < n_chunks) {
             const int64_t o = before + incl - cnt;
-            off[(int64_t)b * n_chunks + c] = (int32_t)(o < max_cand ? o : max_cand);
+            ob[c] = (int32_t)(o < max_cand ? o : max_cand);
         }
         carry = total;
         __syncthreads();  // wsum is rewritten by the next tile
     }
     if (t == 0) {
+        const int32_t kept = (int32_t)(carry < max_cand ? carry : max_cand);
+        ob[n_chunks] = kept;
         plan[4 * b + 0] = top;
         plan[4 * b + 1] = lo;
-        plan[4 * b + 2] = (int32_t)(carry < max_cand ? carry : max_cand);
-        plan[4 * b + 3] = 0;
+        plan[4 * b + 2] = kept;
+        // levels that bring new candidates: the others change no group's count
+        uint32_t levels = 0u;
+        for (int m = lo; m <= top && m < kLexLevels; m++)
+            if (n_at[m] > 0)
+                levels |= 1u << (m - 1);
+        plan[4 * b + 3] = (int32_t)levels;
     }
 }
 
@@ -267,28 +356,59 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
     __shared__ LexScanShared s;
     __shared__ uint32_t bm[kLexGroup][kLexWords];
     __shared__ uint16_t wpre[kLexGroup][kLexWords];
+    __shared__ uint32_t list[kLexList];  // (chunk offset << 12) | (request << 6) | match length
+    __shared__ int32_t n_list;
     const int t = threadIdx.x, c = blockIdx.x, lane = t & (kWave - 1);
     const int g0 = blockIdx.y * kLexGroup;
     const int G = min(kLexGroup, B - g0);
+    int32_t tk[kLexPerThread];
+#pragma unroll
+    for (int j = 0; j < kLexPerThread; j++) {
+        const int64_t p = (int64_t)c * kLexChunk + j * kLexThreads + t;
+        tk[j] = p < n_valid ? tokens[p] : 0;
+    }
     for (int e = t; e < kLexGroup * kLexWords; e += kLexThreads)
         (&bm[0][0])[e] = 0u;
+    int32_t lo_t = kLexLevels;
+    bool busy = false;
+    if (t < G) {
+        const int32_t* ob = off + (int64_t)(g0 + t) * (n_chunks + 1);
+        lo_t = plan[4 * (g0 + t) + 1];
+        busy = ob[c + 1] > ob[c];
+    }
+    // a chunk where no request keeps a candidate has nothing to write
+    if (!__syncthreads_or(busy))
+        return;
     lex_stage(s, ctx, ctx_len, C, g0, G, exclude, min_match);
-    if (t < G)
-        s.lo[t] = plan[4 * (g0 + t) + 1];
+    if (t < kLexGroup)
+        s.lo[t] = lo_t;
+    if (t == 0)
+        n_list = 0;
     __syncthreads();
     const int64_t base = (int64_t)c * kLexChunk;
+    uint32_t hits = 0u;
+#pragma unroll
     for (int j = 0; j < kLexPerThread; j++) {
+        const int64_t p = base + j * kLexThreads + t;
+        if (p < n_valid && lex_lookup(s, tk[j]))
+            hits |= 1u << j;
+    }
+    for (uint32_t hh = hits; hh;) {
+        const int j = __ffs(hh) - 1;
+        hh &= hh - 1;
         const int q = j * kLexThreads + t;
         const int64_t p = base + q;
-        if (p >= n_valid)
-            break;
         uint64_t mk = lex_lookup(s, tokens[p]);
         while (mk) {
             const int g = __ffsll((unsigned long long)mk) - 1;
             mk &= mk - 1;
             const int m = lex_candidate(s, g, p, n_valid, tokens, traces, prompts, min_match);
-            if (m && m >= s.lo[g])
+            if (m && m >= s.lo[g]) {
                 atomicOr(&bm[g][q >> 5], 1u << (q & 31));
+                const int at = atomicAdd(&n_list, 1);
+                if (at < kLexList)
+                    list[at] = ((uint32_t)q << 12) | ((uint32_t)g << 6) | (uint32_t)m;
+            }
         }
     }
     __syncthreads();
@@ -310,11 +430,28 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
         }
     }
     __syncthreads();
-    for (int j = 0; j < kLexPerThread; j++) {
+    const int n_rec = n_list;
+    if (n_rec <= kLexList) {
+        // every kept candidate was recorded with its match length: no second walk
+        for (int e = t; e < n_rec; e += kLexThreads) {
+            const uint32_t r = list[e];
+            const int q = (int)(r >> 12), g = (int)((r >> 6) & 63u), m = (int)(r & 63u);
+            const uint32_t word = bm[g][q >> 5];
+            const int64_t at = (int64_t)off[(int64_t)(g0 + g) * (n_chunks + 1) + c] + wpre[g][q >> 5] +
+                               __popc(word & ((1u << (q & 31)) - 1u));
+            if (at < max_cand) {
+                cand_p[(int64_t)(g0 + g) * max_cand + at] = (int32_t)(base + q);
+                cand_m[(int64_t)(g0 + g) * max_cand + at] = m;
+            }
+        }
+        return;
+    }
+    // more kept candidates than the list holds: walk again
+    for (uint32_t hh = hits; hh;) {
+        const int j = __ffs(hh) - 1;
+        hh &= hh - 1;
         const int q = j * kLexThreads + t;
         const int64_t p = base + q;
-        if (p >= n_valid)
-            break;
         uint64_t mk = lex_lookup(s, tokens[p]);
         while (mk) {
             const int g = __ffsll((unsigned long long)mk) - 1;
@@ -323,7 +460,7 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
             if (!((word >> (q & 31)) & 1u))
                 continue;
             const int m = lex_candidate(s, g, p, n_valid, tokens, traces, prompts, min_match);
-            const int64_t at = (int64_t)off[(int64_t)(g0 + g) * n_chunks + c] + wpre[g][q >> 5] +
+            const int64_t at = (int64_t)off[(int64_t)(g0 + g) * (n_chunks + 1) + c] + wpre[g][q >> 5] +
                                __popc(word & ((1u << (q & 31)) - 1u));
             if (at < max_cand) {
                 cand_p[(int64_t)(g0 + g) * max_cand + at] = (int32_t)p;
@@ -333,42 +470,52 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
     }
 }
 
-__device__ inline int lex_draft_len(const int32_t* __restrict__ traces, int64_t n_valid, int64_t p,
-                                    int32_t L_lex)
+// Length (clipped at L_lex, the end of p's trace and the pool) and a 32-bit
+// hash of the draft x[p+1 ..], read 16 tokens at a time with independent loads.
+__device__ inline uint32_t lex_draft(const int32_t* __restrict__ tokens, const int32_t* __restrict__ traces,
+                                     int64_t n_valid, int64_t p, int32_t L_lex, int& len_out)
 {
     const int32_t trp = traces[p];
+    uint32_t h = 0x811C9DC5u;  // FNV-1a over the tokens
     int len = 0;
-    while (len < L_lex && p + 1 + len < n_valid && traces[p + 1 + len] == trp)
-        len++;
-    return len;
-}
-
-__device__ inline uint32_t lex_draft_hash(const int32_t* __restrict__ tokens, int64_t p, int len)
-{
-    // FNV-1a over the draft's tokens, seeded with its length, then finalised
-    uint32_t h = 0x811C9DC5u ^ ((uint32_t)len * 0x9E3779B9u);
-    for (int j = 1; j <= len; j++)
-        h = (h ^ (uint32_t)tokens[p + j]) * 0x01000193u;
-    h = mix32(h);
+    bool open = true;
+    for (int j0 = 0; j0 < L_lex && open; j0 += 16) {
+        int32_t tk[16], tr[16];
+#pragma unroll
+        for (int u = 0; u < 16; u++) {  // unconditional loads at clamped addresses
+            const int64_t q = p + 1 + j0 + u;
+            const int64_t qc = q < n_valid ? q : n_valid - 1;
+            tk[u] = tokens[qc];
+            tr[u] = traces[qc];
+        }
+#pragma unroll
+        for (int u = 0; u < 16; u++) {
+            open = open && j0 + u < L_lex && p + 1 + j0 + u < n_valid && tr[u] == trp;
+            if (open) {
+                h = (h ^ (uint32_t)tk[u]) * 0x01000193u;
+                len++;
+            }
+        }
+    }
+    len_out = len;
+    h = mix32(h ^ ((uint32_t)len * 0x9E3779B9u));
     return h ? h : 1u;  // 0 marks an empty slot
 }
 
+// Do the drafts after p and q (both of length len >= 1) hold the same tokens?
 __device__ inline bool lex_same_draft(const int32_t* __restrict__ tokens, int64_t p, int64_t q, int len)
 {
-    for (int j = 1; j <= len; j++)
-        if (tokens[p + j] != tokens[q + j])
-            return false;
-    return true;
-}
-
-__device__ inline uint64_t wave_max_u64(uint64_t v)
-{
+    bool same = true;
+    for (int j0 = 0; j0 < len && same; j0 += 16) {
+        bool blk = true;
 #pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint64_t u = __shfl_xor(v, o, kWave);
-        v = u > v ? u : v;
+        for (int u = 0; u < 16; u++) {
+            const int j = min(j0 + u, len - 1);  // in range: repeats the last token
+            blk &= tokens[p + 1 + j] == tokens[q + 1 + j];
+        }
+        same = blk;
     }
-    return v;
+    return same;
 }
 
 __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
@@ -381,9 +528,19 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
     __shared__ int32_t tab_first[kSelTable];
     __shared__ int32_t cnt[OIL_LEX_CAND_MAX];
     __shared__ int32_t first[OIL_LEX_CAND_MAX];
-    __shared__ uint64_t red[2][kSelThreads / kWave];
-    const int t = threadIdx.x, b = blockIdx.x, lane = t & (kWave - 1), w = t / kWave;
+    __shared__ uint8_t lens[OIL_LEX_CAND_MAX];
+    __shared__ int32_t pos[OIL_LEX_CAND_MAX];
+    __shared__ unsigned long long best_slot[3];
+    const int t = threadIdx.x, b = blockIdx.x;
     const int32_t top = plan[4 * b + 0], lo = plan[4 * b + 1], n = plan[4 * b + 2];
+    const uint32_t levels = (uint32_t)plan[4 * b + 3];
+    if (n == 0) {
+        for (int e = t; e < n_lex * L_lex; e += kSelThreads)
+            lex_tokens[(int64_t)b * n_lex * L_lex + e] = -1;
+        for (int e = t; e < n_lex; e += kSelThreads)
+            lex_len[(int64_t)b * n_lex + e] = 0;
+        return;
+    }
     const int32_t* cp = cand_p + (int64_t)b * max_cand;
     const int32_t* cm = cand_m + (int64_t)b * max_cand;
     for (int e = t; e < kSelTable; e += kSelThreads) {
@@ -394,6 +551,8 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
         cnt[e] = 0;
         first[e] = 0x7FFFFFFF;
     }
+    if (t < 3)
+        best_slot[t] = 0ull;
     int64_t p[kSelPer];
     int m[kSelPer], len[kSelPer], slot[kSelPer], rep[kSelPer];
     uint32_t h[kSelPer];
@@ -405,8 +564,9 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
         if (i < n) {
             p[r] = cp[i];
             m[r] = cm[i];
-            len[r] = lex_draft_len(traces, n_valid, p[r], L_lex);
-            h[r] = lex_draft_hash(tokens, p[r], len[r]);
+            h[r] = lex_draft(tokens, traces, n_valid, p[r], L_lex, len[r]);
+            lens[i] = (uint8_t)len[r];
+            pos[i] = (int32_t)p[r];
         } else {
             p[r] = -1;
             m[r] = 0;
@@ -441,24 +601,29 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
         const int j = tab_first[slot[r]];
         if (j == i) {
             rep[r] = i;
-        } else if (lex_draft_len(traces, n_valid, cp[j], L_lex) == len[r] &&
-                   lex_same_draft(tokens, p[r], cp[j], len[r])) {
+        } else if (lens[j] == len[r] && lex_same_draft(tokens, p[r], pos[j], len[r])) {
             rep[r] = j;
         } else {
             // a hash collision: the earliest candidate with the same draft
             rep[r] = i;
             for (int k = 0; k < i; k++) {
-                const int64_t pk = cp[k];
-                if (lex_draft_len(traces, n_valid, pk, L_lex) == len[r] &&
-                    lex_same_draft(tokens, p[r], pk, len[r])) {
+                if (lens[k] == len[r] && lex_same_draft(tokens, p[r], pos[k], len[r])) {
                     rep[r] = k;
                     break;
                 }
             }
         }
     }
-    int n_held = 0, par = 0;
+    // Picks: per round, the largest (count, earliest) key among groups not yet
+    // held, by a 64-bit LDS atomic max.  Round r uses slot r % 3 and clears
+    // slot (r + 2) % 3 after its barrier: every thread has read that slot (in
+    // round r - 1) before the barrier, and nobody writes it before round
+    // r + 2, which starts after the next barrier.
+    int n_held = 0, round = 0;
     for (int level = top; level >= lo && level > 0 && n_held < n_lex; level--) {
+        // a level without new candidates adds nothing the previous one lacked
+        if (!((levels >> (level - 1)) & 1u))
+            continue;
 #pragma unroll
         for (int r = 0; r < kSelPer; r++) {
             const int i = t + r * kSelThreads;
@@ -469,23 +634,23 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
         }
         __syncthreads();
         while (n_held < n_lex) {
-            uint64_t key[kSelPer], best = 0ull;
+            uint64_t key[kSelPer], mine = 0ull;
 #pragma unroll
             for (int r = 0; r < kSelPer; r++) {
                 const int i = t + r * kSelThreads;
                 key[r] = 0ull;
                 if (i < n && rep[r] == i && !held[r] && cnt[i] > 0)
                     key[r] = ((uint64_t)(uint32_t)cnt[i] << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)first[i]);
-                best = key[r] > best ? key[r] : best;
+                mine = key[r] > mine ? key[r] : mine;
             }
-            best = wave_max_u64(best);
-            if (lane == 0)
-                red[par][w] = best;
+            const int sl = round % 3;
+            if (mine)
+                atomicMax(&best_slot[sl], (unsigned long long)mine);
             __syncthreads();
-            best = 0ull;
-            for (int v = 0; v < kSelThreads / kWave; v++)
-                best = red[par][v] > best ? red[par][v] : best;
-            par ^= 1;
+            const uint64_t best = best_slot[sl];
+            if (t == 0)
+                best_slot[(round + 2) % 3] = 0ull;
+            round++;
             if (best == 0ull)
                 break;
 #pragma unroll
@@ -521,8 +686,8 @@ LexWorkspace lex_carve(int64_t capacity, int32_t B, int32_t max_cand)
     const size_t chunks = (size_t)(lex_chunks(capacity) > 0 ? lex_chunks(capacity) : 1);
     LexWorkspace w;
     w.h_off = 0;
-    w.o_off = align256(w.h_off + (size_t)B * chunks * kLexLevels * sizeof(int32_t));
-    w.plan_off = align256(w.o_off + (size_t)B * chunks * sizeof(int32_t));
+    w.o_off = align256(w.h_off + (size_t)B * chunks * kLexHistLd * sizeof(int32_t));
+    w.plan_off = align256(w.o_off + (size_t)B * (chunks + 1) * sizeof(int32_t));
     w.p_off = align256(w.plan_off + (size_t)B * 4 * sizeof(int32_t));
     w.m_off = align256(w.p_off + (size_t)B * max_cand * sizeof(int32_t));
     w.total = align256(w.m_off + (size_t)B * max_cand * sizeof(int32_t));
