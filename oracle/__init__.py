@@ -53,6 +53,9 @@ def _load():
         lib.orc_tree_merge.argtypes = [i32, P, P, P, i32, i32, i32, P, P, i32, i32, i32, i32,
                                        P, P, P, P]
         lib.orc_tree_mask.argtypes = [i32, i32, P, P, P]
+        lib.orc_recycle_records.argtypes = [i32, i32, P, P, P, P, P, P, i32, P, P, P, P, P]
+        lib.orc_recycle_query.argtypes = [P, P, P, P, P, i64, i32, i32, P, P, i32, ctypes.c_float, i32,
+                                          i32, P, P, P]
         lib.orc_lexical_drafts.argtypes = [P, P, P, i64, P, P, i32, i32, P, i32, i32, i32, i64, P, P]
         lib.orc_accept_walk.argtypes = [i32, i32, P, P, P, P, P, P, P]
         _lib = lib
@@ -233,3 +236,77 @@ def lexical_drafts(tokens, traces, prompts, n_valid, ctx, ctx_len, n_lex, L_lex,
                                       _ptr(ol)),
            "lexical_drafts")
     return ot, ol
+
+
+REC_DEPTH = 6
+
+
+def recycle_records(node_token, node_parent, n_nodes, target, accept_len, accept_nodes, depth=REC_DEPTH):
+    """Records of the rejected nodes of verified trees (Sec. 4 (i b)).
+
+    Returns (src_row, token, rollout (n, depth) -1 padded, rollout_len): src_row is
+    b * max_nodes + parent, the row of the per-node state array whose
+    normalisation is the record's key."""
+    nt, npar = _c(node_token, np.int32), _c(node_parent, np.int32)
+    B, mx = nt.shape
+    nn, tg = _c(n_nodes, np.int32), _c(target, np.int32)
+    al, an = _c(accept_len, np.int32), _c(accept_nodes, np.int32)
+    cap = B * mx
+    src = np.empty(cap, np.int32)
+    tok = np.empty(cap, np.int32)
+    roll = np.empty((cap, depth), np.int32)
+    rl = np.empty(cap, np.int32)
+    n = ctypes.c_int64(0)
+    _check(_load().orc_recycle_records(B, mx, _ptr(nt), _ptr(npar), _ptr(nn), _ptr(tg), _ptr(al),
+                                       _ptr(an), depth, _ptr(src), _ptr(tok), _ptr(roll), _ptr(rl),
+                                       ctypes.byref(n)), "recycle_records")
+    k = n.value
+    return src[:k], tok[:k], roll[:k], rl[:k]
+
+
+def recycle_ring(capacity, batches):
+    """The ring buffer after inserting record batches in order (slot = sequence % capacity).
+
+    ``batches`` is a list of dicts of equal-length arrays (any fields); returns
+    (fields per slot, seq per slot with -1 for empty slots, total inserted)."""
+    seq = np.full(capacity, -1, np.int64)
+    out = {}
+    total = 0
+    for recs in batches:
+        m = len(next(iter(recs.values())))
+        for name, a in recs.items():
+            if name not in out:
+                out[name] = np.zeros((capacity,) + a.shape[1:], a.dtype)
+        for j in range(m):
+            slot = (total + j) % capacity
+            seq[slot] = total + j
+            for name, a in recs.items():
+                out[name][slot] = a[j]
+        total += m
+    return out, seq, total
+
+
+def recycle_query(keys, tokens, rollouts, rollout_len, seq, raw_queries, anchor, theta=0.8, n_out=4,
+                  L_out=REC_DEPTH):
+    """Lookup over the records whose seq >= 0 (keys: stored bf16 bit patterns,
+    (n, d)): (scores (B, n_out) f32, -inf padded; rollouts (B, n_out, L_out) -1
+    padded; lengths (B, n_out))."""
+    live = np.asarray(seq) >= 0
+    k = _c(bf16_to_f64(np.asarray(keys, np.uint16)[live]), np.float64)
+    tk = _c(np.asarray(tokens)[live], np.int32)
+    ro = _c(np.asarray(rollouts)[live], np.int32)
+    rl = _c(np.asarray(rollout_len)[live], np.int32)
+    sq = _c(np.asarray(seq)[live], np.int64)
+    n, depth = ro.shape if ro.ndim == 2 and ro.shape[0] else (0, REC_DEPTH)
+    qn = _c(bf16_to_f64(normalize_rows(raw_queries)), np.float64)
+    B, d = qn.shape
+    anc = _c(anchor, np.int32)
+    os_ = np.empty((B, n_out), np.float32)
+    ot = np.empty((B, n_out, L_out), np.int32)
+    ol = np.empty((B, n_out), np.int32)
+    _check(_load().orc_recycle_query(_ptr(k) if n else None, _ptr(tk) if n else None,
+                                     _ptr(ro) if n else None, _ptr(rl) if n else None,
+                                     _ptr(sq) if n else None, n, d, depth, _ptr(qn), _ptr(anc), B,
+                                     ctypes.c_float(theta), n_out, L_out, _ptr(os_), _ptr(ot), _ptr(ol)),
+           "recycle_query")
+    return os_, ot, ol

@@ -643,3 +643,139 @@ int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32
     free(cand), free(mlen), free(group), free(lev), free(picked), free(n_at);
     return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Rejected-branch recycled pool (Sec. 4 (i b); the recycled-pool step of   */
+/* Algorithm 1).                                                             */
+/* Records: after a tree is verified, every drafted node n (n >= 1) that is  */
+/* not on the accepted path becomes a record keyed by the state before its  */
+/* token (the state computed at its parent) and by its token; its value is  */
+/* the continuation the verifier endorses from n: the prediction at n, then */
+/* the prediction at the child of n that carries that prediction, and so on */
+/* while such a child exists, at most `depth` tokens.  Records come in tree */
+/* order, then node order.  The key row is identified by its source:        */
+/* b * max_nodes + parent(n); the caller normalises that state as stored    */
+/* keys are normalised.                                                     */
+/* Lookup: for each request, the records whose token equals its anchor and */
+/* whose similarity to its query state (float32-rounded dot of the unit     */
+/* bf16 operands) reaches theta, best n_out by (score desc, insertion order */
+/* asc), their rollouts clipped to L_out tokens.                            */
+/* Parity pins: hand-worked fixture, closed forms on chain and star trees,   */
+/* counts, a library sort for the lookup.                                   */
+/* ------------------------------------------------------------------------ */
+
+int orc_recycle_records(int32_t B, int32_t max_nodes, const int32_t *node_token, const int32_t *node_parent,
+                        const int32_t *n_nodes, const int32_t *target, const int32_t *accept_len,
+                        const int32_t *accept_nodes, int32_t depth, int32_t *rec_src, int32_t *rec_token,
+                        int32_t *rec_rollout, int32_t *rec_len, int64_t *n_rec)
+{
+    if (B < 1 || max_nodes < 1 || depth < 1 || !node_token || !node_parent || !n_nodes || !target ||
+        !accept_len || !accept_nodes || !rec_src || !rec_token || !rec_rollout || !rec_len || !n_rec)
+        return ORC_EINVAL;
+    char *accepted = (char *)malloc((size_t)max_nodes);
+    if (!accepted)
+        return ORC_EINVAL;
+    int64_t k = 0;
+    for (int32_t b = 0; b < B; b++) {
+        const int64_t o = (int64_t)b * max_nodes;
+        int32_t nn = n_nodes[b] < max_nodes ? n_nodes[b] : max_nodes;
+        memset(accepted, 0, (size_t)max_nodes);
+        for (int32_t j = 0; j < accept_len[b] && j < max_nodes; j++) {
+            int32_t a = accept_nodes[o + j];
+            if (a >= 0 && a < max_nodes)
+                accepted[a] = 1;
+        }
+        for (int32_t n = 1; n < nn; n++) {
+            if (accepted[n])
+                continue;
+            int32_t parent = node_parent[o + n];
+            rec_src[k] = (int32_t)(o + parent);
+            rec_token[k] = node_token[o + n];
+            int32_t *out = rec_rollout + k * depth;
+            for (int32_t j = 0; j < depth; j++)
+                out[j] = -1;
+            int32_t cur = n, len = 0;
+            out[len++] = target[o + cur];
+            while (len < depth) {
+                int32_t next = -1;
+                for (int32_t c = 1; c < nn; c++) {
+                    if (node_parent[o + c] == cur && node_token[o + c] == target[o + cur]) {
+                        next = c;
+                        break;
+                    }
+                }
+                if (next < 0)
+                    break;
+                cur = next;
+                out[len++] = target[o + cur];
+            }
+            rec_len[k] = len;
+            k++;
+        }
+    }
+    free(accepted);
+    *n_rec = k;
+    return ORC_OK;
+}
+
+typedef struct {
+    double s;
+    int64_t seq;
+    int64_t r;
+} orc_rec_hit;
+
+static int rec_hit_cmp(const void *pa, const void *pb)
+{
+    const orc_rec_hit *a = (const orc_rec_hit *)pa, *b = (const orc_rec_hit *)pb;
+    if (a->s != b->s)
+        return a->s > b->s ? -1 : 1;
+    return (a->seq < b->seq) ? -1 : (a->seq > b->seq);
+}
+
+int orc_recycle_query(const double *keys, const int32_t *tokens, const int32_t *rollouts,
+                      const int32_t *rollout_len, const int64_t *seq, int64_t n, int32_t d, int32_t depth,
+                      const double *q, const int32_t *anchor, int32_t B, float theta, int32_t n_out,
+                      int32_t L_out, float *out_s, int32_t *out_tokens, int32_t *out_len)
+{
+    if (n < 0 || d < 1 || depth < 1 || B < 1 || n_out < 1 || L_out < 1 || (n > 0 && (!keys || !tokens ||
+        !rollouts || !rollout_len || !seq)) || !q || !anchor || !out_s || !out_tokens || !out_len)
+        return ORC_EINVAL;
+    orc_rec_hit *hits = (orc_rec_hit *)malloc(sizeof(orc_rec_hit) * (size_t)(n > 0 ? n : 1));
+    if (!hits)
+        return ORC_EINVAL;
+    for (int32_t b = 0; b < B; b++) {
+        int64_t nh = 0;
+        for (int64_t r = 0; r < n; r++) {
+            if (tokens[r] != anchor[b])
+                continue;
+            double acc = 0.0;
+            for (int32_t e = 0; e < d; e++)
+                acc += keys[r * d + e] * q[(int64_t)b * d + e];
+            if ((float)acc < theta)
+                continue;
+            hits[nh].s = acc;
+            hits[nh].seq = seq[r];
+            hits[nh].r = r;
+            nh++;
+        }
+        qsort(hits, (size_t)nh, sizeof(orc_rec_hit), rec_hit_cmp);
+        for (int32_t j = 0; j < n_out; j++) {
+            int64_t ob = (int64_t)b * n_out + j;
+            for (int32_t t = 0; t < L_out; t++)
+                out_tokens[ob * L_out + t] = -1;
+            if (j < nh) {
+                int64_t r = hits[j].r;
+                int32_t len = rollout_len[r] < L_out ? rollout_len[r] : L_out;
+                for (int32_t t = 0; t < len; t++)
+                    out_tokens[ob * L_out + t] = rollouts[r * depth + t];
+                out_len[ob] = len;
+                out_s[ob] = (float)hits[j].s;
+            } else {
+                out_len[ob] = 0;
+                out_s[ob] = -INFINITY;
+            }
+        }
+    }
+    free(hits);
+    return ORC_OK;
+}

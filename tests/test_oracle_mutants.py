@@ -35,6 +35,14 @@ MUTANTS = {
     "draft not clipped at trace end": ("p + 1 + len < n_valid && traces[p + 1 + len] == traces[p]", "p + 1 + len < n_valid"),
     "capacity ignored": ("if (n_ge + n_at[m] > max_cand)", "if (0)"),
     "held draft proposed again": ("if (picked[t] == g)", "if (picked[t] == -7)"),
+    "accepted nodes recycled too": ("            if (accepted[n])\n                continue;", "            if (0)\n                continue;"),
+    "record keyed by the node's own state": ("rec_src[k] = (int32_t)(o + parent);", "rec_src[k] = (int32_t)(o + n);"),
+    "rollout skips the node's own prediction": ("            out[len++] = target[o + cur];\n            while (len < depth) {", "            while (len < depth) {"),
+    "rollout one deeper": ("            while (len < depth) {", "            while (len <= depth) {"),
+    "recycled lookup ignores the token": ("            if (tokens[r] != anchor[b])\n                continue;", "            if (0)\n                continue;"),
+    "recycled threshold exclusive": ("            if ((float)acc < theta)", "            if ((float)acc <= theta)"),
+    "recycled score drops the last dim": ("for (int32_t e = 0; e < d; e++)", "for (int32_t e = 0; e < d - 1; e++)"),
+    "recycled ties by newest": ("    return (a->seq < b->seq) ? -1 : (a->seq > b->seq);", "    return (a->seq > b->seq) ? -1 : (a->seq < b->seq);"),
 }
 
 
@@ -53,6 +61,7 @@ def test_pins_catch_mutant(name):
         r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
                             os.path.join(ROOT, "tests", "test_oracle.py"),
                             os.path.join(ROOT, "tests", "test_oracle_verify.py"),
-                            os.path.join(ROOT, "tests", "test_oracle_lexical.py")],
+                            os.path.join(ROOT, "tests", "test_oracle_lexical.py"),
+                            os.path.join(ROOT, "tests", "test_oracle_recycle.py")],
                            env=env, cwd=ROOT, capture_output=True, text=True, timeout=300)
         assert r.returncode != 0, f"pins did not catch mutant {name!r}"
