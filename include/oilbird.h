@@ -62,6 +62,11 @@ enum { OIL_F32 = 0, OIL_BF16 = 1 };
 #define OIL_LEX_MAX_LEN 64
 #define OIL_LEX_MAX_CAND 4096
 
+/* Recycled pool: tokens per rollout (Sec. 4 (i b): up to six deep) and the
+ * largest number of rollouts a lookup returns per request. */
+#define OIL_REC_DEPTH 6
+#define OIL_REC_MAX_OUT 8
+
 /* Padded key width, in bf16 elements: `dim` rounded up to a multiple of 64.
  * The padding columns are kept zero by the library, so they never change a
  * dot product. */
@@ -208,24 +213,90 @@ int32_t oil_lexical_drafts(const oil_pool *pool, const int32_t *ctx, const int32
 /* Root-first merge (Sec. 4 (iii), Eq. 4; BuildLexical then MergeFromRoot in
  * Algorithm 1).  Per query: node 0 is the root (token anchor[b], parent -1,
  * source 0, charged to no budget).  The n_lex lexical drafts are inserted in
- * order under lex_budget, then the k retrieved chains in rank order under
- * sem_budget (a fixed reservation; unused lexical budget does not roll over).
+ * order under lex_budget, then the k retrieved chains in rank order, then the
+ * n_rec recycled-pool rollouts, both under sem_budget (a fixed reservation;
+ * unused lexical budget does not roll over).
  * Inserting a chain walks from the root: a child carrying the next token is
  * walked for free, otherwise a node is bought while the phase's budget lasts,
  * else the rest of that chain is dropped.
  *   lex_tokens B x n_lex x L_lex int32, lex_len B x n_lex (n_lex 0 .. 64;
  *              with 0 both may be NULL).   sem_tokens B x k x L, sem_len B x k
- *              (k 0 .. 64).   L_lex, L 1 .. 64 (ignored when their count is 0).
+ *              (k 0 .. 64).   rec_tokens B x n_rec x L_rec, rec_len B x n_rec
+ *              (n_rec 0 .. OIL_REC_MAX_OUT, as oil_recycle_query writes them).
+ *              L_lex, L, L_rec 1 .. 64 (ignored when their count is 0).
  *   max_nodes  1 + lex_budget + sem_budget .. OIL_MAX_NODES.
  *   node_token, node_parent  B x max_nodes int32; node_source B x max_nodes
- *              int8 (0 root, 1 lexical, 2 retrieved); nodes in creation
- *              order (parents precede children), slots past n_nodes[b] = -1.
+ *              int8 (0 root, 1 lexical, 2 retrieved, 3 recycled); nodes in
+ *              creation order (parents precede children), slots past
+ *              n_nodes[b] = -1.
  *   n_nodes    B int32. */
 int32_t oil_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens,
                        const int32_t *lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
                        const int32_t *sem_tokens, const int32_t *sem_len, int32_t k, int32_t L,
+                       const int32_t *rec_tokens, const int32_t *rec_len, int32_t n_rec, int32_t L_rec,
                        int32_t sem_budget, int32_t max_nodes, int32_t *node_token,
                        int32_t *node_parent, int8_t *node_source, int32_t *n_nodes, void *stream);
+
+/* ---- Rejected-branch recycled pool (Sec. 4 (i b); Algorithm 1, recycled pool).
+ * A ring buffer of records beside the trace store.  After a step is verified,
+ * every drafted node that verification rejected becomes a record keyed by the
+ * state before its token (the state the forward computed at its parent) and
+ * by its token; its value is the continuation the verifier endorses from
+ * there: the prediction at the node, then the prediction at the child that
+ * carries it, and so on down the tree, at most OIL_REC_DEPTH tokens.  A lookup
+ * returns, per request, the best n_out records whose token equals the anchor
+ * and whose key's cosine with the query state reaches theta; their rollouts
+ * are merged as further retrieved chains (oil_tree_merge, source 3). */
+typedef struct oil_recycle oil_recycle;
+
+/* Bytes of the record key buffer: capacity rows of oil_key_stride(dim) bf16. */
+size_t oil_recycle_key_bytes(int32_t dim, int64_t capacity);
+
+/* Create a ring over caller-owned device buffers:
+ *   key_buf     oil_recycle_key_bytes(dim, capacity) bytes, 16-byte aligned.
+ *   token_buf   capacity int32.
+ *   rollout_buf capacity x 8 int32 (length, OIL_REC_DEPTH tokens, padding),
+ *               16-byte aligned.
+ *   head_buf    1 int64: records inserted so far; set to 0 on `stream` here.
+ * capacity 1 .. 2^31 - 1.  The handle is host memory, freed by destroy. */
+int32_t oil_recycle_create(int32_t dim, int64_t capacity, void *key_buf, int32_t *token_buf,
+                           int32_t *rollout_buf, int64_t *head_buf, void *stream, oil_recycle **out);
+int32_t oil_recycle_destroy(oil_recycle *rp);
+
+/* Workspace bytes of oil_recycle_insert for B trees of max_nodes slots. */
+size_t oil_recycle_insert_workspace_bytes(int32_t B, int32_t max_nodes);
+
+/* Insert the records of B verified trees, in tree order then node order, at
+ * the ring's head (slot = insertion index mod capacity; the oldest records are
+ * overwritten).
+ *   node_token, node_parent, n_nodes  the trees as oil_tree_merge wrote them.
+ *   target      B x max_nodes int32: the verifier's prediction after each node.
+ *   accept_len, accept_nodes  as oil_accept_walk wrote them.
+ *   states      B x max_nodes x dim raw rows (the verifier's state at each
+ *               node), dense, OIL_F32 or OIL_BF16, 16-byte aligned; a record's
+ *               key is its parent's row, normalised as stored keys are.
+ *   workspace   >= oil_recycle_insert_workspace_bytes(B, max_nodes), 256-byte aligned.
+ * B 1 .. OIL_MAX_B, max_nodes 1 .. OIL_MAX_NODES. */
+int32_t oil_recycle_insert(oil_recycle *rp, int32_t B, int32_t max_nodes, const int32_t *node_token,
+                           const int32_t *node_parent, const int32_t *n_nodes, const int32_t *target,
+                           const int32_t *accept_len, const int32_t *accept_nodes, const void *states,
+                           int32_t state_dtype, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes of oil_recycle_query for B requests (sized from capacity). */
+size_t oil_recycle_query_workspace_bytes(const oil_recycle *rp, int32_t B);
+
+/* Lookup: queries B x dim raw rows (normalised as keys are), anchor B int32.
+ * A record qualifies when its token equals anchor[b] and the float32 dot of
+ * the unit bf16 rows is >= theta; the best n_out by (score desc, insertion
+ * order asc) are returned.
+ *   scores       B x n_out float32, -inf where none.
+ *   chain_tokens B x n_out x L_out int32 rollouts clipped to L_out, -1 padded.
+ *   chain_len    B x n_out int32.
+ * n_out 1 .. OIL_REC_MAX_OUT, L_out 1 .. 64, B 1 .. OIL_MAX_B. */
+int32_t oil_recycle_query(const oil_recycle *rp, const void *queries, int32_t q_dtype, const int32_t *anchor,
+                          int32_t B, float theta, int32_t n_out, int32_t L_out, void *workspace,
+                          size_t workspace_bytes, float *scores, int32_t *chain_tokens, int32_t *chain_len,
+                          void *stream);
 
 /* Attention mask of merged trees (Sec. 4 (iii): a node attends to itself and
  * its ancestors and to nothing else; Sec. 4 (iv): one forward verifies the

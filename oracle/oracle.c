@@ -336,13 +336,15 @@ static void insert_chain(orc_node **nodes, int32_t *count, int32_t max_nodes, in
 
 int orc_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens, const int32_t *lex_len,
                    int32_t n_lex, int32_t L_lex, int32_t lex_budget, const int32_t *sem_tokens,
-                   const int32_t *sem_len, int32_t k, int32_t L, int32_t sem_budget, int32_t max_nodes,
+                   const int32_t *sem_len, int32_t k, int32_t L, const int32_t *rec_tokens,
+                   const int32_t *rec_len, int32_t n_rec, int32_t L_rec, int32_t sem_budget, int32_t max_nodes,
                    int32_t *node_token, int32_t *node_parent, int8_t *node_source, int32_t *n_nodes)
 {
-    if (B < 1 || !anchor || n_lex < 0 || k < 0 || lex_budget < 0 || sem_budget < 0 ||
+    if (B < 1 || !anchor || n_lex < 0 || k < 0 || n_rec < 0 || lex_budget < 0 || sem_budget < 0 ||
         max_nodes < 1 + lex_budget + sem_budget || !node_token || !node_parent || !node_source ||
         !n_nodes || (n_lex > 0 && (!lex_tokens || !lex_len || L_lex < 1)) ||
-        (k > 0 && (!sem_tokens || !sem_len || L < 1)))
+        (k > 0 && (!sem_tokens || !sem_len || L < 1)) ||
+        (n_rec > 0 && (!rec_tokens || !rec_len || L_rec < 1)))
         return ORC_EINVAL;
     orc_node **nodes = (orc_node **)calloc((size_t)max_nodes, sizeof(orc_node *));
     for (int32_t b = 0; b < B; b++) {
@@ -362,6 +364,13 @@ int orc_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens, 
             int64_t o = (int64_t)b * k + c;
             int32_t len = sem_len[o] < L ? sem_len[o] : L;
             insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 2, sem_tokens + o * L, len);
+        }
+        /* recycled-pool rollouts join the retrieved chains, after them, inside
+           the same reservation (Algorithm 1, recycled-pool step) */
+        for (int32_t c = 0; c < n_rec; c++) {
+            int64_t o = (int64_t)b * n_rec + c;
+            int32_t len = rec_len[o] < L_rec ? rec_len[o] : L_rec;
+            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 3, rec_tokens + o * L_rec, len);
         }
         for (int32_t j = 0; j < max_nodes; j++) {
             int64_t o = (int64_t)b * max_nodes + j;

@@ -26,6 +26,7 @@ LIB_PATH = os.path.join(_HERE, "liboilbird.so")
 OIL_F32, OIL_BF16 = 0, 1
 MAX_K, MAX_B, MAX_NODES, MAX_BANDS = 64, 512, 256, 4
 LEX_MAX_CTX, LEX_MAX_N, LEX_MAX_LEN, LEX_MAX_CAND = 32, 16, 64, 4096
+REC_DEPTH, REC_MAX_OUT = 6, 8
 
 _lib = None
 
@@ -84,11 +85,18 @@ def lib():
             "oil_pool_query_topk": (i32, [P, P, i32, i32, i32, P, P, sz, P, P, P]),
             "oil_gather_continuations": (i32, [P, P, P, i32, i32, ctypes.POINTER(DepthRule), i32,
                                                P, P, P]),
-            "oil_tree_merge": (i32, [i32, P, P, P, i32, i32, i32, P, P, i32, i32, i32, i32, P, P,
-                                     P, P, P]),
+            "oil_tree_merge": (i32, [i32, P, P, P, i32, i32, i32, P, P, i32, i32, P, P, i32, i32,
+                                     i32, i32, P, P, P, P, P]),
             "oil_status_string": (ctypes.c_char_p, [i32]),
             "oil_tree_mask": (i32, [i32, i32, P, P, P, P]),
             "oil_lexical_workspace_bytes": (sz, [P, i32, i32]),
+            "oil_recycle_key_bytes": (sz, [i32, i64]),
+            "oil_recycle_create": (i32, [i32, i64, P, P, P, P, P, ctypes.POINTER(P)]),
+            "oil_recycle_destroy": (i32, [P]),
+            "oil_recycle_insert_workspace_bytes": (sz, [i32, i32]),
+            "oil_recycle_insert": (i32, [P, i32, i32, P, P, P, P, P, P, P, i32, P, sz, P]),
+            "oil_recycle_query_workspace_bytes": (sz, [P, i32]),
+            "oil_recycle_query": (i32, [P, P, i32, P, i32, ctypes.c_float, i32, i32, P, sz, P, P, P, P]),
             "oil_lexical_drafts": (i32, [P, P, P, i32, i32, P, i32, i32, i32, i32, P, sz, P, P, P]),
             "oil_accept_walk": (i32, [i32, i32, P, P, P, P, P, P, P, P]),
             "oil_scan_timer_start": (i32, [i32]),
@@ -207,18 +215,25 @@ def gather_continuations(handle, idx, scores, rule: DepthRule, L, chain_tokens, 
 
 
 def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget,
-               max_nodes, node_token, node_parent, node_source, n_nodes, stream=None):
-    """Root-first merge.  ``lex_tokens`` (B, n_lex, L_lex) or None; ``sem_tokens`` (B, k, L)."""
+               max_nodes, node_token, node_parent, node_source, n_nodes, stream=None,
+               rec_tokens=None, rec_len=None):
+    """Root-first merge.  ``lex_tokens`` (B, n_lex, L_lex) or None; ``sem_tokens`` (B, k, L);
+    ``rec_tokens`` (B, n_rec, L_rec) recycled-pool rollouts or None."""
     B = anchor.shape[0]
     if lex_tokens is None or lex_tokens.shape[1] == 0:
         n_lex, L_lex, lt, ll = 0, 1, None, None
     else:
         n_lex, L_lex, lt, ll = lex_tokens.shape[1], lex_tokens.shape[2], lex_tokens, lex_len
+    if rec_tokens is None or rec_tokens.shape[1] == 0:
+        n_rec, L_rec, rt, rl = 0, 1, None, None
+    else:
+        n_rec, L_rec, rt, rl = rec_tokens.shape[1], rec_tokens.shape[2], rec_tokens, rec_len
     k, L = sem_tokens.shape[1], sem_tokens.shape[2]
     _check("oil_tree_merge", lib().oil_tree_merge(
         B, _ptr(_i32(anchor, "anchor")), _ptr(lt), _ptr(ll), n_lex, L_lex, lex_budget,
-        _ptr(sem_tokens), _ptr(sem_len), k, L, sem_budget, max_nodes, _ptr(node_token),
-        _ptr(node_parent), _ptr(node_source), _ptr(n_nodes), _stream(stream)))
+        _ptr(sem_tokens), _ptr(sem_len), k, L, _ptr(rt), _ptr(rl), n_rec, L_rec, sem_budget,
+        max_nodes, _ptr(node_token), _ptr(node_parent), _ptr(node_source), _ptr(n_nodes),
+        _stream(stream)))
 
 
 def tree_mask(node_parent, n_nodes, mask=None, stream=None):
@@ -341,8 +356,73 @@ class Pool:
         return ct, cl
 
 
+class RecyclePool:
+    """The rejected-branch recycled pool: a ring of records over device buffers
+    (torch tensors, caller-owned)."""
+
+    def __init__(self, dim: int, capacity: int, device="cuda", stream=None):
+        self.dim, self.capacity = dim, capacity
+        self.device = torch.device(device)
+        nbytes = lib().oil_recycle_key_bytes(dim, capacity)
+        if nbytes == 0:
+            raise ValueError(f"unsupported recycled pool: dim={dim} capacity={capacity}")
+        self.stride = key_stride(dim)
+        self.keys = torch.empty((capacity, self.stride), dtype=torch.bfloat16, device=self.device)
+        self.tokens = torch.empty((capacity,), dtype=torch.int32, device=self.device)
+        self.rollouts = torch.empty((capacity, 8), dtype=torch.int32, device=self.device)
+        self.head = torch.empty((1,), dtype=torch.int64, device=self.device)
+        h = ctypes.c_void_p()
+        _check("oil_recycle_create", lib().oil_recycle_create(
+            dim, capacity, _ptr(self.keys), _ptr(self.tokens), _ptr(self.rollouts), _ptr(self.head),
+            _stream(stream), ctypes.byref(h)))
+        self.handle = h
+        self._ws = {}
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and _lib is not None:
+            _lib.oil_recycle_destroy(h)
+            self.handle = None
+
+    def _workspace(self, key, nbytes):
+        if nbytes == 0:
+            raise ValueError(f"unsupported recycled pool call {key}")
+        if key not in self._ws or self._ws[key].numel() < nbytes:
+            self._ws[key] = torch.empty((nbytes,), dtype=torch.uint8, device=self.device)
+        return self._ws[key]
+
+    def insert(self, node_token, node_parent, n_nodes, target, accept_len, accept_nodes, states,
+               stream=None):
+        """Records of the rejected nodes of B verified trees; ``states`` is
+        (B, max_nodes, dim) float32 or bfloat16."""
+        B, mx = node_token.shape
+        ws = self._workspace(("ins", B, mx), lib().oil_recycle_insert_workspace_bytes(B, mx))
+        _check("oil_recycle_insert", lib().oil_recycle_insert(
+            self.handle, B, mx, _ptr(_i32(node_token, "node_token")), _ptr(_i32(node_parent, "node_parent")),
+            _ptr(_i32(n_nodes, "n_nodes")), _ptr(_i32(target, "target")), _ptr(_i32(accept_len, "accept_len")),
+            _ptr(_i32(accept_nodes, "accept_nodes")), _ptr(states), _dtype_code(states), _ptr(ws),
+            ws.numel(), _stream(stream)))
+
+    def query(self, queries, anchor, theta=0.8, n_out=4, L_out=REC_DEPTH, stream=None, out=None):
+        """Rollouts of the best records per request: (scores (B, n_out), tokens
+        (B, n_out, L_out), lengths (B, n_out))."""
+        B = queries.shape[0]
+        ws = self._workspace(("q", B), lib().oil_recycle_query_workspace_bytes(self.handle, B))
+        if out is None:
+            sc = torch.empty((B, n_out), dtype=torch.float32, device=self.device)
+            tk = torch.empty((B, n_out, L_out), dtype=torch.int32, device=self.device)
+            ln = torch.empty((B, n_out), dtype=torch.int32, device=self.device)
+        else:
+            sc, tk, ln = out
+        _check("oil_recycle_query", lib().oil_recycle_query(
+            self.handle, _ptr(queries), _dtype_code(queries), _ptr(_i32(anchor, "anchor")), B,
+            ctypes.c_float(theta), n_out, L_out, _ptr(ws), ws.numel(), _ptr(sc), _ptr(tk), _ptr(ln),
+            _stream(stream)))
+        return sc, tk, ln
+
+
 def merge_trees(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget,
-                max_nodes, stream=None, out=None):
+                max_nodes, stream=None, out=None, rec_tokens=None, rec_len=None):
     """Allocate outputs and run tree_merge; returns (node_token, node_parent, node_source, n_nodes)."""
     B = anchor.shape[0]
     dev = anchor.device
@@ -354,5 +434,5 @@ def merge_trees(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, se
     else:
         nt, npar, ns, nn = out
     tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget, max_nodes,
-               nt, npar, ns, nn, stream)
+               nt, npar, ns, nn, stream, rec_tokens, rec_len)
     return nt, npar, ns, nn

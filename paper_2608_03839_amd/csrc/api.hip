@@ -12,9 +12,18 @@
 static_assert(OIL_MAX_K == OIL_TOPK_MAX, "top-k capacity");
 static_assert(OIL_MAX_NODES == OIL_NODES_MAX, "tree capacity");
 static_assert(OIL_MAX_BANDS == OIL_BANDS_MAX, "band table");
+static_assert(OIL_REC_DEPTH == OIL_REC_DEPTH_MAX && OIL_REC_MAX_OUT == OIL_REC_OUT_MAX, "recycled pool");
 static_assert(OIL_LEX_MAX_CTX == OIL_LEX_CTX_MAX && OIL_LEX_MAX_N == OIL_LEX_N_MAX &&
                   OIL_LEX_MAX_LEN == OIL_LEX_LEN_MAX && OIL_LEX_MAX_CAND == OIL_LEX_CAND_MAX,
               "lexical limits");
+
+struct oil_recycle {
+    int32_t dim, ld;
+    int64_t capacity;
+    uint16_t* keys;
+    int32_t *tokens, *rollouts;
+    int64_t* head;
+};
 
 struct oil_pool {
     int32_t dim, ld;
@@ -303,27 +312,128 @@ int32_t oil_lexical_drafts(const oil_pool* pool, const int32_t* ctx, const int32
 int32_t oil_tree_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
                        const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
                        const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                       const int32_t* rec_tokens, const int32_t* rec_len, int32_t n_rec, int32_t L_rec,
                        int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                        int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, void* stream)
 {
     if (B < 1 || !anchor || !node_token || !node_parent || !node_source || !n_nodes || n_lex < 0 ||
-        k < 0 || lex_budget < 0 || sem_budget < 0)
+        k < 0 || n_rec < 0 || lex_budget < 0 || sem_budget < 0)
         return OIL_E_INVALID;
     if (n_lex == 0)
         L_lex = 1;  // unused
     if (k == 0)
         L = 1;      // unused
+    if (n_rec == 0)
+        L_rec = 1;  // unused
     if (n_lex > 0 && (!lex_tokens || !lex_len || L_lex < 1))
         return OIL_E_INVALID;
     if (k > 0 && (!sem_tokens || !sem_len || L < 1))
         return OIL_E_INVALID;
+    if (n_rec > 0 && (!rec_tokens || !rec_len || L_rec < 1))
+        return OIL_E_INVALID;
     if ((int64_t)lex_budget + sem_budget + 1 > max_nodes)
         return OIL_E_INVALID;
-    if (max_nodes > OIL_MAX_NODES || L_lex > 64 || L > 64 || n_lex > 64 || k > 64)
+    if (max_nodes > OIL_MAX_NODES || L_lex > 64 || L > 64 || L_rec > 64 || n_lex > 64 || k > 64 ||
+        n_rec > OIL_REC_MAX_OUT)
         return OIL_E_UNSUPPORTED;
     return hip_status(oil::launch_merge(B, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget,
-                                        sem_tokens, sem_len, k, L, sem_budget, max_nodes, node_token,
-                                        node_parent, node_source, n_nodes, (hipStream_t)stream));
+                                        sem_tokens, sem_len, k, L, rec_tokens, rec_len, n_rec, L_rec,
+                                        sem_budget, max_nodes, node_token, node_parent, node_source,
+                                        n_nodes, (hipStream_t)stream));
+}
+
+size_t oil_recycle_key_bytes(int32_t dim, int64_t capacity)
+{
+    if (dim < 1 || capacity < 1)
+        return 0;
+    return (size_t)capacity * (size_t)oil_key_stride(dim) * sizeof(uint16_t);
+}
+
+int32_t oil_recycle_create(int32_t dim, int64_t capacity, void* key_buf, int32_t* token_buf,
+                           int32_t* rollout_buf, int64_t* head_buf, void* stream, oil_recycle** out)
+{
+    if (!out || dim < 1 || capacity < 1 || capacity > 0x7FFFFFFF || !key_buf || !token_buf ||
+        !rollout_buf || !head_buf || !aligned(key_buf, 16) || !aligned(rollout_buf, 16) ||
+        !aligned(head_buf, 8))
+        return OIL_E_INVALID;
+    oil_recycle* r = (oil_recycle*)calloc(1, sizeof(oil_recycle));
+    if (!r)
+        return OIL_E_INVALID;
+    r->dim = dim;
+    r->ld = oil_key_stride(dim);
+    r->capacity = capacity;
+    r->keys = (uint16_t*)key_buf;
+    r->tokens = token_buf;
+    r->rollouts = rollout_buf;
+    r->head = head_buf;
+    const hipError_t e = oil::launch_recycle_init(head_buf, (hipStream_t)stream);
+    if (e != hipSuccess) {
+        free(r);
+        return OIL_E_HIP;
+    }
+    *out = r;
+    return OIL_OK;
+}
+
+int32_t oil_recycle_destroy(oil_recycle* rp)
+{
+    if (!rp)
+        return OIL_E_INVALID;
+    free(rp);
+    return OIL_OK;
+}
+
+size_t oil_recycle_insert_workspace_bytes(int32_t B, int32_t max_nodes)
+{
+    if (B < 1 || B > OIL_MAX_B || max_nodes < 1 || max_nodes > OIL_MAX_NODES)
+        return 0;
+    return oil::recycle_insert_workspace_bytes(B, max_nodes);
+}
+
+int32_t oil_recycle_insert(oil_recycle* rp, int32_t B, int32_t max_nodes, const int32_t* node_token,
+                           const int32_t* node_parent, const int32_t* n_nodes, const int32_t* target,
+                           const int32_t* accept_len, const int32_t* accept_nodes, const void* states,
+                           int32_t state_dtype, void* workspace, size_t workspace_bytes, void* stream)
+{
+    if (!rp || B < 1 || max_nodes < 1 || !node_token || !node_parent || !n_nodes || !target ||
+        !accept_len || !accept_nodes || !states || (state_dtype != OIL_F32 && state_dtype != OIL_BF16))
+        return OIL_E_INVALID;
+    if (B > OIL_MAX_B || max_nodes > OIL_MAX_NODES)
+        return OIL_E_UNSUPPORTED;
+    if (!workspace || workspace_bytes < oil::recycle_insert_workspace_bytes(B, max_nodes) ||
+        !aligned(workspace, kAlign))
+        return OIL_E_WORKSPACE;
+    return hip_status(oil::launch_recycle_insert(B, max_nodes, node_token, node_parent, n_nodes, target,
+                                                 accept_len, accept_nodes, states, state_dtype, rp->dim, rp->ld,
+                                                 rp->capacity, rp->keys, rp->tokens, rp->rollouts, rp->head,
+                                                 workspace, (hipStream_t)stream));
+}
+
+size_t oil_recycle_query_workspace_bytes(const oil_recycle* rp, int32_t B)
+{
+    if (!rp || B < 1 || B > OIL_MAX_B)
+        return 0;
+    return oil::recycle_query_workspace_bytes(B, rp->ld, rp->capacity);
+}
+
+int32_t oil_recycle_query(const oil_recycle* rp, const void* queries, int32_t q_dtype, const int32_t* anchor,
+                          int32_t B, float theta, int32_t n_out, int32_t L_out, void* workspace,
+                          size_t workspace_bytes, float* scores, int32_t* chain_tokens, int32_t* chain_len,
+                          void* stream)
+{
+    if (!rp || !queries || !anchor || !scores || !chain_tokens || !chain_len || B < 1 || n_out < 1 ||
+        L_out < 1 || (q_dtype != OIL_F32 && q_dtype != OIL_BF16) || !aligned(queries, 16) ||
+        theta != theta)
+        return OIL_E_INVALID;
+    if (B > OIL_MAX_B || n_out > OIL_REC_MAX_OUT || L_out > 64)
+        return OIL_E_UNSUPPORTED;
+    if (!workspace || workspace_bytes < oil::recycle_query_workspace_bytes(B, rp->ld, rp->capacity) ||
+        !aligned(workspace, kAlign))
+        return OIL_E_WORKSPACE;
+    return hip_status(oil::launch_recycle_query(queries, q_dtype, B, rp->dim, rp->ld, anchor, rp->keys,
+                                                rp->tokens, rp->rollouts, rp->head, rp->capacity, theta, n_out,
+                                                L_out, workspace, scores, chain_tokens, chain_len,
+                                                (hipStream_t)stream));
 }
 
 int32_t oil_tree_mask(int32_t B, int32_t max_nodes, const int32_t* node_parent, const int32_t* n_nodes,

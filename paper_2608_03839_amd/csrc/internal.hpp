@@ -12,6 +12,8 @@
 #define OIL_LEX_N_MAX 16
 #define OIL_LEX_LEN_MAX 64
 #define OIL_LEX_CAND_MAX 4096
+#define OIL_REC_DEPTH_MAX 6
+#define OIL_REC_OUT_MAX 8
 
 namespace oil {
 
@@ -62,6 +64,7 @@ hipError_t launch_gather(const int32_t* tokens, const int32_t* traces, int64_t n
 hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
                         const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
                         const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                        const int32_t* rec_tokens, const int32_t* rec_len, int32_t n_rec, int32_t L_rec,
                         int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                         int32_t* node_parent, int8_t* node_source, int32_t* n_nodes,
                         hipStream_t stream);
@@ -74,6 +77,20 @@ hipError_t launch_lexical(const int32_t* tokens, const int32_t* traces, const in
                           int32_t B, const int32_t* exclude, int32_t n_lex, int32_t L_lex,
                           int32_t min_match, int32_t max_cand, void* workspace, int64_t capacity,
                           int32_t* lex_tokens, int32_t* lex_len, hipStream_t stream);
+hipError_t launch_recycle_init(int64_t* head, hipStream_t stream);
+size_t recycle_insert_workspace_bytes(int32_t B, int32_t max_nodes);
+hipError_t launch_recycle_insert(int32_t B, int32_t max_nodes, const int32_t* node_token,
+                                 const int32_t* node_parent, const int32_t* n_nodes, const int32_t* target,
+                                 const int32_t* accept_len, const int32_t* accept_nodes, const void* states,
+                                 int dtype, int32_t d, int32_t ld, int64_t capacity, uint16_t* keys,
+                                 int32_t* ring_tokens, int32_t* ring_rollouts, int64_t* head, void* workspace,
+                                 hipStream_t stream);
+size_t recycle_query_workspace_bytes(int32_t B, int32_t ld, int64_t capacity);
+hipError_t launch_recycle_query(const void* queries, int q_dtype, int32_t B, int32_t d, int32_t ld,
+                                const int32_t* anchor, const uint16_t* keys, const int32_t* ring_tokens,
+                                const int32_t* ring_rollouts, const int64_t* head, int64_t capacity,
+                                float theta, int32_t n_out, int32_t L_out, void* workspace, float* out_s,
+                                int32_t* out_tokens, int32_t* out_len, hipStream_t stream);
 hipError_t launch_accept_walk(int32_t B, int32_t max_nodes, const int32_t* node_token,
                               const int32_t* node_parent, const int32_t* n_nodes, const int32_t* target,
                               int32_t* accept_len, int32_t* accept_nodes, int32_t* bonus,

@@ -9,7 +9,8 @@
 // repeat a token, so there is at most one).  A match is walked for free;
 // otherwise the next slot is bought if the phase's budget remains, else the
 // rest of the chain is dropped.  Lexical drafts go first under their
-// allocation, retrieved chains after them under the fixed reservation.
+// allocation, retrieved chains after them under the fixed reservation, and
+// recycled-pool rollouts last, inside that same reservation.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -63,17 +64,25 @@ __global__ __launch_bounds__(64) void merge_kernel(
     const int32_t* __restrict__ anchor, const int32_t* __restrict__ lex_tokens,
     const int32_t* __restrict__ lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
     const int32_t* __restrict__ sem_tokens, const int32_t* __restrict__ sem_len, int32_t k, int32_t L,
-    int32_t sem_budget, int32_t max_nodes, int32_t* __restrict__ node_token,
+    const int32_t* __restrict__ rec_tokens, const int32_t* __restrict__ rec_len, int32_t n_rec,
+    int32_t L_rec, int32_t sem_budget, int32_t max_nodes, int32_t* __restrict__ node_token,
     int32_t* __restrict__ node_parent, int8_t* __restrict__ node_source, int32_t* __restrict__ n_nodes)
 {
-    // LDS: lexical chains, retrieved chains, then the two length arrays
+    // LDS: lexical chains, retrieved chains, rollouts, then the three length arrays
     extern __shared__ int32_t sm[];
     int32_t* lex_s = sm;
     int32_t* sem_s = lex_s + n_lex * L_lex;
-    int32_t* llen_s = sem_s + k * L;
+    int32_t* rec_s = sem_s + k * L;
+    int32_t* llen_s = rec_s + n_rec * L_rec;
     int32_t* slen_s = llen_s + n_lex;
+    int32_t* rlen_s = slen_s + k;
     const int b = blockIdx.x, lane = threadIdx.x;
     {
+        const int32_t* rt = rec_tokens + (int64_t)b * n_rec * L_rec;
+        for (int i = lane; i < n_rec * L_rec; i += 64)
+            rec_s[i] = rt[i];
+        for (int i = lane; i < n_rec; i += 64)
+            rlen_s[i] = rec_len[(int64_t)b * n_rec + i];
         const int32_t* lt = lex_tokens + (int64_t)b * n_lex * L_lex;
         for (int i = lane; i < n_lex * L_lex; i += 64)
             lex_s[i] = lt[i];
@@ -111,6 +120,12 @@ __global__ __launch_bounds__(64) void merge_kernel(
         len = len < L ? len : L;
         insert_chain(ntok, npar, nsrc, count, spent, sem_budget, 2, sem_s + c * L, len);
     }
+    // recycled-pool rollouts: after the retrieved chains, inside the same reservation
+    for (int c = 0; c < n_rec; c++) {
+        int len = rlen_s[c];
+        len = len < L_rec ? len : L_rec;
+        insert_chain(ntok, npar, nsrc, count, spent, sem_budget, 3, rec_s + c * L_rec, len);
+    }
 #pragma unroll
     for (int q = 0; q < kSlotsPerLane; q++) {
         const int slot = q * 64 + lane;
@@ -125,21 +140,23 @@ __global__ __launch_bounds__(64) void merge_kernel(
         n_nodes[b] = count;
 }
 
-size_t merge_lds_bytes(int32_t n_lex, int32_t L_lex, int32_t k, int32_t L)
+size_t merge_lds_bytes(int32_t n_lex, int32_t L_lex, int32_t k, int32_t L, int32_t n_rec, int32_t L_rec)
 {
-    return ((size_t)n_lex * L_lex + (size_t)k * L + n_lex + k) * sizeof(int32_t);
+    return ((size_t)n_lex * L_lex + (size_t)k * L + (size_t)n_rec * L_rec + n_lex + k + n_rec) *
+           sizeof(int32_t);
 }
 
 hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
                         const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
                         const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                        const int32_t* rec_tokens, const int32_t* rec_len, int32_t n_rec, int32_t L_rec,
                         int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                         int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, hipStream_t stream)
 {
-    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(64), merge_lds_bytes(n_lex, L_lex, k, L), stream,
-                       anchor, lex_tokens, lex_len, n_lex,
-                       L_lex, lex_budget, sem_tokens, sem_len, k, L, sem_budget, max_nodes, node_token,
-                       node_parent, node_source, n_nodes);
+    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(64), merge_lds_bytes(n_lex, L_lex, k, L, n_rec, L_rec),
+                       stream, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget, sem_tokens, sem_len, k,
+                       L, rec_tokens, rec_len, n_rec, L_rec, sem_budget, max_nodes, node_token, node_parent,
+                       node_source, n_nodes);
     return hipGetLastError();
 }
 

@@ -8,31 +8,9 @@
 // identical stored bits wherever they sit in the pool.
 #include "common.hpp"
 #include "internal.hpp"
+#include "rowops.hpp"
 
 namespace oil {
-
-__device__ __forceinline__ double load_raw(const void* raw, int dtype, int64_t at)
-{
-    if (dtype == 0)
-        return (double)((const float*)raw)[at];
-    return (double)bf16_bits_to_float(((const uint16_t*)raw)[at]);
-}
-
-// Block-wide sum of one double per thread, fixed order (wave xor-tree, then
-// the four wave totals in wave order).
-__device__ __forceinline__ double block_sum_256(double v, double* red)
-{
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1)
-        v += __shfl_xor(v, o, kWave);
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0)
-        red[wave] = v;
-    __syncthreads();
-    const double t = ((red[0] + red[1]) + red[2]) + red[3];
-    __syncthreads();
-    return t;
-}
 
 // Destination layouts of a normalised row (offsets in bf16 elements; row i,
 // column j; ld = width rounded up to 64):

@@ -100,14 +100,18 @@ def test_merge_validates(L):
     f = _FakeBufs()
     P = f.aligned
     # budgets that do not fit max_nodes
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, 10, 10, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, -1, P, P, 4, 4, 10, 64, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, None, None, 1, 4, 4, P, P, 4, 4, 10, 64, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, 300, 301, P, P, P, P, None) == -3
-    assert L.oil_tree_merge(0, P, None, None, 0, 1, 0, P, P, 4, 4, 10, 64, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, P, P, 65, 4, 4, P, P, 4, 4, 10, 64, P, P, P, P, None) == -3
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 65, 4, 10, 64, P, P, P, P, None) == -3
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 65, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, None, None, 0, 1, 10, 10, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, -1, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 1, 4, 4, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, None, None, 0, 1, 300, 301, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(0, P, None, None, 0, 1, 0, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, P, P, 65, 4, 4, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 65, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 65, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
+    # rollouts: more than OIL_REC_MAX_OUT, missing buffers, too wide
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, P, P, 9, 6, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, None, P, 4, 6, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, P, P, 4, 65, 10, 64, P, P, P, P, None) == -3
 
 
 def test_verify_validates(L):
@@ -166,3 +170,26 @@ def test_lexical_validates(L):
     assert call(ws=f.misaligned) == -5
     assert call(ws=None) == -5
     assert L.oil_pool_destroy(h) == 0
+
+
+def test_recycle_validates(L):
+    f = _FakeBufs()
+    P = f.aligned
+    h = ctypes.c_void_p()
+    assert L.oil_recycle_key_bytes(0, 10) == 0
+    assert L.oil_recycle_key_bytes(100, 10) == 10 * 128 * 2
+    # creation checks (argument errors return before anything is enqueued)
+    assert L.oil_recycle_create(0, 10, P, P, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_recycle_create(16, 0, P, P, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_recycle_create(16, 2**31, P, P, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_recycle_create(16, 10, f.misaligned, P, P, P, None, ctypes.byref(h)) == -1
+    assert L.oil_recycle_create(16, 10, P, P, P, None, None, ctypes.byref(h)) == -1
+    assert L.oil_recycle_create(16, 10, P, P, P, P, None, None) == -1
+    assert L.oil_recycle_insert_workspace_bytes(0, 8) == 0
+    assert L.oil_recycle_insert_workspace_bytes(4, 257) == 0
+    assert L.oil_recycle_insert_workspace_bytes(4, 65) > 0
+    assert L.oil_recycle_destroy(None) == -1
+    # insert/query argument checks on a null handle are rejected first
+    assert L.oil_recycle_insert(None, 4, 65, P, P, P, P, P, P, P, 0, P, 1 << 20, None) == -1
+    assert L.oil_recycle_query(None, P, 0, P, 4, ctypes.c_float(0.8), 4, 6, P, 1 << 20, P, P, P, None) == -1
+    assert L.oil_recycle_query_workspace_bytes(None, 4) == 0

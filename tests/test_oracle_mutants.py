@@ -42,6 +42,7 @@ MUTANTS = {
     "recycled lookup ignores the token": ("            if (tokens[r] != anchor[b])\n                continue;", "            if (0)\n                continue;"),
     "recycled threshold exclusive": ("            if ((float)acc < theta)", "            if ((float)acc <= theta)"),
     "recycled score drops the last dim": ("for (int32_t e = 0; e < d; e++)", "for (int32_t e = 0; e < d - 1; e++)"),
+    "rollouts under their own budget": ("            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 3,", "            spent = 0;\n            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 3,"),
     "recycled ties by newest": ("    return (a->seq < b->seq) ? -1 : (a->seq > b->seq);", "    return (a->seq > b->seq) ? -1 : (a->seq < b->seq);"),
 }
 

@@ -180,3 +180,35 @@ def test_lookup_token_filter_threshold_and_padding():
     assert np.all(l == 0) and np.all(np.isinf(s))
     s, t, l = oracle.recycle_query(kb, tok, roll, rl, np.full(5, -1), e0[None, :], np.array([7]))
     assert np.all(l == 0)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_rollouts_merge_as_further_retrieved_chains(seed):
+    """Rollouts join the retrieved chains after them under the same reservation
+    (Algorithm 1): merging them as a third source equals appending them to the
+    retrieved chains, node for node; only the source tag differs (3 for nodes
+    a rollout bought)."""
+    rng = np.random.default_rng(seed)
+    B, k, L, n_rec, depth = 12, 16, 8, 4, 6
+    base = rng.integers(0, 4, (B, 1, L))
+    st = np.where(rng.random((B, k, L)) < 0.7, base, rng.integers(0, 4, (B, k, L))).astype(np.int32)
+    sl = rng.integers(0, L + 1, (B, k)).astype(np.int32)
+    rt = rng.integers(0, 4, (B, n_rec, depth)).astype(np.int32)
+    rl = rng.integers(0, depth + 1, (B, n_rec)).astype(np.int32)
+    lt = rng.integers(0, 4, (B, 2, 5)).astype(np.int32)
+    ll = rng.integers(0, 6, (B, 2)).astype(np.int32)
+    anchor = rng.integers(0, 9, B)
+    for budget in (8, 20, 60):
+        mx = 1 + 6 + budget
+        got = oracle.tree_merge(anchor, lt, ll, 6, st, sl, budget, mx, rt, rl)
+        pad = np.full((B, n_rec, L), -1, np.int32)
+        pad[:, :, :depth] = rt
+        want = oracle.tree_merge(anchor, lt, ll, 6, np.concatenate([st, pad], 1),
+                                 np.concatenate([sl, rl], 1), budget, mx)
+        assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+        assert np.array_equal(got[3], want[3])
+        # tags: equal except where the rollouts bought nodes (2 -> 3)
+        diff = got[2] != want[2]
+        assert np.all(got[2][diff] == 3) and np.all(want[2][diff] == 2)
+        n_sem_only = oracle.tree_merge(anchor, lt, ll, 6, st, sl, budget, mx)[3]
+        assert np.array_equal((got[2] == 3).sum(1), got[3] - n_sem_only)
