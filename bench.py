@@ -214,6 +214,30 @@ def main():
     torch.cuda.synchronize()
     extras["lexical_us"] = round(1e3 * e0.elapsed_time(e1) / K, 2)
     extras["mean_lexical_drafts"] = round(float((lex_out[1] > 0).float().sum(1).mean()), 2)
+    # the rejected-branch recycled pool: a ring of 65,536 records (512 MiB of
+    # keys at d = 4096), filled from the last step's verified trees with
+    # synthetic per-node verifier states, then timed insert and lookup calls
+    R = 65536
+    rp = oil.RecyclePool(d, R, device=dev)
+    g.manual_seed(6)
+    node_states = torch.randn((B, mx, d), generator=g, device=dev).to(torch.bfloat16)
+    rec_args = (tree[0], tree[1], tree[3], target, walk_out[0], walk_out[1], node_states)
+    per_insert = int((tree[3] - 1 - walk_out[0]).sum())
+    for _ in range(R // max(per_insert, 1) + 1):
+        rp.insert(*rec_args)
+    rq = Qs[-1]
+    rec_out = rp.query(rq, anchors[-1], 0.8, 4, 6)
+    for name, fn in (("recycle_insert_us", lambda: rp.insert(*rec_args)),
+                     ("recycle_query_us", lambda: rp.query(rq, anchors[-1], 0.8, 4, 6, out=rec_out))):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        extras[name] = round(1e3 * e0.elapsed_time(e1) / K, 2)
+    extras["recycle_records_per_insert"] = per_insert
+    extras["mean_recycled_rollouts"] = round(float((rec_out[2] > 0).float().sum(1).mean()), 2)
     extras["mean_tree_nodes"] = round(float(tree[3].float().mean()), 2)
     extras["mean_accepted"] = round(float(walk_out[0].float().mean()), 2)
 

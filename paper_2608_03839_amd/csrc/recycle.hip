@@ -35,7 +35,8 @@ constexpr int kMatchPer = 16;
 constexpr int kMatchChunk = kMatchThreads * kMatchPer;
 constexpr int kMatchGroup = 64;
 constexpr int kMatchTable = 256;
-constexpr int kScoreThreads = 512;
+constexpr int kScoreThreads = 1024;
+constexpr int kScoreChunks = 8;  // 16-byte key chunks per lane per round trip
 constexpr int kScoreWaves = kScoreThreads / kWave;
 
 __device__ inline uint32_t rec_mix32(uint32_t h)
@@ -166,19 +167,8 @@ __global__ __launch_bounds__(256) void recycle_keys_kernel(
     const int64_t first = total > capacity ? total - capacity : 0;
     for (int64_t k = first + blockIdx.x; k < total; k += gridDim.x) {
         const int64_t row = rec_src[k];
-        const int64_t slot = rec_slot[k];
-        double ss = 0.0;
-        for (int32_t j = threadIdx.x; j < d; j += 256) {
-            const double v = load_raw(states, dtype, row * d + j);
-            ss += v * v;
-        }
-        const double norm = sqrt(block_sum_256(ss, red));
-        for (int32_t j = threadIdx.x; j < ld; j += 256) {
-            uint16_t bits = 0;
-            if (j < d && norm > 0.0)
-                bits = double_to_bf16_rne(load_raw(states, dtype, row * d + j) / norm);
-            keys[slot * ld + j] = bits;
-        }
+        uint16_t* dst = keys + (int64_t)rec_slot[k] * ld;
+        normalize_row_256(states, dtype, row, d, ld, true, red, [&](int32_t j, uint16_t bits) { dst[j] = bits; });
     }
 }
 
@@ -288,26 +278,48 @@ __global__ __launch_bounds__(kScoreThreads) void recycle_score_kernel(
         top[j] = 0ull;
     const int n = cnt[b];
     const int32_t* lst = list + (int64_t)b * capacity;
-    for (int e = w; e < n; e += kScoreWaves) {
-        const int64_t r = lst[e];
-        const uint16_t* key = keys + r * ld;
-        float acc = 0.f;
-        for (int c = lane; c < ld / 8; c += kWave) {
-            const u32x4 kv = ((const u32x4*)key)[c];
-            const u32x4 qv = ((const u32x4*)q_lds)[c];
+    const int nc = ld / 8;
+    // two records per wave at a time, their key chunks loaded together
+    for (int e = w; e < n; e += 2 * kScoreWaves) {
+        const bool has2 = e + kScoreWaves < n;
+        const int64_t r1 = lst[e], r2 = lst[has2 ? e + kScoreWaves : e];
+        const u32x4* k1 = (const u32x4*)(keys + r1 * ld);
+        const u32x4* k2 = (const u32x4*)(keys + r2 * ld);
+        float a1 = 0.f, a2 = 0.f;
+        for (int c0 = 0; c0 < nc; c0 += kScoreChunks * kWave) {
+            u32x4 x1[kScoreChunks], x2[kScoreChunks];
 #pragma unroll
-            for (int u = 0; u < 4; u++) {  // two bf16 per word, low half first
-                acc = fmaf(__uint_as_float(kv[u] << 16), __uint_as_float(qv[u] << 16), acc);
-                acc = fmaf(__uint_as_float(kv[u] & 0xFFFF0000u), __uint_as_float(qv[u] & 0xFFFF0000u), acc);
+            for (int i = 0; i < kScoreChunks; i++) {
+                const int c = c0 + i * kWave + lane;
+                const int cc = c < nc ? c : nc - 1;  // clamped, unconditional
+                x1[i] = k1[cc];
+                x2[i] = k2[cc];
+            }
+#pragma unroll
+            for (int i = 0; i < kScoreChunks; i++) {
+                const int c = c0 + i * kWave + lane;
+                if (c < nc) {
+                    const u32x4 qv = ((const u32x4*)q_lds)[c];
+#pragma unroll
+                    for (int u = 0; u < 4; u++) {  // two bf16 per word, low half first
+                        const float qlo = __uint_as_float(qv[u] << 16), qhi = __uint_as_float(qv[u] & 0xFFFF0000u);
+                        a1 = fmaf(__uint_as_float(x1[i][u] << 16), qlo, a1);
+                        a1 = fmaf(__uint_as_float(x1[i][u] & 0xFFFF0000u), qhi, a1);
+                        a2 = fmaf(__uint_as_float(x2[i][u] << 16), qlo, a2);
+                        a2 = fmaf(__uint_as_float(x2[i][u] & 0xFFFF0000u), qhi, a2);
+                    }
+                }
             }
         }
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1)
-            acc += __shfl_xor(acc, o, kWave);
-        if (acc >= theta) {
-            const uint32_t age = (uint32_t)((r - oldest + capacity) % capacity);  // 0 = oldest
-            top_insert(top, n_out, rank_key(acc, age));
+        for (int o = 32; o >= 1; o >>= 1) {
+            a1 += __shfl_xor(a1, o, kWave);
+            a2 += __shfl_xor(a2, o, kWave);
         }
+        if (a1 >= theta)
+            top_insert(top, n_out, rank_key(a1, (uint32_t)((r1 - oldest + capacity) % capacity)));
+        if (has2 && a2 >= theta)
+            top_insert(top, n_out, rank_key(a2, (uint32_t)((r2 - oldest + capacity) % capacity)));
     }
     if (lane == 0)
         for (int j = 0; j < OIL_REC_OUT_MAX; j++)

@@ -42,22 +42,10 @@ __global__ __launch_bounds__(256) void normalize_rows_kernel(
     __shared__ double red[4];
     const int64_t r = blockIdx.x;  // row within this call
     const bool live = r < n_rows_in;
-    double ss = 0.0;
-    if (live) {
-        for (int32_t j = threadIdx.x; j < d; j += 256) {
-            const double v = load_raw(raw, dtype, r * (int64_t)d + j);
-            ss += v * v;
-        }
-    }
-    const double norm = sqrt(block_sum_256(ss, red));
     const int64_t dst_row = row_offset + r;
-    for (int32_t j = threadIdx.x; j < ld; j += 256) {
-        uint16_t b = 0;
-        if (live && j < d && norm > 0.0)
-            b = double_to_bf16_rne(load_raw(raw, dtype, r * (int64_t)d + j) / norm);
-        const int64_t at = layout_offset(layout, dst_row, j, ld, rs, ws);
-        out[at] = b;
-    }
+    normalize_row_256(raw, dtype, r, d, ld, live, red, [&](int32_t j, uint16_t bits) {
+        out[layout_offset(layout, dst_row, j, ld, rs, ws)] = bits;
+    });
     if (threadIdx.x == 0 && live && tok_out) {
         tok_out[dst_row] = tok_in[r];
         trace_out[dst_row] = trace_in[r];
