@@ -56,6 +56,12 @@ def _load():
         lib.orc_recycle_records.argtypes = [i32, i32, P, P, P, P, P, P, i32, P, P, P, P, P]
         lib.orc_recycle_query.argtypes = [P, P, P, P, P, i64, i32, i32, P, P, i32, ctypes.c_float, i32,
                                           i32, P, P, P]
+        lib.orc_e4m3_value.argtypes = [ctypes.c_uint8]
+        lib.orc_e4m3_value.restype = ctypes.c_double
+        lib.orc_e4m3_round.argtypes = [ctypes.c_double]
+        lib.orc_e4m3_round.restype = ctypes.c_uint8
+        lib.orc_quantize_rows_fp8.argtypes = [P, i32, i64, i32, P, P]
+        lib.orc_scores_fp8.argtypes = [P, P, i64, i32, P, P, i32, P]
         lib.orc_lexical_drafts.argtypes = [P, P, P, i64, P, P, i32, i32, P, i32, i32, i32, i64, P, P]
         lib.orc_accept_walk.argtypes = [i32, i32, P, P, P, P, P, P, P]
         _lib = lib
@@ -318,3 +324,49 @@ def recycle_query(keys, tokens, rollouts, rollout_len, seq, raw_queries, anchor,
                                      ctypes.c_float(theta), n_out, L_out, _ptr(os_), _ptr(ot), _ptr(ol)),
            "recycle_query")
     return os_, ot, ol
+
+
+def e4m3_value(code: int) -> float:
+    """Value of an OCP E4M3 code (NaN for 0x7F / 0xFF)."""
+    return _load().orc_e4m3_value(int(code) & 0xFF)
+
+
+def e4m3_round(x) -> np.ndarray:
+    """E4M3 codes (uint8) of the nearest values to x (|x| <= 448), ties to even."""
+    x = np.asarray(x, np.float64)
+    f = _load().orc_e4m3_round
+    return np.array([f(float(v)) for v in x.ravel()], np.uint8).reshape(x.shape)
+
+
+def quantize_rows_fp8(raw):
+    """fp8 store format: (codes (n, d) uint8, inv_scale (n,) float64).
+
+    ``raw`` is float32 or uint16 bf16 bits, shape (n, d)."""
+    raw = np.asarray(raw)
+    if raw.dtype == np.uint16:
+        dt = 1
+    else:
+        raw, dt = _c(raw, np.float32), 0
+    raw = np.ascontiguousarray(raw)
+    n, d = raw.shape
+    codes = np.empty((n, d), np.uint8)
+    inv = np.empty((n,), np.float64)
+    _check(_load().orc_quantize_rows_fp8(_ptr(raw), dt, n, d, _ptr(codes), _ptr(inv)), "quantize_rows_fp8")
+    return codes, inv
+
+
+def scores_fp8(kc, kinv, qc, qinv):
+    """Exact scores of fp8 keys against fp8 queries: (B, n) float64."""
+    kc, qc = _c(kc, np.uint8), _c(qc, np.uint8)
+    kinv, qinv = _c(kinv, np.float64), _c(qinv, np.float64)
+    n, d = kc.shape
+    B = qc.shape[0]
+    s = np.empty((B, n), np.float64)
+    _check(_load().orc_scores_fp8(_ptr(kc), _ptr(kinv), n, d, _ptr(qc), _ptr(qinv), B, _ptr(s)), "scores_fp8")
+    return s
+
+
+def query_topk_fp8(kc, kinv, raw_queries, k, prompt=None, exclude=None):
+    """fp8 variant of query_topk: queries quantized as keys are."""
+    qc, qinv = quantize_rows_fp8(raw_queries)
+    return topk(scores_fp8(kc, kinv, qc, qinv), k, prompt, exclude)

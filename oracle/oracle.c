@@ -788,3 +788,125 @@ int orc_recycle_query(const double *keys, const int32_t *tokens, const int32_t *
     free(hits);
     return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* fp8 key pool variant (the store bounded by quantization, named as future  */
+/* work in the Limitations; not the paper's configuration).                   */
+/* Format: OCP FP8 E4M3 (1 sign, 4 exponent bits with bias 7, 3 fraction     */
+/* bits; largest finite 448; no infinities).  Values: for |v| >= 2^-6 the    */
+/* representable numbers are the multiples of 2^(E-3) in [2^E, 2^(E+1)),     */
+/* E = floor(log2 |v|); below 2^-6 the multiples of 2^-9.  Rounding: nearest */
+/* representable value, ties to the one whose code is even.                  */
+/* Row quantization: the row is normalised as a bf16 key is (x / ||x|| in    */
+/* double), then scaled by a power of two s chosen so that the largest       */
+/* magnitude m lands in [128, 256) (s = 2^(7 - floor(log2 m)); a zero row    */
+/* keeps s = 1), and each scaled value is rounded to E4M3.  The stored        */
+/* score of a key and a query is the exact dot of their E4M3 values times    */
+/* 1/(s_key * s_query).                                                      */
+/* Parity pins: torch's float8_e4m3fn conversion (a library rounding),       */
+/* brute force over all 256 codes, closed forms, numpy matmul.               */
+/* ------------------------------------------------------------------------ */
+
+double orc_e4m3_value(uint8_t code)
+{
+    int sign = code >> 7, e = (code >> 3) & 15, m = code & 7;
+    double v;
+    if (e == 15 && m == 7)
+        return NAN;
+    if (e == 0)
+        v = ldexp((double)m / 8.0, -6);
+    else
+        v = ldexp(1.0 + (double)m / 8.0, e - 7);
+    return sign ? -v : v;
+}
+
+/* code of the E4M3 value nearest to v (|v| <= 448), ties to the even code */
+uint8_t orc_e4m3_round(double v)
+{
+    uint8_t sign = (v < 0 || (v == 0 && signbit(v))) ? 0x80 : 0;
+    double a = fabs(v);
+    double spacing;
+    if (a >= ldexp(1.0, -6)) {
+        int E;
+        frexp(a, &E); /* a = f * 2^E, f in [0.5, 1) */
+        E -= 1;       /* a in [2^E, 2^(E+1)) */
+        spacing = ldexp(1.0, E - 3);
+    } else {
+        spacing = ldexp(1.0, -9);
+    }
+    double q = floor(a / spacing); /* exact: spacing is a power of two */
+    double lo = q * spacing, hi = (q + 1) * spacing;
+    double pick;
+    if (a - lo < hi - a)
+        pick = lo;
+    else if (hi - a < a - lo)
+        pick = hi;
+    else
+        pick = (fmod(q, 2.0) == 0.0) ? lo : hi; /* tie: the even multiple */
+    /* encode pick (a multiple of the grid, <= 448 by the caller's contract) */
+    if (pick == 0.0)
+        return sign;
+    int E;
+    frexp(pick, &E);
+    E -= 1;
+    if (E < -6) /* subnormal: pick = m * 2^-9 */
+        return (uint8_t)(sign | (uint8_t)(pick / ldexp(1.0, -9)));
+    int m = (int)((pick / ldexp(1.0, E) - 1.0) * 8.0);
+    return (uint8_t)(sign | (uint8_t)((E + 7) << 3) | (uint8_t)m);
+}
+
+int orc_quantize_rows_fp8(const void *raw, int dtype, int64_t n, int32_t d, uint8_t *codes, double *inv_scale)
+{
+    if (!raw || !codes || !inv_scale || n < 0 || d < 1 || (dtype != 0 && dtype != 1))
+        return ORC_EINVAL;
+    int rc = ORC_OK;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; i++) {
+        double *h = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!h) {
+            rc = ORC_EINVAL;
+            continue;
+        }
+        double ss = 0.0;
+        for (int32_t j = 0; j < d; j++) {
+            double x = dtype == 0 ? (double)((const float *)raw)[i * d + j]
+                                  : orc_bf16_to_double(((const uint16_t *)raw)[i * d + j]);
+            h[j] = x;
+            ss += x * x;
+        }
+        double norm = sqrt(ss), m = 0.0;
+        for (int32_t j = 0; j < d; j++) {
+            h[j] = norm > 0.0 ? h[j] / norm : 0.0;
+            if (fabs(h[j]) > m)
+                m = fabs(h[j]);
+        }
+        int e = 0;
+        if (m > 0.0) {
+            frexp(m, &e);
+            e -= 1; /* m in [2^e, 2^(e+1)) */
+        }
+        int shift = m > 0.0 ? 7 - e : 0; /* s = 2^shift puts m in [128, 256) */
+        for (int32_t j = 0; j < d; j++)
+            codes[i * d + j] = orc_e4m3_round(ldexp(h[j], shift));
+        inv_scale[i] = ldexp(1.0, -shift);
+        free(h);
+    }
+    return rc;
+}
+
+int orc_scores_fp8(const uint8_t *kc, const double *kinv, int64_t n, int32_t d, const uint8_t *qc,
+                   const double *qinv, int32_t B, double *s)
+{
+    if (!kc || !kinv || !qc || !qinv || !s || n < 0 || d < 1 || B < 1)
+        return ORC_EINVAL;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; i++) {
+        for (int32_t b = 0; b < B; b++) {
+            double acc = 0.0; /* products and sums of E4M3 values are exact in double */
+            for (int32_t c = 0; c < d; c++)
+                acc += orc_e4m3_value(kc[i * d + c]) * orc_e4m3_value(qc[(int64_t)b * d + c]);
+            s[(int64_t)b * n + i] = acc * kinv[i] * qinv[b];
+        }
+    }
+    return ORC_OK;
+}

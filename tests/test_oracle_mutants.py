@@ -43,6 +43,11 @@ MUTANTS = {
     "recycled threshold exclusive": ("            if ((float)acc < theta)", "            if ((float)acc <= theta)"),
     "recycled score drops the last dim": ("for (int32_t e = 0; e < d; e++)", "for (int32_t e = 0; e < d - 1; e++)"),
     "rollouts under their own budget": ("            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 3,", "            spent = 0;\n            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 3,"),
+    "e4m3 ties away from zero": ("        pick = (fmod(q, 2.0) == 0.0) ? lo : hi; /* tie: the even multiple */", "        pick = hi;"),
+    "e4m3 exponent bias 8": ("        v = ldexp(1.0 + (double)m / 8.0, e - 7);", "        v = ldexp(1.0 + (double)m / 8.0, e - 8);"),
+    "fp8 scale one binade up": ("int shift = m > 0.0 ? 7 - e : 0;", "int shift = m > 0.0 ? 8 - e : 0;"),
+    "e4m3 subnormal spacing halved": ("        spacing = ldexp(1.0, -9);", "        spacing = ldexp(1.0, -10);"),
+    "fp8 score drops the query scale": ("s[(int64_t)b * n + i] = acc * kinv[i] * qinv[b];", "s[(int64_t)b * n + i] = acc * kinv[i];"),
     "recycled ties by newest": ("    return (a->seq < b->seq) ? -1 : (a->seq > b->seq);", "    return (a->seq > b->seq) ? -1 : (a->seq < b->seq);"),
 }
 
@@ -63,6 +68,7 @@ def test_pins_catch_mutant(name):
                             os.path.join(ROOT, "tests", "test_oracle.py"),
                             os.path.join(ROOT, "tests", "test_oracle_verify.py"),
                             os.path.join(ROOT, "tests", "test_oracle_lexical.py"),
-                            os.path.join(ROOT, "tests", "test_oracle_recycle.py")],
+                            os.path.join(ROOT, "tests", "test_oracle_recycle.py"),
+                            os.path.join(ROOT, "tests", "test_oracle_fp8.py")],
                            env=env, cwd=ROOT, capture_output=True, text=True, timeout=300)
         assert r.returncode != 0, f"pins did not catch mutant {name!r}"
