@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 METRIC = "retrieval queries/s + pool-scan HBM GB/s (% peak) at N=1M, d=4096 bf16"
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "scan_mfma_n1m_d4096_b32_traffic.txt")
+PROFILE_TRAFFIC_FP8 = os.path.join(ROOT, "profiles", "scan_fp8_n1m_d4096_b32_traffic.txt")
 SCAN_SRC = os.path.join(ROOT, "paper_2608_03839_amd", "csrc", "scan.hip")
 
 
@@ -41,13 +42,13 @@ def scan_source_hash():
     return hashlib.sha256(open(SCAN_SRC, "rb").read()).hexdigest()[:16]
 
 
-def read_traffic(bytes_alg):
+def read_traffic(bytes_alg, path=PROFILE_TRAFFIC):
     """HBM bytes per scan launch from the committed rocprofv3 counter summary,
     or None when it is missing or was taken on another version of the kernel."""
-    if not os.path.exists(PROFILE_TRAFFIC):
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(PROFILE_TRAFFIC):
+    for line in open(path):
         if ":" in line:
             a, b = line.split(":", 1)
             kv[a.strip()] = b.strip()
@@ -65,6 +66,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fp8", action="store_true",
+                    help="skip the fp8 key-pool variant (reported beside the headline, not as it)")
     ap.add_argument("--cpu-sample-rows", type=int, default=262144)
     ap.add_argument("--cpu-sample-queries", type=int, default=4)
     ap.add_argument("--sweep", action="store_true",
@@ -249,7 +252,7 @@ def main():
     traffic = read_traffic(bytes_alg)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "kernel": "scan_mfma_kernel<4,1,1>",
+                "traffic": traffic, "kernel": "scan_mfma_kernel<4,1,1,bf16>",
                 "scan_ms": round(scan_s * 1e3, 4), "bytes_per_launch": int(bytes_alg)}
 
     # ---------------------------------------------------------------- CPU oracle baseline
@@ -279,6 +282,52 @@ def main():
                          f"(1/{scale:g} of N), normalise+score+sort+gather+merge, "
                          f"{c_el:.2f}s, rate scaled by {scale:g} to N={N}"}
 
+    # ---------------------------------------------------------------- fp8 key-pool variant
+    # The same workload on a pool of OCP E4M3 keys (a quantized store; the
+    # headline above is the paper's half-precision store).  Same appends,
+    # queries, gather and merge per step.
+    fp8 = None
+    if not args.no_fp8:
+        del lex_out, rp
+        pool8 = oil.Pool(d, N + extra, device=dev, key_format="fp8")
+        for s0 in range(0, N, chunk):
+            pool8.append(wp.raw_rows(s0, chunk), wp.tokens[s0:s0 + chunk].to(dev),
+                         wp.traces[s0:s0 + chunk].to(dev), wp.prompts[s0:s0 + chunk].to(dev))
+        pool8.workspace(B, k)
+
+        def step8(t):
+            a = app[t]
+            pool8.append(a[0], a[1], a[2], a[3])
+            pool8.query_topk(Qs[t], k, out=(out_s, out_i))
+            pool8.gather(out_i, out_s, rule, L, out=(ct, cl))
+            oil.merge_trees(anchors[t], None, None, 0, ct, cl, sem_budget, mx, out=tree)
+
+        for t in range(W):
+            step8(t)
+        torch.cuda.synchronize()
+        m0 = len(pool8)
+        oil.scan_timer_start(K)
+        torch.cuda.synchronize()
+        f0 = time.perf_counter()
+        for t in range(W, steps):
+            step8(t)
+        torch.cuda.synchronize()
+        f1 = time.perf_counter()
+        n8, ms8 = oil.scan_timer_stop()
+        m1 = len(pool8)
+        ld8 = (d + 127) // 128 * 128
+        b8 = (m0 + m1) / 2.0 * ld8 + B * ld8
+        s8 = ms8 / n8 / 1e3
+        fp8 = {"value": round(B * K / (f1 - f0), 1), "unit": "queries/s",
+               "ms_per_step": round(1e3 * (f1 - f0) / K, 4),
+               "scan_ms": round(s8 * 1e3, 4), "achieved": round(b8 / s8 / 1e9, 1), "unit_roofline": "GB/s",
+               "frac": round(b8 / s8 / 1e9 / HBM_PEAK_GBS, 4), "bytes_per_launch": int(b8),
+               "traffic": read_traffic(b8, PROFILE_TRAFFIC_FP8),
+               "kernel": "scan_mfma_kernel<4,1,1,fp8>",
+               "keys": "OCP FP8 E4M3, power-of-two scale per row (4 GiB at 1M x 4096)"}
+        log(f"fp8 pool: {K} steps in {(f1 - f0) * 1e3:.1f} ms; scan {s8 * 1e3:.4f} ms avg")
+        del pool8
+
     line = {
         "metric": METRIC, "value": round(qps, 1), "unit": "queries/s", "n_gpus": 1, "steps": K,
         "warmup": W, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
@@ -292,6 +341,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "extras": extras,
+        "fp8_variant": fp8,
     }
     print(json.dumps(line), flush=True)
 

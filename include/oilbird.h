@@ -54,6 +54,8 @@ enum { OIL_F32 = 0, OIL_BF16 = 1 };
 #define OIL_MAX_B 512
 #define OIL_MAX_NODES 256
 #define OIL_MAX_BANDS 4
+/* Largest query batch an fp8 pool serves. */
+#define OIL_MAX_B_FP8 64
 
 /* Limits of the exact-suffix lexical source: context tokens, drafts per
  * request, tokens per draft, and the candidate capacity per request. */
@@ -108,6 +110,25 @@ int32_t oil_pool_destroy(oil_pool *pool);
 
 /* (host) Number of stored positions, counted in enqueue order. */
 int32_t oil_pool_size(const oil_pool *pool, int64_t *n_valid);
+
+/* ---- fp8 key pool (the store bounded by quantization, which the paper's
+ * Limitations name as future work; not the paper's configuration).  Keys are
+ * normalised in double as for the bf16 pool, scaled by a power of two per row
+ * that puts the largest magnitude in [128, 256), and rounded to OCP FP8 E4M3
+ * (nearest, ties to even); queries likewise.  A score is the dot of the E4M3
+ * operands (fp32 accumulation of exact products) times the two inverse
+ * scales.  Keys are stored in 4 KiB tiles of 32 rows x 128 columns in the
+ * operand order of the 32x32x16 fp8 MFMA, window-major as in the bf16 pool,
+ * at half the bytes per row.  Append, query, gather and everything after
+ * them take an fp8 pool like a bf16 one; queries are limited to
+ * OIL_MAX_B_FP8 per call. */
+size_t oil_pool_key_bytes_fp8(int32_t dim, int64_t capacity);
+
+/* key_buf: oil_pool_key_bytes_fp8(dim, capacity) bytes, 256-byte aligned;
+ * scale_buf: capacity float32 (the inverse scale of each stored row); other
+ * buffers as for oil_pool_create. */
+int32_t oil_pool_create_fp8(int32_t dim, int64_t capacity, void *key_buf, float *scale_buf,
+                            int32_t *token_buf, int32_t *trace_buf, int32_t *prompt_buf, oil_pool **out);
 
 /* Append n positions at [n_valid, n_valid + n) (Sec. 4 (i), Eq. 1): each raw
  * key row is divided by its L2 norm (evaluated in double precision) and

@@ -899,14 +899,31 @@ int orc_scores_fp8(const uint8_t *kc, const double *kinv, int64_t n, int32_t d, 
 {
     if (!kc || !kinv || !qc || !qinv || !s || n < 0 || d < 1 || B < 1)
         return ORC_EINVAL;
+    /* decode every operand once, then exact double dots (products and sums of
+       E4M3 values at these magnitudes are exact in double) */
+    double *qv = (double *)malloc(sizeof(double) * (size_t)B * (size_t)d);
+    if (!qv)
+        return ORC_EINVAL;
+    for (int64_t e = 0; e < (int64_t)B * d; e++)
+        qv[e] = orc_e4m3_value(qc[e]);
+    int rc = ORC_OK;
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; i++) {
+        double *kv = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!kv) {
+            rc = ORC_EINVAL;
+            continue;
+        }
+        for (int32_t c = 0; c < d; c++)
+            kv[c] = orc_e4m3_value(kc[i * d + c]);
         for (int32_t b = 0; b < B; b++) {
-            double acc = 0.0; /* products and sums of E4M3 values are exact in double */
+            double acc = 0.0;
             for (int32_t c = 0; c < d; c++)
-                acc += orc_e4m3_value(kc[i * d + c]) * orc_e4m3_value(qc[(int64_t)b * d + c]);
+                acc += kv[c] * qv[(int64_t)b * d + c];
             s[(int64_t)b * n + i] = acc * kinv[i] * qinv[b];
         }
+        free(kv);
     }
-    return ORC_OK;
+    free(qv);
+    return rc;
 }

@@ -25,6 +25,7 @@ LIB_PATH = os.path.join(_HERE, "liboilbird.so")
 
 OIL_F32, OIL_BF16 = 0, 1
 MAX_K, MAX_B, MAX_NODES, MAX_BANDS = 64, 512, 256, 4
+MAX_B_FP8 = 64
 LEX_MAX_CTX, LEX_MAX_N, LEX_MAX_LEN, LEX_MAX_CAND = 32, 16, 64, 4096
 REC_DEPTH, REC_MAX_OUT = 6, 8
 
@@ -78,6 +79,8 @@ def lib():
             "oil_key_stride": (i32, [i32]),
             "oil_pool_key_bytes": (sz, [i32, i64]),
             "oil_pool_create": (i32, [i32, i64, P, P, P, P, ctypes.POINTER(P)]),
+            "oil_pool_key_bytes_fp8": (sz, [i32, i64]),
+            "oil_pool_create_fp8": (i32, [i32, i64, P, P, P, P, P, ctypes.POINTER(P)]),
             "oil_pool_destroy": (i32, [P]),
             "oil_pool_size": (i32, [P, ctypes.POINTER(i64)]),
             "oil_pool_append": (i32, [P, P, i32, P, P, P, i64, P]),
@@ -276,21 +279,39 @@ def scan_timer_stop():
 
 # ---------------------------------------------------------------- convenience
 class Pool:
-    """A pool and the device buffers it lives in (torch tensors, caller-owned)."""
+    """A pool and the device buffers it lives in (torch tensors, caller-owned).
 
-    def __init__(self, dim: int, capacity: int, device="cuda", with_prompts: bool = True):
-        self.dim, self.capacity = dim, capacity
+    ``key_format`` is "bf16" (the paper's half-precision store) or "fp8" (OCP
+    E4M3 keys with a power-of-two scale per row)."""
+
+    def __init__(self, dim: int, capacity: int, device="cuda", with_prompts: bool = True,
+                 key_format: str = "bf16"):
+        self.dim, self.capacity, self.key_format = dim, capacity, key_format
         self.device = torch.device(device)
-        self.stride = key_stride(dim)
-        # tiled bf16 storage (see oil_pool_key_bytes); torch's caching allocator
-        # aligns blocks to >= 512 bytes
-        nbytes = pool_key_bytes(dim, capacity)
-        self.keys = torch.empty((nbytes // 2,), dtype=torch.bfloat16, device=self.device)
         self.tokens = torch.empty((capacity,), dtype=torch.int32, device=self.device)
         self.traces = torch.empty((capacity,), dtype=torch.int32, device=self.device)
         self.prompts = (torch.empty((capacity,), dtype=torch.int32, device=self.device)
                         if with_prompts else None)
-        self.handle = pool_create(dim, capacity, self.keys, self.tokens, self.traces, self.prompts)
+        if key_format == "bf16":
+            self.stride = key_stride(dim)
+            # tiled bf16 storage (see oil_pool_key_bytes); torch's caching allocator
+            # aligns blocks to >= 512 bytes
+            nbytes = pool_key_bytes(dim, capacity)
+            self.keys = torch.empty((nbytes // 2,), dtype=torch.bfloat16, device=self.device)
+            self.scales = None
+            self.handle = pool_create(dim, capacity, self.keys, self.tokens, self.traces, self.prompts)
+        elif key_format == "fp8":
+            nbytes = lib().oil_pool_key_bytes_fp8(dim, capacity)
+            self.stride = (dim + 127) // 128 * 128
+            self.keys = torch.empty((nbytes,), dtype=torch.uint8, device=self.device)
+            self.scales = torch.empty((capacity,), dtype=torch.float32, device=self.device)
+            h = ctypes.c_void_p()
+            _check("oil_pool_create_fp8", lib().oil_pool_create_fp8(
+                dim, capacity, _ptr(self.keys), _ptr(self.scales), _ptr(self.tokens), _ptr(self.traces),
+                _ptr(self.prompts), ctypes.byref(h)))
+            self.handle = h
+        else:
+            raise ValueError(f"key_format must be 'bf16' or 'fp8', got {key_format!r}")
         self._ws = {}
 
     def __del__(self):

@@ -26,10 +26,12 @@ struct oil_recycle {
 };
 
 struct oil_pool {
-    int32_t dim, ld;
+    int32_t dim, ld;  // ld: padded row width in elements of the key format
     int64_t capacity, n_valid;
-    int64_t rs, ws;  // tile strides of the key buffer (elements)
+    int64_t rs, ws;   // tile strides of the key buffer, in 16-bit units
+    int fmt;          // oil::kKeyBf16 or oil::kKeyFp8
     uint16_t* keys;
+    float* kscale;    // fp8: inverse scale per row
     int32_t *tokens, *traces, *prompts;
 };
 
@@ -52,7 +54,10 @@ QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
 {
     QueryWorkspace w;
     const int tiles = oil::scan_query_tiles(B);
-    const size_t q_bytes = (size_t)tiles * 32 * (size_t)p->ld * sizeof(uint16_t);
+    // queries (MFMA fragments or rows) plus, for fp8, one inverse scale per fragment row
+    const size_t q_bytes = p->fmt == oil::kKeyFp8
+                               ? (size_t)tiles * 32 * (size_t)p->ld + (size_t)tiles * 32 * sizeof(float)
+                               : (size_t)tiles * 32 * (size_t)p->ld * sizeof(uint16_t);
     const size_t sc_bytes = (size_t)B * (size_t)k * oil::kRowBlock * sizeof(float);
     w.g_ld = oil::topk_block_ld(p->capacity);
     const size_t g_bytes = (size_t)B * (size_t)w.g_ld * sizeof(uint64_t);
@@ -152,6 +157,7 @@ int32_t oil_pool_create(int32_t dim, int64_t capacity, void* key_buf, int32_t* t
     oil_pool* p = (oil_pool*)calloc(1, sizeof(oil_pool));
     if (!p)
         return OIL_E_INVALID;
+    p->fmt = oil::kKeyBf16;
     p->dim = dim;
     p->ld = oil_key_stride(dim);
     p->capacity = capacity;
@@ -160,6 +166,42 @@ int32_t oil_pool_create(int32_t dim, int64_t capacity, void* key_buf, int32_t* t
     p->rs = 2048;
     p->ws = 2048 * (int64_t)round_up((size_t)capacity, oil::kRowBlock) / oil::kRowBlock;
     p->keys = (uint16_t*)key_buf;
+    p->tokens = token_buf;
+    p->traces = trace_buf;
+    p->prompts = prompt_buf;
+    *out = p;
+    return OIL_OK;
+}
+
+size_t oil_pool_key_bytes_fp8(int32_t dim, int64_t capacity)
+{
+    if (dim < 1 || capacity < 1)
+        return 0;
+    return round_up((size_t)dim, oil::kWindowFp8) * round_up((size_t)capacity, oil::kRowBlock);
+}
+
+int32_t oil_pool_create_fp8(int32_t dim, int64_t capacity, void* key_buf, float* scale_buf,
+                            int32_t* token_buf, int32_t* trace_buf, int32_t* prompt_buf, oil_pool** out)
+{
+    if (!out)
+        return OIL_E_INVALID;
+    *out = nullptr;
+    if (dim < 1 || dim > (1 << 20) || capacity < 1 || capacity > INT32_MAX || !key_buf || !scale_buf ||
+        !token_buf || !trace_buf || !aligned(key_buf, kAlign))
+        return OIL_E_INVALID;
+    oil_pool* p = (oil_pool*)calloc(1, sizeof(oil_pool));
+    if (!p)
+        return OIL_E_INVALID;
+    p->fmt = oil::kKeyFp8;
+    p->dim = dim;
+    p->ld = (int32_t)round_up((size_t)dim, oil::kWindowFp8);
+    p->capacity = capacity;
+    p->n_valid = 0;
+    // the same 4 KiB window-major tiles as the bf16 pool, 128 fp8 columns each
+    p->rs = 2048;
+    p->ws = 2048 * (int64_t)round_up((size_t)capacity, oil::kRowBlock) / oil::kRowBlock;
+    p->keys = (uint16_t*)key_buf;
+    p->kscale = scale_buf;
     p->tokens = token_buf;
     p->traces = trace_buf;
     p->prompts = prompt_buf;
@@ -196,10 +238,17 @@ int32_t oil_pool_append(oil_pool* pool, const void* keys, int32_t key_dtype, con
         return OIL_E_INVALID;
     if (n > pool->capacity - pool->n_valid)
         return OIL_E_CAPACITY;
-    hipError_t e = oil::launch_normalize_rows(
-        keys, key_dtype, pool->dim, n, n, pool->keys, pool->n_valid, pool->ld, oil::kLayoutTiled,
-        pool->rs, pool->ws,
-        tokens, trace_ids, prompt_ids, pool->tokens, pool->traces, pool->prompts, (hipStream_t)stream);
+    hipError_t e;
+    if (pool->fmt == oil::kKeyFp8)
+        e = oil::launch_quantize_rows(keys, key_dtype, pool->dim, n, n, (uint8_t*)pool->keys, pool->n_valid,
+                                      pool->ld, 2 * pool->rs, 2 * pool->ws, pool->kscale, tokens, trace_ids,
+                                      prompt_ids, pool->tokens, pool->traces, pool->prompts,
+                                      (hipStream_t)stream);
+    else
+        e = oil::launch_normalize_rows(
+            keys, key_dtype, pool->dim, n, n, pool->keys, pool->n_valid, pool->ld, oil::kLayoutTiled,
+            pool->rs, pool->ws,
+            tokens, trace_ids, prompt_ids, pool->tokens, pool->traces, pool->prompts, (hipStream_t)stream);
     if (e != hipSuccess)
         return OIL_E_HIP;
     pool->n_valid += n;
@@ -220,7 +269,7 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
     if (!pool || !queries || !scores || !idx || B < 1 || k < 1 ||
         (q_dtype != OIL_F32 && q_dtype != OIL_BF16) || !aligned(queries, 16))
         return OIL_E_INVALID;
-    if (B > OIL_MAX_B || k > OIL_MAX_K)
+    if (B > OIL_MAX_B || k > OIL_MAX_K || (pool->fmt == oil::kKeyFp8 && B > OIL_MAX_B_FP8))
         return OIL_E_UNSUPPORTED;
     if (exclude_prompt && !pool->prompts)
         return OIL_E_INVALID;
@@ -236,16 +285,24 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
     uint64_t* cb = (uint64_t*)(ws + w.cb_off);
     const int64_t n_valid = pool->n_valid;
 
-    const bool mfma = oil::scan_uses_mfma(B, pool->ld);
+    const bool fp8 = pool->fmt == oil::kKeyFp8;
+    const bool mfma = fp8 || oil::scan_uses_mfma(B, pool->ld);
     const int tiles = oil::scan_query_tiles(B);
-    hipError_t e = oil::launch_normalize_rows(
-        queries, q_dtype, pool->dim, B, mfma ? (int64_t)tiles * 32 : B, qbuf, 0, pool->ld,
-        mfma ? oil::kLayoutTiled : oil::kLayoutRows, 2048, 2048 * (int64_t)tiles, nullptr, nullptr,
-        nullptr, nullptr, nullptr, nullptr, st);
+    float* qscale = fp8 ? (float*)(ws + w.q_off + (size_t)tiles * 32 * (size_t)pool->ld) : nullptr;
+    hipError_t e;
+    if (fp8)
+        e = oil::launch_quantize_rows(queries, q_dtype, pool->dim, B, (int64_t)tiles * 32, (uint8_t*)qbuf, 0,
+                                      pool->ld, 4096, 4096 * (int64_t)tiles, qscale, nullptr, nullptr, nullptr,
+                                      nullptr, nullptr, nullptr, st);
+    else
+        e = oil::launch_normalize_rows(
+            queries, q_dtype, pool->dim, B, mfma ? (int64_t)tiles * 32 : B, qbuf, 0, pool->ld,
+            mfma ? oil::kLayoutTiled : oil::kLayoutRows, 2048, 2048 * (int64_t)tiles, nullptr, nullptr,
+            nullptr, nullptr, nullptr, nullptr, st);
     if (e == hipSuccess) {
         timer_mark(st, 0);
         e = oil::launch_scan(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, pool->prompts,
-                             exclude_prompt, G, w.g_ld, st);
+                             exclude_prompt, G, w.g_ld, st, pool->fmt, pool->kscale, qscale);
         timer_mark(st, 1);
         if (g_timer.ev && g_timer.used < g_timer.cap)
             g_timer.used++;
@@ -255,7 +312,7 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
         e = oil::launch_topk_blocks(G, w.g_ld, n_valid, B, k, ca, cb, &chosen, st);
     if (e == hipSuccess)
         e = oil::launch_rescore(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, chosen, k,
-                                pool->prompts, exclude_prompt, SC, st);
+                                pool->prompts, exclude_prompt, SC, st, pool->fmt, pool->kscale, qscale);
     if (e == hipSuccess)
         e = oil::launch_topk_final(chosen, B, k, SC, n_valid, scores, idx, st);
     return hip_status(e);

@@ -14,6 +14,7 @@
 #define OIL_LEX_CAND_MAX 4096
 #define OIL_REC_DEPTH_MAX 6
 #define OIL_REC_OUT_MAX 8
+#define OIL_MAX_B_FP8 64
 
 namespace oil {
 
@@ -29,7 +30,11 @@ enum { kLayoutRows = 0, kLayoutTiled = 1 };
 
 // Key pool geometry: rows in blocks of 32, columns padded to 64.
 constexpr int kRowBlock = 32;
-constexpr int kWindow = 64;
+constexpr int kWindow = 64;      // bf16 columns per 4 KiB tile (32 rows)
+constexpr int kWindowFp8 = 128;  // fp8 columns per 4 KiB tile (32 rows)
+
+// Key formats of a pool.
+enum { kKeyBf16 = 0, kKeyFp8 = 1 };
 
 hipError_t launch_normalize_rows(const void* raw, int dtype, int32_t d, int64_t n_rows_in,
                                  int64_t n_rows_out, uint16_t* out, int64_t row_offset, int32_t ld,
@@ -39,13 +44,25 @@ hipError_t launch_normalize_rows(const void* raw, int dtype, int32_t d, int64_t 
 
 int scan_uses_mfma(int32_t B, int32_t ld);
 int scan_query_tiles(int32_t B);
+// fmt: kKeyBf16, or kKeyFp8 (B <= 64; ld = fp8 row width, a multiple of
+// 128; kscale per stored row and qscale per query are the inverse scales).
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
-                       uint64_t* G, int64_t g_ld, hipStream_t stream);
+                       uint64_t* G, int64_t g_ld, hipStream_t stream, int fmt = kKeyBf16,
+                       const float* kscale = nullptr, const float* qscale = nullptr);
 hipError_t launch_rescore(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                           const void* qbuf, int32_t B, const uint64_t* blocks, int32_t k,
                           const int32_t* prompt, const int32_t* exclude, float* SC,
-                          hipStream_t stream);
+                          hipStream_t stream, int fmt = kKeyBf16, const float* kscale = nullptr,
+                          const float* qscale = nullptr);
+// Quantize raw rows to the fp8 store format (normalise in double, per-row
+// power-of-two scale putting the largest magnitude in [128, 256), E4M3
+// nearest-even) into 4 KiB fp8 tiles (rs_bytes, ws_bytes) or rows.
+hipError_t launch_quantize_rows(const void* raw, int dtype, int32_t d, int64_t n_rows_in, int64_t n_rows_out,
+                                uint8_t* out, int64_t row_offset, int32_t ld8, int64_t rs_bytes,
+                                int64_t ws_bytes, float* inv_scale, const int32_t* tok_in,
+                                const int32_t* trace_in, const int32_t* prompt_in, int32_t* tok_out,
+                                int32_t* trace_out, int32_t* prompt_out, hipStream_t stream);
 
 int64_t topk_chunks(int64_t n);
 int64_t topk_block_ld(int64_t capacity);

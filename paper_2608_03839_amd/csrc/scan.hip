@@ -139,6 +139,23 @@ __global__ __launch_bounds__(256) void scan_gemv_kernel(
 }
 
 // ----------------------------------------------------------------- MFMA (4 < B <= 64)
+// One 16-byte operand register per lane and sub-step: eight bf16 (one
+// 32x32x16 bf16 MFMA), or sixteen OCP E4M3 values (two 32x32x16 fp8 MFMAs,
+// the low 8 bytes first: columns 32 p .. 32 p + 15, then 32 p + 16 .. + 31 of
+// a 128-column fp8 window).
+template <int FMT>
+__device__ __forceinline__ floatx16 mfma_step(const bf16x8& a, const bf16x8& b, floatx16 acc)
+{
+    if constexpr (FMT == kKeyBf16) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+    } else {
+        typedef long long2v __attribute__((ext_vector_type(2)));
+        const long2v a2 = __builtin_bit_cast(long2v, a), b2 = __builtin_bit_cast(long2v, b);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(a2[0], b2[0], acc, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(a2[1], b2[1], acc, 0, 0, 0);
+    }
+}
+
 template <int MT, int NT>
 __device__ __forceinline__ void load_window(bf16x8 (&a)[MT][4], bf16x8 (&b)[NT][4],
                                             const bf16x8* const (&tile)[MT], int64_t ws8,
@@ -156,11 +173,12 @@ __device__ __forceinline__ void load_window(bf16x8 (&a)[MT][4], bf16x8 (&b)[NT][
             b[nt][s] = qf[(((int64_t)w * NT + nt) * 4 + s) * 64];
 }
 
-template <int MT, int NT, int PF>
+template <int MT, int NT, int PF, int FMT>
 __global__ __launch_bounds__(256) void scan_mfma_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
-    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld)
+    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld,
+    const float* __restrict__ kscale, const float* __restrict__ qscale)
 {
     constexpr int NS = PF + 1;
     const int lane = threadIdx.x & 63;
@@ -169,7 +187,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     if (rb0 * kRowBlock >= n_valid)
         return;
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
-    const int nwin = ld / kWindow;
+    const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
     const int64_t ws8 = ws / 8;
 
     const bf16x8* tile[MT];
@@ -204,8 +222,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
                     for (int mt = 0; mt < MT; mt++)
 #pragma unroll
                         for (int nt = 0; nt < NT; nt++)
-                            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                a[u][mt][s], b[u][nt][s], acc[mt][nt], 0, 0, 0);
+                            acc[mt][nt] = mfma_step<FMT>(a[u][mt][s], b[u][nt][s], acc[mt][nt]);
             }
         }
     }
@@ -218,6 +235,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
         const int qb = nt * 32 + r;
         const bool qlive = qb < B;
         const int32_t ex = (exclude && qlive) ? exclude[qb] : -1;
+        const float qs = (FMT == kKeyBf16 || !qlive) ? 1.f : qscale[qb];
 #pragma unroll
         for (int mt = 0; mt < MT; mt++) {
             const int64_t rb = rb0 + mt;
@@ -229,6 +247,8 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
                 for (int j = 0; j < 4; j++) {
                     if (row + j < n_valid) {
                         float v = acc[mt][nt][4 * i + j];
+                        if constexpr (FMT == kKeyFp8)
+                            v = v * (kscale[row + j] * qs);  // powers of two: exact
                         if (ex >= 0)
                             v = masked_score(v, row + j, ex, prompt);
                         const uint64_t key = rank_key(v, (uint32_t)(row + j));
@@ -401,11 +421,12 @@ __global__ __launch_bounds__(256) void scan_mfma_wide_kernel(
 // in order, sub-steps in order, starting from zero) on the block's tile and
 // the query's 32-query fragment tile, so element (row, query) is bit-identical
 // to the scan's; the wave keeps the query's column.
-template <int PF>
+template <int PF, int FMT>
 __global__ __launch_bounds__(64) void rescore_mfma_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const bf16x8* __restrict__ qfrag, int n_qtiles, const uint64_t* __restrict__ blocks, int k,
-    const int32_t* __restrict__ prompt, const int32_t* __restrict__ exclude, float* __restrict__ SC)
+    const int32_t* __restrict__ prompt, const int32_t* __restrict__ exclude, float* __restrict__ SC,
+    const float* __restrict__ kscale, const float* __restrict__ qscale)
 {
     constexpr int NS = PF + 1;
     const int slot = blockIdx.x, qb = blockIdx.y, lane = threadIdx.x;
@@ -419,7 +440,7 @@ __global__ __launch_bounds__(64) void rescore_mfma_kernel(
     }
     const int64_t rb = key_pos(bk) / kRowBlock;
     const int t = qb >> 5, n = qb & 31;
-    const int nwin = ld / kWindow;
+    const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
     const int64_t ws8 = ws / 8;
     const bf16x8* tile = (const bf16x8*)(keys + rb * rs) + lane;
     const bf16x8* qf = qfrag + lane;
@@ -444,7 +465,7 @@ __global__ __launch_bounds__(64) void rescore_mfma_kernel(
             if (w0 + u < nwin) {
 #pragma unroll
                 for (int s = 0; s < 4; s++)
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[u][s], b[u][s], acc, 0, 0, 0);
+                    acc = mfma_step<FMT>(a[u][s], b[u][s], acc);
             }
         }
     }
@@ -458,6 +479,9 @@ __global__ __launch_bounds__(64) void rescore_mfma_kernel(
             const int rr = i * 8 + h * 4 + j;
             const int64_t row = rb * kRowBlock + rr;
             float v = acc[4 * i + j];
+            if constexpr (FMT == kKeyFp8)
+                if (row < n_valid)
+                    v = v * (kscale[row] * qscale[qb]);  // as the scan scales it
             if (row >= n_valid)
                 v = __uint_as_float(kNoScoreBits);
             else if (ex >= 0)
@@ -544,11 +568,24 @@ static void launch_gemv(dim3 g, size_t lds, hipStream_t st, const uint16_t* keys
 
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
-                       uint64_t* G, int64_t g_ld, hipStream_t stream)
+                       uint64_t* G, int64_t g_ld, hipStream_t stream, int fmt, const float* kscale,
+                       const float* qscale)
 {
     if (n_valid <= 0)
         return hipSuccess;
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
+    if (fmt == kKeyFp8) {  // B <= 64 (checked by the caller)
+        constexpr int MT = 4, PF = 1;
+        const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
+        const bf16x8* qf = (const bf16x8*)qbuf;
+        if (scan_query_tiles(B) == 1)
+            hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyFp8>), g, dim3(256), 0, stream, keys, ld, rs,
+                               ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+        else
+            hipLaunchKernelGGL((scan_mfma_kernel<MT, 2, PF, kKeyFp8>), g, dim3(256), 0, stream, keys, ld, rs,
+                               ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+        return hipGetLastError();
+    }
     if (!scan_uses_mfma(B, ld)) {
         const dim3 g((unsigned)((n_rb + 3) / 4));
         const size_t lds = (size_t)B * ld * sizeof(uint16_t);
@@ -580,25 +617,31 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
     constexpr int MT = 4, PF = 1;
     const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
     if (scan_query_tiles(B) == 1)
-        hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF>), g, dim3(256), 0, stream, keys, ld, rs, ws,
-                           n_valid, qf, B, prompt, exclude, G, g_ld);
+        hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyBf16>), g, dim3(256), 0, stream, keys, ld, rs, ws,
+                           n_valid, qf, B, prompt, exclude, G, g_ld, nullptr, nullptr);
     else
-        hipLaunchKernelGGL((scan_mfma_kernel<MT, 2, PF>), g, dim3(256), 0, stream, keys, ld, rs, ws,
-                           n_valid, qf, B, prompt, exclude, G, g_ld);
+        hipLaunchKernelGGL((scan_mfma_kernel<MT, 2, PF, kKeyBf16>), g, dim3(256), 0, stream, keys, ld, rs, ws,
+                           n_valid, qf, B, prompt, exclude, G, g_ld, nullptr, nullptr);
     return hipGetLastError();
 }
 
 hipError_t launch_rescore(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                           const void* qbuf, int32_t B, const uint64_t* blocks, int32_t k,
-                          const int32_t* prompt, const int32_t* exclude, float* SC, hipStream_t stream)
+                          const int32_t* prompt, const int32_t* exclude, float* SC, hipStream_t stream,
+                          int fmt, const float* kscale, const float* qscale)
 {
     const dim3 g((unsigned)k, (unsigned)B);
-    if (!scan_uses_mfma(B, ld))
+    if (fmt == kKeyFp8)
+        hipLaunchKernelGGL((rescore_mfma_kernel<3, kKeyFp8>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
+                           (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC, kscale,
+                           qscale);
+    else if (!scan_uses_mfma(B, ld))
         hipLaunchKernelGGL((rescore_gemv_kernel<3>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
                            (const uint16_t*)qbuf, blocks, k, prompt, exclude, SC);
     else
-        hipLaunchKernelGGL((rescore_mfma_kernel<3>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
-                           (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC);
+        hipLaunchKernelGGL((rescore_mfma_kernel<3, kKeyBf16>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
+                           (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC, nullptr,
+                           nullptr);
     return hipGetLastError();
 }
 

@@ -69,3 +69,104 @@ hipError_t launch_normalize_rows(const void* raw, int dtype, int32_t d, int64_t 
 }
 
 }  // namespace oil
+
+namespace oil {
+
+// Nearest OCP E4M3 code of v (|v| <= 448: larger magnitudes saturate to
+// 448), ties to the even code.  The representable magnitudes are multiples of
+// 2^(E - 3) in [2^E, 2^(E + 1)) for E >= -6 and of 2^-9 below 2^-6; scaling by
+// the spacing is exact, so one rint (nearest-even) does the rounding.  The
+// multiple r lands in [8, 16] (16 carries into the next binade) or, below
+// 2^-6, in [0, 8]; either way the code's low 7 bits are ((E + 7) << 3) + r - 8
+// or r.
+__device__ __forceinline__ uint8_t double_to_e4m3_rne(double v)
+{
+    const uint8_t sign = __double_as_longlong(v) < 0 ? 0x80 : 0;
+    const double a = fabs(v);
+    if (!(a < 448.0))
+        return (uint8_t)(sign | 0x7E);
+    if (a >= 0x1p-6) {
+        const int E = ilogb(a);
+        const double r = rint(ldexp(a, 3 - E));
+        return (uint8_t)(sign | (uint8_t)(((E + 7) << 3) + (int)r - 8));
+    }
+    return (uint8_t)(sign | (uint8_t)rint(ldexp(a, 9)));
+}
+
+// fp8 tile layout (bytes): rows in blocks of 32, columns in windows of 128;
+// each (row block, window) pair is a 4 KiB tile in the operand order of the
+// 32x32x16 fp8 MFMA, two operands per 16-byte lane load:
+//   (i / 32) * rs + (j / 128) * ws + (p * 64 + lane) * 16 + hh * 8 + e,
+//   s = (j % 128) / 16, p = s / 2, hh = s % 2, e = j % 8,
+//   lane = i % 32 + 32 * ((j % 16) / 8).
+__device__ __forceinline__ int64_t fp8_offset(int64_t i, int32_t j, int64_t rs, int64_t ws)
+{
+    const int jw = j & 127, s = jw >> 4, p = s >> 1, hh = s & 1, e = jw & 7;
+    const int lane = (int)(i & 31) + 32 * ((jw >> 3) & 1);
+    return (i >> 5) * rs + (int64_t)(j >> 7) * ws + (p * 64 + lane) * 16 + hh * 8 + e;
+}
+
+__global__ __launch_bounds__(256) void quantize_rows_kernel(
+    const void* __restrict__ raw, int dtype, int32_t d, int64_t n_rows_in, uint8_t* __restrict__ out,
+    int64_t row_offset, int32_t ld8, int64_t rs, int64_t ws, float* __restrict__ inv_scale,
+    const int32_t* __restrict__ tok_in, const int32_t* __restrict__ trace_in,
+    const int32_t* __restrict__ prompt_in, int32_t* __restrict__ tok_out, int32_t* __restrict__ trace_out,
+    int32_t* __restrict__ prompt_out)
+{
+    __shared__ double red[4];
+    const int64_t r = blockIdx.x;
+    const bool live = r < n_rows_in;
+    const int64_t dst_row = row_offset + r;
+    const int t = threadIdx.x;
+    // the unit row in double, exactly as the bf16 store computes it
+    double ss = 0.0;
+    if (live)
+        for (int32_t j = t; j < d; j += 256) {
+            const double x = load_raw(raw, dtype, r * d + j);
+            ss += x * x;
+        }
+    const double norm = sqrt(block_sum_256(ss, red));
+    double m = 0.0;
+    if (live && norm > 0.0)
+        for (int32_t j = t; j < d; j += 256)
+            m = fmax(m, fabs(load_raw(raw, dtype, r * d + j) / norm));
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        m = fmax(m, __shfl_xor(m, o, kWave));
+    if ((t & 63) == 0)
+        red[t >> 6] = m;
+    __syncthreads();
+    m = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+    const int shift = m > 0.0 ? 7 - ilogb(m) : 0;  // largest magnitude in [128, 256)
+    for (int32_t j = t; j < ld8; j += 256) {
+        uint8_t c = 0;
+        if (live && j < d && norm > 0.0)
+            c = double_to_e4m3_rne(ldexp(load_raw(raw, dtype, r * d + j) / norm, shift));
+        out[rs > 0 ? fp8_offset(dst_row, j, rs, ws) : dst_row * ld8 + j] = c;
+    }
+    if (t == 0) {
+        inv_scale[dst_row] = live ? ldexpf(1.f, -shift) : 1.f;
+        if (live && tok_out) {
+            tok_out[dst_row] = tok_in[r];
+            trace_out[dst_row] = trace_in[r];
+            if (prompt_out)
+                prompt_out[dst_row] = prompt_in[r];
+        }
+    }
+}
+
+hipError_t launch_quantize_rows(const void* raw, int dtype, int32_t d, int64_t n_rows_in, int64_t n_rows_out,
+                                uint8_t* out, int64_t row_offset, int32_t ld8, int64_t rs_bytes,
+                                int64_t ws_bytes, float* inv_scale, const int32_t* tok_in,
+                                const int32_t* trace_in, const int32_t* prompt_in, int32_t* tok_out,
+                                int32_t* trace_out, int32_t* prompt_out, hipStream_t stream)
+{
+    if (n_rows_out <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)n_rows_out), dim3(256), 0, stream, raw, dtype, d,
+                       n_rows_in, out, row_offset, ld8, rs_bytes, ws_bytes, inv_scale, tok_in, trace_in,
+                       prompt_in, tok_out, trace_out, prompt_out);
+    return hipGetLastError();
+}
+
+}  // namespace oil

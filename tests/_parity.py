@@ -33,6 +33,22 @@ def untile_keys(buf_bits, n, dim, capacity):
     return np.ascontiguousarray(rows[:n, :dim])
 
 
+def untile_keys_fp8(buf, n, dim, capacity):
+    """Rows [0, n) of a tiled fp8 key buffer (numpy uint8), as an (n, dim) array.
+
+    Layout: 4 KiB tiles of 32 rows x 128 columns ordered (register p, lane =
+    row % 32 + 32 * ((col % 16) // 8), half hh, element e) with column
+    (p * 2 + hh) * 16 + ((col % 16) // 8) * 8 + e inside the window, stored
+    window-major like the bf16 tiles."""
+    ld = (dim + 127) // 128 * 128
+    R = (capacity + 31) // 32
+    t = np.asarray(buf)[: R * 32 * ld].reshape(ld // 128, R, 4, 2, 32, 2, 8)
+    # axes: window, row block, p, lane half, row in block, hh, e
+    # column in window = p * 32 + hh * 16 + half * 8 + e
+    rows = t.transpose(1, 4, 0, 2, 5, 3, 6).reshape(R * 32, ld)
+    return np.ascontiguousarray(rows[:n, :dim])
+
+
 def oracle_rows(keys_bits, raw_q, prompt=None, exclude=None):
     """Oracle scores of every position (excluded -> -inf) for each raw query."""
     q = oracle.normalize_rows(raw_q)

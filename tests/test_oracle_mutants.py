@@ -48,6 +48,7 @@ MUTANTS = {
     "fp8 scale one binade up": ("int shift = m > 0.0 ? 7 - e : 0;", "int shift = m > 0.0 ? 8 - e : 0;"),
     "e4m3 subnormal spacing halved": ("        spacing = ldexp(1.0, -9);", "        spacing = ldexp(1.0, -10);"),
     "fp8 score drops the query scale": ("s[(int64_t)b * n + i] = acc * kinv[i] * qinv[b];", "s[(int64_t)b * n + i] = acc * kinv[i];"),
+    "fp8 score drops the last dim": ("            for (int32_t c = 0; c < d; c++)\n                acc += kv[c]", "            for (int32_t c = 0; c < d - 1; c++)\n                acc += kv[c]"),
     "recycled ties by newest": ("    return (a->seq < b->seq) ? -1 : (a->seq > b->seq);", "    return (a->seq > b->seq) ? -1 : (a->seq < b->seq);"),
 }
 
