@@ -60,6 +60,44 @@ __device__ __forceinline__ void insert_chain(int32_t (&ntok)[kSlotsPerLane], int
     }
 }
 
+// Copy the tree's six input arrays from global memory to LDS with one wave:
+// their elements are taken as one concatenated index range, eight loads per
+// lane in flight at clamped (always valid) addresses, then the stores.  An
+// empty array (which may be NULL) owns no index.
+__device__ __forceinline__ void stage_lds(const int32_t* const (&src)[6], int32_t* const (&dst)[6],
+                                          const int (&n)[6])
+{
+    constexpr int kU = 8;
+    const int lane = threadIdx.x;
+    int end[6], total = 0;
+#pragma unroll
+    for (int a = 0; a < 6; a++) {
+        total += n[a];
+        end[a] = total;
+    }
+    for (int i0 = 0; i0 < total; i0 += 64 * kU) {
+        int32_t v[kU];
+        int32_t* to[kU];
+#pragma unroll
+        for (int u = 0; u < kU; u++) {
+            const int i = min(i0 + u * 64 + lane, total - 1);
+            int a = 0, base = 0;
+#pragma unroll
+            for (int q = 0; q < 5; q++)
+                if (i >= end[q]) {
+                    a = q + 1;
+                    base = end[q];
+                }
+            v[u] = src[a][i - base];
+            to[u] = dst[a] + (i - base);
+        }
+#pragma unroll
+        for (int u = 0; u < kU; u++)
+            if (i0 + u * 64 + lane < total)
+                *to[u] = v[u];
+    }
+}
+
 __global__ __launch_bounds__(64) void merge_kernel(
     const int32_t* __restrict__ anchor, const int32_t* __restrict__ lex_tokens,
     const int32_t* __restrict__ lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
@@ -78,21 +116,12 @@ __global__ __launch_bounds__(64) void merge_kernel(
     int32_t* rlen_s = slen_s + k;
     const int b = blockIdx.x, lane = threadIdx.x;
     {
-        const int32_t* rt = rec_tokens + (int64_t)b * n_rec * L_rec;
-        for (int i = lane; i < n_rec * L_rec; i += 64)
-            rec_s[i] = rt[i];
-        for (int i = lane; i < n_rec; i += 64)
-            rlen_s[i] = rec_len[(int64_t)b * n_rec + i];
-        const int32_t* lt = lex_tokens + (int64_t)b * n_lex * L_lex;
-        for (int i = lane; i < n_lex * L_lex; i += 64)
-            lex_s[i] = lt[i];
-        const int32_t* st = sem_tokens + (int64_t)b * k * L;
-        for (int i = lane; i < k * L; i += 64)
-            sem_s[i] = st[i];
-        for (int i = lane; i < n_lex; i += 64)
-            llen_s[i] = lex_len[(int64_t)b * n_lex + i];
-        for (int i = lane; i < k; i += 64)
-            slen_s[i] = sem_len[(int64_t)b * k + i];
+        const int32_t* const src[6] = {lex_tokens + (int64_t)b * n_lex * L_lex, sem_tokens + (int64_t)b * k * L,
+                                       rec_tokens + (int64_t)b * n_rec * L_rec, lex_len + (int64_t)b * n_lex,
+                                       sem_len + (int64_t)b * k, rec_len + (int64_t)b * n_rec};
+        int32_t* const dst[6] = {lex_s, sem_s, rec_s, llen_s, slen_s, rlen_s};
+        const int n[6] = {n_lex * L_lex, k * L, n_rec * L_rec, n_lex, k, n_rec};
+        stage_lds(src, dst, n);
     }
     __syncthreads();
 

@@ -39,6 +39,20 @@
 #include "common.hpp"
 #include "internal.hpp"
 
+// Row blocks per wave and prefetch depth of the scans for B <= 64.
+#ifndef OIL_BF16_MT
+#define OIL_BF16_MT 4
+#endif
+#ifndef OIL_BF16_PF
+#define OIL_BF16_PF 1
+#endif
+#ifndef OIL_FP8_MT
+#define OIL_FP8_MT 2
+#endif
+#ifndef OIL_FP8_PF
+#define OIL_FP8_PF 1
+#endif
+
 namespace oil {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -575,7 +589,7 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
         return hipSuccess;
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
     if (fmt == kKeyFp8) {  // B <= 64 (checked by the caller)
-        constexpr int MT = 4, PF = 1;
+        constexpr int MT = OIL_FP8_MT, PF = OIL_FP8_PF;
         const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
         const bf16x8* qf = (const bf16x8*)qbuf;
         if (scan_query_tiles(B) == 1)
@@ -614,7 +628,7 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
                                stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
         return hipGetLastError();
     }
-    constexpr int MT = 4, PF = 1;
+    constexpr int MT = OIL_BF16_MT, PF = OIL_BF16_PF;
     const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
     if (scan_query_tiles(B) == 1)
         hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyBf16>), g, dim3(256), 0, stream, keys, ld, rs, ws,
