@@ -73,6 +73,9 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the step benchmark: retrieval calls on the same pool for "
                          "B in 1..512, one JSON line with the scan's GB/s and MFMA TFLOP/s per B")
+    ap.add_argument("--workloads", action="store_true",
+                    help="instead of the step benchmark: the single-stream decode, streaming-growth and "
+                         "full-draft-step workloads, one JSON line with their per-step latencies")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (3 launches), the reference "
                          "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
@@ -111,6 +114,8 @@ def main():
 
     if args.sweep:
         return sweep(args, oil, workloads, dev, cfg)
+    if args.workloads:
+        return other_workloads(args, oil, workloads, dev)
 
     # ---------------------------------------------------------------- inputs
     t0 = time.time()
@@ -241,6 +246,14 @@ def main():
         extras[name] = round(1e3 * e0.elapsed_time(e1) / K, 2)
     extras["recycle_records_per_insert"] = per_insert
     extras["mean_recycled_rollouts"] = round(float((rec_out[2] > 0).float().sum(1).mean()), 2)
+    # tree merges alone: one tree per query
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(K):
+        oil.merge_trees(anchors[-1], None, None, 0, ct, cl, sem_budget, mx, out=tree)
+    e1.record()
+    torch.cuda.synchronize()
+    extras["tree_merges_per_s"] = round(B * K / (1e-3 * e0.elapsed_time(e1)), 1)
     extras["mean_tree_nodes"] = round(float(tree[3].float().mean()), 2)
     extras["mean_accepted"] = round(float(walk_out[0].float().mean()), 2)
 
@@ -387,6 +400,123 @@ def sweep(args, oil, workloads, dev, cfg):
         log(f"B={B}: scan {scan_s * 1e3:.3f} ms, {gbs:.0f} GB/s, {tflops:.0f} TFLOP/s")
     print(json.dumps({"sweep": rows, "pool_rows": N, "dim": d, "k": k,
                       "kernels": "B<=4 scan_gemv, B<=64 scan_mfma, B>64 scan_mfma_wide"}), flush=True)
+
+
+def _timed(torch, fn, steps):
+    """Per-step wall time (ms) of fn(t) over the given step indices, synchronised around."""
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in steps:
+        fn(t)
+    torch.cuda.synchronize()
+    return 1e3 * (time.perf_counter() - t0) / len(steps)
+
+
+def other_workloads(args, oil, workloads, dev):
+    """Per-step latencies of the single-stream decode, streaming-growth and
+    full-draft-step workloads (synthetic, seeded; the workloads' parity cases
+    live in the GPU tests)."""
+    import torch
+    out = {}
+    K, W = 30, 3
+
+    # single-stream decode: N = 65,536, d = 4,096, one query per step, k = 16, L = 16, 64 nodes
+    cfg = workloads.DECODE_64K
+    ps, k, L, sb = cfg["pool"], cfg["k"], cfg["L"], cfg["sem_budget"]
+    wp = workloads.Pool(ps, device=dev)
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    pool.append(wp.raw_rows(0, ps.n), wp.tokens.to(dev), wp.traces.to(dev), wp.prompts.to(dev))
+    qs = [workloads.queries(wp, workloads.QuerySpec(B=1, noise=0.05, seed=500 + t)) for t in range(K + W)]
+    Q = [q.contiguous() for q, _ in qs]
+    A = [workloads.anchors(wp, src).to(dev) for _, src in qs]
+    rule = oil.DepthRule.fixed(L)
+
+    def dec(t):
+        s_, i_ = pool.query_topk(Q[t], k)
+        c_, l_ = pool.gather(i_, s_, rule, L)
+        oil.merge_trees(A[t], None, None, 0, c_, l_, sb, 1 + sb)
+
+    _timed(torch, dec, range(W))
+    out["decode_64k"] = {"ms_per_step": round(_timed(torch, dec, range(W, W + K)), 4),
+                         "step": "query top-16 + gather 16 + merge (64 nodes), B = 1"}
+    log(f"decode_64k: {out['decode_64k']['ms_per_step']} ms/step")
+    del pool, wp
+
+    # streaming growth: d = 5,120, 262,144 -> 2,097,152 positions, append 1-8 + 16 queries per step
+    cfg = workloads.STREAM_5120
+    ps, qsp, k = cfg["pool"], cfg["query"], cfg["k"]
+    wp = workloads.Pool(ps, device=dev)
+    checkpoints = [262144, 524288, 1048576, ps.n - 8 * (K + W)]
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    sizes = workloads.append_sizes(41, len(checkpoints) * (K + W)).view(len(checkpoints), K + W).tolist()
+    rows, at = [], 0
+    for j, c in enumerate(checkpoints):
+        for s0 in range(at, c, 65536):
+            m = min(65536, c - s0)
+            pool.append(wp.raw_rows(s0, m), wp.tokens[s0:s0 + m].to(dev), wp.traces[s0:s0 + m].to(dev),
+                        wp.prompts[s0:s0 + m].to(dev))
+        at = c
+        apps = []
+        for m in sizes[j]:
+            apps.append((wp.raw_rows(at, m), wp.tokens[at:at + m].to(dev), wp.traces[at:at + m].to(dev),
+                         wp.prompts[at:at + m].to(dev)))
+            at += m
+        q, _ = workloads.queries(wp, workloads.QuerySpec(B=qsp.B, noise=qsp.noise, p_random=qsp.p_random,
+                                                         seed=qsp.seed + j), n_valid=c)
+        q = q.contiguous()
+
+        def stream(t):
+            a = apps[t]
+            pool.append(a[0], a[1], a[2], a[3])
+            pool.query_topk(q, k)
+
+        _timed(torch, stream, range(W))
+        n0 = len(pool)
+        oil.scan_timer_start(K)
+        ms = _timed(torch, stream, range(W, W + K))
+        nt, sms = oil.scan_timer_stop()
+        n_mean = (n0 + len(pool)) / 2
+        scan_s = sms / nt / 1e3
+        gbs = (n_mean * ps.d * 2 + qsp.B * ps.d * 2) / scan_s / 1e9
+        rows.append({"pool_rows": int(n_mean), "ms_per_step": round(ms, 4), "scan_ms": round(scan_s * 1e3, 4),
+                     "scan_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)})
+        log(f"stream_5120 at {int(n_mean)}: {ms:.3f} ms/step, scan {gbs:.0f} GB/s")
+        at = c + sum(sizes[j])
+    out["stream_5120"] = {"checkpoints": rows, "step": "append 1-8 positions + query top-16 for 16 queries"}
+    del pool, wp
+
+    # full draft step: N = 524,288, d = 8,192, 64 queries: lexical drafts (GPU) + retrieval +
+    # gather (L = 12) + merge under 48 + 16 nodes
+    cfg = workloads.FULL_STEP_8192
+    ps, qsp, k, L = cfg["pool"], cfg["query"], cfg["k"], cfg["L"]
+    n_lex, L_lex, lb, sb = cfg["n_lex"], cfg["L_lex"], cfg["lex_budget"], cfg["sem_budget"]
+    wp = workloads.Pool(ps, device=dev)
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    for s0 in range(0, ps.n, 65536):
+        pool.append(wp.raw_rows(s0, 65536), wp.tokens[s0:s0 + 65536].to(dev),
+                    wp.traces[s0:s0 + 65536].to(dev), wp.prompts[s0:s0 + 65536].to(dev))
+    steps = []
+    for t in range(K + W):
+        q, src = workloads.queries(wp, workloads.QuerySpec(B=qsp.B, noise=qsp.noise, p_random=qsp.p_random,
+                                                           seed=qsp.seed + 11 * t))
+        ctx, cl, ex = workloads.lexical_contexts(wp, src, ps.n)
+        steps.append((q.contiguous(), workloads.anchors(wp, src).to(dev), ctx.to(dev), cl.to(dev), ex.to(dev)))
+    rule = oil.DepthRule.fixed(L)
+    mx = 1 + lb + sb
+
+    def full(t):
+        q, anc, ctx, cl, ex = steps[t]
+        lt, ll = pool.lexical(ctx, cl, n_lex, L_lex, ex)
+        s_, i_ = pool.query_topk(q, k, exclude_prompt=ex)
+        c_, l_ = pool.gather(i_, s_, rule, L)
+        oil.merge_trees(anc, lt, ll, lb, c_, l_, sb, mx)
+
+    _timed(torch, full, range(W))
+    ms = _timed(torch, full, range(W, W + K))
+    out["full_step_8192"] = {"ms_per_step": round(ms, 4), "trees_per_s": round(qsp.B / (ms / 1e3), 1),
+                             "step": "lexical drafts + query top-32 + gather 12 + merge (48 + 16 nodes), B = 64"}
+    log(f"full_step_8192: {ms:.3f} ms/step")
+    print(json.dumps({"workloads": out}), flush=True)
 
 
 if __name__ == "__main__":
