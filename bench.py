@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -39,7 +40,12 @@ def log(msg):
 
 
 def scan_source_hash():
-    return hashlib.sha256(open(SCAN_SRC, "rb").read()).hexdigest()[:16]
+    """Hash of the scan source's code: comments and whitespace do not count,
+    so a counter summary stays valid until the code itself changes."""
+    src = open(SCAN_SRC).read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return hashlib.sha256(" ".join(src.split()).encode()).hexdigest()[:16]
 
 
 def read_traffic(bytes_alg, path=PROFILE_TRAFFIC):

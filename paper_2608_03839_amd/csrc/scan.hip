@@ -25,10 +25,11 @@
 //  * scan_mfma_wide (64 < B <= 512): the same instruction, keys shared by all
 //    query tiles through LDS (the contraction turns MFMA-bound near B ~ 300).
 //
-// Both run a software pipeline: a ring of PF + 1 register stages, window
-// w + PF requested before window w is consumed.  Loads are unconditional
-// (window index clamped; the repeats at the end hit in cache) so the compiler
-// counts outstanding loads exactly.
+// The first two run a software pipeline: a ring of PF + 1 register stages,
+// window w + PF requested before window w is consumed.  Loads are
+// unconditional (window index clamped; the repeats at the end hit in cache)
+// so the compiler counts outstanding loads exactly.  The wide scan pipelines
+// through LDS instead (below).
 //
 // Tile (row block rb, window w) starts at element rb * rs + w * ws, so the
 // kernels serve both tile orders (row-block-major and window-major).
@@ -51,6 +52,17 @@
 #endif
 #ifndef OIL_FP8_PF
 #define OIL_FP8_PF 1
+#endif
+// Row blocks per workgroup of the wide scan (B > 64) with 1, 2 and 4 query
+// tiles per wave.
+#ifndef OIL_WIDE_MT1
+#define OIL_WIDE_MT1 4
+#endif
+#ifndef OIL_WIDE_MT2
+#define OIL_WIDE_MT2 4
+#endif
+#ifndef OIL_WIDE_MT4
+#define OIL_WIDE_MT4 4
 #endif
 
 namespace oil {
@@ -283,11 +295,29 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 // once and reused by every query tile.  A block owns MT row blocks; its four
 // waves split the query tiles (NTW tiles each).  Each 64-column window of the
 // block's keys (MT tiles of 4 KiB) is copied into LDS once with gfx950's
-// 16-byte global->LDS loads (the four waves share the copies), double
-// buffered with one barrier per window; every wave reads its A operands from
-// LDS (lane l's 16 bytes sit at 16 l: conflict-free) and its own query
-// fragments from L2.  Per (row block, query tile) the MFMA sequence is the
-// same as in scan_mfma_kernel (windows in order, sub-steps in order).
+// 16-byte global->LDS loads (the four waves share the copies), through a
+// three-window ring with one barrier per window; every wave reads its A
+// operands from LDS (lane l's 16 bytes sit at 16 l: conflict-free) and its
+// own query fragments from L2.  Per (row block, query tile) the MFMA sequence
+// is the same as in scan_mfma_kernel (windows in order, sub-steps in order).
+// With at most 2 query tiles per wave and 4 row blocks the register budget is
+// capped for two waves per SIMD (the accumulators then fit beside the rest).
+// A workgroup barrier without the memory fence __syncthreads() carries: that
+// fence would wait for every outstanding global-to-LDS copy, the ones meant to
+// stay in flight included.  The caller waits (vmcnt) for the copies the next
+// stage reads before calling this; the scheduling barriers keep LDS accesses
+// on their side of it.
+__device__ __forceinline__ void block_barrier()
+{
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+#ifndef OIL_WIDE_WPE
+#define OIL_WIDE_WPE(MT, NTW) ((MT) <= 4 && (NTW) <= 2 ? 2 : 1)
+#endif
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt_at_most()
 {
@@ -298,35 +328,41 @@ __device__ __forceinline__ void wait_vmcnt_at_most()
 }
 
 template <int MT, int NTW>
-__global__ __launch_bounds__(256) void scan_mfma_wide_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OIL_WIDE_WPE(MT, NTW)))) void
+scan_mfma_wide_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
     const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld)
 {
-    __shared__ bf16x8 ring[2][MT][4][64];  // two windows of the block's MT key tiles
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    // three windows of the block's MT key tiles, as three separate LDS objects
+    // so that the slot each access uses is known at compile time
+    __shared__ bf16x8 ring0[MT][4][64], ring1[MT][4][64], ring2[MT][4][64];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
     const int h = lane >> 5, r = lane & 31;
     const int64_t rb0 = (int64_t)blockIdx.x * MT;
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
     const int nwin = ld / kWindow;
     const int n_qt = (B + 31) / 32;
-    const int64_t ws8 = ws / 8;
+    // Addresses are a wave-uniform base plus the lane's 16-byte slot, so the
+    // loads take a scalar base and one shared 32-bit lane offset.
+    const uint32_t loff = (uint32_t)lane * 16;
 
     // this wave's share of the block's key copies: (mt, s) pairs with (4 mt + s) % 4 == wave
-    const bf16x8* src[MT];
+    const char* src[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; mt++) {
         const int64_t rb = rb0 + mt < n_rb ? rb0 + mt : n_rb - 1;  // clamp: stays inside the pool
-        src[mt] = (const bf16x8*)(keys + rb * rs) + wave * 64 + lane;
+        src[mt] = (const char*)(keys + rb * rs) + wave * 1024;
     }
-    auto copy_keys = [&](int buf, int w) {
+    const int64_t wbytes = ws * 2;
+    auto copy_keys = [&](bf16x8 (&buf)[MT][4][64], int w) {
 #pragma unroll
         for (int mt = 0; mt < MT; mt++)
             __builtin_amdgcn_global_load_lds(
-                (const void __attribute__((address_space(1)))*)(src[mt] + w * ws8),
-                (void __attribute__((address_space(3)))*)&ring[buf][mt][wave][0], 16, 0, 0);
+                (const void __attribute__((address_space(1)))*)(src[mt] + w * wbytes + loff),
+                (void __attribute__((address_space(3)))*)&buf[mt][wave][0], 16, 0, 0);
     };
-    const bf16x8* qf = qfrag + lane;
     int qt[NTW];
 #pragma unroll
     for (int nt = 0; nt < NTW; nt++) {
@@ -337,8 +373,10 @@ __global__ __launch_bounds__(256) void scan_mfma_wide_kernel(
 #pragma unroll
         for (int nt = 0; nt < NTW; nt++)
 #pragma unroll
-            for (int s = 0; s < 4; s++)
-                b[nt][s] = qf[(((int64_t)w * n_qt + qt[nt]) * 4 + s) * 64];
+            for (int s = 0; s < 4; s++) {
+                const char* base = (const char*)(qfrag + (((int64_t)w * n_qt + qt[nt]) * 4 + s) * 64);
+                b[nt][s] = *(const bf16x8*)(base + loff);
+            }
     };
 
     floatx16 acc[MT][NTW];
@@ -348,51 +386,89 @@ __global__ __launch_bounds__(256) void scan_mfma_wide_kernel(
         for (int nt = 0; nt < NTW; nt++)
             acc[mt][nt] = floatx16{};
 
-    // Two-stage ping-pong: stage 0 holds even windows (ring[0], b0), stage 1
-    // odd ones (ring[1], b1).  Each stage reads its keys out of LDS, starts
-    // the next window's copies into the other buffers (window index clamped:
-    // the extra copy past the end is harmless), multiplies, then waits for
-    // its copies and meets the other waves at the barrier.
-    auto mma = [&](const bf16x8 (&a)[MT][4], const bf16x8 (&b)[NTW][4]) {
+    // Keys run two windows ahead through a three-window LDS ring, query
+    // fragments one window ahead in two register sets.  Stage w reads window
+    // w's keys out of LDS, issues the fragments of w + 1 (index clamped) and
+    // the key copies of w + 2 (none past the last window), multiplies, and
+    // waits until at most the MT copies of w + 2 are outstanding (loads retire
+    // in order, so the fragments of w + 1 and the copies of w + 1 are in;
+    // with no copies issued it waits for all); the barrier then publishes
+    // window w + 1 and tells every wave that the ring slot of w is free.
+    auto read_sub = [&](bf16x8 (&a)[MT], const bf16x8 (&buf)[MT][4][64], int s) {
 #pragma unroll
-        for (int s = 0; s < 4; s++)
-#pragma unroll
-            for (int mt = 0; mt < MT; mt++)
-#pragma unroll
-                for (int nt = 0; nt < NTW; nt++)
-                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt][s], b[nt][s], acc[mt][nt],
-                                                                          0, 0, 0);
+        for (int mt = 0; mt < MT; mt++)
+            a[mt] = buf[mt][s][lane];
     };
-    auto read_keys = [&](bf16x8 (&a)[MT][4], int buf) {
+    auto mma_sub = [&](const bf16x8 (&a)[MT], const bf16x8 (&b)[NTW][4], int s) {
 #pragma unroll
         for (int mt = 0; mt < MT; mt++)
 #pragma unroll
-            for (int s = 0; s < 4; s++)
-                a[mt][s] = ring[buf][mt][s][lane];
+            for (int nt = 0; nt < NTW; nt++)
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt][s], acc[mt][nt], 0, 0, 0);
     };
-    bf16x8 b0[NTW][4], b1[NTW][4], a[MT][4];
-    copy_keys(0, 0);
+    auto clampw = [&](int w) { return w < nwin ? w : nwin - 1; };
+    bf16x8 b0[NTW][4], b1[NTW][4];
+    // one stage: window w sits in `cur`, its fragments in `bq`; `bn` receives
+    // the fragments of w + 1 and `nxt2` the keys of w + 2.  MORE: w + 2 is a
+    // window (the main loop's stages always are; the tail's test it).
+    auto stage = [&](auto more_t, const bf16x8 (&cur)[MT][4][64], bf16x8 (&nxt2)[MT][4][64],
+                     const bf16x8 (&bq)[NTW][4], bf16x8 (&bn)[NTW][4], int w) {
+        constexpr bool always = decltype(more_t)::value;
+        const bool more = always || w + 2 < nwin;
+        load_q(bn, clampw(w + 1));
+        if (more)
+            copy_keys(nxt2, w + 2);
+        // LDS reads one sub-step ahead of the MFMAs that use them
+        bf16x8 a0[MT], a1[MT];
+        read_sub(a0, cur, 0);
+        read_sub(a1, cur, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_sub(a0, bq, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        read_sub(a0, cur, 2);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_sub(a1, bq, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        read_sub(a1, cur, 3);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_sub(a0, bq, 2);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_sub(a1, bq, 3);
+        __builtin_amdgcn_sched_barrier(0);
+        if (more)
+            wait_vmcnt_at_most<MT>();
+        else
+            wait_vmcnt_at_most<0>();
+        block_barrier();
+    };
+    copy_keys(ring0, 0);
+    if (nwin > 1)
+        copy_keys(ring1, 1);
     load_q(b0, 0);
+    __builtin_amdgcn_sched_barrier(0);
     wait_vmcnt_at_most<0>();
     __syncthreads();
-    const int nloop = (nwin + 1) / 2 * 2;
-    for (int w0 = 0; w0 < nloop; w0 += 2) {
-        const int w1 = w0 + 1 < nwin ? w0 + 1 : nwin - 1;
-        const int w2 = w0 + 2 < nwin ? w0 + 2 : nwin - 1;
-        read_keys(a, 0);
-        copy_keys(1, w1);
-        load_q(b1, w1);
-        mma(a, b0);
-        wait_vmcnt_at_most<0>();
-        __syncthreads();
-        read_keys(a, 1);
-        copy_keys(0, w2);
-        load_q(b0, w2);
-        if (w0 + 1 < nwin)
-            mma(a, b1);
-        wait_vmcnt_at_most<0>();
-        __syncthreads();
+    // six stages per trip, so that ring slots and fragment sets return to
+    // their start; the main loop runs while every stage has a window two
+    // ahead, the tail (2 to 7 windows) tests it per stage
+    const std::integral_constant<bool, true> yes;
+    const std::integral_constant<bool, false> no;
+    int w = 0;
+    for (; w + 7 < nwin; w += 6) {
+        stage(yes, ring0, ring2, b0, b1, w);
+        stage(yes, ring1, ring0, b1, b0, w + 1);
+        stage(yes, ring2, ring1, b0, b1, w + 2);
+        stage(yes, ring0, ring2, b1, b0, w + 3);
+        stage(yes, ring1, ring0, b0, b1, w + 4);
+        stage(yes, ring2, ring1, b1, b0, w + 5);
     }
+    stage(no, ring0, ring2, b0, b1, w);
+    if (w + 1 < nwin) stage(no, ring1, ring0, b1, b0, w + 1);
+    if (w + 2 < nwin) stage(no, ring2, ring1, b0, b1, w + 2);
+    if (w + 3 < nwin) stage(no, ring0, ring2, b1, b0, w + 3);
+    if (w + 4 < nwin) stage(no, ring1, ring0, b0, b1, w + 4);
+    if (w + 5 < nwin) stage(no, ring2, ring1, b1, b0, w + 5);
+    if (w + 6 < nwin) stage(no, ring0, ring2, b0, b1, w + 6);
 
     // block keys, as in scan_mfma_kernel
 #pragma unroll
@@ -403,6 +479,9 @@ __global__ __launch_bounds__(256) void scan_mfma_wide_kernel(
 #pragma unroll
         for (int mt = 0; mt < MT; mt++) {
             const int64_t rb = rb0 + mt;
+            // the tile moves out of the accumulation registers here, one tile at a time
+            floatx16 t = acc[mt][nt];
+            asm volatile("" : "+v"(t));
             uint64_t best = 0;
 #pragma unroll
             for (int i = 0; i < 4; i++) {
@@ -410,7 +489,7 @@ __global__ __launch_bounds__(256) void scan_mfma_wide_kernel(
 #pragma unroll
                 for (int j = 0; j < 4; j++) {
                     if (row + j < n_valid) {
-                        float v = acc[mt][nt][4 * i + j];
+                        float v = t[4 * i + j];
                         if (ex >= 0)
                             v = masked_score(v, row + j, ex, prompt);
                         const uint64_t key = rank_key(v, (uint32_t)(row + j));
@@ -422,6 +501,7 @@ __global__ __launch_bounds__(256) void scan_mfma_wide_kernel(
             best = other > best ? other : best;
             if (qlive && h == 0 && rb * kRowBlock < n_valid)
                 G[qb * g_ld + rb] = best;
+            __builtin_amdgcn_sched_barrier(0);  // one tile at a time: bounds the live registers
         }
     }
 }
@@ -614,17 +694,16 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
     }
     const bf16x8* qf = (const bf16x8*)qbuf;
     if (B > 64) {
-        constexpr int MTW = 4;
-        const dim3 gw((unsigned)((n_rb + MTW - 1) / MTW));
         const int ntw = (scan_query_tiles(B) + 3) / 4;
+        constexpr int M1 = OIL_WIDE_MT1, M2 = OIL_WIDE_MT2, M4 = OIL_WIDE_MT4;
         if (ntw == 1)
-            hipLaunchKernelGGL((scan_mfma_wide_kernel<MTW, 1>), gw, dim3(256), 0, stream, keys, ld, rs, ws,
-                               n_valid, qf, B, prompt, exclude, G, g_ld);
+            hipLaunchKernelGGL((scan_mfma_wide_kernel<M1, 1>), dim3((unsigned)((n_rb + M1 - 1) / M1)), dim3(256), 0,
+                               stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
         else if (ntw == 2)
-            hipLaunchKernelGGL((scan_mfma_wide_kernel<MTW, 2>), gw, dim3(256), 0, stream, keys, ld, rs, ws,
-                               n_valid, qf, B, prompt, exclude, G, g_ld);
-        else  // 4 query tiles per wave: 2 row blocks keep the accumulators in registers
-            hipLaunchKernelGGL((scan_mfma_wide_kernel<2, 4>), dim3((unsigned)((n_rb + 1) / 2)), dim3(256), 0,
+            hipLaunchKernelGGL((scan_mfma_wide_kernel<M2, 2>), dim3((unsigned)((n_rb + M2 - 1) / M2)), dim3(256), 0,
+                               stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
+        else
+            hipLaunchKernelGGL((scan_mfma_wide_kernel<M4, 4>), dim3((unsigned)((n_rb + M4 - 1) / M4)), dim3(256), 0,
                                stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
         return hipGetLastError();
     }
