@@ -53,6 +53,10 @@
 #ifndef OIL_FP8_PF
 #define OIL_FP8_PF 1
 #endif
+// Prefetch depth (windows in flight per wave) of the MFMA rescore.
+#ifndef OIL_RESCORE_PF
+#define OIL_RESCORE_PF 3
+#endif
 // Row blocks per workgroup of the wide scan (B > 64) with 1, 2 and 4 query
 // tiles per wave.
 #ifndef OIL_WIDE_MT1
@@ -209,9 +213,10 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     constexpr int NS = PF + 1;
     const int lane = threadIdx.x & 63;
     const int h = lane >> 5, r = lane & 31;
-    const int64_t rb0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * MT;
-    if (rb0 * kRowBlock >= n_valid)
-        return;
+    const int wave = threadIdx.x >> 6;
+    const int64_t rbb = (int64_t)blockIdx.x * 4 * MT;  // the block's first row block
+    const int64_t rb0 = rbb + wave * MT;
+    const bool live = rb0 * kRowBlock < n_valid;  // waves past the pool only join the block store
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
     const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
     const int64_t ws8 = ws / 8;
@@ -235,7 +240,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 #pragma unroll
     for (int p = 0; p < PF; p++)
         load_window<MT, NT>(a[p], b[p], tile, ws8, qf, p < nwin ? p : nwin - 1);
-    const int nloop = (nwin + NS - 1) / NS * NS;
+    const int nloop = live ? (nwin + NS - 1) / NS * NS : 0;
     for (int w0 = 0; w0 < nloop; w0 += NS) {
 #pragma unroll
         for (int u = 0; u < NS; u++) {
@@ -255,7 +260,11 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 
     // Accumulator layout of a 32x32 MFMA tile: lane l, element 4 i + j holds
     // row 8 i + 4 (l / 32) + j (a key) and column l % 32 (a query).  Each
-    // (query, row block) keeps its best (score, position) key.
+    // (query, row block) keeps its best (score, position) key.  The keys of
+    // the block's 4 MT row blocks are gathered in LDS and stored row by row
+    // (consecutive threads, consecutive row blocks of one query): whole
+    // cache lines instead of one scattered 8-byte store per query.
+    __shared__ uint64_t gk[4][NT * 32][MT + 1];  // per wave; +1: rows land in different banks
 #pragma unroll
     for (int nt = 0; nt < NT; nt++) {
         const int qb = nt * 32 + r;
@@ -284,9 +293,20 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
             }
             const uint64_t other = __shfl_xor(best, 32, kWave);
             best = other > best ? other : best;
-            if (qlive && h == 0 && rb * kRowBlock < n_valid)
-                G[qb * g_ld + rb] = best;
+            if (h == 0)
+                gk[wave][qb][mt] = best;
         }
+    }
+    // the wave's own LDS rows: no barrier, only the wave's LDS writes must land
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    __builtin_amdgcn_wave_barrier();
+    const int nq = B < NT * 32 ? B : NT * 32;
+#pragma unroll
+    for (int c0 = 0; c0 < NT * 32 * MT; c0 += 64) {
+        const int c = c0 + lane;
+        const int q = c / MT, j = c % MT;
+        if (q < nq && rb0 + j < n_rb)
+            G[q * g_ld + rb0 + j] = gk[wave][q][j];
     }
 }
 
@@ -725,14 +745,14 @@ hipError_t launch_rescore(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
 {
     const dim3 g((unsigned)k, (unsigned)B);
     if (fmt == kKeyFp8)
-        hipLaunchKernelGGL((rescore_mfma_kernel<3, kKeyFp8>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
+        hipLaunchKernelGGL((rescore_mfma_kernel<OIL_RESCORE_PF, kKeyFp8>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
                            (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC, kscale,
                            qscale);
     else if (!scan_uses_mfma(B, ld))
         hipLaunchKernelGGL((rescore_gemv_kernel<3>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
                            (const uint16_t*)qbuf, blocks, k, prompt, exclude, SC);
     else
-        hipLaunchKernelGGL((rescore_mfma_kernel<3, kKeyBf16>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
+        hipLaunchKernelGGL((rescore_mfma_kernel<OIL_RESCORE_PF, kKeyBf16>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
                            (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC, nullptr,
                            nullptr);
     return hipGetLastError();

@@ -207,3 +207,27 @@ def test_full_step_8192(oil):
             assert np.array_equal(cl.cpu().numpy()[b], ocl[j])
             for a, e in zip(tree, otree):
                 assert np.array_equal(a.cpu().numpy()[b], e[j])
+
+
+def test_wide_batches_1m_full_size(oil):
+    """N = 1,048,576, d = 4,096 bf16, k = 32 with B = 200 (ragged, 2 query
+    tiles per wave) and B = 512 (4 per wave): the wide scan's launches on the
+    full pool.  Sampled queries span every wave's tiles and the ragged tail."""
+    cfg = workloads.BATCHED_1M
+    ps, qs, k = cfg["pool"], cfg["query"], cfg["k"]
+    dev = torch.device("cuda")
+    wp = workloads.Pool(ps, device=dev)
+    batches = {}
+    for B, sample in ((200, [0, 31, 63, 64, 127, 150, 192, 199]),
+                      (512, [0, 31, 127, 128, 255, 256, 383, 511])):
+        q, _ = workloads.queries(wp, workloads.QuerySpec(B=B, noise=qs.noise, p_random=qs.p_random,
+                                                         seed=qs.seed + B))
+        batches[B] = (q, sample, StreamedOracle(_bits(q[sample]), ps.n))
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    _fill(pool, wp, 0, ps.n, dev, [b[2] for b in batches.values()])
+    for B, (q, sample, orc) in batches.items():
+        s, i = pool.query_topk(q, k)
+        torch.cuda.synchronize()
+        gs, gi = s.cpu().numpy(), i.cpu().numpy()
+        check_topk(gs[sample], gi[sample], orc.s, k)
+        _rescore_returned(wp, gs[::25], gi[::25], _bits(q[::25]))
