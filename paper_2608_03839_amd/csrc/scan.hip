@@ -95,6 +95,23 @@ __device__ __forceinline__ float masked_score(float s, int64_t row, int32_t ex,
     return s;
 }
 
+// Per-row data (inverse key scales, prompt ids) of the 16 rows a lane holds
+// in a 32-row MFMA tile starting at row0: element 4 i + j is row
+// row0 + 8 i + 4 h + j.  The 16 loads are issued together; indices past the
+// last stored row are clamped to it (those rows are never scored).
+template <typename T>
+__device__ __forceinline__ void tile_rows_load(T (&out)[16], const T* __restrict__ src, int64_t row0, int h,
+                                               int64_t n_valid)
+{
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const int64_t row = row0 + i * 8 + h * 4 + j;
+            out[4 * i + j] = src[row < n_valid ? row : n_valid - 1];
+        }
+}
+
 // ----------------------------------------------------------------- GEMV (B <= 4)
 template <int NB, int PF>
 __global__ __launch_bounds__(256) void scan_gemv_kernel(
@@ -265,36 +282,44 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     // (consecutive threads, consecutive row blocks of one query): whole
     // cache lines instead of one scattered 8-byte store per query.
     __shared__ uint64_t gk[4][NT * 32][MT + 1];  // per wave; +1: rows land in different banks
+    int32_t ex[NT];
+    float qs[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; nt++) {
         const int qb = nt * 32 + r;
         const bool qlive = qb < B;
-        const int32_t ex = (exclude && qlive) ? exclude[qb] : -1;
-        const float qs = (FMT == kKeyBf16 || !qlive) ? 1.f : qscale[qb];
+        ex[nt] = (exclude && qlive) ? exclude[qb] : -1;
+        qs[nt] = (FMT == kKeyBf16 || !qlive) ? 1.f : qscale[qb];
+    }
 #pragma unroll
-        for (int mt = 0; mt < MT; mt++) {
-            const int64_t rb = rb0 + mt;
+    for (int mt = 0; mt < MT; mt++) {
+        const int64_t rb = rb0 + mt;
+        float ks[16];
+        int32_t pr[16];
+        if constexpr (FMT == kKeyFp8)
+            tile_rows_load(ks, kscale, rb * kRowBlock, h, n_valid);
+        if (exclude)
+            tile_rows_load(pr, prompt, rb * kRowBlock, h, n_valid);
+#pragma unroll
+        for (int nt = 0; nt < NT; nt++) {
             uint64_t best = 0;
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
-                const int64_t row = rb * kRowBlock + i * 8 + h * 4;
-#pragma unroll
-                for (int j = 0; j < 4; j++) {
-                    if (row + j < n_valid) {
-                        float v = acc[mt][nt][4 * i + j];
-                        if constexpr (FMT == kKeyFp8)
-                            v = v * (kscale[row + j] * qs);  // powers of two: exact
-                        if (ex >= 0)
-                            v = masked_score(v, row + j, ex, prompt);
-                        const uint64_t key = rank_key(v, (uint32_t)(row + j));
-                        best = key > best ? key : best;
-                    }
+            for (int e = 0; e < 16; e++) {
+                const int64_t row = rb * kRowBlock + (e / 4) * 8 + h * 4 + e % 4;
+                if (row < n_valid) {
+                    float v = acc[mt][nt][e];
+                    if constexpr (FMT == kKeyFp8)
+                        v = v * (ks[e] * qs[nt]);  // powers of two: exact
+                    if (ex[nt] >= 0 && pr[e] == ex[nt])
+                        v = __uint_as_float(kNoScoreBits);
+                    const uint64_t key = rank_key(v, (uint32_t)row);
+                    best = key > best ? key : best;
                 }
             }
             const uint64_t other = __shfl_xor(best, 32, kWave);
             best = other > best ? other : best;
             if (h == 0)
-                gk[wave][qb][mt] = best;
+                gk[wave][nt * 32 + r][mt] = best;
         }
     }
     // the wave's own LDS rows: no barrier, only the wave's LDS writes must land
@@ -491,35 +516,39 @@ scan_mfma_wide_kernel(
     if (w + 6 < nwin) stage(no, ring0, ring2, b0, b1, w + 6);
 
     // block keys, as in scan_mfma_kernel
+    int32_t ex[NTW];
 #pragma unroll
     for (int nt = 0; nt < NTW; nt++) {
         const int qb = (wave * NTW + nt) * 32 + r;
-        const bool qlive = qb < B;
-        const int32_t ex = (exclude && qlive) ? exclude[qb] : -1;
+        ex[nt] = (exclude && qb < B) ? exclude[qb] : -1;
+    }
 #pragma unroll
-        for (int mt = 0; mt < MT; mt++) {
-            const int64_t rb = rb0 + mt;
+    for (int mt = 0; mt < MT; mt++) {
+        const int64_t rb = rb0 + mt;
+        int32_t pr[16];
+        if (exclude)
+            tile_rows_load(pr, prompt, rb * kRowBlock, h, n_valid);
+#pragma unroll
+        for (int nt = 0; nt < NTW; nt++) {
+            const int qb = (wave * NTW + nt) * 32 + r;
             // the tile moves out of the accumulation registers here, one tile at a time
             floatx16 t = acc[mt][nt];
             asm volatile("" : "+v"(t));
             uint64_t best = 0;
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
-                const int64_t row = rb * kRowBlock + i * 8 + h * 4;
-#pragma unroll
-                for (int j = 0; j < 4; j++) {
-                    if (row + j < n_valid) {
-                        float v = t[4 * i + j];
-                        if (ex >= 0)
-                            v = masked_score(v, row + j, ex, prompt);
-                        const uint64_t key = rank_key(v, (uint32_t)(row + j));
-                        best = key > best ? key : best;
-                    }
+            for (int e = 0; e < 16; e++) {
+                const int64_t row = rb * kRowBlock + (e / 4) * 8 + h * 4 + e % 4;
+                if (row < n_valid) {
+                    float v = t[e];
+                    if (ex[nt] >= 0 && pr[e] == ex[nt])
+                        v = __uint_as_float(kNoScoreBits);
+                    const uint64_t key = rank_key(v, (uint32_t)row);
+                    best = key > best ? key : best;
                 }
             }
             const uint64_t other = __shfl_xor(best, 32, kWave);
             best = other > best ? other : best;
-            if (qlive && h == 0 && rb * kRowBlock < n_valid)
+            if (qb < B && h == 0 && rb * kRowBlock < n_valid)
                 G[qb * g_ld + rb] = best;
             __builtin_amdgcn_sched_barrier(0);  // one tile at a time: bounds the live registers
         }
@@ -586,22 +615,24 @@ __global__ __launch_bounds__(64) void rescore_mfma_kernel(
     if (r != n)
         return;
     const int32_t ex = exclude ? exclude[qb] : -1;
+    float ks[16];
+    int32_t pr[16];
+    if constexpr (FMT == kKeyFp8)
+        tile_rows_load(ks, kscale, rb * kRowBlock, h, n_valid);
+    if (ex >= 0)
+        tile_rows_load(pr, prompt, rb * kRowBlock, h, n_valid);
+    const float qs = FMT == kKeyFp8 ? qscale[qb] : 1.f;
 #pragma unroll
-    for (int i = 0; i < 4; i++)
-#pragma unroll
-        for (int j = 0; j < 4; j++) {
-            const int rr = i * 8 + h * 4 + j;
-            const int64_t row = rb * kRowBlock + rr;
-            float v = acc[4 * i + j];
-            if constexpr (FMT == kKeyFp8)
-                if (row < n_valid)
-                    v = v * (kscale[row] * qscale[qb]);  // as the scan scales it
-            if (row >= n_valid)
-                v = __uint_as_float(kNoScoreBits);
-            else if (ex >= 0)
-                v = masked_score(v, row, ex, prompt);
-            out[rr] = v;
-        }
+    for (int e = 0; e < 16; e++) {
+        const int rr = (e / 4) * 8 + h * 4 + e % 4;
+        const int64_t row = rb * kRowBlock + rr;
+        float v = acc[e];
+        if constexpr (FMT == kKeyFp8)
+            v = v * (ks[e] * qs);  // as the scan scales it
+        if (row >= n_valid || (ex >= 0 && pr[e] == ex))
+            v = __uint_as_float(kNoScoreBits);
+        out[rr] = v;
+    }
 }
 
 // GEMV path: the scan's per-query order (windows, then sub-steps, v_dot2 in
