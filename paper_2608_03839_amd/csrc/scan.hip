@@ -50,6 +50,13 @@
 #ifndef OIL_FP8_MT
 #define OIL_FP8_MT 2
 #endif
+// Row blocks per wave for two query tiles (33 <= B <= 64).
+#ifndef OIL_BF16_MT2
+#define OIL_BF16_MT2 OIL_BF16_MT
+#endif
+#ifndef OIL_FP8_MT2
+#define OIL_FP8_MT2 4
+#endif
 #ifndef OIL_FP8_PF
 #define OIL_FP8_PF 1
 #endif
@@ -720,15 +727,16 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
         return hipSuccess;
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
     if (fmt == kKeyFp8) {  // B <= 64 (checked by the caller)
-        constexpr int MT = OIL_FP8_MT, PF = OIL_FP8_PF;
-        const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
+        constexpr int MT = OIL_FP8_MT, MT2 = OIL_FP8_MT2, PF = OIL_FP8_PF;
         const bf16x8* qf = (const bf16x8*)qbuf;
         if (scan_query_tiles(B) == 1)
-            hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyFp8>), g, dim3(256), 0, stream, keys, ld, rs,
-                               ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+            hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyFp8>), dim3((unsigned)((n_rb + 4 * MT - 1) / (4 * MT))),
+                               dim3(256), 0, stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld,
+                               kscale, qscale);
         else
-            hipLaunchKernelGGL((scan_mfma_kernel<MT, 2, PF, kKeyFp8>), g, dim3(256), 0, stream, keys, ld, rs,
-                               ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+            hipLaunchKernelGGL((scan_mfma_kernel<MT2, 2, PF, kKeyFp8>),
+                               dim3((unsigned)((n_rb + 4 * MT2 - 1) / (4 * MT2))), dim3(256), 0, stream, keys, ld,
+                               rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
         return hipGetLastError();
     }
     if (!scan_uses_mfma(B, ld)) {
@@ -758,14 +766,15 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
                                stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
         return hipGetLastError();
     }
-    constexpr int MT = OIL_BF16_MT, PF = OIL_BF16_PF;
-    const dim3 g((unsigned)((n_rb + 4 * MT - 1) / (4 * MT)));
+    constexpr int MT = OIL_BF16_MT, MT2 = OIL_BF16_MT2, PF = OIL_BF16_PF;
     if (scan_query_tiles(B) == 1)
-        hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyBf16>), g, dim3(256), 0, stream, keys, ld, rs, ws,
-                           n_valid, qf, B, prompt, exclude, G, g_ld, nullptr, nullptr);
+        hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyBf16>), dim3((unsigned)((n_rb + 4 * MT - 1) / (4 * MT))),
+                           dim3(256), 0, stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, nullptr,
+                           nullptr);
     else
-        hipLaunchKernelGGL((scan_mfma_kernel<MT, 2, PF, kKeyBf16>), g, dim3(256), 0, stream, keys, ld, rs, ws,
-                           n_valid, qf, B, prompt, exclude, G, g_ld, nullptr, nullptr);
+        hipLaunchKernelGGL((scan_mfma_kernel<MT2, 2, PF, kKeyBf16>),
+                           dim3((unsigned)((n_rb + 4 * MT2 - 1) / (4 * MT2))), dim3(256), 0, stream, keys, ld, rs,
+                           ws, n_valid, qf, B, prompt, exclude, G, g_ld, nullptr, nullptr);
     return hipGetLastError();
 }
 
