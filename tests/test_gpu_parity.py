@@ -107,6 +107,14 @@ def test_topk_wide_batches(oil, B):
     _query_case(oil, 5000, 512, B, 16, seed=40 + B)
 
 
+@pytest.mark.parametrize("d,B", [(64, 100), (128, 300), (320, 129), (448, 512), (832, 257)])
+def test_wide_batches_window_counts(oil, d, B):
+    """The wide scan's three-slot ring over 1, 2, 5, 7 and 13 key windows:
+    main loop trips of six windows plus a tail of two to seven (or the tail
+    alone), with one, two and four query tiles per wave."""
+    _query_case(oil, 3000 + d, d, B, 16, seed=60 + d)
+
+
 def test_wide_batch_ragged_width_and_exclusion(oil):
     n, d, B = 4100, 200, 130
     wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=50, seed=31, n_clusters=8,
