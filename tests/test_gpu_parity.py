@@ -322,6 +322,30 @@ def test_merge_bit_exact(oil, n_lex, lb, sb, mx):
     assert np.array_equal(ns.cpu().numpy(), ens)
 
 
+@pytest.mark.parametrize("n_lex,k,L,lb,sb", [
+    (0, 64, 16, 0, 255),     # 64 chains of 16 filling a 256-node tree
+    (4, 60, 16, 20, 100),    # lexical drafts and retrieved chains, both budgets binding
+    (4, 64, 8, 16, 120),     # 68 chains: more chains than lanes
+    (2, 32, 20, 30, 150),    # chains of 20
+    (1, 1, 16, 3, 5),        # two chains, tight budgets
+])
+def test_merge_chain_counts_and_lengths(oil, n_lex, k, L, lb, sb):
+    rng = np.random.default_rng(k * 31 + L)
+    B, L_lex = 40, L
+    lt, ll = _chains(rng, B, n_lex, L_lex, 4)
+    st, sl = _chains(rng, B, k, L, 4)
+    anchor = rng.integers(0, 1000, B).astype(np.int32)
+    mx = 1 + lb + sb
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    got = oil.merge_trees(cu(anchor), cu(lt) if n_lex else None, cu(ll) if n_lex else None, lb, cu(st),
+                          cu(sl), sb, mx)
+    torch.cuda.synchronize()
+    want = oracle.tree_merge(anchor, lt if n_lex else np.zeros((B, 0, 1), np.int32),
+                             ll if n_lex else np.zeros((B, 0), np.int32), lb, st, sl, sb, mx)
+    for a, e in zip(got, want):
+        assert np.array_equal(a.cpu().numpy(), e)
+
+
 def test_merge_golden(oil):
     import json
     import os
