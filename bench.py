@@ -48,6 +48,54 @@ def scan_source_hash():
     return hashlib.sha256(" ".join(src.split()).encode()).hexdigest()[:16]
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def read_ceiling(torch, oil, buf, dev, reps=5):
+    """A plain streaming read of the same key buffer (the library's read-stream
+    kernel, non-temporal 16-byte loads): the practical HBM read ceiling."""
+    sink = torch.zeros(1, dtype=torch.int64, device=dev)
+    oil.read_stream(buf, sink)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        oil.read_stream(buf, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    nbytes = buf.numel() * buf.element_size()
+    ms = e0.elapsed_time(e1) / reps
+    return {"GBps": round(nbytes / (ms / 1e3) / 1e9, 1), "bytes": nbytes, "ms": round(ms, 4),
+            "frac_of_peak": round(nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+def _pcts(torch, ev):
+    """p50 / p99 / mean (ms) of the intervals between consecutive recorded events."""
+    import numpy as np
+    torch.cuda.synchronize()
+    x = np.array([ev[j].elapsed_time(ev[j + 1]) for j in range(len(ev) - 1)])
+    return {"p50": round(float(np.percentile(x, 50)), 4), "p99": round(float(np.percentile(x, 99)), 4),
+            "mean": round(float(x.mean()), 4)}
+
+
+def _timed_events(torch, fn, steps):
+    """Per-step GPU latency distribution of fn(t): an event at every step boundary."""
+    steps = list(steps)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(steps) + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for j, t in enumerate(steps):
+        fn(t)
+        ev[j + 1].record()
+    return _pcts(torch, ev)
+
+
 def read_traffic(bytes_alg, path=PROFILE_TRAFFIC):
     """HBM bytes per scan launch from the committed rocprofv3 counter summary,
     or None when it is missing or was taken on another version of the kernel."""
@@ -181,13 +229,19 @@ def main():
         step(t)
     torch.cuda.synchronize()
     n_before = len(pool)
+    # one HIP event at every step boundary (recording adds no GPU work): the
+    # per-step latency distribution of the same timed run
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     oil.scan_timer_start(K)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
+    bounds[0].record()
     for t in range(W, steps):
         step(t)
+        bounds[t - W + 1].record()
     torch.cuda.synchronize()
     t_end = time.perf_counter()
+    step_ms = np.array([bounds[j].elapsed_time(bounds[j + 1]) for j in range(K)])
     n_timed, scan_ms_total = oil.scan_timer_stop()
     n_after = len(pool)
     elapsed = t_end - t_start
@@ -269,10 +323,17 @@ def main():
     scan_s = scan_ms_total / n_timed / 1e3
     achieved = bytes_alg / scan_s / 1e9
     traffic = read_traffic(bytes_alg)
+    ceiling = read_ceiling(torch, oil, pool.keys, dev)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "kernel": "scan_mfma_kernel<4,1,1,bf16>",
-                "scan_ms": round(scan_s * 1e3, 4), "bytes_per_launch": int(bytes_alg)}
+                "scan_ms": round(scan_s * 1e3, 4), "bytes_per_launch": int(bytes_alg),
+                "read_ceiling": ceiling,
+                "frac_of_read_ceiling": round(achieved / ceiling["GBps"], 4)}
+    extras["step_latency_ms"] = {"p10": round(float(np.percentile(step_ms, 10)), 4),
+                                 "p50": round(float(np.percentile(step_ms, 50)), 4),
+                                 "p90": round(float(np.percentile(step_ms, 90)), 4),
+                                 "source": "HIP events at the timed run's step boundaries"}
 
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu = None
@@ -297,6 +358,7 @@ def main():
         scale = N / sample_rows
         cpu = {"value": round(nq / (c_el * scale), 4), "unit": "queries/s",
                "cores": oracle.max_threads(), "kind": "oracle",
+               "nproc": os.cpu_count(), "cpu_model": cpu_model(),
                "sample": f"{nq} queries of the same batch against the first {sample_rows} pool rows "
                          f"(1/{scale:g} of N), normalise+score+sort+gather+merge, "
                          f"{c_el:.2f}s, rate scaled by {scale:g} to N={N}"}
@@ -443,7 +505,15 @@ def other_workloads(args, oil, workloads, dev):
         oil.merge_trees(A[t], None, None, 0, c_, l_, sb, 1 + sb)
 
     _timed(torch, dec, range(W))
-    out["decode_64k"] = {"ms_per_step": round(_timed(torch, dec, range(W, W + K)), 4),
+    oil.scan_timer_start(K)
+    ms = _timed(torch, dec, range(W, W + K))
+    nt, sms = oil.scan_timer_stop()
+    scan_s = sms / nt / 1e3
+    gbs = (ps.n * ps.d * 2 + ps.d * 2) / scan_s / 1e9
+    out["decode_64k"] = {"ms_per_step": round(ms, 4), "latency_ms": _timed_events(torch, dec, range(W, W + K)),
+                         "scan_ms": round(scan_s * 1e3, 4), "scan_GBps": round(gbs, 1),
+                         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                         "note": "512 MiB pool, twice the 256 MB Infinity Cache: read mostly from HBM",
                          "step": "query top-16 + gather 16 + merge (64 nodes), B = 1"}
     log(f"decode_64k: {out['decode_64k']['ms_per_step']} ms/step")
     del pool, wp
@@ -451,6 +521,8 @@ def other_workloads(args, oil, workloads, dev):
     # streaming growth: d = 5,120, 262,144 -> 2,097,152 positions, append 1-8 + 16 queries per step
     cfg = workloads.STREAM_5120
     ps, qsp, k = cfg["pool"], cfg["query"], cfg["k"]
+    K_all = K
+    K = 200  # streaming steps per checkpoint (append + query), p50 / p99 from per-step events
     wp = workloads.Pool(ps, device=dev)
     checkpoints = [262144, 524288, 1048576, ps.n - 8 * (K + W)]
     pool = oil.Pool(ps.d, ps.n, device=dev)
@@ -479,17 +551,20 @@ def other_workloads(args, oil, workloads, dev):
         _timed(torch, stream, range(W))
         n0 = len(pool)
         oil.scan_timer_start(K)
-        ms = _timed(torch, stream, range(W, W + K))
+        lat = _timed_events(torch, stream, range(W, W + K))
         nt, sms = oil.scan_timer_stop()
+        ms = lat["mean"]
         n_mean = (n0 + len(pool)) / 2
         scan_s = sms / nt / 1e3
         gbs = (n_mean * ps.d * 2 + qsp.B * ps.d * 2) / scan_s / 1e9
-        rows.append({"pool_rows": int(n_mean), "ms_per_step": round(ms, 4), "scan_ms": round(scan_s * 1e3, 4),
+        rows.append({"pool_rows": int(n_mean), "ms_per_step": round(ms, 4), "latency_ms": lat,
+                     "steps": K, "scan_ms": round(scan_s * 1e3, 4),
                      "scan_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)})
         log(f"stream_5120 at {int(n_mean)}: {ms:.3f} ms/step, scan {gbs:.0f} GB/s")
         at = c + sum(sizes[j])
     out["stream_5120"] = {"checkpoints": rows, "step": "append 1-8 positions + query top-16 for 16 queries"}
     del pool, wp
+    K = K_all
 
     # full draft step: N = 524,288, d = 8,192, 64 queries: lexical drafts (GPU) + retrieval +
     # gather (L = 12) + merge under 48 + 16 nodes
@@ -520,6 +595,7 @@ def other_workloads(args, oil, workloads, dev):
     _timed(torch, full, range(W))
     ms = _timed(torch, full, range(W, W + K))
     out["full_step_8192"] = {"ms_per_step": round(ms, 4), "trees_per_s": round(qsp.B / (ms / 1e3), 1),
+                             "latency_ms": _timed_events(torch, full, range(W, W + K)),
                              "step": "lexical drafts + query top-32 + gather 12 + merge (48 + 16 nodes), B = 64"}
     log(f"full_step_8192: {ms:.3f} ms/step")
     print(json.dumps({"workloads": out}), flush=True)

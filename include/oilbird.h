@@ -353,6 +353,16 @@ int32_t oil_accept_walk(int32_t B, int32_t max_nodes, const int32_t *node_token,
 int32_t oil_scan_timer_start(int32_t max_launches);
 int32_t oil_scan_timer_stop(int32_t *n_launches, double *total_ms);
 
+/* Measurement aid: a plain streaming read of a device buffer, the practical
+ * HBM read ceiling against which the pool scan's bandwidth is judged (the
+ * scan's own access pattern without its arithmetic).  Not part of the method.
+ *   buf    device buffer, 16-byte aligned, read as bytes / 16 16-byte words
+ *          (bytes a multiple of 16, > 0).
+ *   sink   device uint64: the XOR of all 64-bit words of buf is XOR-ed into
+ *          it (so the reads cannot be elided; callers zero it to check it).
+ * Returns OIL_E_INVALID for NULL pointers, misalignment or a bad size. */
+int32_t oil_read_stream(const void *buf, size_t bytes, uint64_t *sink, void *stream);
+
 /* (host) Static description of a status code. */
 const char *oil_status_string(int32_t status);
 

@@ -102,6 +102,7 @@ def lib():
             "oil_recycle_query": (i32, [P, P, i32, P, i32, ctypes.c_float, i32, i32, P, sz, P, P, P, P]),
             "oil_lexical_drafts": (i32, [P, P, P, i32, i32, P, i32, i32, i32, i32, P, sz, P, P, P]),
             "oil_accept_walk": (i32, [i32, i32, P, P, P, P, P, P, P, P]),
+            "oil_read_stream": (i32, [P, sz, P, P]),
             "oil_scan_timer_start": (i32, [i32]),
             "oil_scan_timer_stop": (i32, [ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]),
         }
@@ -264,6 +265,17 @@ def accept_walk(node_token, node_parent, n_nodes, target, out=None, stream=None)
         _ptr(_i32(n_nodes, "n_nodes")), _ptr(_i32(target, "target")), _ptr(al), _ptr(an), _ptr(bo),
         _stream(stream)))
     return al, an, bo
+
+
+def read_stream(buf, sink, stream=None):
+    """Plain streaming read of a device tensor's bytes (measurement aid): the
+    XOR of its 64-bit words is XOR-ed into ``sink`` (one int64 on the device)."""
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("read_stream: buf must be a contiguous device tensor")
+    if sink.dtype != torch.int64 or sink.numel() != 1 or not sink.is_cuda:
+        raise ValueError("read_stream: sink must be one int64 on the device")
+    nbytes = buf.numel() * buf.element_size()
+    _check("oil_read_stream", lib().oil_read_stream(_ptr(buf), nbytes, _ptr(sink), _stream(stream)))
 
 
 def scan_timer_start(max_launches: int):

@@ -88,6 +88,13 @@ void timer_mark(hipStream_t st, int which)
 
 extern "C" {
 
+int32_t oil_read_stream(const void* buf, size_t bytes, uint64_t* sink, void* stream)
+{
+    if (!buf || !sink || bytes == 0 || bytes % 16 != 0 || !aligned(buf, 16) || !aligned(sink, 8))
+        return OIL_E_INVALID;
+    return hip_status(oil::launch_read_stream(buf, (int64_t)(bytes / 16), sink, (hipStream_t)stream));
+}
+
 int32_t oil_scan_timer_start(int32_t max_launches)
 {
     if (max_launches < 1 || max_launches > 65536 || g_timer.ev)

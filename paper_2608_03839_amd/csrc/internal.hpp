@@ -73,6 +73,10 @@ hipError_t launch_topk_blocks(const uint64_t* G, int64_t g_ld, int64_t n_valid, 
 hipError_t launch_topk_final(const uint64_t* chosen, int32_t B, int32_t k, const float* SC,
                              int64_t n_valid, float* out_s, int32_t* out_i, hipStream_t stream);
 
+// Plain streaming read of n16 16-byte words (measurement aid); XOR of the
+// words folded into *sink.
+hipError_t launch_read_stream(const void* buf, int64_t n16, uint64_t* sink, hipStream_t stream);
+
 hipError_t launch_gather(const int32_t* tokens, const int32_t* traces, int64_t n_valid,
                          const int32_t* idx, const float* scores, int32_t B, int32_t k,
                          const DepthRule& rule, int32_t L, int32_t* chain_tokens, int32_t* chain_len,

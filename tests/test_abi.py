@@ -193,3 +193,13 @@ def test_recycle_validates(L):
     assert L.oil_recycle_insert(None, 4, 65, P, P, P, P, P, P, P, 0, P, 1 << 20, None) == -1
     assert L.oil_recycle_query(None, P, 0, P, 4, ctypes.c_float(0.8), 4, 6, P, 1 << 20, P, P, P, None) == -1
     assert L.oil_recycle_query_workspace_bytes(None, 4) == 0
+
+
+def test_read_stream_rejects_bad_arguments(L):
+    buf = ctypes.c_void_p(4096)   # never dereferenced: every case fails on the host
+    sink = ctypes.c_void_p(8192)
+    assert L.oil_read_stream(None, 16, sink, None) != 0
+    assert L.oil_read_stream(buf, 16, None, None) != 0
+    assert L.oil_read_stream(buf, 0, sink, None) != 0
+    assert L.oil_read_stream(buf, 24, sink, None) != 0            # not a multiple of 16
+    assert L.oil_read_stream(ctypes.c_void_p(4104), 16, sink, None) != 0   # misaligned
