@@ -101,6 +101,36 @@ def test_topk_over_query_batches(oil, B):
     _query_case(oil, 5000, 512, B, 16, seed=20 + B)
 
 
+@pytest.mark.parametrize("key_format,B,k", [("bf16", 8, 32), ("bf16", 40, 64), ("fp8", 8, 32),
+                                             ("fp8", 40, 64), ("bf16", 3, 16)])
+def test_topk_runs_of_neighbours(oil, key_format, B, k):
+    """Most of each query's top k packed into a few 32-row blocks (runs of
+    near-copies at consecutive positions, straddling block edges), the rest
+    scattered one per block: chosen blocks contribute from 32 positions down
+    to one."""
+    n, d = 6000, 256
+    g = torch.Generator().manual_seed(B * 100 + k)
+    raw = torch.randn((n, d), generator=g)
+    q = torch.randn((B, d), generator=g)
+    for b in range(B):
+        start = 37 + 67 * b                        # a run of 50 near-copies: 2-3 blocks
+        raw[start:start + 50] = q[b] + 0.05 * torch.randn((50, d), generator=g)
+        for j in range(12):                        # scattered, weaker neighbours
+            raw[3000 + 200 * j + b] = q[b] + 0.6 * torch.randn(d, generator=g)
+    ids = torch.arange(n, dtype=torch.int32)
+    pool = oil.Pool(d, n, key_format=key_format)
+    pool.append(raw.cuda(), ids.cuda(), ids.cuda(), ids.cuda())
+    s_, i_ = pool.query_topk(q.cuda(), k)
+    torch.cuda.synchronize()
+    if key_format == "fp8":
+        kc, ki = oracle.quantize_rows_fp8(raw.numpy())
+        qc, qi = oracle.quantize_rows_fp8(q.numpy())
+        o = oracle.scores_fp8(kc, ki, qc, qi)
+    else:
+        o = oracle_rows(_stored(pool, n), q.numpy())
+    check_topk(s_.cpu().numpy(), i_.cpu().numpy(), o, k)
+
+
 @pytest.mark.parametrize("B", [65, 96, 128, 200, 256, 512])
 def test_topk_wide_batches(oil, B):
     """Wide batches share every key window through LDS across query tiles."""
