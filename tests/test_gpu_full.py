@@ -209,25 +209,36 @@ def test_full_step_8192(oil):
                 assert np.array_equal(a.cpu().numpy()[b], e[j])
 
 
-def test_wide_batches_1m_full_size(oil):
-    """N = 1,048,576, d = 4,096 bf16, k = 32 with B = 200 (ragged, 2 query
-    tiles per wave) and B = 512 (4 per wave): the wide scan's launches on the
-    full pool.  Sampled queries span every wave's tiles and the ragged tail."""
+def test_batches_1m_full_size(oil):
+    """N = 1,048,576, d = 4,096 bf16, k = 32 with B = 64 and prompt exclusion
+    (the MFMA scan with two query tiles), B = 200 (wide scan, ragged, 2 query
+    tiles per wave) and B = 512 (4 per wave), all on the full pool.  Sampled
+    queries span every tile and the ragged tail."""
     cfg = workloads.BATCHED_1M
     ps, qs, k = cfg["pool"], cfg["query"], cfg["k"]
     dev = torch.device("cuda")
     wp = workloads.Pool(ps, device=dev)
     batches = {}
-    for B, sample in ((200, [0, 31, 63, 64, 127, 150, 192, 199]),
+    for B, sample in ((64, [0, 5, 31, 32, 40, 63]),
+                      (200, [0, 31, 63, 64, 127, 150, 192, 199]),
                       (512, [0, 31, 127, 128, 255, 256, 383, 511])):
-        q, _ = workloads.queries(wp, workloads.QuerySpec(B=B, noise=qs.noise, p_random=qs.p_random,
-                                                         seed=qs.seed + B))
-        batches[B] = (q, sample, StreamedOracle(_bits(q[sample]), ps.n))
+        q, src = workloads.queries(wp, workloads.QuerySpec(B=B, noise=qs.noise, p_random=qs.p_random,
+                                                           seed=qs.seed + B))
+        ex = None
+        if B == 64:
+            ex = torch.where(src >= 0, wp.prompts[src.clamp(min=0).long()], torch.full_like(src, -1))
+        batches[B] = (q, sample, StreamedOracle(_bits(q[sample]), ps.n), ex)
     pool = oil.Pool(ps.d, ps.n, device=dev)
     _fill(pool, wp, 0, ps.n, dev, [b[2] for b in batches.values()])
-    for B, (q, sample, orc) in batches.items():
-        s, i = pool.query_topk(q, k)
+    prompts = wp.prompts.numpy()
+    for B, (q, sample, orc, ex) in batches.items():
+        s, i = pool.query_topk(q, k, exclude_prompt=None if ex is None else ex.to(dev))
         torch.cuda.synchronize()
         gs, gi = s.cpu().numpy(), i.cpu().numpy()
+        if ex is not None:
+            for j, b in enumerate(sample):
+                if int(ex[b]) >= 0:
+                    orc.s[j, prompts == int(ex[b])] = -np.inf
+                    assert not np.isin(gi[b][gi[b] >= 0], np.flatnonzero(prompts == int(ex[b]))).any()
         check_topk(gs[sample], gi[sample], orc.s, k)
         _rescore_returned(wp, gs[::25], gi[::25], _bits(q[::25]))
