@@ -64,6 +64,14 @@
 #ifndef OIL_RESCORE_PF
 #define OIL_RESCORE_PF 3
 #endif
+// Windows in flight per wave of the remainder launch of the B <= 64 scan,
+// for one and two query tiles.
+#ifndef OIL_TAIL_PF1
+#define OIL_TAIL_PF1 7
+#endif
+#ifndef OIL_TAIL_PF2
+#define OIL_TAIL_PF2 3
+#endif
 // Row blocks per workgroup of the wide scan (B > 64) with 1, 2 and 4 query
 // tiles per wave.
 #ifndef OIL_WIDE_MT1
@@ -232,13 +240,13 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
     const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld,
-    const float* __restrict__ kscale, const float* __restrict__ qscale)
+    const float* __restrict__ kscale, const float* __restrict__ qscale, int64_t rb_base)
 {
     constexpr int NS = PF + 1;
     const int lane = threadIdx.x & 63;
     const int h = lane >> 5, r = lane & 31;
     const int wave = threadIdx.x >> 6;
-    const int64_t rbb = (int64_t)blockIdx.x * 4 * MT;  // the block's first row block
+    const int64_t rbb = rb_base + (int64_t)blockIdx.x * 4 * MT;  // the block's first row block
     const int64_t rb0 = rbb + wave * MT;
     const bool live = rb0 * kRowBlock < n_valid;  // waves past the pool only join the block store
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
@@ -718,6 +726,58 @@ static void launch_gemv(dim3 g, size_t lds, hipStream_t st, const uint16_t* keys
                        prompt, exclude, G, g_ld);
 }
 
+// Compute units of the current device (cached per device).
+static int device_cus()
+{
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 256;
+    if (cus[dev] == 0) {
+        int n = 0;
+        cus[dev] = (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+                       ? n
+                       : 256;
+    }
+    return cus[dev];
+}
+
+// The MFMA scan for B <= 64.  Each wave walks every key window of its MT row
+// blocks, so a wave lives as long as the whole scan when the chip is full.
+// Row blocks that fill whole generations of waves (all the SIMDs can hold)
+// go to the main grid; a small remainder would leave a few waves walking every window
+// nearly alone at the end (latency-bound, about 2-3 us per window pair), so
+// it goes to a second launch with one row block per wave and TPF windows in
+// flight.  Every row block's MFMA sequence is the same in both launches.
+template <int MT, int NT, int PF, int TPF, int FMT>
+static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid, int64_t n_rb,
+                          const bf16x8* qf, int32_t B, const int32_t* prompt, const int32_t* exclude,
+                          uint64_t* G, int64_t g_ld, const float* kscale, const float* qscale, hipStream_t stream)
+{
+    constexpr int kWavesPerSimd = NT == 1 ? 2 : 1;  // what the kernels' register use allows
+    const int64_t gen = (int64_t)device_cus() * 4 * kWavesPerSimd * MT;
+    // Measured on 1M x 4096 (B = 32): a remainder of 1-15 row blocks costs the
+    // main grid 0-30 us (its waves start early enough to hide), the second
+    // launch 14-30 us; from 16 on the main grid pays 30-75 us, the second
+    // launch 23-34 us.
+    constexpr int64_t kTailMin = 16;
+    int64_t n_main = n_rb, n_tail = 0;
+    if (n_rb > gen) {
+        const int64_t rem = n_rb % gen;
+        if (rem >= kTailMin && rem <= gen / 4) {
+            n_main = n_rb - rem;
+            n_tail = rem;
+        }
+    }
+    hipLaunchKernelGGL((scan_mfma_kernel<MT, NT, PF, FMT>), dim3((unsigned)((n_main + 4 * MT - 1) / (4 * MT))),
+                       dim3(256), 0, stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale,
+                       qscale, (int64_t)0);
+    if (n_tail > 0)
+        hipLaunchKernelGGL((scan_mfma_kernel<1, NT, TPF, FMT>), dim3((unsigned)((n_tail + 3) / 4)), dim3(256), 0,
+                           stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale,
+                           n_main);
+}
+
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
                        uint64_t* G, int64_t g_ld, hipStream_t stream, int fmt, const float* kscale,
@@ -730,13 +790,11 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
         constexpr int MT = OIL_FP8_MT, MT2 = OIL_FP8_MT2, PF = OIL_FP8_PF;
         const bf16x8* qf = (const bf16x8*)qbuf;
         if (scan_query_tiles(B) == 1)
-            hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyFp8>), dim3((unsigned)((n_rb + 4 * MT - 1) / (4 * MT))),
-                               dim3(256), 0, stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld,
-                               kscale, qscale);
+            launch_narrow<MT, 1, PF, OIL_TAIL_PF1, kKeyFp8>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude,
+                                                            G, g_ld, kscale, qscale, stream);
         else
-            hipLaunchKernelGGL((scan_mfma_kernel<MT2, 2, PF, kKeyFp8>),
-                               dim3((unsigned)((n_rb + 4 * MT2 - 1) / (4 * MT2))), dim3(256), 0, stream, keys, ld,
-                               rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+            launch_narrow<MT2, 2, PF, OIL_TAIL_PF2, kKeyFp8>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude,
+                                                             G, g_ld, kscale, qscale, stream);
         return hipGetLastError();
     }
     if (!scan_uses_mfma(B, ld)) {
@@ -768,13 +826,11 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
     }
     constexpr int MT = OIL_BF16_MT, MT2 = OIL_BF16_MT2, PF = OIL_BF16_PF;
     if (scan_query_tiles(B) == 1)
-        hipLaunchKernelGGL((scan_mfma_kernel<MT, 1, PF, kKeyBf16>), dim3((unsigned)((n_rb + 4 * MT - 1) / (4 * MT))),
-                           dim3(256), 0, stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, nullptr,
-                           nullptr);
+        launch_narrow<MT, 1, PF, OIL_TAIL_PF1, kKeyBf16>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G,
+                                                         g_ld, nullptr, nullptr, stream);
     else
-        hipLaunchKernelGGL((scan_mfma_kernel<MT2, 2, PF, kKeyBf16>),
-                           dim3((unsigned)((n_rb + 4 * MT2 - 1) / (4 * MT2))), dim3(256), 0, stream, keys, ld, rs,
-                           ws, n_valid, qf, B, prompt, exclude, G, g_ld, nullptr, nullptr);
+        launch_narrow<MT2, 2, PF, OIL_TAIL_PF2, kKeyBf16>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G,
+                                                          g_ld, nullptr, nullptr, stream);
     return hipGetLastError();
 }
 

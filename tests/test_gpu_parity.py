@@ -131,6 +131,41 @@ def test_topk_runs_of_neighbours(oil, key_format, B, k):
     check_topk(s_.cpu().numpy(), i_.cpu().numpy(), o, k)
 
 
+@pytest.mark.parametrize("key_format,B,extra", [("bf16", 8, 1000), ("bf16", 40, 1000), ("fp8", 8, 777),
+                                                 ("fp8", 40, 4000), ("bf16", 16, 0), ("bf16", 16, 100)])
+def test_topk_pool_past_whole_waves(oil, key_format, B, extra):
+    """Pools a little past a whole number of scan waves (262,144 rows plus up
+    to a few thousand): from 16 row blocks on, the rows beyond go to the
+    scan's remainder launch (one row block per wave, deeper prefetch); fewer
+    stay in the main grid.  With prompt exclusion."""
+    n, d = 262144 + extra, 64
+    g = torch.Generator().manual_seed(B + extra)
+    raw = torch.randn((n, d), generator=g)
+    q = torch.randn((B, d), generator=g)
+    for b in range(B):                       # near-copies in the remainder and in the main part
+        raw[n - 1 - 3 * b] = q[b] + 0.1 * torch.randn(d, generator=g)
+        raw[1000 + 97 * b] = q[b] + 0.1 * torch.randn(d, generator=g)
+    ids = torch.arange(n, dtype=torch.int32)
+    prompts = ids // 48
+    ex = prompts[torch.arange(B) * 97 + 1000].clone()
+    ex[::3] = -1
+    pool = oil.Pool(d, n, key_format=key_format)
+    pool.append(raw.cuda(), ids.cuda(), ids.cuda(), prompts.cuda())
+    s_, i_ = pool.query_topk(q.cuda(), 16, exclude_prompt=ex.cuda())
+    torch.cuda.synchronize()
+    if key_format == "fp8":
+        kc, ki = oracle.quantize_rows_fp8(raw.numpy())
+        qc, qi = oracle.quantize_rows_fp8(q.numpy())
+        o = oracle.scores_fp8(kc, ki, qc, qi)
+    else:
+        o = oracle_rows(_stored(pool, n), q.numpy())
+    pr = prompts.numpy()
+    for b in range(B):
+        if ex[b] >= 0:
+            o[b, pr == int(ex[b])] = -np.inf
+    check_topk(s_.cpu().numpy(), i_.cpu().numpy(), o, 16)
+
+
 @pytest.mark.parametrize("B", [65, 96, 128, 200, 256, 512])
 def test_topk_wide_batches(oil, B):
     """Wide batches share every key window through LDS across query tiles."""
