@@ -60,6 +60,11 @@
 #ifndef OIL_FP8_PF
 #define OIL_FP8_PF 1
 #endif
+// Windows in flight per wave of the GEMV rescore (B <= 4: few waves, each
+// walking every window of one block, so latency-bound).
+#ifndef OIL_RESCORE_GEMV_PF
+#define OIL_RESCORE_GEMV_PF 7
+#endif
 // Prefetch depth (windows in flight per wave) of the MFMA rescore.
 #ifndef OIL_RESCORE_PF
 #define OIL_RESCORE_PF 3
@@ -674,27 +679,30 @@ __global__ __launch_bounds__(64) void rescore_gemv_kernel(
     const bf16x8* tile = (const bf16x8*)(keys + rb * rs) + lane;
     const uint16_t* qrow = q + (int64_t)qb * ld;
     float acc = 0.f;
-    bf16x8 a[NS][4];
+    // the block's key tiles and the query's matching columns, both in the
+    // prefetch ring (the query read from global memory each window would put
+    // an L2 round trip on every step)
+    bf16x8 a[NS][4], b[NS][4];
+    auto load = [&](int stage, int w) {
 #pragma unroll
-    for (int p = 0; p < PF; p++) {
-        const int w = p < nwin ? p : nwin - 1;
+        for (int s = 0; s < 4; s++) {
+            a[stage][s] = __builtin_nontemporal_load(tile + w * ws8 + s * 64);
+            b[stage][s] = *(const bf16x8*)(qrow + w * kWindow + 32 * h + 8 * s);
+        }
+    };
 #pragma unroll
-        for (int s = 0; s < 4; s++)
-            a[p][s] = __builtin_nontemporal_load(tile + w * ws8 + s * 64);
-    }
+    for (int p = 0; p < PF; p++)
+        load(p, p < nwin ? p : nwin - 1);
     const int nloop = (nwin + NS - 1) / NS * NS;
     for (int w0 = 0; w0 < nloop; w0 += NS) {
 #pragma unroll
         for (int u = 0; u < NS; u++) {
             const int wl = w0 + u + PF < nwin ? w0 + u + PF : nwin - 1;
-#pragma unroll
-            for (int s = 0; s < 4; s++)
-                a[(u + PF) % NS][s] = __builtin_nontemporal_load(tile + wl * ws8 + s * 64);
+            load((u + PF) % NS, wl);
             if (w0 + u < nwin) {
-                const int col = (w0 + u) * kWindow + 32 * h;
 #pragma unroll
                 for (int s = 0; s < 4; s++)
-                    acc = dot8_bf16(a[u][s], *(const bf16x8*)(qrow + col + 8 * s), acc);
+                    acc = dot8_bf16(a[u][s], b[u][s], acc);
             }
         }
     }
@@ -845,7 +853,7 @@ hipError_t launch_rescore(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
                            (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC, kscale,
                            qscale);
     else if (!scan_uses_mfma(B, ld))
-        hipLaunchKernelGGL((rescore_gemv_kernel<3>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
+        hipLaunchKernelGGL((rescore_gemv_kernel<OIL_RESCORE_GEMV_PF>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
                            (const uint16_t*)qbuf, blocks, k, prompt, exclude, SC);
     else
         hipLaunchKernelGGL((rescore_mfma_kernel<OIL_RESCORE_PF, kKeyBf16>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
