@@ -107,11 +107,21 @@ def test_batched_1m_full_size(oil):
         assert np.array_equal(a.cpu().numpy(), e)
     # end to end where the retrieval is unambiguous and away from theta
     gct, gcl = pool.gather(i, s, rule_g, L)
+    gtree = oil.merge_trees(workloads.anchors(wp, src).to(dev), None, None, 0, gct, gcl, cfg["sem_budget"], mx)
     torch.cuda.synchronize()
+    gct_t, gcl_t = gct, gcl
     gct, gcl = gct.cpu().numpy(), gcl.cpu().numpy()
     for j, b in enumerate(sample):
         if flags[j][1] and away_from_edges(os32[j], [0.8]):
             assert np.array_equal(gcl[b], ecl[j]) and np.array_equal(gct[b], ect[j])
+    # every query: the GPU's own (idx, score) lists through the oracle's gather,
+    # and the GPU's chains through the oracle's merge, bit-exact
+    oct2, ocl2 = oracle.gather(tok, tr, ps.n, gi, gs, rule_o, L)
+    assert np.array_equal(gct, oct2) and np.array_equal(gcl, ocl2)
+    otree = oracle.tree_merge(workloads.anchors(wp, src).numpy(), np.zeros((len(gi), 0, 1), np.int32),
+                              np.zeros((len(gi), 0), np.int32), 0, gct, gcl, cfg["sem_budget"], mx)
+    for a, e in zip(gtree, otree):
+        assert np.array_equal(a.cpu().numpy(), e)
 
 
 def test_stream_5120_checkpoints(oil):
@@ -207,6 +217,13 @@ def test_full_step_8192(oil):
             assert np.array_equal(cl.cpu().numpy()[b], ocl[j])
             for a, e in zip(tree, otree):
                 assert np.array_equal(a.cpu().numpy()[b], e[j])
+    # all 64 queries: the GPU's (idx, score) lists through the oracle's gather,
+    # and the GPU's chains with the lexical drafts through the oracle's merge
+    oct3, ocl3 = oracle.gather(tok, tr, ps.n, gi, gs, rule_o, L)
+    assert np.array_equal(ct.cpu().numpy(), oct3) and np.array_equal(cl.cpu().numpy(), ocl3)
+    otree3 = oracle.tree_merge(anchor.numpy(), lt.numpy(), ll.numpy(), lb, oct3, ocl3, sb, mx)
+    for a, e in zip(tree, otree3):
+        assert np.array_equal(a.cpu().numpy(), e)
 
 
 def test_batches_1m_full_size(oil):
