@@ -436,46 +436,55 @@ def main():
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
+MFMA_FP8_PEAK_TFLOPS = 5000.0
 
 
 def sweep(args, oil, workloads, dev, cfg):
-    """Scan throughput across query batches on the 1M x 4096 pool."""
+    """Scan throughput across query batches on the 1M x 4096 pool, bf16 keys,
+    then (unless --no-fp8) the same queries on an fp8 pool of the same rows."""
     import torch
     ps, qs, k = cfg["pool"], cfg["query"], cfg["k"]
     N, d = ps.n, ps.d
     wp = workloads.Pool(ps, device=dev)
-    pool = oil.Pool(d, N, device=dev)
-    for s0 in range(0, N, 65536):
-        pool.append(wp.raw_rows(s0, 65536), wp.tokens[s0:s0 + 65536].to(dev),
-                    wp.traces[s0:s0 + 65536].to(dev), wp.prompts[s0:s0 + 65536].to(dev))
-    rows = []
     K, W = max(args.steps // 10, 5), 2
-    for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
-        q, _ = workloads.queries(wp, workloads.QuerySpec(B=B, noise=qs.noise, p_random=qs.p_random,
-                                                         seed=qs.seed + 1000 + B))
-        q = q.contiguous()
-        out = (torch.empty((B, k), dtype=torch.float32, device=dev),
-               torch.empty((B, k), dtype=torch.int32, device=dev))
-        for _ in range(W):
-            pool.query_topk(q, k, out=out)
-        torch.cuda.synchronize()
-        oil.scan_timer_start(K)
-        t0 = time.perf_counter()
-        for _ in range(K):
-            pool.query_topk(q, k, out=out)
-        torch.cuda.synchronize()
-        el = time.perf_counter() - t0
-        n_t, ms = oil.scan_timer_stop()
-        scan_s = ms / n_t / 1e3
-        gbs = (N * d * 2 + B * d * 2) / scan_s / 1e9
-        tflops = 2.0 * B * N * d / scan_s / 1e12
-        rows.append({"B": B, "scan_ms": round(scan_s * 1e3, 4), "scan_GBps": round(gbs, 1),
-                     "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "scan_TFLOPs": round(tflops, 1),
-                     "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "query_topk_ms": round(1e3 * el / K, 4), "queries_per_s": round(B * K / el, 1)})
-        log(f"B={B}: scan {scan_s * 1e3:.3f} ms, {gbs:.0f} GB/s, {tflops:.0f} TFLOP/s")
-    print(json.dumps({"sweep": rows, "pool_rows": N, "dim": d, "k": k,
-                      "kernels": "B<=4 scan_gemv, B<=64 scan_mfma, B>64 scan_mfma_wide"}), flush=True)
+    out = {"pool_rows": N, "dim": d, "k": k,
+           "kernels": "B<=4 scan_gemv, B<=64 scan_mfma, B>64 scan_mfma_wide (fp8: scan_mfma up to 64)"}
+    fmts = [("bf16", 2, MFMA_BF16_PEAK_TFLOPS)] + ([] if args.no_fp8 else [("fp8", 1, MFMA_FP8_PEAK_TFLOPS)])
+    for fmt, key_bytes, mfma_peak in fmts:
+        pool = oil.Pool(d, N, device=dev, key_format=fmt)
+        for s0 in range(0, N, 65536):
+            pool.append(wp.raw_rows(s0, 65536), wp.tokens[s0:s0 + 65536].to(dev),
+                        wp.traces[s0:s0 + 65536].to(dev), wp.prompts[s0:s0 + 65536].to(dev))
+        ldk = (d + 127) // 128 * 128 if fmt == "fp8" else (d + 63) // 64 * 64
+        rows = []
+        for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
+            q, _ = workloads.queries(wp, workloads.QuerySpec(B=B, noise=qs.noise, p_random=qs.p_random,
+                                                             seed=qs.seed + 1000 + B))
+            q = q.contiguous()
+            res = (torch.empty((B, k), dtype=torch.float32, device=dev),
+                   torch.empty((B, k), dtype=torch.int32, device=dev))
+            for _ in range(W):
+                pool.query_topk(q, k, out=res)
+            torch.cuda.synchronize()
+            oil.scan_timer_start(K)
+            t0 = time.perf_counter()
+            for _ in range(K):
+                pool.query_topk(q, k, out=res)
+            torch.cuda.synchronize()
+            el = time.perf_counter() - t0
+            n_t, ms = oil.scan_timer_stop()
+            scan_s = ms / n_t / 1e3
+            gbs = (N * ldk * key_bytes + B * ldk * key_bytes) / scan_s / 1e9
+            tflops = 2.0 * B * N * d / scan_s / 1e12
+            rows.append({"B": B, "scan_ms": round(scan_s * 1e3, 4), "scan_GBps": round(gbs, 1),
+                         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "scan_TFLOPs": round(tflops, 1),
+                         "mfma_frac": round(tflops / mfma_peak, 4),
+                         "query_topk_ms": round(1e3 * el / K, 4), "queries_per_s": round(B * K / el, 1)})
+            log(f"{fmt} B={B}: scan {scan_s * 1e3:.3f} ms, {gbs:.0f} GB/s, {tflops:.0f} TFLOP/s")
+        out["sweep" if fmt == "bf16" else "sweep_fp8"] = rows
+        del pool
+        torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
 
 
 def _timed(torch, fn, steps):

@@ -55,7 +55,7 @@ enum { OIL_F32 = 0, OIL_BF16 = 1 };
 #define OIL_MAX_NODES 256
 #define OIL_MAX_BANDS 4
 /* Largest query batch an fp8 pool serves. */
-#define OIL_MAX_B_FP8 64
+#define OIL_MAX_B_FP8 512
 
 /* Limits of the exact-suffix lexical source: context tokens, drafts per
  * request, tokens per draft, and the candidate capacity per request. */
@@ -120,8 +120,8 @@ int32_t oil_pool_size(const oil_pool *pool, int64_t *n_valid);
  * scales.  Keys are stored in 4 KiB tiles of 32 rows x 128 columns in the
  * operand order of the 32x32x16 fp8 MFMA, window-major as in the bf16 pool,
  * at half the bytes per row.  Append, query, gather and everything after
- * them take an fp8 pool like a bf16 one; queries are limited to
- * OIL_MAX_B_FP8 per call. */
+ * them take an fp8 pool like a bf16 one, for the same query batches
+ * (OIL_MAX_B_FP8 = OIL_MAX_B per call). */
 size_t oil_pool_key_bytes_fp8(int32_t dim, int64_t capacity);
 
 /* key_buf: oil_pool_key_bytes_fp8(dim, capacity) bytes, 256-byte aligned;

@@ -25,7 +25,7 @@ LIB_PATH = os.path.join(_HERE, "liboilbird.so")
 
 OIL_F32, OIL_BF16 = 0, 1
 MAX_K, MAX_B, MAX_NODES, MAX_BANDS = 64, 512, 256, 4
-MAX_B_FP8 = 64
+MAX_B_FP8 = 512
 LEX_MAX_CTX, LEX_MAX_N, LEX_MAX_LEN, LEX_MAX_CAND = 32, 16, 64, 4096
 REC_DEPTH, REC_MAX_OUT = 6, 8
 

@@ -14,7 +14,6 @@
 #define OIL_LEX_CAND_MAX 4096
 #define OIL_REC_DEPTH_MAX 6
 #define OIL_REC_OUT_MAX 8
-#define OIL_MAX_B_FP8 64
 
 namespace oil {
 
@@ -44,7 +43,7 @@ hipError_t launch_normalize_rows(const void* raw, int dtype, int32_t d, int64_t 
 
 int scan_uses_mfma(int32_t B, int32_t ld);
 int scan_query_tiles(int32_t B);
-// fmt: kKeyBf16, or kKeyFp8 (B <= 64; ld = fp8 row width, a multiple of
+// fmt: kKeyBf16, or kKeyFp8 (ld = fp8 row width, a multiple of
 // 128; kscale per stored row and qscale per query are the inverse scales).
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,

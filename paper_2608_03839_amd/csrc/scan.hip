@@ -392,12 +392,13 @@ __device__ __forceinline__ void wait_vmcnt_at_most()
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <int MT, int NTW>
+template <int MT, int NTW, int FMT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OIL_WIDE_WPE(MT, NTW)))) void
 scan_mfma_wide_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
-    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld)
+    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld,
+    const float* __restrict__ kscale, const float* __restrict__ qscale)
 {
     // three windows of the block's MT key tiles, as three separate LDS objects
     // so that the slot each access uses is known at compile time
@@ -407,7 +408,7 @@ scan_mfma_wide_kernel(
     const int h = lane >> 5, r = lane & 31;
     const int64_t rb0 = (int64_t)blockIdx.x * MT;
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
-    const int nwin = ld / kWindow;
+    const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
     const int n_qt = (B + 31) / 32;
     // Addresses are a wave-uniform base plus the lane's 16-byte slot, so the
     // loads take a scalar base and one shared 32-bit lane offset.
@@ -469,7 +470,7 @@ scan_mfma_wide_kernel(
         for (int mt = 0; mt < MT; mt++)
 #pragma unroll
             for (int nt = 0; nt < NTW; nt++)
-                acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt][s], acc[mt][nt], 0, 0, 0);
+                acc[mt][nt] = mfma_step<FMT>(a[mt], b[nt][s], acc[mt][nt]);
     };
     auto clampw = [&](int w) { return w < nwin ? w : nwin - 1; };
     bf16x8 b0[NTW][4], b1[NTW][4];
@@ -537,17 +538,22 @@ scan_mfma_wide_kernel(
 
     // block keys, as in scan_mfma_kernel
     int32_t ex[NTW];
+    float qs[NTW];
 #pragma unroll
     for (int nt = 0; nt < NTW; nt++) {
         const int qb = (wave * NTW + nt) * 32 + r;
         ex[nt] = (exclude && qb < B) ? exclude[qb] : -1;
+        qs[nt] = (FMT == kKeyBf16 || qb >= B) ? 1.f : qscale[qb];
     }
 #pragma unroll
     for (int mt = 0; mt < MT; mt++) {
         const int64_t rb = rb0 + mt;
         int32_t pr[16];
+        float ks[16];
         if (exclude)
             tile_rows_load(pr, prompt, rb * kRowBlock, h, n_valid);
+        if constexpr (FMT == kKeyFp8)
+            tile_rows_load(ks, kscale, rb * kRowBlock, h, n_valid);
 #pragma unroll
         for (int nt = 0; nt < NTW; nt++) {
             const int qb = (wave * NTW + nt) * 32 + r;
@@ -560,6 +566,8 @@ scan_mfma_wide_kernel(
                 const int64_t row = rb * kRowBlock + (e / 4) * 8 + h * 4 + e % 4;
                 if (row < n_valid) {
                     float v = t[e];
+                    if constexpr (FMT == kKeyFp8)
+                        v = v * (ks[e] * qs[nt]);  // powers of two: exact, as the narrow scan scales it
                     if (ex[nt] >= 0 && pr[e] == ex[nt])
                         v = __uint_as_float(kNoScoreBits);
                     const uint64_t key = rank_key(v, (uint32_t)row);
@@ -786,6 +794,25 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
                            n_main);
 }
 
+// The wide scan (64 < B <= 512), either key format.
+template <int FMT>
+static void launch_wide(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid, int64_t n_rb,
+                        const bf16x8* qf, int32_t B, const int32_t* prompt, const int32_t* exclude, uint64_t* G,
+                        int64_t g_ld, const float* kscale, const float* qscale, hipStream_t stream)
+{
+    const int ntw = (scan_query_tiles(B) + 3) / 4;
+    constexpr int M1 = OIL_WIDE_MT1, M2 = OIL_WIDE_MT2, M4 = OIL_WIDE_MT4;
+    if (ntw == 1)
+        hipLaunchKernelGGL((scan_mfma_wide_kernel<M1, 1, FMT>), dim3((unsigned)((n_rb + M1 - 1) / M1)), dim3(256), 0,
+                           stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+    else if (ntw == 2)
+        hipLaunchKernelGGL((scan_mfma_wide_kernel<M2, 2, FMT>), dim3((unsigned)((n_rb + M2 - 1) / M2)), dim3(256), 0,
+                           stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+    else
+        hipLaunchKernelGGL((scan_mfma_wide_kernel<M4, 4, FMT>), dim3((unsigned)((n_rb + M4 - 1) / M4)), dim3(256), 0,
+                           stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+}
+
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
                        uint64_t* G, int64_t g_ld, hipStream_t stream, int fmt, const float* kscale,
@@ -794,10 +821,13 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
     if (n_valid <= 0)
         return hipSuccess;
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
-    if (fmt == kKeyFp8) {  // B <= 64 (checked by the caller)
+    if (fmt == kKeyFp8) {
         constexpr int MT = OIL_FP8_MT, MT2 = OIL_FP8_MT2, PF = OIL_FP8_PF;
         const bf16x8* qf = (const bf16x8*)qbuf;
-        if (scan_query_tiles(B) == 1)
+        if (B > 64)
+            launch_wide<kKeyFp8>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G, g_ld, kscale, qscale,
+                                 stream);
+        else if (scan_query_tiles(B) == 1)
             launch_narrow<MT, 1, PF, OIL_TAIL_PF1, kKeyFp8>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude,
                                                             G, g_ld, kscale, qscale, stream);
         else
@@ -819,17 +849,8 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
     }
     const bf16x8* qf = (const bf16x8*)qbuf;
     if (B > 64) {
-        const int ntw = (scan_query_tiles(B) + 3) / 4;
-        constexpr int M1 = OIL_WIDE_MT1, M2 = OIL_WIDE_MT2, M4 = OIL_WIDE_MT4;
-        if (ntw == 1)
-            hipLaunchKernelGGL((scan_mfma_wide_kernel<M1, 1>), dim3((unsigned)((n_rb + M1 - 1) / M1)), dim3(256), 0,
-                               stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
-        else if (ntw == 2)
-            hipLaunchKernelGGL((scan_mfma_wide_kernel<M2, 2>), dim3((unsigned)((n_rb + M2 - 1) / M2)), dim3(256), 0,
-                               stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
-        else
-            hipLaunchKernelGGL((scan_mfma_wide_kernel<M4, 4>), dim3((unsigned)((n_rb + M4 - 1) / M4)), dim3(256), 0,
-                               stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld);
+        launch_wide<kKeyBf16>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G, g_ld, nullptr, nullptr,
+                              stream);
         return hipGetLastError();
     }
     constexpr int MT = OIL_BF16_MT, MT2 = OIL_BF16_MT2, PF = OIL_BF16_PF;
