@@ -448,7 +448,7 @@ def sweep(args, oil, workloads, dev, cfg):
     wp = workloads.Pool(ps, device=dev)
     K, W = max(args.steps // 10, 5), 2
     out = {"pool_rows": N, "dim": d, "k": k,
-           "kernels": "B<=4 scan_gemv, B<=64 scan_mfma, B>64 scan_mfma_wide (fp8: scan_mfma up to 64)"}
+           "kernels": "bf16: B<=4 scan_gemv, B<=64 scan_mfma, B>64 scan_mfma_wide; fp8: B<=64 scan_mfma, B>64 scan_mfma_wide"}
     fmts = [("bf16", 2, MFMA_BF16_PEAK_TFLOPS)] + ([] if args.no_fp8 else [("fp8", 1, MFMA_FP8_PEAK_TFLOPS)])
     for fmt, key_bytes, mfma_peak in fmts:
         pool = oil.Pool(d, N, device=dev, key_format=fmt)
