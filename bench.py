@@ -29,6 +29,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+TIMED_SCANS = 20        # about this many scan launches of the timed run carry HIP events
+LATENCY_STEPS = 50      # steps after the timed run, timed one by one
 METRIC = "retrieval queries/s + pool-scan HBM GB/s (% peak) at N=1M, d=4096 bf16"
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "scan_mfma_n1m_d4096_b32_traffic.txt")
 PROFILE_TRAFFIC_FP8 = os.path.join(ROOT, "profiles", "scan_fp8_n1m_d4096_b32_traffic.txt")
@@ -170,7 +172,9 @@ def main():
     k, L, sem_budget = cfg["k"], cfg["L"], cfg["sem_budget"]
     B, N, d = qs.B, ps.n, ps.d
     K, W = args.steps, args.warmup
-    steps = K + W
+    # steps after the timed run, timed one by one for the latency distribution
+    LAT = min(K, LATENCY_STEPS)
+    steps = W + K + LAT
 
     if args.sweep:
         return sweep(args, oil, workloads, dev, cfg)
@@ -238,26 +242,33 @@ def main():
         step(t)
     torch.cuda.synchronize()
     n_before = len(pool)
-    # one HIP event at every step boundary (recording adds no GPU work): the
-    # per-step latency distribution of the same timed run
-    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
-    oil.scan_timer_start(K)
+    # the scan's duration from HIP events bound to every `every`-th scan
+    # launch of the timed run (an event on the stream delays the kernel after
+    # it by a few microseconds, so only a sample carries them)
+    every = max(1, K // TIMED_SCANS)
+    oil.scan_timer_start(K, every)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    bounds[0].record()
-    for t in range(W, steps):
+    for t in range(W, W + K):
         step(t)
-        bounds[t - W + 1].record()
     torch.cuda.synchronize()
     t_end = time.perf_counter()
-    step_ms = np.array([bounds[j].elapsed_time(bounds[j + 1]) for j in range(K)])
     n_timed, scan_ms_total = oil.scan_timer_stop()
     n_after = len(pool)
     elapsed = t_end - t_start
     ms_per_step = 1e3 * elapsed / K
     qps = B * K / elapsed
     fired = float((out_s[:, 0] >= 0.8).float().mean())
-    log(f"{K} steps in {elapsed * 1e3:.1f} ms; scan timed {n_timed}x, {scan_ms_total / n_timed:.4f} ms avg")
+    log(f"{K} steps in {elapsed * 1e3:.1f} ms; scan timed {n_timed}x (every {every}), "
+        f"{scan_ms_total / n_timed:.4f} ms avg")
+    # per-step latency: LAT more steps with a HIP event at every step boundary
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(LAT + 1)]
+    bounds[0].record()
+    for t in range(W + K, steps):
+        step(t)
+        bounds[t - W - K + 1].record()
+    torch.cuda.synchronize()
+    step_ms = np.array([bounds[j].elapsed_time(bounds[j + 1]) for j in range(LAT)])
 
     # the calls after the merge (tree mask for the verifying forward, greedy
     # accept-walk on synthetic verifier predictions), timed separately so the
@@ -336,12 +347,15 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "kernel": "scan_mfma_kernel<4,1,1,bf16>",
                 "scan_ms": round(scan_s * 1e3, 4), "bytes_per_launch": int(bytes_alg),
+                "timed_launches": n_timed, "timed_every": every,
                 "read_ceiling": ceiling,
                 "frac_of_read_ceiling": round(achieved / ceiling["GBps"], 4)}
     extras["step_latency_ms"] = {"p10": round(float(np.percentile(step_ms, 10)), 4),
                                  "p50": round(float(np.percentile(step_ms, 50)), 4),
                                  "p90": round(float(np.percentile(step_ms, 90)), 4),
-                                 "source": "HIP events at the timed run's step boundaries"}
+                                 "steps": LAT,
+                                 "source": "HIP events at the step boundaries of the steps after "
+                                           "the timed run (same workload, next appends and queries)"}
 
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu = None
@@ -395,10 +409,10 @@ def main():
             step8(t)
         torch.cuda.synchronize()
         m0 = len(pool8)
-        oil.scan_timer_start(K)
+        oil.scan_timer_start(K, every)
         torch.cuda.synchronize()
         f0 = time.perf_counter()
-        for t in range(W, steps):
+        for t in range(W, W + K):
             step8(t)
         torch.cuda.synchronize()
         f1 = time.perf_counter()
@@ -522,12 +536,16 @@ def other_workloads(args, oil, workloads, dev):
         oil.merge_trees(A[t], None, None, 0, c_, l_, sb, 1 + sb)
 
     _timed(torch, dec, range(W))
-    oil.scan_timer_start(K)
     ms = _timed(torch, dec, range(W, W + K))
+    lat = _timed_events(torch, dec, range(W, W + K))
+    # the scan's duration from events bound to it, in a pass of its own (an
+    # event delays the kernel after it by a few microseconds)
+    oil.scan_timer_start(K)
+    _timed(torch, dec, range(W, W + K))
     nt, sms = oil.scan_timer_stop()
     scan_s = sms / nt / 1e3
     gbs = (ps.n * ps.d * 2 + ps.d * 2) / scan_s / 1e9
-    out["decode_64k"] = {"ms_per_step": round(ms, 4), "latency_ms": _timed_events(torch, dec, range(W, W + K)),
+    out["decode_64k"] = {"ms_per_step": round(ms, 4), "latency_ms": lat,
                          "scan_ms": round(scan_s * 1e3, 4), "scan_GBps": round(gbs, 1),
                          "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
                          "note": "512 MiB pool, twice the 256 MB Infinity Cache: read mostly from HBM",
@@ -567,7 +585,7 @@ def other_workloads(args, oil, workloads, dev):
 
         _timed(torch, stream, range(W))
         n0 = len(pool)
-        oil.scan_timer_start(K)
+        oil.scan_timer_start(K, max(1, K // TIMED_SCANS))
         lat = _timed_events(torch, stream, range(W, W + K))
         nt, sms = oil.scan_timer_stop()
         ms = lat["mean"]

@@ -343,14 +343,18 @@ int32_t oil_accept_walk(int32_t B, int32_t max_nodes, const int32_t *node_token,
                         const int32_t *node_parent, const int32_t *n_nodes, const int32_t *target,
                         int32_t *accept_len, int32_t *accept_nodes, int32_t *bonus, void *stream);
 
-/* Benchmark instrumentation (host; not thread-safe).  While enabled, each
- * oil_pool_query_topk call records a HIP event pair around its pool-scan
- * kernel on the call's stream, for up to max_launches calls (1 .. 65536).
- * oil_scan_timer_stop waits for those events, returns how many launches were
+/* Benchmark instrumentation (host; not thread-safe).  While enabled, the
+ * pool scans of oil_pool_query_topk calls on non-empty pools are counted
+ * from 0, and scans 0, every, 2 * every, ... (up to max_launches of them,
+ * 1 .. 65536; every >= 1) each get a HIP event pair bound to the scan itself
+ * (the start of its first kernel, the end of its last: hipExtLaunchKernel).
+ * The runtime still separates a kernel that carries events from its
+ * neighbours on the stream by a few microseconds, hence the sampling.
+ * oil_scan_timer_stop waits for those events, returns how many scans were
  * timed and their summed duration in milliseconds, and disables timing.
  * Events are created by start and destroyed by stop; no device memory is
  * allocated. */
-int32_t oil_scan_timer_start(int32_t max_launches);
+int32_t oil_scan_timer_start(int32_t max_launches, int32_t every);
 int32_t oil_scan_timer_stop(int32_t *n_launches, double *total_ms);
 
 /* Measurement aid: a plain streaming read of a device buffer, the practical

@@ -103,7 +103,7 @@ def lib():
             "oil_lexical_drafts": (i32, [P, P, P, i32, i32, P, i32, i32, i32, i32, P, sz, P, P, P]),
             "oil_accept_walk": (i32, [i32, i32, P, P, P, P, P, P, P, P]),
             "oil_read_stream": (i32, [P, sz, P, P]),
-            "oil_scan_timer_start": (i32, [i32]),
+            "oil_scan_timer_start": (i32, [i32, i32]),
             "oil_scan_timer_stop": (i32, [ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]),
         }
         for name, (res, args) in sig.items():
@@ -278,8 +278,10 @@ def read_stream(buf, sink, stream=None):
     _check("oil_read_stream", lib().oil_read_stream(_ptr(buf), nbytes, _ptr(sink), _stream(stream)))
 
 
-def scan_timer_start(max_launches: int):
-    _check("oil_scan_timer_start", lib().oil_scan_timer_start(max_launches))
+def scan_timer_start(max_launches: int, every: int = 1):
+    """Time pool scans 0, every, 2 * every, ... of the following queries (at
+    most max_launches of them)."""
+    _check("oil_scan_timer_start", lib().oil_scan_timer_start(max_launches, every))
 
 
 def scan_timer_stop():

@@ -74,14 +74,19 @@ QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
 // Scan-kernel timing for the benchmark (see oil_scan_timer_start).
 struct ScanTimer {
     hipEvent_t* ev = nullptr;
-    int32_t cap = 0, used = 0;
+    int32_t cap = 0, used = 0;  // event pairs made / bound to a scan
+    int32_t every = 1;          // time scans 0, every, 2 * every, ... since start
+    int64_t seen = 0;           // scans dispatched since start
 };
 ScanTimer g_timer;
 
-void timer_mark(hipStream_t st, int which)
+// The events of the next scan (both null when the timer is off or full, or
+// the scan is not one of the sampled ones).
+void timer_slot(hipEvent_t* start, hipEvent_t* stop)
 {
-    if (g_timer.ev && g_timer.used < g_timer.cap)
-        (void)hipEventRecord(g_timer.ev[2 * g_timer.used + which], st);
+    const bool on = g_timer.ev && g_timer.used < g_timer.cap && g_timer.seen % g_timer.every == 0;
+    *start = on ? g_timer.ev[2 * g_timer.used] : nullptr;
+    *stop = on ? g_timer.ev[2 * g_timer.used + 1] : nullptr;
 }
 
 }  // namespace
@@ -95,9 +100,9 @@ int32_t oil_read_stream(const void* buf, size_t bytes, uint64_t* sink, void* str
     return hip_status(oil::launch_read_stream(buf, (int64_t)(bytes / 16), sink, (hipStream_t)stream));
 }
 
-int32_t oil_scan_timer_start(int32_t max_launches)
+int32_t oil_scan_timer_start(int32_t max_launches, int32_t every)
 {
-    if (max_launches < 1 || max_launches > 65536 || g_timer.ev)
+    if (max_launches < 1 || max_launches > 65536 || every < 1 || g_timer.ev)
         return OIL_E_INVALID;
     g_timer.ev = (hipEvent_t*)calloc(2 * (size_t)max_launches, sizeof(hipEvent_t));
     if (!g_timer.ev)
@@ -113,6 +118,8 @@ int32_t oil_scan_timer_start(int32_t max_launches)
     }
     g_timer.cap = max_launches;
     g_timer.used = 0;
+    g_timer.every = every;
+    g_timer.seen = 0;
     return OIL_OK;
 }
 
@@ -307,12 +314,15 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
             mfma ? oil::kLayoutTiled : oil::kLayoutRows, 2048, 2048 * (int64_t)tiles, nullptr, nullptr,
             nullptr, nullptr, nullptr, nullptr, st);
     if (e == hipSuccess) {
-        timer_mark(st, 0);
+        hipEvent_t ev0, ev1;
+        timer_slot(&ev0, &ev1);
         e = oil::launch_scan(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, pool->prompts,
-                             exclude_prompt, G, w.g_ld, st, pool->fmt, pool->kscale, qscale);
-        timer_mark(st, 1);
-        if (g_timer.ev && g_timer.used < g_timer.cap)
-            g_timer.used++;
+                             exclude_prompt, G, w.g_ld, st, pool->fmt, pool->kscale, qscale, ev0, ev1);
+        if (g_timer.ev && e == hipSuccess && n_valid > 0) {
+            g_timer.seen++;
+            if (ev0)
+                g_timer.used++;
+        }
     }
     const uint64_t* chosen = nullptr;
     if (e == hipSuccess)

@@ -168,7 +168,7 @@ __global__ __launch_bounds__(256) void recycle_keys_kernel(
     for (int64_t k = first + blockIdx.x; k < total; k += gridDim.x) {
         const int64_t row = rec_src[k];
         uint16_t* dst = keys + (int64_t)rec_slot[k] * ld;
-        normalize_row_256(states, dtype, row, d, ld, true, red, [&](int32_t j, uint16_t bits) { dst[j] = bits; });
+        normalize_row<256>(states, dtype, row, d, ld, true, red, [&](int32_t j, uint16_t bits) { dst[j] = bits; });
     }
 }
 

@@ -37,6 +37,8 @@
 // A key's accumulation order never depends on where the key sits, so
 // identical keys score identically.  Positions whose prompt id equals the
 // query's exclusion id get the "no position" bit pattern.
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -733,13 +735,35 @@ int scan_uses_mfma(int32_t B, int32_t ld) { return B > 4 || (int64_t)B * ld * 2 
 
 int scan_query_tiles(int32_t B) { return (B + 31) / 32; }
 
+// Where a scan's kernels go: the stream, and two events (or null) bound to
+// the start of the scan's first kernel and the end of its last.  Events
+// bound to the dispatches themselves take their times from the kernels'
+// own timestamps and put nothing between kernels on the stream (an event
+// recorded between two kernels delays the second by a few microseconds).
+struct ScanLaunch {
+    hipStream_t stream;
+    hipEvent_t start, stop;
+};
+
+// Launch one 256-thread scan kernel; first / last say whether it is the
+// scan's first / last kernel (which carry the events).
+template <class K, class... A>
+static void dispatch(const ScanLaunch& sl, bool first, bool last, K kernel, dim3 grid, size_t lds, A... args)
+{
+    hipEvent_t s = first ? sl.start : nullptr, e = last ? sl.stop : nullptr;
+    if (s || e)
+        hipExtLaunchKernelGGL(kernel, grid, dim3(256), (uint32_t)lds, sl.stream, s, e, 0u, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, dim3(256), lds, sl.stream, args...);
+}
+
 template <int NB>
-static void launch_gemv(dim3 g, size_t lds, hipStream_t st, const uint16_t* keys, int32_t ld,
+static void launch_gemv(dim3 g, size_t lds, const ScanLaunch& sl, const uint16_t* keys, int32_t ld,
                         int64_t rs, int64_t ws, int64_t n_valid, const uint16_t* q,
                         const int32_t* prompt, const int32_t* exclude, uint64_t* G, int64_t g_ld)
 {
-    hipLaunchKernelGGL((scan_gemv_kernel<NB, 3>), g, dim3(256), lds, st, keys, ld, rs, ws, n_valid, q,
-                       prompt, exclude, G, g_ld);
+    dispatch(sl, true, true, scan_gemv_kernel<NB, 3>, g, lds, keys, ld, rs, ws, n_valid, q, prompt, exclude, G,
+             g_ld);
 }
 
 // Compute units of the current device (cached per device).
@@ -768,7 +792,7 @@ static int device_cus()
 template <int MT, int NT, int PF, int TPF, int FMT>
 static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid, int64_t n_rb,
                           const bf16x8* qf, int32_t B, const int32_t* prompt, const int32_t* exclude,
-                          uint64_t* G, int64_t g_ld, const float* kscale, const float* qscale, hipStream_t stream)
+                          uint64_t* G, int64_t g_ld, const float* kscale, const float* qscale, const ScanLaunch& sl)
 {
     constexpr int kWavesPerSimd = NT == 1 ? 2 : 1;  // what the kernels' register use allows
     const int64_t gen = (int64_t)device_cus() * 4 * kWavesPerSimd * MT;
@@ -785,54 +809,54 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
             n_tail = rem;
         }
     }
-    hipLaunchKernelGGL((scan_mfma_kernel<MT, NT, PF, FMT>), dim3((unsigned)((n_main + 4 * MT - 1) / (4 * MT))),
-                       dim3(256), 0, stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale,
-                       qscale, (int64_t)0);
+    dispatch(sl, true, n_tail == 0, scan_mfma_kernel<MT, NT, PF, FMT>,
+             dim3((unsigned)((n_main + 4 * MT - 1) / (4 * MT))), 0, keys, ld, rs, ws, n_valid, qf, B, prompt,
+             exclude, G, g_ld, kscale, qscale, (int64_t)0);
     if (n_tail > 0)
-        hipLaunchKernelGGL((scan_mfma_kernel<1, NT, TPF, FMT>), dim3((unsigned)((n_tail + 3) / 4)), dim3(256), 0,
-                           stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale,
-                           n_main);
+        dispatch(sl, false, true, scan_mfma_kernel<1, NT, TPF, FMT>, dim3((unsigned)((n_tail + 3) / 4)), 0, keys,
+                 ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale, n_main);
 }
 
 // The wide scan (64 < B <= 512), either key format.
 template <int FMT>
 static void launch_wide(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid, int64_t n_rb,
                         const bf16x8* qf, int32_t B, const int32_t* prompt, const int32_t* exclude, uint64_t* G,
-                        int64_t g_ld, const float* kscale, const float* qscale, hipStream_t stream)
+                        int64_t g_ld, const float* kscale, const float* qscale, const ScanLaunch& sl)
 {
     const int ntw = (scan_query_tiles(B) + 3) / 4;
     constexpr int M1 = OIL_WIDE_MT1, M2 = OIL_WIDE_MT2, M4 = OIL_WIDE_MT4;
     if (ntw == 1)
-        hipLaunchKernelGGL((scan_mfma_wide_kernel<M1, 1, FMT>), dim3((unsigned)((n_rb + M1 - 1) / M1)), dim3(256), 0,
-                           stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+        dispatch(sl, true, true, scan_mfma_wide_kernel<M1, 1, FMT>, dim3((unsigned)((n_rb + M1 - 1) / M1)), 0, keys,
+                 ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
     else if (ntw == 2)
-        hipLaunchKernelGGL((scan_mfma_wide_kernel<M2, 2, FMT>), dim3((unsigned)((n_rb + M2 - 1) / M2)), dim3(256), 0,
-                           stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+        dispatch(sl, true, true, scan_mfma_wide_kernel<M2, 2, FMT>, dim3((unsigned)((n_rb + M2 - 1) / M2)), 0, keys,
+                 ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
     else
-        hipLaunchKernelGGL((scan_mfma_wide_kernel<M4, 4, FMT>), dim3((unsigned)((n_rb + M4 - 1) / M4)), dim3(256), 0,
-                           stream, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+        dispatch(sl, true, true, scan_mfma_wide_kernel<M4, 4, FMT>, dim3((unsigned)((n_rb + M4 - 1) / M4)), 0, keys,
+                 ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
 }
 
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
                        uint64_t* G, int64_t g_ld, hipStream_t stream, int fmt, const float* kscale,
-                       const float* qscale)
+                       const float* qscale, hipEvent_t ev_start, hipEvent_t ev_stop)
 {
     if (n_valid <= 0)
         return hipSuccess;
+    const ScanLaunch sl{stream, ev_start, ev_stop};
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
     if (fmt == kKeyFp8) {
         constexpr int MT = OIL_FP8_MT, MT2 = OIL_FP8_MT2, PF = OIL_FP8_PF;
         const bf16x8* qf = (const bf16x8*)qbuf;
         if (B > 64)
             launch_wide<kKeyFp8>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G, g_ld, kscale, qscale,
-                                 stream);
+                                 sl);
         else if (scan_query_tiles(B) == 1)
             launch_narrow<MT, 1, PF, OIL_TAIL_PF1, kKeyFp8>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude,
-                                                            G, g_ld, kscale, qscale, stream);
+                                                            G, g_ld, kscale, qscale, sl);
         else
             launch_narrow<MT2, 2, PF, OIL_TAIL_PF2, kKeyFp8>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude,
-                                                             G, g_ld, kscale, qscale, stream);
+                                                             G, g_ld, kscale, qscale, sl);
         return hipGetLastError();
     }
     if (!scan_uses_mfma(B, ld)) {
@@ -840,26 +864,26 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
         const size_t lds = (size_t)B * ld * sizeof(uint16_t);
         const uint16_t* q = (const uint16_t*)qbuf;
         switch (B) {
-        case 1: launch_gemv<1>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
-        case 2: launch_gemv<2>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
-        case 3: launch_gemv<3>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
-        default: launch_gemv<4>(g, lds, stream, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
+        case 1: launch_gemv<1>(g, lds, sl, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
+        case 2: launch_gemv<2>(g, lds, sl, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
+        case 3: launch_gemv<3>(g, lds, sl, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
+        default: launch_gemv<4>(g, lds, sl, keys, ld, rs, ws, n_valid, q, prompt, exclude, G, g_ld); break;
         }
         return hipGetLastError();
     }
     const bf16x8* qf = (const bf16x8*)qbuf;
     if (B > 64) {
         launch_wide<kKeyBf16>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G, g_ld, nullptr, nullptr,
-                              stream);
+                              sl);
         return hipGetLastError();
     }
     constexpr int MT = OIL_BF16_MT, MT2 = OIL_BF16_MT2, PF = OIL_BF16_PF;
     if (scan_query_tiles(B) == 1)
         launch_narrow<MT, 1, PF, OIL_TAIL_PF1, kKeyBf16>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G,
-                                                         g_ld, nullptr, nullptr, stream);
+                                                         g_ld, nullptr, nullptr, sl);
     else
         launch_narrow<MT2, 2, PF, OIL_TAIL_PF2, kKeyBf16>(keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G,
-                                                          g_ld, nullptr, nullptr, stream);
+                                                          g_ld, nullptr, nullptr, sl);
     return hipGetLastError();
 }
 

@@ -10,9 +10,9 @@
 // largest keys of the pool lie inside the k row blocks with the largest
 // block keys: if a top-k key's block were not among them, those k blocks
 // would hold k keys above it.  So:
-//   1. select the k largest block keys per query (chunks of 4096 block keys
-//      per workgroup, then merges of the candidate lists, until one list of k
-//      remains);
+//   1. select the k largest block keys per query (chunks of 1024 block keys
+//      per workgroup, then merges of up to 4096 candidates per workgroup,
+//      until one list of k remains);
 //   2. the rescore kernels (scan.hip) recompute the 32 scores of each chosen
 //      block, bit-identical to the scan's;
 //   3. select the k largest of those k * 32 keys, ranked and written in order.
@@ -24,9 +24,18 @@
 
 namespace oil {
 
+// Block keys per thread of the first level.  Small chunks keep the chip busy
+// (B * N / 32 / 1024 workgroups: 1024 at 1M positions and B = 32) and make
+// each radix pass short; the merge levels take 4096 candidates each.
+#ifndef OIL_TOPK_VPT
+#define OIL_TOPK_VPT 4
+#endif
+
 constexpr int kSelThreads = 256;
-constexpr int kSelVpt = 16;                         // keys per thread, list selection
-constexpr int kSelSpan = kSelThreads * kSelVpt;     // 4096 keys per workgroup
+constexpr int kBlkVpt = OIL_TOPK_VPT;               // keys per thread, first level
+constexpr int kBlkSpan = kSelThreads * kBlkVpt;     // block keys per first-level workgroup
+constexpr int kSelVpt = 16;                         // keys per thread, merge levels
+constexpr int kSelSpan = kSelThreads * kSelVpt;     // 4096 candidates per merge workgroup
 constexpr int kFinalVpt = OIL_TOPK_MAX * kRowBlock / kSelThreads;  // 8: k blocks x 32 rows
 
 struct SelShared {
@@ -115,18 +124,18 @@ __device__ void block_select(const uint64_t (&v)[VPT], int k, SelShared& sh)
     __syncthreads();
 }
 
-// Step 1, first level: block keys -> k candidates per 4096-key chunk.
+// Step 1, first level: block keys -> k candidates per kBlkSpan-key chunk.
 __global__ __launch_bounds__(kSelThreads) void topk_blocks_kernel(
     const uint64_t* __restrict__ G, int64_t g_ld, int64_t n_rb, int k, uint64_t* __restrict__ cand,
     int n_chunks)
 {
     __shared__ SelShared sh;
     const int b = blockIdx.y, c = blockIdx.x;
-    const int64_t base = (int64_t)c * kSelSpan;
+    const int64_t base = (int64_t)c * kBlkSpan;
     const uint64_t* row = G + (int64_t)b * g_ld;
-    uint64_t v[kSelVpt];
+    uint64_t v[kBlkVpt];
 #pragma unroll
-    for (int j = 0; j < kSelVpt; j++) {
+    for (int j = 0; j < kBlkVpt; j++) {
         const int64_t at = base + j * kSelThreads + threadIdx.x;
         v[j] = at < n_rb ? row[at] : 0ull;
     }
@@ -204,7 +213,7 @@ __global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
     }
 }
 
-int64_t topk_chunks(int64_t n) { return n <= 0 ? 1 : (n + kSelSpan - 1) / kSelSpan; }
+int64_t topk_chunks(int64_t n) { return n <= 0 ? 1 : (n + kBlkSpan - 1) / kBlkSpan; }
 
 int64_t topk_block_ld(int64_t capacity)
 {

@@ -203,3 +203,13 @@ def test_read_stream_rejects_bad_arguments(L):
     assert L.oil_read_stream(buf, 0, sink, None) != 0
     assert L.oil_read_stream(buf, 24, sink, None) != 0            # not a multiple of 16
     assert L.oil_read_stream(ctypes.c_void_p(4104), 16, sink, None) != 0   # misaligned
+
+
+def test_scan_timer_rejects_bad_arguments(L):
+    # every case fails before any event is created
+    assert L.oil_scan_timer_start(0, 1) != 0
+    assert L.oil_scan_timer_start(65537, 1) != 0
+    assert L.oil_scan_timer_start(4, 0) != 0
+    assert L.oil_scan_timer_start(4, -3) != 0
+    n, ms = ctypes.c_int32(), ctypes.c_double()
+    assert L.oil_scan_timer_stop(ctypes.byref(n), ctypes.byref(ms)) != 0   # never started
