@@ -346,10 +346,11 @@ int32_t oil_accept_walk(int32_t B, int32_t max_nodes, const int32_t *node_token,
 /* Benchmark instrumentation (host; not thread-safe).  While enabled, the
  * pool scans of oil_pool_query_topk calls on non-empty pools are counted
  * from 0, and scans 0, every, 2 * every, ... (up to max_launches of them,
- * 1 .. 65536; every >= 1) each get a HIP event pair bound to the scan itself
- * (the start of its first kernel, the end of its last: hipExtLaunchKernel).
- * The runtime still separates a kernel that carries events from its
- * neighbours on the stream by a few microseconds, hence the sampling.
+ * 1 .. 65536; every >= 1) each get a HIP event pair bound to the scan's first
+ * and last kernels (hipExtLaunchKernel).  The span they measure runs about
+ * 1% above the kernel trace's duration, and the runtime separates a kernel
+ * that carries events from its neighbours on the stream by a few
+ * microseconds, hence the sampling.
  * oil_scan_timer_stop waits for those events, returns how many scans were
  * timed and their summed duration in milliseconds, and disables timing.
  * Events are created by start and destroyed by stop; no device memory is

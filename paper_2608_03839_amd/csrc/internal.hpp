@@ -45,8 +45,8 @@ int scan_uses_mfma(int32_t B, int32_t ld);
 int scan_query_tiles(int32_t B);
 // fmt: kKeyBf16, or kKeyFp8 (ld = fp8 row width, a multiple of
 // 128; kscale per stored row and qscale per query are the inverse scales).
-// ev_start / ev_stop (or null): events bound to the start of the scan's first
-// kernel and the end of its last (hipExtLaunchKernel), for timing.
+// ev_start / ev_stop (or null): events bound to the scan's first and last
+// kernels (hipExtLaunchKernel), for timing.
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
                        uint64_t* G, int64_t g_ld, hipStream_t stream, int fmt = kKeyBf16,

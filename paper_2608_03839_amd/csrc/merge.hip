@@ -5,12 +5,13 @@
 // coalesced loads; the tree itself lives in registers: node slot j belongs to
 // lane j % 64, register j / 64 (up to 256 slots).  Each token of a chain is
 // one wave-wide step: every lane tests its slots for "child of the current
-// node carrying this token" and a ballot names the match (siblings never
-// repeat a token, so there is at most one).  A match is walked for free;
-// otherwise the next slot is bought if the phase's budget remains, else the
-// rest of the chain is dropped.  Lexical drafts go first under their
-// allocation, retrieved chains after them under the fixed reservation, and
-// recycled-pool rollouts last, inside that same reservation.
+// node carrying this token" (two compares, two ballots, one scalar AND) and
+// the result names the match (siblings never repeat a token, so there is at
+// most one).  A match is walked for free; otherwise the next slot is bought
+// if the phase's budget remains, else the rest of the chain is dropped.
+// Lexical drafts go first under their allocation, retrieved chains after them
+// under the fixed reservation, and recycled-pool rollouts last, inside that
+// same reservation.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -18,45 +19,73 @@ namespace oil {
 
 constexpr int kSlotsPerLane = OIL_NODES_MAX / 64;
 
+// Insert one chain (token m in lane m's `mine`, len <= 64) from the root.
+// Unused slots hold parent -1, and the current node is never -1, so a slot
+// matches only if it is a live child of the current node.  The walk follows
+// existing nodes while they match; from the first token that matches no
+// child on, every token is a new node (a node just bought has no children),
+// bought while the budget lasts.
 __device__ __forceinline__ void insert_chain(int32_t (&ntok)[kSlotsPerLane], int32_t (&npar)[kSlotsPerLane],
                                              int32_t (&nsrc)[kSlotsPerLane], int& count, int& spent,
-                                             int budget, int src, const int32_t* chain, int len)
+                                             int budget, int src, int32_t mine, int len)
 {
     const int lane = threadIdx.x;
-    const int32_t mine = lane < len ? chain[lane] : -1;
-    int cur = 0;
-    for (int m = 0; m < len; m++) {
+    int cur = 0, m = 0;
+    for (; m < len; m++) {
         const int32_t t = __builtin_amdgcn_readlane(mine, m);
         int found = -1;
 #pragma unroll
         for (int q = 0; q < kSlotsPerLane; q++) {
             if (q * 64 >= count)
                 break;
-            const int slot = q * 64 + lane;
-            const bool hit = slot < count && npar[q] == cur && ntok[q] == t;
-            const uint64_t msk = __ballot(hit);
+            // two ballots ANDed on the scalar unit: cheaper than one ballot of a
+            // combined predicate, which the compiler materialises in a register
+            const uint64_t msk = __ballot(npar[q] == cur) & __ballot(ntok[q] == t);
             if (msk) {
                 found = q * 64 + __ffsll((unsigned long long)msk) - 1;
                 break;
             }
         }
-        if (found >= 0) {
-            cur = found;
-            continue;
-        }
-        if (spent >= budget)
-            return;
+        if (found < 0)
+            break;
+        cur = found;
+    }
+    for (; m < len && spent < budget; m++) {
+        const int32_t t = __builtin_amdgcn_readlane(mine, m);
         const int j = count++;
         spent++;
+        if (lane == (j & 63)) {
+            const int q = j >> 6;
 #pragma unroll
-        for (int q = 0; q < kSlotsPerLane; q++) {
-            if (q * 64 + lane == j) {
-                ntok[q] = t;
-                npar[q] = cur;
-                nsrc[q] = src;
-            }
+            for (int qq = 0; qq < kSlotsPerLane; qq++)
+                if (qq == q) {
+                    ntok[qq] = t;
+                    npar[qq] = cur;
+                    nsrc[qq] = src;
+                }
         }
         cur = j;
+    }
+}
+
+// Insert n chains of one source, stored in LDS with stride Lc (lengths in
+// lens[], clamped to Lc), in order.  The next chain's tokens are read from LDS
+// while the current one is inserted.
+__device__ __forceinline__ void insert_source(int32_t (&ntok)[kSlotsPerLane], int32_t (&npar)[kSlotsPerLane],
+                                              int32_t (&nsrc)[kSlotsPerLane], int& count, int& spent,
+                                              int budget, int src, const int32_t* chains, const int32_t* lens,
+                                              int n, int Lc)
+{
+    const int lane = threadIdx.x;
+    if (n <= 0)
+        return;
+    const int32_t len_r = lane < n ? min(lens[lane], Lc) : 0;  // n <= 64
+    int32_t mine = lane < Lc ? chains[lane] : -1;
+    for (int c = 0; c < n; c++) {
+        const int len = __builtin_amdgcn_readlane(len_r, c);
+        const int32_t next = (c + 1 < n && lane < Lc) ? chains[(c + 1) * Lc + lane] : -1;
+        insert_chain(ntok, npar, nsrc, count, spent, budget, src, mine, len);
+        mine = next;
     }
 }
 
@@ -138,23 +167,11 @@ __global__ __launch_bounds__(64) void merge_kernel(
     }
     int count = 1;
     int spent = 0;
-    for (int c = 0; c < n_lex; c++) {
-        int len = llen_s[c];
-        len = len < L_lex ? len : L_lex;
-        insert_chain(ntok, npar, nsrc, count, spent, lex_budget, 1, lex_s + c * L_lex, len);
-    }
+    insert_source(ntok, npar, nsrc, count, spent, lex_budget, 1, lex_s, llen_s, n_lex, L_lex);
     spent = 0;
-    for (int c = 0; c < k; c++) {
-        int len = slen_s[c];
-        len = len < L ? len : L;
-        insert_chain(ntok, npar, nsrc, count, spent, sem_budget, 2, sem_s + c * L, len);
-    }
+    insert_source(ntok, npar, nsrc, count, spent, sem_budget, 2, sem_s, slen_s, k, L);
     // recycled-pool rollouts: after the retrieved chains, inside the same reservation
-    for (int c = 0; c < n_rec; c++) {
-        int len = rlen_s[c];
-        len = len < L_rec ? len : L_rec;
-        insert_chain(ntok, npar, nsrc, count, spent, sem_budget, 3, rec_s + c * L_rec, len);
-    }
+    insert_source(ntok, npar, nsrc, count, spent, sem_budget, 3, rec_s, rlen_s, n_rec, L_rec);
 #pragma unroll
     for (int q = 0; q < kSlotsPerLane; q++) {
         const int slot = q * 64 + lane;

@@ -735,11 +735,11 @@ int scan_uses_mfma(int32_t B, int32_t ld) { return B > 4 || (int64_t)B * ld * 2 
 
 int scan_query_tiles(int32_t B) { return (B + 31) / 32; }
 
-// Where a scan's kernels go: the stream, and two events (or null) bound to
-// the start of the scan's first kernel and the end of its last.  Events
-// bound to the dispatches themselves take their times from the kernels'
-// own timestamps and put nothing between kernels on the stream (an event
-// recorded between two kernels delays the second by a few microseconds).
+// Where a scan's kernels go: the stream, and two events (or null) that
+// hipExtLaunchKernel binds to the scan's first and last kernels, for timing.
+// Either way of taking events (bound, or recorded between kernels) delays
+// the kernel after each event by a few microseconds, so callers time a
+// sample of the scans.
 struct ScanLaunch {
     hipStream_t stream;
     hipEvent_t start, stop;

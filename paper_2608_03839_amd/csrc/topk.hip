@@ -145,7 +145,8 @@ __global__ __launch_bounds__(kSelThreads) void topk_blocks_kernel(
 }
 
 // Step 1, further levels: merge groups of `group` candidate lists
-// (group * k <= 4096 keys per workgroup).
+// (group * k <= VPT * 256 keys per workgroup).
+template <int VPT>
 __global__ __launch_bounds__(kSelThreads) void topk_merge_kernel(
     const uint64_t* __restrict__ cand_in, int n_lists, int k, int group, uint64_t* __restrict__ cand_out,
     int n_out)
@@ -155,9 +156,9 @@ __global__ __launch_bounds__(kSelThreads) void topk_merge_kernel(
     const int64_t first = (int64_t)g * group;
     const int64_t n_keys = ((int64_t)(n_lists - first < group ? n_lists - first : group)) * k;
     const uint64_t* in = cand_in + ((int64_t)b * n_lists + first) * k;
-    uint64_t v[kSelVpt];
+    uint64_t v[VPT];
 #pragma unroll
-    for (int j = 0; j < kSelVpt; j++) {
+    for (int j = 0; j < VPT; j++) {
         const int64_t at = j * kSelThreads + threadIdx.x;
         v[j] = at < n_keys ? in[at] : 0ull;
     }
@@ -168,6 +169,8 @@ __global__ __launch_bounds__(kSelThreads) void topk_merge_kernel(
 
 // Step 3: the 32 rescored scores of each of the k chosen row blocks -> the k
 // best positions, ranked (descending; equal keys, i.e. padding, in slot order).
+// VPT * 256 >= k * 32.
+template <int VPT>
 __global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
     const uint64_t* __restrict__ blocks, int k, const float* __restrict__ SC, int64_t n_valid,
     float* __restrict__ out_s, int32_t* __restrict__ out_i)
@@ -181,9 +184,9 @@ __global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
     }
     __syncthreads();
     const float* sc = SC + (int64_t)b * k * kRowBlock;
-    uint64_t v[kFinalVpt];
+    uint64_t v[VPT];
 #pragma unroll
-    for (int j = 0; j < kFinalVpt; j++) {
+    for (int j = 0; j < VPT; j++) {
         const int slot = j * kSelThreads + t;
         const int g = slot / kRowBlock;
         v[j] = 0ull;
@@ -240,8 +243,17 @@ hipError_t launch_topk_blocks(const uint64_t* G, int64_t g_ld, int64_t n_valid, 
     uint64_t *src = cand_a, *dst = cand_b;
     while (e == hipSuccess && n_lists > 1) {
         const int n_out = (n_lists + group - 1) / group;
-        hipLaunchKernelGGL(topk_merge_kernel, dim3(n_out, B), dim3(kSelThreads), 0, stream, src,
-                           n_lists, k, group, dst, n_out);
+        // the widest workgroup's keys decide the keys per thread
+        const int widest = (n_lists < group ? n_lists : group) * k;
+        if (widest <= kSelThreads * 4)
+            hipLaunchKernelGGL(topk_merge_kernel<4>, dim3(n_out, B), dim3(kSelThreads), 0, stream, src,
+                               n_lists, k, group, dst, n_out);
+        else if (widest <= kSelThreads * 8)
+            hipLaunchKernelGGL(topk_merge_kernel<8>, dim3(n_out, B), dim3(kSelThreads), 0, stream, src,
+                               n_lists, k, group, dst, n_out);
+        else
+            hipLaunchKernelGGL(topk_merge_kernel<kSelVpt>, dim3(n_out, B), dim3(kSelThreads), 0, stream, src,
+                               n_lists, k, group, dst, n_out);
         e = hipGetLastError();
         n_lists = n_out;
         uint64_t* t = src;
@@ -255,8 +267,12 @@ hipError_t launch_topk_blocks(const uint64_t* G, int64_t g_ld, int64_t n_valid, 
 hipError_t launch_topk_final(const uint64_t* chosen, int32_t B, int32_t k, const float* SC,
                              int64_t n_valid, float* out_s, int32_t* out_i, hipStream_t stream)
 {
-    hipLaunchKernelGGL(topk_final_kernel, dim3(B), dim3(kSelThreads), 0, stream, chosen, k, SC,
-                       n_valid, out_s, out_i);
+    if (k * kRowBlock <= kSelThreads * 4)
+        hipLaunchKernelGGL(topk_final_kernel<4>, dim3(B), dim3(kSelThreads), 0, stream, chosen, k, SC,
+                           n_valid, out_s, out_i);
+    else
+        hipLaunchKernelGGL(topk_final_kernel<kFinalVpt>, dim3(B), dim3(kSelThreads), 0, stream, chosen, k, SC,
+                           n_valid, out_s, out_i);
     return hipGetLastError();
 }
 
