@@ -67,9 +67,10 @@
 #ifndef OIL_RESCORE_GEMV_PF
 #define OIL_RESCORE_GEMV_PF 7
 #endif
-// Prefetch depth (windows in flight per wave) of the MFMA rescore.
+// Prefetch depth (windows in flight per wave) of the MFMA rescore.  At 1M x
+// 4096, B = k = 32 (1024 waves, one per SIMD): depth 0 73 us, 1 45, 2 46, 3 47.5.
 #ifndef OIL_RESCORE_PF
-#define OIL_RESCORE_PF 3
+#define OIL_RESCORE_PF 1
 #endif
 // Windows in flight per wave of the remainder launch of the B <= 64 scan,
 // for one and two query tiles.
@@ -616,7 +617,11 @@ __global__ __launch_bounds__(64) void rescore_mfma_kernel(
     const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
     const int64_t ws8 = ws / 8;
     const bf16x8* tile = (const bf16x8*)(keys + rb * rs) + lane;
-    const bf16x8* qf = qfrag + lane;
+    // Every column of the B operand gets this query's fragment (lane h * 32 + c
+    // reads lane h * 32 + n's): an MFMA output element depends only on its own
+    // row and column, so column n comes out as in the scan, and the wave reads
+    // 32 bytes of query per sub-step instead of the whole query tile's 1 KiB.
+    const bf16x8* qf = qfrag + ((lane & 32) | n);
     floatx16 acc = floatx16{};
     bf16x8 a[NS][4], b[NS][4];
     auto load = [&](int stage, int w) {

@@ -560,3 +560,32 @@ def test_streaming_appends(oil):
             assert len(pool) == at
             o = oracle_rows(_stored(pool, at), _raw_np(q))
             check_topk(s.cpu().numpy(), i.cpu().numpy(), o, 16)
+
+
+@pytest.mark.parametrize("key_format", ["bf16", "fp8"])
+def test_scores_independent_of_batch_companions(oil, key_format):
+    """A query's top-k (scores and positions) is bit-identical whatever other
+    queries share its batch and wherever it sits in the batch: every score is
+    one fixed instruction sequence over that query and that key alone (the
+    block selection of the scan and the recomputation of the chosen blocks
+    must agree bit for bit for the top-k to be exact)."""
+    n, d, k = 9000, 256, 16
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=100, seed=21, n_clusters=64, key_dtype="f32"))
+    raw = wp.raw_rows(0, n)
+    pool = oil.Pool(d, n, key_format=key_format)
+    pool.append(raw.cuda(), wp.tokens.cuda(), wp.traces.cuda(), wp.prompts.cuda())
+    g = torch.Generator().manual_seed(3)
+    q = raw[1234] + 0.05 * torch.randn(d, generator=g)
+    results = []
+    for B, at, seed in ((8, 2, 4), (40, 37, 5), (64, 63, 6), (64, 0, 7), (5, 4, 8), (100, 77, 9), (300, 261, 10)):
+        others = torch.randn((B, d), generator=torch.Generator().manual_seed(seed))
+        batch = others.clone()
+        batch[at] = q
+        s, i = pool.query_topk(batch.cuda(), k)
+        torch.cuda.synchronize()
+        results.append((s[at].cpu(), i[at].cpu()))
+    s0, i0 = results[0]
+    assert i0[0] == 1234
+    for s_, i_ in results[1:]:
+        assert torch.equal(i_, i0)
+        assert torch.equal(s_.view(torch.int32), s0.view(torch.int32))
