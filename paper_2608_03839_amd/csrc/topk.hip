@@ -124,18 +124,19 @@ __device__ void block_select(const uint64_t (&v)[VPT], int k, SelShared& sh)
     __syncthreads();
 }
 
-// Step 1, first level: block keys -> k candidates per kBlkSpan-key chunk.
+// Step 1, first level: block keys -> k candidates per chunk of VPT * 256 keys.
+template <int VPT>
 __global__ __launch_bounds__(kSelThreads) void topk_blocks_kernel(
     const uint64_t* __restrict__ G, int64_t g_ld, int64_t n_rb, int k, uint64_t* __restrict__ cand,
     int n_chunks)
 {
     __shared__ SelShared sh;
     const int b = blockIdx.y, c = blockIdx.x;
-    const int64_t base = (int64_t)c * kBlkSpan;
+    const int64_t base = (int64_t)c * (kSelThreads * VPT);
     const uint64_t* row = G + (int64_t)b * g_ld;
-    uint64_t v[kBlkVpt];
+    uint64_t v[VPT];
 #pragma unroll
-    for (int j = 0; j < kBlkVpt; j++) {
+    for (int j = 0; j < VPT; j++) {
         const int64_t at = base + j * kSelThreads + threadIdx.x;
         v[j] = at < n_rb ? row[at] : 0ull;
     }
@@ -235,8 +236,15 @@ hipError_t launch_topk_blocks(const uint64_t* G, int64_t g_ld, int64_t n_valid, 
                               hipStream_t stream)
 {
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
+    if (n_rb > kBlkSpan && n_rb <= kSelSpan) {
+        // one workgroup per query takes every block key: no merge level
+        hipLaunchKernelGGL(topk_blocks_kernel<kSelVpt>, dim3(1, B), dim3(kSelThreads), 0, stream, G, g_ld, n_rb,
+                           k, cand_a, 1);
+        *chosen = cand_a;
+        return hipGetLastError();
+    }
     int n_lists = (int)topk_chunks(n_rb);
-    hipLaunchKernelGGL(topk_blocks_kernel, dim3(n_lists, B), dim3(kSelThreads), 0, stream, G, g_ld,
+    hipLaunchKernelGGL(topk_blocks_kernel<kBlkVpt>, dim3(n_lists, B), dim3(kSelThreads), 0, stream, G, g_ld,
                        n_rb, k, cand_a, n_lists);
     hipError_t e = hipGetLastError();
     const int group = kSelSpan / k;

@@ -206,10 +206,21 @@ def test_topk_widths(oil, d):
     _query_case(oil, 3000, d, 1, 16, seed=d + 1, dtype="bf16", clusters=16)
 
 
+@pytest.mark.parametrize("n", [32_769, 65_613, 131_072, 131_073])
+def test_topk_single_level_bounds(oil, n):
+    """From 1025 to 4096 block keys per query one workgroup selects from all of
+    them (no merge level); 4097 block keys go back to 1024-key chunks and a
+    merge (bounds of the first level, with a ragged last row block)."""
+    _query_case(oil, n, 64, 3, 16, seed=n)
+    _query_case(oil, n, 64, 40, 64, seed=n + 1)
+
+
 def test_topk_many_merge_levels(oil):
-    """A pool of 600k rows at k = 64 needs two merge passes of candidate lists."""
-    _query_case(oil, 600_000, 64, 3, 64, seed=5)
-    _query_case(oil, 600_000, 64, 40, 64, seed=6)
+    """A pool of 2.2M rows at k = 64: 68,750 block keys per query make 68
+    first-level lists, more than one merge workgroup takes (64), so the
+    candidate lists merge twice."""
+    _query_case(oil, 2_200_000, 64, 3, 64, seed=5)
+    _query_case(oil, 2_200_000, 64, 40, 64, seed=6)
 
 
 def test_empty_pool_returns_padding(oil):
