@@ -117,8 +117,8 @@ int32_t oil_pool_size(const oil_pool *pool, int64_t *n_valid);
  * that puts the largest magnitude in [128, 256), and rounded to OCP FP8 E4M3
  * (nearest, ties to even); queries likewise.  A score is the dot of the E4M3
  * operands (fp32 accumulation of exact products) times the two inverse
- * scales.  Keys are stored in 4 KiB tiles of 32 rows x 128 columns in the
- * operand order of the 32x32x16 fp8 MFMA, window-major as in the bf16 pool,
+ * scales.  Keys are stored in 4 KiB tiles of 32 rows x 128 columns in fp8
+ * MFMA operand order (16 bytes per lane and sub-step), window-major as in the bf16 pool,
  * at half the bytes per row.  Append, query, gather and everything after
  * them take an fp8 pool like a bf16 one, for the same query batches
  * (OIL_MAX_B_FP8 = OIL_MAX_B per call). */

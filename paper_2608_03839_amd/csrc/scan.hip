@@ -210,20 +210,28 @@ __global__ __launch_bounds__(256) void scan_gemv_kernel(
 
 // ----------------------------------------------------------------- MFMA (4 < B <= 64)
 // One 16-byte operand register per lane and sub-step: eight bf16 (one
-// 32x32x16 bf16 MFMA), or sixteen OCP E4M3 values (two 32x32x16 fp8 MFMAs,
-// the low 8 bytes first: columns 32 p .. 32 p + 15, then 32 p + 16 .. + 31 of
-// a 128-column fp8 window).
-template <int FMT>
+// 32x32x16 bf16 MFMA), or sixteen OCP E4M3 values of a 128-column fp8 window
+// (two sub-steps per fp8 MFMA, below).
 __device__ __forceinline__ floatx16 mfma_step(const bf16x8& a, const bf16x8& b, floatx16 acc)
 {
-    if constexpr (FMT == kKeyBf16) {
-        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
-    } else {
-        typedef long long2v __attribute__((ext_vector_type(2)));
-        const long2v a2 = __builtin_bit_cast(long2v, a), b2 = __builtin_bit_cast(long2v, b);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(a2[0], b2[0], acc, 0, 0, 0);
-        return __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(a2[1], b2[1], acc, 0, 0, 0);
-    }
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+}
+
+// fp8 keys: two 16-byte sub-steps (32 fp8 values per lane, for keys and
+// queries alike) feed one v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales
+// (E8M0 127 = 2^0).  Keys and query fragments share one tile layout, so
+// operand slot j of a lane holds the same column for both: the instruction's
+// own k order pairs every key column with its query column.
+__device__ __forceinline__ floatx16 mfma_pair_fp8(const bf16x8& a0, const bf16x8& a1, const bf16x8& b0,
+                                                  const bf16x8& b1, floatx16 acc)
+{
+    typedef int int4v __attribute__((ext_vector_type(4)));
+    typedef int int8v __attribute__((ext_vector_type(8)));
+    const int4v x0 = __builtin_bit_cast(int4v, a0), x1 = __builtin_bit_cast(int4v, a1);
+    const int4v y0 = __builtin_bit_cast(int4v, b0), y1 = __builtin_bit_cast(int4v, b1);
+    const int8v a = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+    const int8v b = {y0[0], y0[1], y0[2], y0[3], y1[0], y1[1], y1[2], y1[3]};
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc, 0, 0, 0, 127, 0, 127);
 }
 
 template <int MT, int NT>
@@ -287,13 +295,24 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
             const int wl = w0 + u + PF < nwin ? w0 + u + PF : nwin - 1;
             load_window<MT, NT>(a[(u + PF) % NS], b[(u + PF) % NS], tile, ws8, qf, wl);
             if (w0 + u < nwin) {
+                if constexpr (FMT == kKeyFp8) {
 #pragma unroll
-                for (int s = 0; s < 4; s++)
+                    for (int s = 0; s < 4; s += 2)
 #pragma unroll
-                    for (int mt = 0; mt < MT; mt++)
+                        for (int mt = 0; mt < MT; mt++)
 #pragma unroll
-                        for (int nt = 0; nt < NT; nt++)
-                            acc[mt][nt] = mfma_step<FMT>(a[u][mt][s], b[u][nt][s], acc[mt][nt]);
+                            for (int nt = 0; nt < NT; nt++)
+                                acc[mt][nt] = mfma_pair_fp8(a[u][mt][s], a[u][mt][s + 1], b[u][nt][s],
+                                                            b[u][nt][s + 1], acc[mt][nt]);
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 4; s++)
+#pragma unroll
+                        for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+                            for (int nt = 0; nt < NT; nt++)
+                                acc[mt][nt] = mfma_step(a[u][mt][s], b[u][nt][s], acc[mt][nt]);
+                }
             }
         }
     }
@@ -473,7 +492,15 @@ scan_mfma_wide_kernel(
         for (int mt = 0; mt < MT; mt++)
 #pragma unroll
             for (int nt = 0; nt < NTW; nt++)
-                acc[mt][nt] = mfma_step<FMT>(a[mt], b[nt][s], acc[mt][nt]);
+                acc[mt][nt] = mfma_step(a[mt], b[nt][s], acc[mt][nt]);
+    };
+    // fp8: sub-steps s and s + 1 in one instruction
+    auto mma_pair = [&](const bf16x8 (&a0)[MT], const bf16x8 (&a1)[MT], const bf16x8 (&b)[NTW][4], int s) {
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+            for (int nt = 0; nt < NTW; nt++)
+                acc[mt][nt] = mfma_pair_fp8(a0[mt], a1[mt], b[nt][s], b[nt][s + 1], acc[mt][nt]);
     };
     auto clampw = [&](int w) { return w < nwin ? w : nwin - 1; };
     bf16x8 b0[NTW][4], b1[NTW][4];
@@ -487,23 +514,39 @@ scan_mfma_wide_kernel(
         load_q(bn, clampw(w + 1));
         if (more)
             copy_keys(nxt2, w + 2);
-        // LDS reads one sub-step ahead of the MFMAs that use them
-        bf16x8 a0[MT], a1[MT];
-        read_sub(a0, cur, 0);
-        read_sub(a1, cur, 1);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_sub(a0, bq, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        read_sub(a0, cur, 2);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_sub(a1, bq, 1);
-        __builtin_amdgcn_sched_barrier(0);
-        read_sub(a1, cur, 3);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_sub(a0, bq, 2);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_sub(a1, bq, 3);
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (FMT == kKeyFp8) {
+            // two sub-steps out of LDS, one paired MFMA, twice (two register
+            // sets, as the bf16 schedule keeps: four spill at two query tiles)
+            bf16x8 a0[MT], a1[MT];
+            read_sub(a0, cur, 0);
+            read_sub(a1, cur, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_pair(a0, a1, bq, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            read_sub(a0, cur, 2);
+            read_sub(a1, cur, 3);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_pair(a0, a1, bq, 2);
+            __builtin_amdgcn_sched_barrier(0);
+        } else {
+            // LDS reads one sub-step ahead of the MFMAs that use them
+            bf16x8 a0[MT], a1[MT];
+            read_sub(a0, cur, 0);
+            read_sub(a1, cur, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_sub(a0, bq, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            read_sub(a0, cur, 2);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_sub(a1, bq, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            read_sub(a1, cur, 3);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_sub(a0, bq, 2);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_sub(a1, bq, 3);
+            __builtin_amdgcn_sched_barrier(0);
+        }
         if (more)
             wait_vmcnt_at_most<MT>();
         else
@@ -641,9 +684,14 @@ __global__ __launch_bounds__(64) void rescore_mfma_kernel(
             const int wl = w0 + u + PF < nwin ? w0 + u + PF : nwin - 1;
             load((u + PF) % NS, wl);
             if (w0 + u < nwin) {
+                if constexpr (FMT == kKeyFp8) {
+                    acc = mfma_pair_fp8(a[u][0], a[u][1], b[u][0], b[u][1], acc);
+                    acc = mfma_pair_fp8(a[u][2], a[u][3], b[u][2], b[u][3], acc);
+                } else {
 #pragma unroll
-                for (int s = 0; s < 4; s++)
-                    acc = mfma_step<FMT>(a[u][s], b[u][s], acc);
+                    for (int s = 0; s < 4; s++)
+                        acc = mfma_step(a[u][s], b[u][s], acc);
+                }
             }
         }
     }

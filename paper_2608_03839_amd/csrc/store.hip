@@ -99,8 +99,10 @@ __device__ __forceinline__ uint8_t double_to_e4m3_rne(double v)
 }
 
 // fp8 tile layout (bytes): rows in blocks of 32, columns in windows of 128;
-// each (row block, window) pair is a 4 KiB tile in the operand order of the
-// 32x32x16 fp8 MFMA, two operands per 16-byte lane load:
+// each (row block, window) pair is a 4 KiB tile, one 16-byte load per lane
+// and sub-step p (lane i % 32 + 32 h holds row i % 32), two sub-steps per
+// fp8 MFMA operand (keys and query fragments share the layout, so an
+// operand slot holds the same column for both):
 //   (i / 32) * rs + (j / 128) * ws + (p * 64 + lane) * 16 + hh * 8 + e,
 //   s = (j % 128) / 16, p = s / 2, hh = s % 2, e = j % 8,
 //   lane = i % 32 + 32 * ((j % 16) / 8).
