@@ -12,7 +12,8 @@
 // would hold k keys above it.  So:
 //   1. select the k largest block keys per query (chunks of 1024 block keys
 //      per workgroup, then merges of up to 4096 candidates per workgroup,
-//      until one list of k remains);
+//      until one list of k remains; up to 4096 block keys, one workgroup
+//      takes them all);
 //   2. the rescore kernels (scan.hip) recompute the 32 scores of each chosen
 //      block, bit-identical to the scan's;
 //   3. select the k largest of those k * 32 keys, ranked and written in order.
@@ -26,7 +27,7 @@ namespace oil {
 
 // Block keys per thread of the first level.  Small chunks keep the chip busy
 // (B * N / 32 / 1024 workgroups: 1024 at 1M positions and B = 32) and make
-// each radix pass short; the merge levels take 4096 candidates each.
+// each radix pass short; the merge levels take up to 4096 candidates each.
 #ifndef OIL_TOPK_VPT
 #define OIL_TOPK_VPT 4
 #endif
