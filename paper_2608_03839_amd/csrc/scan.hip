@@ -849,15 +849,19 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
 {
     constexpr int kWavesPerSimd = NT == 1 ? 2 : 1;  // what the kernels' register use allows
     const int64_t gen = (int64_t)device_cus() * 4 * kWavesPerSimd * MT;
-    // Measured on 1M x 4096 (B = 32): a remainder of 1-15 row blocks costs the
-    // main grid 0-30 us (its waves start early enough to hide), the second
-    // launch 14-30 us; from 16 on the main grid pays 30-75 us, the second
-    // launch 23-34 us.
-    constexpr int64_t kTailMin = 16;
+    // Measured on 1M x 4096 (B = 32, four generations): a remainder of 1-15
+    // row blocks costs the main grid 0-30 us (its waves start while the last
+    // generation runs), the second launch 14-30 us; from 16 on the main grid
+    // pays 30-75 us, the second launch 23-34 us.  With one generation
+    // (262,144 x 5,120, B = 16) the remainder's waves start only when the
+    // generation ends: 2 / 7 / 15 row blocks cost the main grid 16 / 37 /
+    // 87 us, the second launch 28 / 41 / 41 us.
+    constexpr int64_t kTailMin = 16, kTailMinOneGen = 8;
     int64_t n_main = n_rb, n_tail = 0;
     if (n_rb > gen) {
         const int64_t rem = n_rb % gen;
-        if (rem >= kTailMin && rem <= gen / 4) {
+        const int64_t tail_min = n_rb < 2 * gen ? kTailMinOneGen : kTailMin;
+        if (rem >= tail_min && rem <= gen / 4) {
             n_main = n_rb - rem;
             n_tail = rem;
         }

@@ -132,12 +132,14 @@ def test_topk_runs_of_neighbours(oil, key_format, B, k):
 
 
 @pytest.mark.parametrize("key_format,B,extra", [("bf16", 8, 1000), ("bf16", 40, 1000), ("fp8", 8, 777),
-                                                 ("fp8", 40, 4000), ("bf16", 16, 0), ("bf16", 16, 100)])
+                                                 ("fp8", 40, 4000), ("bf16", 16, 0), ("bf16", 16, 100),
+                                                 ("bf16", 16, 400)])
 def test_topk_pool_past_whole_waves(oil, key_format, B, extra):
     """Pools a little past a whole number of scan waves (262,144 rows plus up
-    to a few thousand): from 16 row blocks on, the rows beyond go to the
-    scan's remainder launch (one row block per wave, deeper prefetch); fewer
-    stay in the main grid.  With prompt exclusion."""
+    to a few thousand): from 16 row blocks on (8 when the main grid is a
+    single generation of waves), the rows beyond go to the scan's remainder
+    launch (one row block per wave, deeper prefetch); fewer stay in the main
+    grid.  With prompt exclusion."""
     n, d = 262144 + extra, 64
     g = torch.Generator().manual_seed(B + extra)
     raw = torch.randn((n, d), generator=g)
