@@ -134,13 +134,13 @@ def test_topk_runs_of_neighbours(oil, key_format, B, k):
 @pytest.mark.parametrize("key_format,B,extra", [("bf16", 8, 1000), ("bf16", 40, 1000), ("fp8", 8, 777),
                                                  ("fp8", 40, 4000), ("bf16", 16, 0), ("bf16", 16, 100),
                                                  ("bf16", 16, 400)])
-def test_topk_pool_past_whole_waves(oil, key_format, B, extra):
+def test_topk_pool_past_whole_waves(oil, key_format, B, extra, base=262144):
     """Pools a little past a whole number of scan waves (262,144 rows plus up
     to a few thousand): from 16 row blocks on (8 when the main grid is a
     single generation of waves), the rows beyond go to the scan's remainder
     launch (one row block per wave, deeper prefetch); fewer stay in the main
     grid.  With prompt exclusion."""
-    n, d = 262144 + extra, 64
+    n, d = base + extra, 64
     g = torch.Generator().manual_seed(B + extra)
     raw = torch.randn((n, d), generator=g)
     q = torch.randn((B, d), generator=g)
@@ -166,6 +166,15 @@ def test_topk_pool_past_whole_waves(oil, key_format, B, extra):
         if ex[b] >= 0:
             o[b, pr == int(ex[b])] = -np.inf
     check_topk(s_.cpu().numpy(), i_.cpu().numpy(), o, 16)
+
+
+@pytest.mark.parametrize("key_format,extra", [("fp8", 300), ("fp8", 100), ("bf16", 300)])
+def test_topk_pool_past_one_generation(oil, key_format, extra):
+    """131,072 rows are one generation of the fp8 scan's waves (two row blocks
+    per wave) and half of one for bf16: 10 extra row blocks go to the
+    remainder launch for fp8, 4 stay in the main grid; bf16 keeps all of
+    them in its single partial generation."""
+    test_topk_pool_past_whole_waves(oil, key_format, 8, extra, base=131072)
 
 
 @pytest.mark.parametrize("B", [65, 96, 128, 200, 256, 512])
