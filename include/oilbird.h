@@ -12,8 +12,9 @@
  *
  * Conventions shared by every call:
  *   - Buffers are DEVICE pointers owned by the caller unless marked (host).
- *     The library allocates no device memory; the only thing it owns is the
- *     small host-side pool handle.
+ *     The library allocates no device memory; it owns the small host-side
+ *     handles and one static device array per GPU, the scratch of
+ *     oil_pool_query_topk_noalloc.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Every call validates its arguments on the host, enqueues its kernels on
  *     `stream` and returns without synchronising.  Outputs are valid once the
@@ -44,7 +45,8 @@ enum {
     OIL_E_CAPACITY = -2,    /* an append would exceed the pool's capacity */
     OIL_E_UNSUPPORTED = -3, /* a valid request this build does not serve (e.g. k > 64) */
     OIL_E_HIP = -4,         /* the HIP runtime reported an error while enqueuing */
-    OIL_E_WORKSPACE = -5    /* workspace too small or misaligned */
+    OIL_E_WORKSPACE = -5,   /* workspace too small or misaligned */
+    OIL_E_SCRATCH = -6      /* request larger than the library's static scratch buffer */
 };
 
 enum { OIL_F32 = 0, OIL_BF16 = 1 };
@@ -167,6 +169,26 @@ size_t oil_query_workspace_bytes(const oil_pool *pool, int32_t B, int32_t k);
 int32_t oil_pool_query_topk(const oil_pool *pool, const void *queries, int32_t q_dtype, int32_t B,
                             int32_t k, const int32_t *exclude_prompt, void *workspace,
                             size_t workspace_bytes, float *scores, int32_t *idx, void *stream);
+
+/* Allocation-free variant of oil_pool_query_topk, for callers that cannot
+ * allocate device memory or pass a workspace (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  Same arguments,
+ * checks, kernels and results as oil_pool_query_topk, except that the
+ * workspace is a static device array inside the library, one copy per GPU,
+ * OIL_QUERY_SCRATCH_BYTES long, held by each GPU the library runs on until
+ * the process ends.  A request whose workspace
+ * (oil_query_workspace_bytes(pool, B, k), sized from the pool's capacity)
+ * exceeds it returns OIL_E_SCRATCH and enqueues nothing; 32 MiB covers, e.g.,
+ * B = 64 queries with k = 32 over a pool of 1,048,576 positions of width 4096.
+ * `stream` must belong to the current device (else OIL_E_INVALID).  No device
+ * memory is allocated or freed and nothing needs to start at zero.  Calls on
+ * one GPU share its array: calls that may overlap (different streams, or
+ * threads) race and must be ordered by the caller; a call's outputs are
+ * written to the caller's `scores` and `idx`, so only the scratch is shared. */
+#define OIL_QUERY_SCRATCH_BYTES (32u << 20)
+int32_t oil_pool_query_topk_noalloc(const oil_pool *pool, const void *queries, int32_t q_dtype,
+                                    int32_t B, int32_t k, const int32_t *exclude_prompt, float *scores,
+                                    int32_t *idx, void *stream);
 
 /* Copy-depth rule (Eq. 3).  A query fires when its best score is >= theta
  * (Eq. 2).  A fired entry with score s copies band_depth[j] tokens for the

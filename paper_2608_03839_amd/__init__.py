@@ -86,6 +86,7 @@ def lib():
             "oil_pool_append": (i32, [P, P, i32, P, P, P, i64, P]),
             "oil_query_workspace_bytes": (sz, [P, i32, i32]),
             "oil_pool_query_topk": (i32, [P, P, i32, i32, i32, P, P, sz, P, P, P]),
+            "oil_pool_query_topk_noalloc": (i32, [P, P, i32, i32, i32, P, P, P, P]),
             "oil_gather_continuations": (i32, [P, P, P, i32, i32, ctypes.POINTER(DepthRule), i32,
                                                P, P, P]),
             "oil_tree_merge": (i32, [i32, P, P, P, i32, i32, i32, P, P, i32, i32, P, P, i32, i32,
@@ -194,6 +195,18 @@ def pool_query_topk(handle, queries, k, workspace, scores, idx, exclude_prompt=N
         _ptr(None if exclude_prompt is None else _i32(exclude_prompt, "exclude_prompt")),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(scores),
         _ptr(_i32(idx, "idx")), _stream(stream)))
+
+
+def pool_query_topk_noalloc(handle, queries, k, scores, idx, exclude_prompt=None, stream=None):
+    """oil_pool_query_topk on the library's static scratch (no workspace)."""
+    B = queries.shape[0]
+    _check("oil_pool_query_topk_noalloc", lib().oil_pool_query_topk_noalloc(
+        handle, _ptr(queries), _dtype_code(queries), B, k,
+        _ptr(None if exclude_prompt is None else _i32(exclude_prompt, "exclude_prompt")),
+        _ptr(scores), _ptr(_i32(idx, "idx")), _stream(stream)))
+
+
+QUERY_SCRATCH_BYTES = 32 << 20
 
 
 def lexical_workspace_bytes(handle, B, max_cand) -> int:

@@ -5,6 +5,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/oilbird.h"
 #include "common.hpp"
 #include "internal.hpp"
@@ -34,6 +36,9 @@ struct oil_pool {
     float* kscale;    // fp8: inverse scale per row
     int32_t *tokens, *traces, *prompts;
 };
+
+// Scratch of oil_pool_query_topk_noalloc (see scratch_for_stream).
+static __device__ __align__(256) unsigned char scratch[OIL_QUERY_SCRATCH_BYTES];
 
 namespace {
 
@@ -87,6 +92,95 @@ void timer_slot(hipEvent_t* start, hipEvent_t* stop)
     const bool on = g_timer.ev && g_timer.used < g_timer.cap && g_timer.seen % g_timer.every == 0;
     *start = on ? g_timer.ev[2 * g_timer.used] : nullptr;
     *stop = on ? g_timer.ev[2 * g_timer.used + 1] : nullptr;
+}
+
+// Steps a2-a5 of one query call over an already-carved workspace `ws`
+// (layout w): query normalisation, scan, block top-k, rescore, final top-k.
+int32_t query_topk_enqueue(const oil_pool* pool, const void* queries, int32_t q_dtype, int32_t B, int32_t k,
+                           const int32_t* exclude_prompt, char* ws, const QueryWorkspace& w, float* scores,
+                           int32_t* idx, hipStream_t st)
+{
+    uint16_t* qbuf = (uint16_t*)(ws + w.q_off);
+    float* SC = (float*)(ws + w.sc_off);
+    uint64_t* G = (uint64_t*)(ws + w.g_off);
+    uint64_t* ca = (uint64_t*)(ws + w.ca_off);
+    uint64_t* cb = (uint64_t*)(ws + w.cb_off);
+    const int64_t n_valid = pool->n_valid;
+
+    const bool fp8 = pool->fmt == oil::kKeyFp8;
+    const bool mfma = fp8 || oil::scan_uses_mfma(B, pool->ld);
+    const int tiles = oil::scan_query_tiles(B);
+    float* qscale = fp8 ? (float*)(ws + w.q_off + (size_t)tiles * 32 * (size_t)pool->ld) : nullptr;
+    hipError_t e;
+    if (fp8)
+        e = oil::launch_quantize_rows(queries, q_dtype, pool->dim, B, (int64_t)tiles * 32, (uint8_t*)qbuf, 0,
+                                      pool->ld, 4096, 4096 * (int64_t)tiles, qscale, nullptr, nullptr, nullptr,
+                                      nullptr, nullptr, nullptr, st);
+    else
+        e = oil::launch_normalize_rows(
+            queries, q_dtype, pool->dim, B, mfma ? (int64_t)tiles * 32 : B, qbuf, 0, pool->ld,
+            mfma ? oil::kLayoutTiled : oil::kLayoutRows, 2048, 2048 * (int64_t)tiles, nullptr, nullptr,
+            nullptr, nullptr, nullptr, nullptr, st);
+    if (e == hipSuccess) {
+        hipEvent_t ev0, ev1;
+        timer_slot(&ev0, &ev1);
+        e = oil::launch_scan(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, pool->prompts,
+                             exclude_prompt, G, w.g_ld, st, pool->fmt, pool->kscale, qscale, ev0, ev1);
+        if (g_timer.ev && e == hipSuccess && n_valid > 0) {
+            g_timer.seen++;
+            if (ev0)
+                g_timer.used++;
+        }
+    }
+    const uint64_t* chosen = nullptr;
+    if (e == hipSuccess)
+        e = oil::launch_topk_blocks(G, w.g_ld, n_valid, B, k, ca, cb, &chosen, st);
+    if (e == hipSuccess)
+        e = oil::launch_rescore(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, chosen, k,
+                                pool->prompts, exclude_prompt, SC, st, pool->fmt, pool->kscale, qscale);
+    if (e == hipSuccess)
+        e = oil::launch_topk_final(chosen, B, k, SC, n_valid, scores, idx, st);
+    return hip_status(e);
+}
+
+// Host-side checks shared by both query entry points (before any launch).
+int32_t query_args_status(const oil_pool* pool, const void* queries, int32_t q_dtype, int32_t B, int32_t k,
+                          const int32_t* exclude_prompt, const float* scores, const int32_t* idx)
+{
+    if (!pool || !queries || !scores || !idx || B < 1 || k < 1 ||
+        (q_dtype != OIL_F32 && q_dtype != OIL_BF16) || !aligned(queries, 16))
+        return OIL_E_INVALID;
+    if (B > OIL_MAX_B || k > OIL_MAX_K || (pool->fmt == oil::kKeyFp8 && B > OIL_MAX_B_FP8))
+        return OIL_E_UNSUPPORTED;
+    if (exclude_prompt && !pool->prompts)
+        return OIL_E_INVALID;
+    return OIL_OK;
+}
+
+// Scratch of the allocation-free query call: a file-scope device array, one
+// copy per GPU, alive until the process ends.  Host code never uses its name
+// as an address; it uses the per-device pointer that hipGetSymbolAddress
+// returns, looked up once per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+int32_t scratch_for_stream(hipStream_t stream, char** out)
+{
+    int dev = -1, sdev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return OIL_E_HIP;
+    if (stream && (hipStreamGetDevice(stream, &sdev) != hipSuccess || sdev != dev))
+        return OIL_E_INVALID;  // the scratch looked up must be the stream's device's copy
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+            return OIL_E_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = (char*)g_scratch_ptr[dev];
+    return OIL_OK;
 }
 
 }  // namespace
@@ -280,59 +374,32 @@ int32_t oil_pool_query_topk(const oil_pool* pool, const void* queries, int32_t q
                             int32_t k, const int32_t* exclude_prompt, void* workspace,
                             size_t workspace_bytes, float* scores, int32_t* idx, void* stream)
 {
-    if (!pool || !queries || !scores || !idx || B < 1 || k < 1 ||
-        (q_dtype != OIL_F32 && q_dtype != OIL_BF16) || !aligned(queries, 16))
-        return OIL_E_INVALID;
-    if (B > OIL_MAX_B || k > OIL_MAX_K || (pool->fmt == oil::kKeyFp8 && B > OIL_MAX_B_FP8))
-        return OIL_E_UNSUPPORTED;
-    if (exclude_prompt && !pool->prompts)
-        return OIL_E_INVALID;
+    const int32_t st = query_args_status(pool, queries, q_dtype, B, k, exclude_prompt, scores, idx);
+    if (st != OIL_OK)
+        return st;
     const QueryWorkspace w = carve(pool, B, k);
     if (!workspace || workspace_bytes < w.total || !aligned(workspace, kAlign))
         return OIL_E_WORKSPACE;
-    hipStream_t st = (hipStream_t)stream;
-    char* ws = (char*)workspace;
-    uint16_t* qbuf = (uint16_t*)(ws + w.q_off);
-    float* SC = (float*)(ws + w.sc_off);
-    uint64_t* G = (uint64_t*)(ws + w.g_off);
-    uint64_t* ca = (uint64_t*)(ws + w.ca_off);
-    uint64_t* cb = (uint64_t*)(ws + w.cb_off);
-    const int64_t n_valid = pool->n_valid;
+    return query_topk_enqueue(pool, queries, q_dtype, B, k, exclude_prompt, (char*)workspace, w, scores, idx,
+                              (hipStream_t)stream);
+}
 
-    const bool fp8 = pool->fmt == oil::kKeyFp8;
-    const bool mfma = fp8 || oil::scan_uses_mfma(B, pool->ld);
-    const int tiles = oil::scan_query_tiles(B);
-    float* qscale = fp8 ? (float*)(ws + w.q_off + (size_t)tiles * 32 * (size_t)pool->ld) : nullptr;
-    hipError_t e;
-    if (fp8)
-        e = oil::launch_quantize_rows(queries, q_dtype, pool->dim, B, (int64_t)tiles * 32, (uint8_t*)qbuf, 0,
-                                      pool->ld, 4096, 4096 * (int64_t)tiles, qscale, nullptr, nullptr, nullptr,
-                                      nullptr, nullptr, nullptr, st);
-    else
-        e = oil::launch_normalize_rows(
-            queries, q_dtype, pool->dim, B, mfma ? (int64_t)tiles * 32 : B, qbuf, 0, pool->ld,
-            mfma ? oil::kLayoutTiled : oil::kLayoutRows, 2048, 2048 * (int64_t)tiles, nullptr, nullptr,
-            nullptr, nullptr, nullptr, nullptr, st);
-    if (e == hipSuccess) {
-        hipEvent_t ev0, ev1;
-        timer_slot(&ev0, &ev1);
-        e = oil::launch_scan(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, pool->prompts,
-                             exclude_prompt, G, w.g_ld, st, pool->fmt, pool->kscale, qscale, ev0, ev1);
-        if (g_timer.ev && e == hipSuccess && n_valid > 0) {
-            g_timer.seen++;
-            if (ev0)
-                g_timer.used++;
-        }
-    }
-    const uint64_t* chosen = nullptr;
-    if (e == hipSuccess)
-        e = oil::launch_topk_blocks(G, w.g_ld, n_valid, B, k, ca, cb, &chosen, st);
-    if (e == hipSuccess)
-        e = oil::launch_rescore(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, chosen, k,
-                                pool->prompts, exclude_prompt, SC, st, pool->fmt, pool->kscale, qscale);
-    if (e == hipSuccess)
-        e = oil::launch_topk_final(chosen, B, k, SC, n_valid, scores, idx, st);
-    return hip_status(e);
+int32_t oil_pool_query_topk_noalloc(const oil_pool* pool, const void* queries, int32_t q_dtype, int32_t B,
+                                    int32_t k, const int32_t* exclude_prompt, float* scores, int32_t* idx,
+                                    void* stream)
+{
+    const int32_t st = query_args_status(pool, queries, q_dtype, B, k, exclude_prompt, scores, idx);
+    if (st != OIL_OK)
+        return st;
+    const QueryWorkspace w = carve(pool, B, k);
+    if (w.total > OIL_QUERY_SCRATCH_BYTES)
+        return OIL_E_SCRATCH;
+    char* ws = nullptr;
+    const int32_t sst = scratch_for_stream((hipStream_t)stream, &ws);
+    if (sst != OIL_OK)
+        return sst;
+    return query_topk_enqueue(pool, queries, q_dtype, B, k, exclude_prompt, ws, w, scores, idx,
+                              (hipStream_t)stream);
 }
 
 int32_t oil_gather_continuations(const oil_pool* pool, const int32_t* idx, const float* scores,
@@ -542,6 +609,7 @@ const char* oil_status_string(int32_t status)
     case OIL_E_UNSUPPORTED: return "unsupported size";
     case OIL_E_HIP: return "HIP runtime error";
     case OIL_E_WORKSPACE: return "workspace too small or misaligned";
+    case OIL_E_SCRATCH: return "request needs more than the library's static scratch buffer";
     default: return "unknown status";
     }
 }

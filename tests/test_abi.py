@@ -86,6 +86,11 @@ def test_create_validates(L):
     assert L.oil_pool_query_topk(h, P, 0, 4, 8, None, P, ws - 1, P, P, None) == -5
     assert L.oil_pool_query_topk(h, P, 0, 4, 8, None, f.misaligned, ws, P, P, None) == -5
     assert L.oil_pool_query_topk(h, P, 0, 4, 8, P, P, ws, P, P, None) == -1  # no prompt buffer
+    # the allocation-free variant: the same host checks, before it looks up its scratch
+    assert L.oil_pool_query_topk_noalloc(h, P, 0, 4, 65, None, P, P, None) == -3
+    assert L.oil_pool_query_topk_noalloc(h, P, 0, 0, 8, None, P, P, None) == -1
+    assert L.oil_pool_query_topk_noalloc(h, None, 0, 4, 8, None, P, P, None) == -1
+    assert L.oil_pool_query_topk_noalloc(h, P, 0, 4, 8, P, P, P, None) == -1
     rule = oil.DepthRule.paper()
     assert L.oil_gather_continuations(h, P, P, 1, 8, ctypes.byref(rule), 0, P, P, None) == -1
     assert L.oil_gather_continuations(h, P, P, 1, 65, ctypes.byref(rule), 8, P, P, None) == -3
@@ -94,6 +99,19 @@ def test_create_validates(L):
     assert L.oil_gather_continuations(h, P, P, 1, 8, ctypes.byref(bad), 8, P, P, None) == -3
     assert L.oil_pool_destroy(h) == 0
     assert L.oil_pool_destroy(None) == -1
+
+
+def test_noalloc_query_rejects_oversized_requests(L):
+    """Workspaces beyond OIL_QUERY_SCRATCH_BYTES (32 MiB) are refused with
+    OIL_E_SCRATCH on the host: 512 queries, k = 64, over 2^21 positions of
+    width 4096 need 300+ MiB."""
+    f = _FakeBufs()
+    P = f.aligned
+    h = ctypes.c_void_p()
+    assert L.oil_pool_create(4096, 1 << 21, P, P, P, None, ctypes.byref(h)) == 0
+    assert L.oil_query_workspace_bytes(h, 512, 64) > 32 << 20
+    assert L.oil_pool_query_topk_noalloc(h, P, 0, 512, 64, None, P, P, None) == -6
+    assert L.oil_pool_destroy(h) == 0
 
 
 def test_merge_validates(L):
@@ -126,7 +144,7 @@ def test_verify_validates(L):
 
 
 def test_status_strings(L):
-    for s in (0, -1, -2, -3, -4, -5, 99):
+    for s in (0, -1, -2, -3, -4, -5, -6, 99):
         assert isinstance(L.oil_status_string(s), bytes)
 
 
