@@ -50,8 +50,8 @@ def _load():
         lib.orc_scores.argtypes = [P, i64, i32, P, i32, P]
         lib.orc_topk.argtypes = [P, i64, i32, P, P, i32, P, P]
         lib.orc_gather.argtypes = [P, P, i64, P, P, i32, i32, f32, i32, P, P, i32, P, P]
-        lib.orc_tree_merge.argtypes = [i32, P, P, P, i32, i32, i32, P, P, i32, i32, P, P, i32, i32,
-                                       i32, i32, P, P, P, P]
+        lib.orc_tree_merge.argtypes = [i32, P, P, P, i32, i32, i32, i32, i32, P, P, i32, i32, P, P,
+                                       i32, i32, i32, i32, P, P, P, P]
         lib.orc_tree_mask.argtypes = [i32, i32, P, P, P]
         lib.orc_recycle_records.argtypes = [i32, i32, P, P, P, P, P, P, i32, P, P, P, P, P]
         lib.orc_recycle_query.argtypes = [P, P, P, P, P, i64, i32, i32, P, P, i32, ctypes.c_float, i32,
@@ -174,13 +174,19 @@ def gather(tokens, traces, n_valid, idx, top_scores, rule, L):
     return ct, cl
 
 
+LEX_RET, LEX_RET_LEN = 3, 32   # Algorithm 1: top-3 automaton branches, <= 32 tokens, join C
+
+
 def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget,
-               max_nodes, rec_tokens=None, rec_len=None):
+               max_nodes, rec_tokens=None, rec_len=None, lex_ret=None, lex_ret_len=LEX_RET_LEN):
     """Eq. 4 root-first merge -> (node_token, node_parent, node_source, n_nodes).
 
-    ``lex_tokens`` is (B, n_lex, L_lex) (n_lex may be 0); ``sem_tokens`` is (B, k, L);
-    ``rec_tokens`` (B, n_rec, L_rec), optional, are recycled-pool rollouts merged
-    after the retrieved chains under the same budget (node source 3).
+    ``lex_tokens`` is (B, n_lex, L_lex) (n_lex may be 0), merged first under
+    ``lex_budget`` (source 1); ``sem_tokens`` is (B, k, L).  Under ``sem_budget``
+    (B_ret) come, in order: the retrieved chains (source 2), the first
+    ``lex_ret`` lexical drafts (default min(3, n_lex)) cut to ``lex_ret_len``
+    tokens (source 4 for the nodes they buy there), and ``rec_tokens``
+    (B, n_rec, L_rec), optional recycled-pool rollouts (source 3).
     """
     anchor = _c(anchor, np.int32)
     B = anchor.shape[0]
@@ -195,12 +201,14 @@ def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem
     rec_tokens = _c(rec_tokens, np.int32)
     rec_len = _c(rec_len, np.int32)
     n_rec, L_rec = rec_tokens.shape[1], rec_tokens.shape[2]
+    lex_ret = min(LEX_RET, n_lex) if lex_ret is None else lex_ret
     nt = np.empty((B, max_nodes), dtype=np.int32)
     npar = np.empty((B, max_nodes), dtype=np.int32)
     ns = np.empty((B, max_nodes), dtype=np.int8)
     nn = np.empty((B,), dtype=np.int32)
     _check(_load().orc_tree_merge(B, _ptr(anchor), _ptr(lex_tokens), _ptr(lex_len), n_lex,
-                                  max(L_lex, 1), lex_budget, _ptr(sem_tokens), _ptr(sem_len), k,
+                                  max(L_lex, 1), lex_budget, lex_ret, lex_ret_len, _ptr(sem_tokens),
+                                  _ptr(sem_len), k,
                                   max(L, 1), _ptr(rec_tokens), _ptr(rec_len), n_rec, max(L_rec, 1),
                                   sem_budget, max_nodes, _ptr(nt), _ptr(npar), _ptr(ns), _ptr(nn)),
            "tree_merge")

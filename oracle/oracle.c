@@ -281,13 +281,19 @@ int orc_gather(const int32_t *tokens, const int32_t *traces, int64_t n_valid, co
 /* Root-first merge (Sec. 4 (iii), Eq. 4; BuildLexical, MergeFromRoot).       */
 /*                                                                            */
 /* A pointer trie.  The root carries the anchor (the last committed token)    */
-/* and is not charged to any budget.  Phase 1 inserts the lexical drafts in   */
-/* the order given under lex_budget; phase 2 inserts the retrieved chains in  */
-/* rank order under sem_budget (a fixed reservation: lexical leftovers do not */
-/* roll over).  Inserting a chain walks from the root: a child carrying the   */
-/* next token is walked for free; otherwise a node is bought if the phase's   */
-/* budget remains, else the rest of that chain is dropped.  Nodes are         */
-/* numbered in creation order; unused slots are padded with -1.               */
+/* and is not charged to any budget.  Phase 1 (BuildLexical) inserts the      */
+/* lexical drafts in the order given under lex_budget.  Phase 2               */
+/* (MergeFromRoot over the candidate set C, until B_ret = sem_budget is       */
+/* spent; a fixed reservation: lexical leftovers do not roll over) inserts C  */
+/* in the order Algorithm 1 builds it: the retrieved chains in rank order     */
+/* (source 2), then the first n_lex_ret lexical drafts cut to L_lex_ret       */
+/* tokens (the top automaton branches; source 4 for the nodes they buy        */
+/* here), then the recycled-pool rollouts (source 3).  A lexical branch that  */
+/* phase 1 bought whole re-walks for free; one that the lexical allocation    */
+/* cut short buys its rest from B_ret.  Inserting a chain walks from the      */
+/* root: a child carrying the next token is walked for free; otherwise a node */
+/* is bought if the phase's budget remains, else the rest of that chain is    */
+/* dropped.  Nodes are numbered in creation order; unused slots hold -1.      */
 /* ------------------------------------------------------------------------ */
 
 typedef struct orc_node {
@@ -335,17 +341,21 @@ static void insert_chain(orc_node **nodes, int32_t *count, int32_t max_nodes, in
 }
 
 int orc_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens, const int32_t *lex_len,
-                   int32_t n_lex, int32_t L_lex, int32_t lex_budget, const int32_t *sem_tokens,
+                   int32_t n_lex, int32_t L_lex, int32_t lex_budget, int32_t n_lex_ret, int32_t L_lex_ret,
+                   const int32_t *sem_tokens,
                    const int32_t *sem_len, int32_t k, int32_t L, const int32_t *rec_tokens,
                    const int32_t *rec_len, int32_t n_rec, int32_t L_rec, int32_t sem_budget, int32_t max_nodes,
                    int32_t *node_token, int32_t *node_parent, int8_t *node_source, int32_t *n_nodes)
 {
     if (B < 1 || !anchor || n_lex < 0 || k < 0 || n_rec < 0 || lex_budget < 0 || sem_budget < 0 ||
+        n_lex_ret < 0 || (n_lex_ret > 0 && L_lex_ret < 1) ||
         max_nodes < 1 + lex_budget + sem_budget || !node_token || !node_parent || !node_source ||
         !n_nodes || (n_lex > 0 && (!lex_tokens || !lex_len || L_lex < 1)) ||
         (k > 0 && (!sem_tokens || !sem_len || L < 1)) ||
         (n_rec > 0 && (!rec_tokens || !rec_len || L_rec < 1)))
         return ORC_EINVAL;
+    if (n_lex_ret > n_lex)
+        n_lex_ret = n_lex; /* "top-3" of fewer drafts is all of them */
     orc_node **nodes = (orc_node **)calloc((size_t)max_nodes, sizeof(orc_node *));
     for (int32_t b = 0; b < B; b++) {
         int32_t count = 0, spent = 0;
@@ -365,8 +375,17 @@ int orc_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens, 
             int32_t len = sem_len[o] < L ? sem_len[o] : L;
             insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 2, sem_tokens + o * L, len);
         }
-        /* recycled-pool rollouts join the retrieved chains, after them, inside
-           the same reservation (Algorithm 1, recycled-pool step) */
+        /* the top lexical branches join C after the retrieved chains (Algorithm 1,
+           lexical step), cut to L_lex_ret tokens */
+        for (int32_t c = 0; c < n_lex_ret; c++) {
+            int64_t o = (int64_t)b * n_lex + c;
+            int32_t len = lex_len[o] < L_lex ? lex_len[o] : L_lex;
+            if (len > L_lex_ret)
+                len = L_lex_ret;
+            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 4, lex_tokens + o * L_lex, len);
+        }
+        /* recycled-pool rollouts come last in C, inside the same reservation
+           (Algorithm 1, recycled-pool step) */
         for (int32_t c = 0; c < n_rec; c++) {
             int64_t o = (int64_t)b * n_rec + c;
             int32_t len = rec_len[o] < L_rec ? rec_len[o] : L_rec;

@@ -262,6 +262,59 @@ def test_merge_golden():
         assert np.all(nt[0, n:] == -1) and np.all(npar[0, n:] == -1) and np.all(ns[0, n:] == -1)
 
 
+def _chains(xs, min_len=1):
+    L = max([len(x) for x in xs] + [min_len])
+    t = np.full((1, len(xs), L), -1, np.int32)
+    ln = np.zeros((1, len(xs)), np.int32)
+    for i, x in enumerate(xs):
+        t[0, i, :len(x)] = x
+        ln[0, i] = len(x)
+    return t, ln
+
+
+def test_merge_golden_candidate_set():
+    """Algorithm 1's C: retrieved chains, then the top lexical branches (cut to
+    their token limit) re-walked inside B_ret, then rollouts."""
+    g = json.load(open(os.path.join(GOLDEN, "merge_alg1_candidates.json")))
+    for c in g["cases"]:
+        lt, ll = _chains(c["lex"])
+        st, sl = _chains(c["sem"])
+        rt, rl = _chains(c["rec"])
+        nt, npar, ns, nn = oracle.tree_merge(np.array([c["anchor"]]), lt, ll, c["lex_budget"], st, sl,
+                                             c["sem_budget"], c["max_nodes"], rt, rl,
+                                             lex_ret=c["lex_ret"], lex_ret_len=c["lex_ret_len"])
+        n = c["n_nodes"]
+        assert nn[0] == n, c["why"]
+        assert nt[0, :n].tolist() == c["node_token"], c["why"]
+        assert npar[0, :n].tolist() == c["node_parent"], c["why"]
+        assert ns[0, :n].tolist() == c["node_source"], c["why"]
+
+
+def test_merge_lexical_branches_complete_cut_drafts():
+    """With a reservation large enough, the top lexical branches end up whole
+    (up to the token limit) whatever the lexical allocation cut: the tree's
+    root paths then hold every prefix of each branch; drafts past the top
+    lex_ret stay as the allocation left them."""
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        lt, ll = _random_chains(rng, 1, 5, 20, 3)
+        st, sl = _random_chains(rng, 1, 4, 6, 3)
+        lb = int(rng.integers(0, 12))
+        nt, npar, ns, nn = oracle.tree_merge([9], lt, ll, lb, st, sl, 200, 1 + lb + 200,
+                                             lex_ret=3, lex_ret_len=16)
+        paths = set(_root_paths(nt[0], npar[0], nn[0]).values())
+        for i in range(3):
+            c = tuple(lt[0, i, :min(ll[0, i], 16)])
+            assert all(c[:m] in paths for m in range(1, len(c) + 1))
+        # bought from B_ret: at most what the branches add beyond the allocation
+        assert (ns[0, :nn[0]] == 4).sum() <= sum(min(ll[0, i], 16) for i in range(3))
+        # lex_ret = 0 gives the tree without the phase, a subtree in node order
+        nt0, npar0, ns0, nn0 = oracle.tree_merge([9], lt, ll, lb, st, sl, 200, 1 + lb + 200, lex_ret=0)
+        keep = ns[0, :nn[0]] != 4
+        assert nn0[0] == keep.sum()
+        assert set(_root_paths(nt0[0], npar0[0], nn0[0]).values()) <= paths
+
+
 def _root_paths(nt, npar, n):
     paths = {}
     for j in range(1, n):
@@ -294,7 +347,7 @@ def test_merge_invariants(seed):
         n = nn[b]
         assert nt[b, 0] == anchor[b] and npar[b, 0] == -1 and ns[b, 0] == 0
         assert n <= 1 + lb + sb
-        assert (ns[b, :n] == 1).sum() <= lb and (ns[b, :n] == 2).sum() <= sb
+        assert (ns[b, :n] == 1).sum() <= lb and np.isin(ns[b, :n], (2, 4)).sum() <= sb
         paths = _root_paths(nt[b], npar[b], n)
         # no duplicate siblings: every root path is unique
         assert len(set(paths.values())) == len(paths)

@@ -49,6 +49,29 @@ MUTANTS = {
     "e4m3 subnormal spacing halved": ("        spacing = ldexp(1.0, -9);", "        spacing = ldexp(1.0, -10);"),
     "fp8 score drops the query scale": ("s[(int64_t)b * n + i] = acc * kinv[i] * qinv[b];", "s[(int64_t)b * n + i] = acc * kinv[i];"),
     "fp8 score drops the last dim": ("            for (int32_t c = 0; c < d; c++)\n                acc += kv[c]", "            for (int32_t c = 0; c < d - 1; c++)\n                acc += kv[c]"),
+    "lexical branches left out of C": ("        for (int32_t c = 0; c < n_lex_ret; c++) {", "        for (int32_t c = 0; c < 0; c++) {"),
+    "lexical branches not cut to their limit": ("            if (len > L_lex_ret)\n                len = L_lex_ret;", "            if (0)\n                len = L_lex_ret;"),
+    "lexical branch nodes tagged as the allocation's": ("insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 4,", "insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 1,"),
+    "every lexical draft joins C": ("    if (n_lex_ret > n_lex)\n        n_lex_ret = n_lex;", "    if (1)\n        n_lex_ret = n_lex;"),
+    "lexical branches before the retrieved chains": (
+        "        for (int32_t c = 0; c < k; c++) {\n            int64_t o = (int64_t)b * k + c;\n"
+        "            int32_t len = sem_len[o] < L ? sem_len[o] : L;\n"
+        "            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 2, sem_tokens + o * L, len);\n"
+        "        }\n"
+        "        /* the top lexical branches join C after the retrieved chains (Algorithm 1,\n"
+        "           lexical step), cut to L_lex_ret tokens */\n"
+        "        for (int32_t c = 0; c < n_lex_ret; c++) {",
+        "        for (int32_t c = 0; c < n_lex_ret; c++) {\n"
+        "            int64_t o = (int64_t)b * n_lex + c;\n"
+        "            int32_t len = lex_len[o] < L_lex ? lex_len[o] : L_lex;\n"
+        "            if (len > L_lex_ret)\n                len = L_lex_ret;\n"
+        "            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 4, lex_tokens + o * L_lex, len);\n"
+        "        }\n"
+        "        for (int32_t c = 0; c < k; c++) {\n            int64_t o = (int64_t)b * k + c;\n"
+        "            int32_t len = sem_len[o] < L ? sem_len[o] : L;\n"
+        "            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 2, sem_tokens + o * L, len);\n"
+        "        }\n"
+        "        for (int32_t c = 0; c < 0; c++) {"),
     "recycled ties by newest": ("    return (a->seq < b->seq) ? -1 : (a->seq > b->seq);", "    return (a->seq > b->seq) ? -1 : (a->seq < b->seq);"),
 }
 

@@ -184,10 +184,11 @@ def test_lookup_token_filter_threshold_and_padding():
 
 @pytest.mark.parametrize("seed", range(3))
 def test_rollouts_merge_as_further_retrieved_chains(seed):
-    """Rollouts join the retrieved chains after them under the same reservation
-    (Algorithm 1): merging them as a third source equals appending them to the
-    retrieved chains, node for node; only the source tag differs (3 for nodes
-    a rollout bought)."""
+    """Rollouts join the candidate set C last, under the same reservation
+    (Algorithm 1: retrieved chains, then the top lexical branches, then
+    rollouts): merging them as a third source equals appending the lexical
+    branches and the rollouts to the retrieved chains, node for node; only the
+    source tags differ (4 and 3 for the nodes they bought)."""
     rng = np.random.default_rng(seed)
     B, k, L, n_rec, depth = 12, 16, 8, 4, 6
     base = rng.integers(0, 4, (B, 1, L))
@@ -203,12 +204,14 @@ def test_rollouts_merge_as_further_retrieved_chains(seed):
         got = oracle.tree_merge(anchor, lt, ll, 6, st, sl, budget, mx, rt, rl)
         pad = np.full((B, n_rec, L), -1, np.int32)
         pad[:, :, :depth] = rt
-        want = oracle.tree_merge(anchor, lt, ll, 6, np.concatenate([st, pad], 1),
-                                 np.concatenate([sl, rl], 1), budget, mx)
+        lpad = np.full((B, 2, L), -1, np.int32)
+        lpad[:, :, :5] = lt
+        want = oracle.tree_merge(anchor, lt, ll, 6, np.concatenate([st, lpad, pad], 1),
+                                 np.concatenate([sl, ll, rl], 1), budget, mx, lex_ret=0)
         assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
         assert np.array_equal(got[3], want[3])
-        # tags: equal except where the rollouts bought nodes (2 -> 3)
+        # tags: equal except where lexical branches or rollouts bought nodes (2 -> 4, 3)
         diff = got[2] != want[2]
-        assert np.all(got[2][diff] == 3) and np.all(want[2][diff] == 2)
-        n_sem_only = oracle.tree_merge(anchor, lt, ll, 6, st, sl, budget, mx)[3]
-        assert np.array_equal((got[2] == 3).sum(1), got[3] - n_sem_only)
+        assert np.all(np.isin(got[2][diff], (3, 4))) and np.all(want[2][diff] == 2)
+        n_no_rollouts = oracle.tree_merge(anchor, lt, ll, 6, st, sl, budget, mx)[3]
+        assert np.array_equal((got[2] == 3).sum(1), got[3] - n_no_rollouts)
