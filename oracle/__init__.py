@@ -62,7 +62,7 @@ def _load():
         lib.orc_e4m3_round.restype = ctypes.c_uint8
         lib.orc_quantize_rows_fp8.argtypes = [P, i32, i64, i32, P, P]
         lib.orc_scores_fp8.argtypes = [P, P, i64, i32, P, P, i32, P]
-        lib.orc_lexical_drafts.argtypes = [P, P, P, i64, P, P, i32, i32, P, i32, i32, i32, i64, P, P]
+        lib.orc_lexical_drafts.argtypes = [P, P, P, i64, P, P, i32, i32, P, i32, i32, i32, i64, P, P, P]
         lib.orc_accept_walk.argtypes = [i32, i32, P, P, P, P, P, P, P]
         _lib = lib
     return _lib
@@ -241,8 +241,10 @@ def accept_walk(node_token, node_parent, n_nodes, target):
 
 
 def lexical_drafts(tokens, traces, prompts, n_valid, ctx, ctx_len, n_lex, L_lex, exclude_prompt=None,
-                   min_match=2, max_cand=1 << 62):
-    """Exact-suffix drafts: (tokens (B, n_lex, L_lex) -1 padded, lengths (B, n_lex)).
+                   min_match=2, max_cand=1 << 62, with_capped=False):
+    """Exact-suffix drafts: (tokens (B, n_lex, L_lex) -1 padded, lengths (B, n_lex)),
+    plus, with ``with_capped``, the per-request flag (B,) marking where the
+    candidate capacity may have changed the drafts.
 
     ``ctx`` is (B, C) right-aligned (most recent token last); the last
     ``ctx_len[b]`` entries of row b are the request's context."""
@@ -253,11 +255,12 @@ def lexical_drafts(tokens, traces, prompts, n_valid, ctx, ctx_len, n_lex, L_lex,
     ex = None if exclude_prompt is None else _c(exclude_prompt, np.int32)
     ot = np.empty((B, n_lex, L_lex), np.int32)
     ol = np.empty((B, n_lex), np.int32)
+    cap = np.empty((B,), np.int32)
     _check(_load().orc_lexical_drafts(_ptr(tok), _ptr(tr), _ptr(pr), int(n_valid), _ptr(ctx), _ptr(cl),
                                       C, B, _ptr(ex), n_lex, L_lex, min_match, int(max_cand), _ptr(ot),
-                                      _ptr(ol)),
+                                      _ptr(ol), _ptr(cap)),
            "lexical_drafts")
-    return ot, ol
+    return (ot, ol, cap) if with_capped else (ot, ol)
 
 
 REC_DEPTH = 6

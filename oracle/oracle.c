@@ -545,10 +545,16 @@ static int level_cmp(const void *pa, const void *pb)
     return (a->p < b->p) ? -1 : (a->p > b->p);
 }
 
+/* out_capped (B entries, or NULL): 1 when the capacity rule may have changed
+ * request b's drafts from the uncapped key's -- the longest level alone held
+ * more than max_cand candidates, or back-off stopped above min_match at a
+ * level holding candidates while fewer than n_lex drafts were held -- else 0,
+ * in which case the drafts are exactly the uncapped key's (the levels both
+ * visit hold the same candidates, so they pick the same drafts). */
 int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32_t *prompts, int64_t n_valid,
                        const int32_t *ctx, const int32_t *ctx_len, int32_t C, int32_t B,
                        const int32_t *exclude_prompt, int32_t n_lex, int32_t L_lex, int32_t min_match,
-                       int64_t max_cand, int32_t *out_tokens, int32_t *out_len)
+                       int64_t max_cand, int32_t *out_tokens, int32_t *out_len, int32_t *out_capped)
 {
     if (!tokens || !traces || !prompts || !ctx || !ctx_len || !out_tokens || !out_len || n_valid < 0 ||
         C < 1 || B < 1 || n_lex < 1 || L_lex < 1 || min_match < 1 || max_cand < 1)
@@ -571,6 +577,8 @@ int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32
             ot[j] = -1;
         for (int32_t j = 0; j < n_lex; j++)
             ol[j] = 0;
+        if (out_capped)
+            out_capped[b] = 0;
         int32_t cl = ctx_len[b] < C ? ctx_len[b] : C;
         if (cl < min_match)
             continue;
@@ -599,9 +607,12 @@ int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32
         /* 3: visited levels [m_lo, mtop]; n(m) accumulated from the top */
         int32_t m_lo = mtop;
         int64_t n_ge = n_at[mtop];
+        int cut_below = 0; /* back-off stopped by the capacity at a level with candidates */
         for (int32_t m = mtop - 1; m >= min_match; m--) {
-            if (n_ge + n_at[m] > max_cand)
+            if (n_ge + n_at[m] > max_cand) {
+                cut_below = 1;
                 break;
+            }
             n_ge += n_at[m];
             m_lo = m;
         }
@@ -667,6 +678,8 @@ int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32
                 picked[n_picked++] = lev[e].group;
             }
         }
+        if (out_capped)
+            out_capped[b] = (n_at[mtop] > max_cand || (cut_below && n_picked < n_lex)) ? 1 : 0;
     }
     free(cand), free(mlen), free(group), free(lev), free(picked), free(n_at);
     return ORC_OK;

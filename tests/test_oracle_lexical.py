@@ -205,6 +205,40 @@ def test_capacity_is_a_raised_minimum_key():
     assert checked > 10
 
 
+def test_capped_flag():
+    """The per-request capacity flag: where it is 0 the drafts equal the
+    uncapped key's; it is 1 exactly when the longest level alone exceeds the
+    capacity, or when back-off stopped at a level holding candidates (its
+    count above the capacity, counted by numpy window matching) while fewer
+    than n_lex drafts were held; and on these pools it does flag requests
+    whose drafts differ from the uncapped key's."""
+    rng = np.random.default_rng(17)
+    tok, tr, pr = _random_pool(rng, 4000, 3, 40)
+    L_lex, mm = 3, 1
+    flagged = differs = top_over = 0
+    for trial in range(40):
+        s0 = int(rng.integers(0, 3990))
+        ctx = tok[s0:s0 + 6].tolist()
+        occ = {m: len(_occurrences(tok, tr, ctx, m)) for m in range(1, 7)}
+        top = max([m for m in occ if occ[m] > 0], default=0)
+        for cap, n_lex in ((3, 4), (12, 4), (60, 4), (400, 4), (2, 1), (4, 2)):
+            C = 6
+            ctx_a = np.asarray([ctx], np.int32)
+            ot, ol, fl = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx_a, np.array([6], np.int32), n_lex,
+                                               L_lex, None, mm, cap, with_capped=True)
+            got = [[int(t) for t in ot[0, j, :ol[0, j]]] for j in range(n_lex) if ol[0, j] > 0]
+            free = _run((tok, tr, pr), [ctx], n_lex, L_lex, C=C, min_match=mm)[0]
+            want_flag = top > 0 and (occ[top] > cap or (any(occ[m] > cap for m in range(mm, top))
+                                                        and len(got) < n_lex))
+            assert int(fl[0]) == int(want_flag)
+            if not fl[0]:
+                assert got == free
+            flagged += int(fl[0])
+            differs += int(got != free)
+            top_over += int(top > 0 and occ[top] > cap and len(got) == n_lex)
+    assert flagged > 5 and differs > 3 and top_over > 3
+
+
 def _occurrences(tok, tr, ctx, m):
     """Positions ending an in-trace occurrence of the context's last m tokens
     that have a continuation."""

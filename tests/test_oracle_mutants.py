@@ -72,6 +72,8 @@ MUTANTS = {
         "            insert_chain(nodes, &count, max_nodes, &spent, sem_budget, 2, sem_tokens + o * L, len);\n"
         "        }\n"
         "        for (int32_t c = 0; c < 0; c++) {"),
+    "capacity flag misses an overflowing longest level": ("out_capped[b] = (n_at[mtop] > max_cand || (cut_below", "out_capped[b] = (0 || (cut_below"),
+    "capacity flag ignores how many drafts are held": ("(cut_below && n_picked < n_lex)) ? 1 : 0;", "(cut_below)) ? 1 : 0;"),
     "recycled ties by newest": ("    return (a->seq < b->seq) ? -1 : (a->seq > b->seq);", "    return (a->seq > b->seq) ? -1 : (a->seq < b->seq);"),
 }
 
