@@ -246,19 +246,28 @@ size_t oil_lexical_workspace_bytes(const oil_pool *pool, int32_t B, int32_t max_
  *   min_match  1 .. OIL_LEX_MAX_CTX.   max_cand  1 .. OIL_LEX_MAX_CAND.
  *   workspace  >= oil_lexical_workspace_bytes(pool, B, max_cand), 256-byte aligned.
  *   lex_tokens B x n_lex x L_lex int32 in pick order, -1 padded;
- *   lex_len    B x n_lex int32, 0 for unused slots. */
+ *   lex_len    B x n_lex int32, 0 for unused slots.
+ *   lex_capped B int32 or NULL: 1 where the capacity rule of step 3 may have
+ *              changed the drafts from the paper's key (no capacity): n(m*)
+ *              exceeded max_cand, or back-off stopped above min_match at a
+ *              level holding candidates while fewer than n_lex drafts were
+ *              held; 0 guarantees the drafts are exactly the uncapped key's. */
 int32_t oil_lexical_drafts(const oil_pool *pool, const int32_t *ctx, const int32_t *ctx_len, int32_t C,
                            int32_t B, const int32_t *exclude_prompt, int32_t n_lex, int32_t L_lex,
                            int32_t min_match, int32_t max_cand, void *workspace,
                            size_t workspace_bytes, int32_t *lex_tokens, int32_t *lex_len,
-                           void *stream);
+                           int32_t *lex_capped, void *stream);
 
 /* Root-first merge (Sec. 4 (iii), Eq. 4; BuildLexical then MergeFromRoot in
  * Algorithm 1).  Per query: node 0 is the root (token anchor[b], parent -1,
  * source 0, charged to no budget).  The n_lex lexical drafts are inserted in
- * order under lex_budget, then the k retrieved chains in rank order, then the
- * n_rec recycled-pool rollouts, both under sem_budget (a fixed reservation;
- * unused lexical budget does not roll over).
+ * order under lex_budget (BuildLexical).  Then Algorithm 1's candidate set C
+ * is inserted in its order under sem_budget (B_ret, a fixed reservation;
+ * unused lexical budget does not roll over): the k retrieved chains in rank
+ * order, the first n_lex_ret lexical drafts cut to L_lex_ret tokens (the top
+ * automaton branches: top 3 of at most 32 tokens in Algorithm 1; a draft the
+ * lexical allocation cut short buys its rest here, one bought whole re-walks
+ * for free), and the n_rec recycled-pool rollouts.
  * Inserting a chain walks from the root: a child carrying the next token is
  * walked for free, otherwise a node is bought while the phase's budget lasts,
  * else the rest of that chain is dropped.
@@ -267,14 +276,18 @@ int32_t oil_lexical_drafts(const oil_pool *pool, const int32_t *ctx, const int32
  *              (k 0 .. 64).   rec_tokens B x n_rec x L_rec, rec_len B x n_rec
  *              (n_rec 0 .. OIL_REC_MAX_OUT, as oil_recycle_query writes them).
  *              L_lex, L, L_rec 1 .. 64 (ignored when their count is 0).
+ *   n_lex_ret  >= 0; values above n_lex mean n_lex.   L_lex_ret >= 1 when
+ *              n_lex_ret > 0 (ignored otherwise).
  *   max_nodes  1 + lex_budget + sem_budget .. OIL_MAX_NODES.
  *   node_token, node_parent  B x max_nodes int32; node_source B x max_nodes
- *              int8 (0 root, 1 lexical, 2 retrieved, 3 recycled); nodes in
+ *              int8 (0 root, 1 lexical allocation, 2 retrieved, 3 recycled,
+ *              4 lexical branch bought from the reservation); nodes in
  *              creation order (parents precede children), slots past
  *              n_nodes[b] = -1.
  *   n_nodes    B int32. */
 int32_t oil_tree_merge(int32_t B, const int32_t *anchor, const int32_t *lex_tokens,
                        const int32_t *lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
+                       int32_t n_lex_ret, int32_t L_lex_ret,
                        const int32_t *sem_tokens, const int32_t *sem_len, int32_t k, int32_t L,
                        const int32_t *rec_tokens, const int32_t *rec_len, int32_t n_rec, int32_t L_rec,
                        int32_t sem_budget, int32_t max_nodes, int32_t *node_token,

@@ -89,8 +89,8 @@ def lib():
             "oil_pool_query_topk_noalloc": (i32, [P, P, i32, i32, i32, P, P, P, P]),
             "oil_gather_continuations": (i32, [P, P, P, i32, i32, ctypes.POINTER(DepthRule), i32,
                                                P, P, P]),
-            "oil_tree_merge": (i32, [i32, P, P, P, i32, i32, i32, P, P, i32, i32, P, P, i32, i32,
-                                     i32, i32, P, P, P, P, P]),
+            "oil_tree_merge": (i32, [i32, P, P, P, i32, i32, i32, i32, i32, P, P, i32, i32, P, P, i32,
+                                     i32, i32, i32, P, P, P, P, P]),
             "oil_status_string": (ctypes.c_char_p, [i32]),
             "oil_tree_mask": (i32, [i32, i32, P, P, P, P]),
             "oil_lexical_workspace_bytes": (sz, [P, i32, i32]),
@@ -101,7 +101,7 @@ def lib():
             "oil_recycle_insert": (i32, [P, i32, i32, P, P, P, P, P, P, P, i32, P, sz, P]),
             "oil_recycle_query_workspace_bytes": (sz, [P, i32]),
             "oil_recycle_query": (i32, [P, P, i32, P, i32, ctypes.c_float, i32, i32, P, sz, P, P, P, P]),
-            "oil_lexical_drafts": (i32, [P, P, P, i32, i32, P, i32, i32, i32, i32, P, sz, P, P, P]),
+            "oil_lexical_drafts": (i32, [P, P, P, i32, i32, P, i32, i32, i32, i32, P, sz, P, P, P, P]),
             "oil_accept_walk": (i32, [i32, i32, P, P, P, P, P, P, P, P]),
             "oil_read_stream": (i32, [P, sz, P, P]),
             "oil_scan_timer_start": (i32, [i32, i32]),
@@ -214,13 +214,14 @@ def lexical_workspace_bytes(handle, B, max_cand) -> int:
 
 
 def lexical_drafts(handle, ctx, ctx_len, n_lex, L_lex, workspace, lex_tokens, lex_len,
-                   exclude_prompt=None, min_match=2, max_cand=LEX_MAX_CAND, stream=None):
+                   exclude_prompt=None, min_match=2, max_cand=LEX_MAX_CAND, stream=None, lex_capped=None):
     B, C = ctx.shape
     _check("oil_lexical_drafts", lib().oil_lexical_drafts(
         handle, _ptr(_i32(ctx, "ctx")), _ptr(_i32(ctx_len, "ctx_len")), C, B,
         _ptr(None if exclude_prompt is None else _i32(exclude_prompt, "exclude_prompt")), n_lex,
         L_lex, min_match, max_cand, _ptr(workspace), workspace.numel() * workspace.element_size(),
-        _ptr(_i32(lex_tokens, "lex_tokens")), _ptr(_i32(lex_len, "lex_len")), _stream(stream)))
+        _ptr(_i32(lex_tokens, "lex_tokens")), _ptr(_i32(lex_len, "lex_len")),
+        _ptr(None if lex_capped is None else _i32(lex_capped, "lex_capped")), _stream(stream)))
 
 
 def gather_continuations(handle, idx, scores, rule: DepthRule, L, chain_tokens, chain_len,
@@ -231,11 +232,16 @@ def gather_continuations(handle, idx, scores, rule: DepthRule, L, chain_tokens, 
         _ptr(chain_tokens), _ptr(chain_len), _stream(stream)))
 
 
+LEX_RET, LEX_RET_LEN = 3, 32   # Algorithm 1: top-3 automaton branches, <= 32 tokens, join C
+
+
 def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget,
                max_nodes, node_token, node_parent, node_source, n_nodes, stream=None,
-               rec_tokens=None, rec_len=None):
+               rec_tokens=None, rec_len=None, lex_ret=None, lex_ret_len=LEX_RET_LEN):
     """Root-first merge.  ``lex_tokens`` (B, n_lex, L_lex) or None; ``sem_tokens`` (B, k, L);
-    ``rec_tokens`` (B, n_rec, L_rec) recycled-pool rollouts or None."""
+    ``rec_tokens`` (B, n_rec, L_rec) recycled-pool rollouts or None.  The first
+    ``lex_ret`` lexical drafts (default min(3, n_lex)), cut to ``lex_ret_len``
+    tokens, re-walk the tree inside sem_budget after the retrieved chains."""
     B = anchor.shape[0]
     if lex_tokens is None or lex_tokens.shape[1] == 0:
         n_lex, L_lex, lt, ll = 0, 1, None, None
@@ -246,9 +252,10 @@ def tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem
     else:
         n_rec, L_rec, rt, rl = rec_tokens.shape[1], rec_tokens.shape[2], rec_tokens, rec_len
     k, L = sem_tokens.shape[1], sem_tokens.shape[2]
+    lex_ret = min(LEX_RET, n_lex) if lex_ret is None else lex_ret
     _check("oil_tree_merge", lib().oil_tree_merge(
-        B, _ptr(_i32(anchor, "anchor")), _ptr(lt), _ptr(ll), n_lex, L_lex, lex_budget,
-        _ptr(sem_tokens), _ptr(sem_len), k, L, _ptr(rt), _ptr(rl), n_rec, L_rec, sem_budget,
+        B, _ptr(_i32(anchor, "anchor")), _ptr(lt), _ptr(ll), n_lex, L_lex, lex_budget, lex_ret,
+        lex_ret_len, _ptr(sem_tokens), _ptr(sem_len), k, L, _ptr(rt), _ptr(rl), n_rec, L_rec, sem_budget,
         max_nodes, _ptr(node_token), _ptr(node_parent), _ptr(node_source), _ptr(n_nodes),
         _stream(stream)))
 
@@ -374,8 +381,9 @@ class Pool:
         return scores, idx
 
     def lexical(self, ctx, ctx_len, n_lex, L_lex, exclude_prompt=None, min_match=2,
-                max_cand=None, stream=None, out=None):
-        """Exact-suffix lexical drafts: (tokens (B, n_lex, L_lex), lengths (B, n_lex))."""
+                max_cand=None, stream=None, out=None, capped=None):
+        """Exact-suffix lexical drafts: (tokens (B, n_lex, L_lex), lengths (B, n_lex)).
+        ``capped``, a (B,) int32 device tensor or None, receives the capacity flags."""
         B = ctx.shape[0]
         max_cand = LEX_MAX_CAND if max_cand is None else max_cand
         key = ("lex", B, max_cand)
@@ -390,7 +398,7 @@ class Pool:
         else:
             lt, ll = out
         lexical_drafts(self.handle, ctx, ctx_len, n_lex, L_lex, self._ws[key], lt, ll,
-                       exclude_prompt, min_match, max_cand, stream)
+                       exclude_prompt, min_match, max_cand, stream, lex_capped=capped)
         return lt, ll
 
     def gather(self, idx, scores, rule: DepthRule, L, stream=None, out=None):
@@ -470,7 +478,8 @@ class RecyclePool:
 
 
 def merge_trees(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget,
-                max_nodes, stream=None, out=None, rec_tokens=None, rec_len=None):
+                max_nodes, stream=None, out=None, rec_tokens=None, rec_len=None, lex_ret=None,
+                lex_ret_len=LEX_RET_LEN):
     """Allocate outputs and run tree_merge; returns (node_token, node_parent, node_source, n_nodes)."""
     B = anchor.shape[0]
     dev = anchor.device
@@ -482,5 +491,5 @@ def merge_trees(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, se
     else:
         nt, npar, ns, nn = out
     tree_merge(anchor, lex_tokens, lex_len, lex_budget, sem_tokens, sem_len, sem_budget, max_nodes,
-               nt, npar, ns, nn, stream, rec_tokens, rec_len)
+               nt, npar, ns, nn, stream, rec_tokens, rec_len, lex_ret, lex_ret_len)
     return nt, npar, ns, nn

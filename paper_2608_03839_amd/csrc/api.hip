@@ -431,7 +431,8 @@ size_t oil_lexical_workspace_bytes(const oil_pool* pool, int32_t B, int32_t max_
 int32_t oil_lexical_drafts(const oil_pool* pool, const int32_t* ctx, const int32_t* ctx_len, int32_t C,
                            int32_t B, const int32_t* exclude_prompt, int32_t n_lex, int32_t L_lex,
                            int32_t min_match, int32_t max_cand, void* workspace,
-                           size_t workspace_bytes, int32_t* lex_tokens, int32_t* lex_len, void* stream)
+                           size_t workspace_bytes, int32_t* lex_tokens, int32_t* lex_len, int32_t* lex_capped,
+                           void* stream)
 {
     if (!pool || !ctx || !ctx_len || !lex_tokens || !lex_len || C < 1 || B < 1 || n_lex < 1 ||
         L_lex < 1 || min_match < 1 || max_cand < 1)
@@ -447,19 +448,24 @@ int32_t oil_lexical_drafts(const oil_pool* pool, const int32_t* ctx, const int32
     return hip_status(oil::launch_lexical(pool->tokens, pool->traces, pool->prompts, pool->n_valid, ctx,
                                           ctx_len, C, B, exclude_prompt, n_lex, L_lex, min_match,
                                           max_cand, workspace, pool->capacity, lex_tokens, lex_len,
-                                          (hipStream_t)stream));
+                                          lex_capped, (hipStream_t)stream));
 }
 
 int32_t oil_tree_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
                        const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
-                       const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                       int32_t n_lex_ret, int32_t L_lex_ret, const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
                        const int32_t* rec_tokens, const int32_t* rec_len, int32_t n_rec, int32_t L_rec,
                        int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                        int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, void* stream)
 {
     if (B < 1 || !anchor || !node_token || !node_parent || !node_source || !n_nodes || n_lex < 0 ||
-        k < 0 || n_rec < 0 || lex_budget < 0 || sem_budget < 0)
+        k < 0 || n_rec < 0 || lex_budget < 0 || sem_budget < 0 || n_lex_ret < 0)
         return OIL_E_INVALID;
+    n_lex_ret = n_lex_ret < n_lex ? n_lex_ret : n_lex;
+    if (n_lex_ret > 0 && L_lex_ret < 1)
+        return OIL_E_INVALID;
+    if (n_lex_ret == 0)
+        L_lex_ret = 1;  // unused
     if (n_lex == 0)
         L_lex = 1;  // unused
     if (k == 0)
@@ -477,8 +483,8 @@ int32_t oil_tree_merge(int32_t B, const int32_t* anchor, const int32_t* lex_toke
     if (max_nodes > OIL_MAX_NODES || L_lex > 64 || L > 64 || L_rec > 64 || n_lex > 64 || k > 64 ||
         n_rec > OIL_REC_MAX_OUT)
         return OIL_E_UNSUPPORTED;
-    return hip_status(oil::launch_merge(B, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget,
-                                        sem_tokens, sem_len, k, L, rec_tokens, rec_len, n_rec, L_rec,
+    return hip_status(oil::launch_merge(B, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget, n_lex_ret,
+                                        L_lex_ret, sem_tokens, sem_len, k, L, rec_tokens, rec_len, n_rec, L_rec,
                                         sem_budget, max_nodes, node_token, node_parent, node_source,
                                         n_nodes, (hipStream_t)stream));
 }

@@ -86,7 +86,7 @@ hipError_t launch_gather(const int32_t* tokens, const int32_t* traces, int64_t n
 
 hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
                         const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
-                        const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                        int32_t n_lex_ret, int32_t L_lex_ret, const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
                         const int32_t* rec_tokens, const int32_t* rec_len, int32_t n_rec, int32_t L_rec,
                         int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                         int32_t* node_parent, int8_t* node_source, int32_t* n_nodes,
@@ -99,7 +99,7 @@ hipError_t launch_lexical(const int32_t* tokens, const int32_t* traces, const in
                           int64_t n_valid, const int32_t* ctx, const int32_t* ctx_len, int32_t C,
                           int32_t B, const int32_t* exclude, int32_t n_lex, int32_t L_lex,
                           int32_t min_match, int32_t max_cand, void* workspace, int64_t capacity,
-                          int32_t* lex_tokens, int32_t* lex_len, hipStream_t stream);
+                          int32_t* lex_tokens, int32_t* lex_len, int32_t* lex_capped, hipStream_t stream);
 hipError_t launch_recycle_init(int64_t* head, hipStream_t stream);
 size_t recycle_insert_workspace_bytes(int32_t B, int32_t max_nodes);
 hipError_t launch_recycle_insert(int32_t B, int32_t max_nodes, const int32_t* node_token,

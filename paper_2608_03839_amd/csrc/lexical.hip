@@ -40,6 +40,7 @@ constexpr int kLexTable = 256;                          // last-token table slot
 constexpr int kLexWords = kLexChunk / 32;               // bitmap words per request
 constexpr int kLexList = 2048;                          // kept candidates a chunk records in LDS
 
+constexpr int kPlan = 8;                                // int32 entries of a request's plan
 constexpr int kSelThreads = 1024;
 constexpr int kSelPer = OIL_LEX_CAND_MAX / kSelThreads;
 constexpr int kSelTable = 2 * OIL_LEX_CAND_MAX;         // draft hash slots (load <= 1/2)
@@ -246,8 +247,10 @@ __device__ inline void lex_hist_row(const int32_t* __restrict__ Hb, int c, int n
 }
 
 // plan[b] = {m*, shortest visited level, kept candidates, mask of visited
-// levels holding candidates (bit m - 1)}; off[b][c] = the list index of chunk
-// c's first kept candidate, off[b][n_chunks] = the number kept.
+// levels holding candidates (bit m - 1), capacity bits (1: the longest level
+// alone exceeds max_cand; 2: back-off stopped above min_match at a level
+// holding candidates), unused x 3}; off[b][c] = the list index of chunk c's
+// first kept candidate, off[b][n_chunks] = the number kept.
 __global__ __launch_bounds__(kLexThreads) void lex_plan_kernel(const int32_t* __restrict__ H,
                                                                int32_t n_chunks, int32_t min_match,
                                                                int32_t max_cand, int32_t* __restrict__ off,
@@ -281,19 +284,25 @@ __global__ __launch_bounds__(kLexThreads) void lex_plan_kernel(const int32_t* __
         }
     if (t == 0) {
         int32_t lo = kLexLevels;  // nothing kept
+        int32_t capbits = 0;
         if (top) {
             lo = top;
             int64_t n_ge = n_at[top];
             if (n_ge <= max_cand) {
                 for (int m = top - 1; m >= min_match; m--) {
-                    if (n_ge + n_at[m] > max_cand)
+                    if (n_ge + n_at[m] > max_cand) {
+                        capbits = 2;
                         break;
+                    }
                     n_ge += n_at[m];
                     lo = m;
                 }
+            } else {
+                capbits = 1;
             }
         }
         s_lo = lo;
+        plan[kPlan * b + 4] = capbits;
     }
     __syncthreads();
     const int32_t lo = s_lo;
@@ -334,15 +343,15 @@ __global__ __launch_bounds__(kLexThreads) void lex_plan_kernel(const int32_t* __
     if (t == 0) {
         const int32_t kept = (int32_t)(carry < max_cand ? carry : max_cand);
         ob[n_chunks] = kept;
-        plan[4 * b + 0] = top;
-        plan[4 * b + 1] = lo;
-        plan[4 * b + 2] = kept;
+        plan[kPlan * b + 0] = top;
+        plan[kPlan * b + 1] = lo;
+        plan[kPlan * b + 2] = kept;
         // levels that bring new candidates: the others change no group's count
         uint32_t levels = 0u;
         for (int m = lo; m <= top && m < kLexLevels; m++)
             if (n_at[m] > 0)
                 levels |= 1u << (m - 1);
-        plan[4 * b + 3] = (int32_t)levels;
+        plan[kPlan * b + 3] = (int32_t)levels;
     }
 }
 
@@ -373,7 +382,7 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
     bool busy = false;
     if (t < G) {
         const int32_t* ob = off + (int64_t)(g0 + t) * (n_chunks + 1);
-        lo_t = plan[4 * (g0 + t) + 1];
+        lo_t = plan[kPlan * (g0 + t) + 1];
         busy = ob[c + 1] > ob[c];
     }
     // a chunk where no request keeps a candidate has nothing to write
@@ -522,7 +531,7 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
     const int32_t* __restrict__ tokens, const int32_t* __restrict__ traces, int64_t n_valid,
     const int32_t* __restrict__ cand_p, const int32_t* __restrict__ cand_m, int32_t max_cand,
     const int32_t* __restrict__ plan, int32_t n_lex, int32_t L_lex, int32_t* __restrict__ lex_tokens,
-    int32_t* __restrict__ lex_len)
+    int32_t* __restrict__ lex_len, int32_t* __restrict__ lex_capped)
 {
     __shared__ uint32_t tab_h[kSelTable];
     __shared__ int32_t tab_first[kSelTable];
@@ -532,13 +541,16 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
     __shared__ int32_t pos[OIL_LEX_CAND_MAX];
     __shared__ unsigned long long best_slot[3];
     const int t = threadIdx.x, b = blockIdx.x;
-    const int32_t top = plan[4 * b + 0], lo = plan[4 * b + 1], n = plan[4 * b + 2];
-    const uint32_t levels = (uint32_t)plan[4 * b + 3];
+    const int32_t top = plan[kPlan * b + 0], lo = plan[kPlan * b + 1], n = plan[kPlan * b + 2];
+    const uint32_t levels = (uint32_t)plan[kPlan * b + 3];
+    const int32_t capbits = plan[kPlan * b + 4];
     if (n == 0) {
         for (int e = t; e < n_lex * L_lex; e += kSelThreads)
             lex_tokens[(int64_t)b * n_lex * L_lex + e] = -1;
         for (int e = t; e < n_lex; e += kSelThreads)
             lex_len[(int64_t)b * n_lex + e] = 0;
+        if (lex_capped && t == 0)
+            lex_capped[b] = 0;  // no candidate at all: nothing for the capacity to cut
         return;
     }
     const int32_t* cp = cand_p + (int64_t)b * max_cand;
@@ -666,6 +678,10 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
             n_held++;
         }
     }
+    // the capacity may have changed the drafts: the longest level was cut, or
+    // back-off was stopped while drafts were still missing
+    if (lex_capped && t == 0)
+        lex_capped[b] = ((capbits & 1) || ((capbits & 2) && n_held < n_lex)) ? 1 : 0;
     // unused slots
     for (int e = n_held * L_lex + t; e < n_lex * L_lex; e += kSelThreads)
         lex_tokens[(int64_t)b * n_lex * L_lex + e] = -1;
@@ -688,7 +704,7 @@ LexWorkspace lex_carve(int64_t capacity, int32_t B, int32_t max_cand)
     w.h_off = 0;
     w.o_off = align256(w.h_off + (size_t)B * chunks * kLexHistLd * sizeof(int32_t));
     w.plan_off = align256(w.o_off + (size_t)B * (chunks + 1) * sizeof(int32_t));
-    w.p_off = align256(w.plan_off + (size_t)B * 4 * sizeof(int32_t));
+    w.p_off = align256(w.plan_off + (size_t)B * kPlan * sizeof(int32_t));
     w.m_off = align256(w.p_off + (size_t)B * max_cand * sizeof(int32_t));
     w.total = align256(w.m_off + (size_t)B * max_cand * sizeof(int32_t));
     return w;
@@ -705,7 +721,7 @@ hipError_t launch_lexical(const int32_t* tokens, const int32_t* traces, const in
                           int64_t n_valid, const int32_t* ctx, const int32_t* ctx_len, int32_t C,
                           int32_t B, const int32_t* exclude, int32_t n_lex, int32_t L_lex,
                           int32_t min_match, int32_t max_cand, void* workspace, int64_t capacity,
-                          int32_t* lex_tokens, int32_t* lex_len, hipStream_t stream)
+                          int32_t* lex_tokens, int32_t* lex_len, int32_t* lex_capped, hipStream_t stream)
 {
     const LexWorkspace w = lex_carve(capacity, B, max_cand);
     char* ws = (char*)workspace;
@@ -737,7 +753,7 @@ hipError_t launch_lexical(const int32_t* tokens, const int32_t* traces, const in
             return e;
     }
     hipLaunchKernelGGL(lex_select_kernel, dim3(B), dim3(kSelThreads), 0, stream, tokens, traces, n_valid,
-                       cp, cm, max_cand, plan, n_lex, L_lex, lex_tokens, lex_len);
+                       cp, cm, max_cand, plan, n_lex, L_lex, lex_tokens, lex_len, lex_capped);
     return hipGetLastError();
 }
 

@@ -9,9 +9,11 @@
 // the result names the match (siblings never repeat a token, so there is at
 // most one).  A match is walked for free; otherwise the next slot is bought
 // if the phase's budget remains, else the rest of the chain is dropped.
-// Lexical drafts go first under their allocation, retrieved chains after them
-// under the fixed reservation, and recycled-pool rollouts last, inside that
-// same reservation.
+// Lexical drafts go first under their allocation (BuildLexical).  The fixed
+// reservation then takes Algorithm 1's candidate set C in its order: the
+// retrieved chains, the top n_lex_ret lexical drafts cut to L_lex_ret tokens
+// (a draft the allocation cut short buys its rest here; source 4), and the
+// recycled-pool rollouts.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -69,17 +71,17 @@ __device__ __forceinline__ void insert_chain(int32_t (&ntok)[kSlotsPerLane], int
 }
 
 // Insert n chains of one source, stored in LDS with stride Lc (lengths in
-// lens[], clamped to Lc), in order.  The next chain's tokens are read from LDS
-// while the current one is inserted.
+// lens[], clamped to Lc and to Lmax), in order.  The next chain's tokens are
+// read from LDS while the current one is inserted.
 __device__ __forceinline__ void insert_source(int32_t (&ntok)[kSlotsPerLane], int32_t (&npar)[kSlotsPerLane],
                                               int32_t (&nsrc)[kSlotsPerLane], int& count, int& spent,
                                               int budget, int src, const int32_t* chains, const int32_t* lens,
-                                              int n, int Lc)
+                                              int n, int Lc, int Lmax = 64)
 {
     const int lane = threadIdx.x;
     if (n <= 0)
         return;
-    const int32_t len_r = lane < n ? min(lens[lane], Lc) : 0;  // n <= 64
+    const int32_t len_r = lane < n ? min(min(lens[lane], Lc), Lmax) : 0;  // n <= 64
     int32_t mine = lane < Lc ? chains[lane] : -1;
     for (int c = 0; c < n; c++) {
         const int len = __builtin_amdgcn_readlane(len_r, c);
@@ -129,8 +131,9 @@ __device__ __forceinline__ void stage_lds(const int32_t* const (&src)[6], int32_
 
 __global__ __launch_bounds__(64) void merge_kernel(
     const int32_t* __restrict__ anchor, const int32_t* __restrict__ lex_tokens,
-    const int32_t* __restrict__ lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
-    const int32_t* __restrict__ sem_tokens, const int32_t* __restrict__ sem_len, int32_t k, int32_t L,
+    const int32_t* __restrict__ lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget, int32_t n_lex_ret,
+    int32_t L_lex_ret, const int32_t* __restrict__ sem_tokens, const int32_t* __restrict__ sem_len, int32_t k,
+    int32_t L,
     const int32_t* __restrict__ rec_tokens, const int32_t* __restrict__ rec_len, int32_t n_rec,
     int32_t L_rec, int32_t sem_budget, int32_t max_nodes, int32_t* __restrict__ node_token,
     int32_t* __restrict__ node_parent, int8_t* __restrict__ node_source, int32_t* __restrict__ n_nodes)
@@ -170,7 +173,8 @@ __global__ __launch_bounds__(64) void merge_kernel(
     insert_source(ntok, npar, nsrc, count, spent, lex_budget, 1, lex_s, llen_s, n_lex, L_lex);
     spent = 0;
     insert_source(ntok, npar, nsrc, count, spent, sem_budget, 2, sem_s, slen_s, k, L);
-    // recycled-pool rollouts: after the retrieved chains, inside the same reservation
+    // the top lexical branches, then the recycled-pool rollouts, inside the same reservation
+    insert_source(ntok, npar, nsrc, count, spent, sem_budget, 4, lex_s, llen_s, n_lex_ret, L_lex, L_lex_ret);
     insert_source(ntok, npar, nsrc, count, spent, sem_budget, 3, rec_s, rlen_s, n_rec, L_rec);
 #pragma unroll
     for (int q = 0; q < kSlotsPerLane; q++) {
@@ -194,13 +198,14 @@ size_t merge_lds_bytes(int32_t n_lex, int32_t L_lex, int32_t k, int32_t L, int32
 
 hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
                         const int32_t* lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget,
-                        const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
+                        int32_t n_lex_ret, int32_t L_lex_ret, const int32_t* sem_tokens, const int32_t* sem_len, int32_t k, int32_t L,
                         const int32_t* rec_tokens, const int32_t* rec_len, int32_t n_rec, int32_t L_rec,
                         int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                         int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, hipStream_t stream)
 {
     hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(64), merge_lds_bytes(n_lex, L_lex, k, L, n_rec, L_rec),
-                       stream, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget, sem_tokens, sem_len, k,
+                       stream, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget, n_lex_ret, L_lex_ret,
+                       sem_tokens, sem_len, k,
                        L, rec_tokens, rec_len, n_rec, L_rec, sem_budget, max_nodes, node_token, node_parent,
                        node_source, n_nodes);
     return hipGetLastError();

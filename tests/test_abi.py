@@ -118,18 +118,21 @@ def test_merge_validates(L):
     f = _FakeBufs()
     P = f.aligned
     # budgets that do not fit max_nodes
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, None, None, 0, 1, 10, 10, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, -1, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, None, None, 1, 4, 4, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, None, None, 0, 1, 300, 301, P, P, P, P, None) == -3
-    assert L.oil_tree_merge(0, P, None, None, 0, 1, 0, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, P, P, 65, 4, 4, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 65, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 65, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, 3, 32, P, P, 4, 4, None, None, 0, 1, 10, 10, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, -1, 3, 32, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 1, 4, 4, 3, 32, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, 3, 32, P, P, 4, 4, None, None, 0, 1, 300, 301, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(0, P, None, None, 0, 1, 0, 3, 32, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, P, P, 65, 4, 4, 3, 32, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, 3, 32, P, P, 65, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, 3, 32, P, P, 4, 65, None, None, 0, 1, 10, 64, P, P, P, P, None) == -3
     # rollouts: more than OIL_REC_MAX_OUT, missing buffers, too wide
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, P, P, 9, 6, 10, 64, P, P, P, P, None) == -3
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, None, P, 4, 6, 10, 64, P, P, P, P, None) == -1
-    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, P, P, 4, 4, P, P, 4, 65, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, 3, 32, P, P, 4, 4, P, P, 9, 6, 10, 64, P, P, P, P, None) == -3
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, 3, 32, P, P, 4, 4, None, P, 4, 6, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, None, None, 0, 1, 0, 3, 32, P, P, 4, 4, P, P, 4, 65, 10, 64, P, P, P, P, None) == -3
+    # lexical branches of the reservation: a negative count, a zero length
+    assert L.oil_tree_merge(1, P, P, P, 2, 4, 4, -1, 32, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
+    assert L.oil_tree_merge(1, P, P, P, 2, 4, 4, 2, 0, P, P, 4, 4, None, None, 0, 1, 10, 64, P, P, P, P, None) == -1
 
 
 def test_verify_validates(L):
@@ -160,12 +163,13 @@ def test_lexical_validates(L):
     ws = L.oil_lexical_workspace_bytes(h, 4, 64)
     assert ws > 0 and ws % 256 == 0
     assert L.oil_lexical_workspace_bytes(h, 4, 4096) > ws
-    # (pool, ctx, ctx_len, C, B, exclude, n_lex, L_lex, min_match, max_cand, ws, ws_bytes, tok, len, stream)
-    ok = (h, P, P, 16, 4, None, 4, 12, 2, 64, P, ws, P, P, None)
+    # (pool, ctx, ctx_len, C, B, exclude, n_lex, L_lex, min_match, max_cand, ws, ws_bytes, tok, len,
+    #  capped, stream)
+    ok = (h, P, P, 16, 4, None, 4, 12, 2, 64, P, ws, P, P, None, None)
 
     def call(**kw):
         names = ["pool", "ctx", "ctx_len", "C", "B", "exclude", "n_lex", "L_lex", "min_match",
-                 "max_cand", "ws", "ws_bytes", "tok", "len", "stream"]
+                 "max_cand", "ws", "ws_bytes", "tok", "len", "capped", "stream"]
         a = dict(zip(names, ok))
         a.update(kw)
         return L.oil_lexical_drafts(*[a[n] for n in names])

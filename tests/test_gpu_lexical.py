@@ -66,14 +66,17 @@ def _contexts(rng, tok, B, C, vocab):
     return ctx, cl
 
 
-def _compare(oil, pool, tok, tr, pr, ctx, cl, n_lex, L_lex, excl, mm, cap):
+def _compare(oil, pool, tok, tr, pr, ctx, cl, n_lex, L_lex, excl, mm, cap, with_flag=False):
+    fl = torch.full((ctx.shape[0],), 7, dtype=torch.int32, device="cuda")
     lt, ll = pool.lexical(_cu(ctx), _cu(cl), n_lex, L_lex,
-                          None if excl is None else _cu(excl), mm, cap)
+                          None if excl is None else _cu(excl), mm, cap, capped=fl)
     torch.cuda.synchronize()
-    et, el = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, excl, mm, cap)
+    et, el, ef = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, excl, mm, cap,
+                                       with_capped=True)
     assert np.array_equal(ll.cpu().numpy(), el)
     assert np.array_equal(lt.cpu().numpy(), et)
-    return el
+    assert np.array_equal(fl.cpu().numpy(), ef)
+    return (el, ef) if with_flag else el
 
 
 @pytest.mark.parametrize("seed,n,vocab,B,C", [
@@ -131,6 +134,34 @@ def test_capacity_overflow_keeps_earliest(oil):
     for cap in (1, 50, 4096):
         for L_lex in (1, 12, 64):
             _compare(oil, pool, tok, tr, pr, ctx, cl, 8, L_lex, None, 2, cap)
+
+
+@pytest.mark.parametrize("cap,n_lex,L_lex", [(4096, 16, 5), (4096, 4, 3), (512, 8, 6), (64, 2, 4)])
+def test_capacity_flag_against_uncapped_oracle(oil, cap, n_lex, L_lex):
+    """A pool where the candidate capacity binds (three symbols, 120,000
+    positions: two-token suffixes recur ~13,000 times).  Every request's drafts
+    and flag equal the capped oracle's; where the flag is 0 they also equal the
+    uncapped oracle's (the paper's key), so the flag marks every request the
+    capacity may have changed."""
+    rng = np.random.default_rng(cap + n_lex)
+    tok, tr, pr = _random_pool(rng, 120000, 3, 400)
+    pool = _pool(oil, tok, tr, pr)
+    C, B = 16, 40
+    ctx = np.full((B, C), -1, np.int32)
+    cl = rng.integers(2, C + 1, B).astype(np.int32)
+    for b in range(B):
+        s0 = int(rng.integers(0, len(tok) - C))
+        ctx[b, C - cl[b]:] = tok[s0:s0 + cl[b]]
+    el, ef = _compare(oil, pool, tok, tr, pr, ctx, cl, n_lex, L_lex, None, 2, cap, with_flag=True)
+    ut, ul = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, None, 2)
+    ct, cl_ = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, None, 2, cap)
+    free = ef == 0
+    assert np.array_equal(cl_[free], ul[free]) and np.array_equal(ct[free], ut[free])
+    # the capacity binds on this pool: some request's back-off or longest level was cut
+    _, _, f_any = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, 1, 1, None, 2, cap, with_capped=True)
+    assert f_any.sum() > 0
+    print(f"cap={cap}: {int(ef.sum())} of {B} requests flagged, "
+          f"{int((np.any(ct != ut, axis=(1, 2)) | np.any(cl_ != ul, axis=1)).sum())} differ from the uncapped key")
 
 
 def test_empty_and_degenerate(oil):

@@ -465,6 +465,70 @@ def test_merge_golden(oil):
         assert ns[0, :n].tolist() == c["node_source"]
 
 
+def _pad(xs):
+    L = max([len(x) for x in xs] + [1])
+    t = np.full((1, max(len(xs), 1), L), -1, np.int32)
+    ln = np.zeros((1, max(len(xs), 1)), np.int32)
+    for j, x in enumerate(xs):
+        t[0, j, :len(x)] = x
+        ln[0, j] = len(x)
+    return t, ln
+
+
+def test_merge_golden_candidate_set(oil):
+    """Algorithm 1's C on the GPU: the hand-worked cases (retrieved chains,
+    then the top lexical branches cut to their limit, then rollouts, all
+    inside B_ret)."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "merge_alg1_candidates.json")))
+    cu = lambda a: torch.from_numpy(a).cuda()
+    for c in g["cases"]:
+        lt, ll = _pad(c["lex"])
+        st, sl = _pad(c["sem"])
+        rt, rl = _pad(c["rec"])
+        nt, npar, ns, nn = oil.merge_trees(cu(np.array([c["anchor"]], np.int32)), cu(lt), cu(ll),
+                                           c["lex_budget"], cu(st), cu(sl), c["sem_budget"],
+                                           c["max_nodes"], rec_tokens=cu(rt) if c["rec"] else None,
+                                           rec_len=cu(rl) if c["rec"] else None, lex_ret=c["lex_ret"],
+                                           lex_ret_len=c["lex_ret_len"])
+        torch.cuda.synchronize()
+        n = c["n_nodes"]
+        assert nn.item() == n, c["why"]
+        assert nt[0, :n].tolist() == c["node_token"], c["why"]
+        assert npar[0, :n].tolist() == c["node_parent"], c["why"]
+        assert ns[0, :n].tolist() == c["node_source"], c["why"]
+
+
+@pytest.mark.parametrize("n_lex,L_lex,lb,sb,lex_ret,lex_ret_len,n_rec,k,buys", [
+    (3, 32, 44, 16, 3, 32, 4, 2, True),    # the paper's split: 44 lexical + 16 reserved nodes, branches <= 32
+    (3, 32, 44, 16, 3, 32, 4, 16, False),  # the same with 16 chains, which spend the reservation first
+    (4, 12, 10, 40, 3, 32, 0, 16, False),  # allocation cuts most drafts; retrieved chains spend first
+    (5, 40, 20, 60, 5, 17, 2, 16, True),   # branch limit below the draft length
+    (2, 64, 0, 100, 2, 64, 8, 16, True),   # no lexical allocation: branches bought from the reservation alone
+    (16, 8, 30, 200, 16, 8, 8, 16, True),  # every draft a branch, large tree
+])
+def test_merge_lexical_branches_bit_exact(oil, n_lex, L_lex, lb, sb, lex_ret, lex_ret_len, n_rec, k, buys):
+    rng = np.random.default_rng(n_lex * 101 + lb + k)
+    B, L = 48, 12
+    lt, ll = _chains(rng, B, n_lex, L_lex, 4)
+    st, sl = _chains(rng, B, k, L, 4)
+    rt, rl = _chains(rng, B, n_rec, 6, 4) if n_rec else (None, None)
+    anchor = rng.integers(0, 1000, B).astype(np.int32)
+    mx = 1 + lb + sb
+    cu = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    got = oil.merge_trees(cu(anchor), cu(lt), cu(ll), lb, cu(st), cu(sl), sb, mx,
+                          rec_tokens=cu(rt) if n_rec else None, rec_len=cu(rl) if n_rec else None,
+                          lex_ret=lex_ret, lex_ret_len=lex_ret_len)
+    torch.cuda.synchronize()
+    want = oracle.tree_merge(anchor, lt, ll, lb, st, sl, sb, mx, rt, rl, lex_ret=lex_ret,
+                             lex_ret_len=lex_ret_len)
+    for a, e in zip(got, want):
+        assert np.array_equal(a.cpu().numpy(), e)
+    # the phase is exercised: some trees buy lexical-branch nodes from the reservation
+    assert (want[2] == 4).any() == buys
+
+
 # ---------------------------------------------------------------- end to end
 def _end_to_end(oil, cfg, n=None, device_gen="cpu"):
     ps, qs = cfg["pool"], cfg["query"]
