@@ -135,6 +135,8 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the step benchmark: retrieval calls on the same pool for "
                          "B in 1..512, one JSON line with the scan's GB/s and MFMA TFLOP/s per B")
+    ap.add_argument("--batches", type=str, default="1,2,4,8,16,32,64,128,256,512",
+                    help="query batches of --sweep (comma separated)")
     ap.add_argument("--workloads", action="store_true",
                     help="instead of the step benchmark: the single-stream decode, streaming-growth and "
                          "full-draft-step workloads, one JSON line with their per-step latencies")
@@ -471,7 +473,7 @@ def sweep(args, oil, workloads, dev, cfg):
                         wp.traces[s0:s0 + 65536].to(dev), wp.prompts[s0:s0 + 65536].to(dev))
         ldk = (d + 127) // 128 * 128 if fmt == "fp8" else (d + 63) // 64 * 64
         rows = []
-        for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
+        for B in [int(x) for x in args.batches.split(",")]:
             q, _ = workloads.queries(wp, workloads.QuerySpec(B=B, noise=qs.noise, p_random=qs.p_random,
                                                              seed=qs.seed + 1000 + B))
             q = q.contiguous()

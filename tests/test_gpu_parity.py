@@ -183,12 +183,33 @@ def test_topk_wide_batches(oil, B):
     _query_case(oil, 5000, 512, B, 16, seed=40 + B)
 
 
-@pytest.mark.parametrize("d,B", [(64, 100), (128, 300), (320, 129), (448, 512), (832, 257)])
+@pytest.mark.parametrize("d,B", [(64, 100), (128, 300), (256, 100), (320, 129), (384, 200), (448, 512),
+                                 (640, 256), (704, 128), (768, 300), (832, 257)])
 def test_wide_batches_window_counts(oil, d, B):
-    """The wide scan's three-slot ring over 1, 2, 5, 7 and 13 key windows:
-    main loop trips of six windows plus a tail of two to seven (or the tail
-    alone), with one, two and four query tiles per wave."""
+    """The wide scan's three-slot ring over 1 to 13 key windows: main loop
+    trips of six windows plus a tail of two to seven (or the tail alone), with
+    one, two and four query tiles per wave."""
     _query_case(oil, 3000 + d, d, B, 16, seed=60 + d)
+
+
+@pytest.mark.parametrize("d,B", [(128, 100), (640, 200), (768, 130), (1408, 300), (1536, 512)])
+def test_wide_batches_window_counts_fp8(oil, d, B):
+    """The same ring on fp8 keys (128-column windows): 1, 5, 6, 11 and 12
+    windows, one to four query tiles per wave."""
+    wp = workloads.Pool(workloads.PoolSpec(n=2500 + d, d=d, vocab=5000, seed=90 + d, n_clusters=16))
+    n = wp.spec.n
+    pool = oil.Pool(d, n, key_format="fp8")
+    raw = wp.raw_rows(0, n)
+    pool.append(raw.cuda(), wp.tokens.cuda(), wp.traces.cuda(), wp.prompts.cuda())
+    q, _ = workloads.queries(wp, workloads.QuerySpec(B=B, p_random=0.25, seed=91 + d))
+    q = q.float()
+    s, i = pool.query_topk(q.cuda(), 16)
+    torch.cuda.synchronize()
+    from tests._parity import untile_keys_fp8
+    codes = untile_keys_fp8(pool.keys.cpu().numpy(), n, d, n)
+    kinv = pool.scales[:n].cpu().numpy().astype(np.float64)
+    qc, qinv = oracle.quantize_rows_fp8(q.numpy())
+    check_topk(s.cpu().numpy(), i.cpu().numpy(), oracle.scores_fp8(codes, kinv, qc, qinv), 16)
 
 
 def test_wide_batch_ragged_width_and_exclusion(oil):
