@@ -54,6 +54,18 @@ __device__ __forceinline__ uint16_t double_to_bf16_rne(double x)
     return (uint16_t)(sign | mag);
 }
 
+// MurmurHash3's 32-bit finaliser (public domain): the hash of the LDS tables
+// that map tokens to requests (lexical source, recycled pool).
+__device__ __forceinline__ uint32_t mix32(uint32_t h)
+{
+    h ^= h >> 16;
+    h *= 0x85EBCA6Bu;
+    h ^= h >> 13;
+    h *= 0xC2B2AE35u;
+    h ^= h >> 16;
+    return h;
+}
+
 // Order-preserving 32-bit code of a float score: a larger code is a larger
 // score.  0 is reserved: the bit pattern 0xFFFFFFFF (a NaN) marks "no
 // position" (outside the pool, or excluded) and maps to it.

@@ -55,17 +55,6 @@ struct LexScanShared {
     uint64_t mask[kLexTable];                // requests whose last token is the slot's
 };
 
-__device__ inline uint32_t mix32(uint32_t h)
-{
-    // MurmurHash3's 32-bit finaliser
-    h ^= h >> 16;
-    h *= 0x85EBCA6Bu;
-    h ^= h >> 13;
-    h *= 0xC2B2AE35u;
-    h ^= h >> 16;
-    return h;
-}
-
 // Stage the contexts of requests [g0, g0 + G) and build the last-token table.
 __device__ void lex_stage(LexScanShared& s, const int32_t* __restrict__ ctx,
                           const int32_t* __restrict__ ctx_len, int32_t C, int32_t g0, int32_t G,

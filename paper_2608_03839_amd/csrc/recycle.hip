@@ -39,17 +39,6 @@ constexpr int kScoreThreads = 1024;
 constexpr int kScoreChunks = 8;  // 16-byte key chunks per lane per round trip
 constexpr int kScoreWaves = kScoreThreads / kWave;
 
-__device__ inline uint32_t rec_mix32(uint32_t h)
-{
-    // MurmurHash3's 32-bit finaliser
-    h ^= h >> 16;
-    h *= 0x85EBCA6Bu;
-    h ^= h >> 13;
-    h *= 0xC2B2AE35u;
-    h ^= h >> 16;
-    return h;
-}
-
 __global__ void recycle_init_kernel(int64_t* head) { *head = 0; }
 
 __global__ __launch_bounds__(256) void recycle_plan_kernel(
@@ -208,7 +197,7 @@ __global__ __launch_bounds__(kMatchThreads) void recycle_match_kernel(
     __syncthreads();
     if (t < G) {
         const int32_t v = anc[t];
-        uint32_t h = rec_mix32((uint32_t)v) & (kMatchTable - 1);
+        uint32_t h = mix32((uint32_t)v) & (kMatchTable - 1);
         for (;;) {  // at most kMatchGroup of kMatchTable slots are taken
             const int o = atomicCAS(&owner[h], -1, t);
             if (o == -1 || anc[o] == v) {
@@ -224,7 +213,7 @@ __global__ __launch_bounds__(kMatchThreads) void recycle_match_kernel(
         const int64_t r = base + j * kMatchThreads + t;
         if (r >= valid)
             continue;
-        uint32_t h = rec_mix32((uint32_t)tk[j]) & (kMatchTable - 1);
+        uint32_t h = mix32((uint32_t)tk[j]) & (kMatchTable - 1);
         uint64_t mk = 0ull;
         for (int probe = 0; probe < kMatchTable; probe++) {
             const int o = owner[h];
