@@ -12,6 +12,17 @@ best, o_k1 the (k+1)-th):
       inside the oracle's top-k is >= TOL the order is equal too.
 Padding (-1) appears exactly when fewer than k positions are eligible.
 Gather and merge are integer procedures: bit-exact on identical inputs.
+
+A tighter bar for bf16 keys, derived from the arithmetic (fp32_bound): the
+product of two bf16 values is exact in fp32, so any order of fp32 additions of
+d of them is within gamma_d * sum |q_j k_j| of the exact dot (gamma_d = d u /
+(1 - d u), u = 2^-24), and sum |q_j k_j| <= |q| |k| (Cauchy-Schwarz), which is
+1 up to the rounding of the stored operands.  With eps that bound, check_topk
+also requires |s_gpu - s_oracle| <= eps and T1-T3 at tol = 2 eps (the rules
+hold whenever every score is within eps, so their tolerance is twice it).
+The fp8 MFMA (v_mfma_scale_f32_32x32x64_f8f6f4) does not accumulate like a
+sequence of fp32 additions: its errors sit near 1e-5 at every width (above
+d u at d = 64), so fp8 pools keep the 2e-3 rule, with the error logged.
 """
 import numpy as np
 
@@ -60,9 +71,42 @@ def oracle_rows(keys_bits, raw_q, prompt=None, exclude=None):
     return s
 
 
-def check_topk(gpu_s, gpu_i, orc_full, k, tol=TOL):
+def fp32_bound(d, fmt="bf16"):
+    """eps: fp32 accumulation of d exact products of unit-norm bf16 operands
+    (stored rows have norm within 2^-8 of 1, both factors included); None for
+    fp8 keys, whose MFMA accumulation this model does not describe."""
+    if fmt != "bf16":
+        return None
+    u = 2.0 ** -24
+    gamma = d * u / (1 - d * u)
+    return gamma * (1 + 2.0 ** -8) ** 2
+
+
+LAST_MAX_ERR = [0.0]     # max |s_gpu - s_oracle| of the latest check_topk call
+
+
+def check_topk(gpu_s, gpu_i, orc_full, k, tol=TOL, eps=None):
     """Apply T1-T3 and the score tolerance; returns per-query flags
-    (unambiguous set, unambiguous order)."""
+    (unambiguous set, unambiguous order).  With eps (fp32_bound), the same
+    rules are applied again at the derived bound (scores within eps, T1-T3
+    at 2 eps).  The largest score error is printed and kept in LAST_MAX_ERR."""
+    flags = _check_topk(gpu_s, gpu_i, orc_full, k, tol)
+    B = gpu_i.shape[0]
+    err = 0.0
+    for b in range(B):
+        got = gpu_i[b][gpu_i[b] >= 0].astype(np.int64)
+        if len(got):
+            err = max(err, float(np.max(np.abs(gpu_s[b][:len(got)] - orc_full[b][got]))))
+    LAST_MAX_ERR[0] = err
+    print(f"check_topk: B={B} k={k} max |s_gpu - s_oracle| = {err:.3g}"
+          + (f" (fp32 bound {eps:.3g})" if eps is not None else ""))
+    if eps is not None:
+        assert err <= eps, f"score error {err} above the fp32 accumulation bound {eps}"
+        _check_topk(gpu_s, gpu_i, orc_full, k, 2 * eps)
+    return flags
+
+
+def _check_topk(gpu_s, gpu_i, orc_full, k, tol):
     B = gpu_i.shape[0]
     flags = []
     for b in range(B):

@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import workloads
-from tests._parity import TOL, away_from_edges, check_topk, oracle_rows, untile_keys
+from tests._parity import TOL, away_from_edges, check_topk, fp32_bound, oracle_rows, untile_keys
 
 pytestmark = pytest.mark.gpu
 
@@ -85,7 +85,7 @@ def _query_case(oil, n, d, B, k, seed, dtype="f32", p_random=0.25, clusters=0):
     torch.cuda.synchronize()
     keys = _stored(pool, n)
     o = oracle_rows(keys, _raw_np(q))
-    flags = check_topk(s.cpu().numpy(), i.cpu().numpy(), o, k)
+    flags = check_topk(s.cpu().numpy(), i.cpu().numpy(), o, k, eps=fp32_bound(d))
     if clusters == 0 and n > k:
         # a noisy copy of a stored key (cos ~ 0.999) has that key as its unique best
         top1 = i[:, 0].cpu().numpy()
@@ -131,16 +131,20 @@ def test_topk_runs_of_neighbours(oil, key_format, B, k):
     check_topk(s_.cpu().numpy(), i_.cpu().numpy(), o, k)
 
 
-@pytest.mark.parametrize("key_format,B,extra", [("bf16", 8, 1000), ("bf16", 40, 1000), ("fp8", 8, 777),
-                                                 ("fp8", 40, 4000), ("bf16", 16, 0), ("bf16", 16, 100),
-                                                 ("bf16", 16, 400)])
-def test_topk_pool_past_whole_waves(oil, key_format, B, extra, base=262144):
+@pytest.mark.parametrize("key_format,B,extra,d", [("bf16", 8, 1000, 64), ("bf16", 40, 1000, 64),
+                                                   ("fp8", 8, 777, 64), ("fp8", 40, 4000, 64),
+                                                   ("bf16", 16, 0, 64), ("bf16", 16, 100, 64),
+                                                   ("bf16", 16, 400, 64), ("bf16", 16, 400, 576),
+                                                   ("bf16", 40, 1000, 576), ("fp8", 8, 777, 576)])
+def test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=262144):
     """Pools a little past a whole number of scan waves (262,144 rows plus up
     to a few thousand): from 16 row blocks on (8 when the main grid is a
     single generation of waves), the rows beyond go to the scan's remainder
     launch (one row block per wave, deeper prefetch); fewer stay in the main
-    grid.  With prompt exclusion."""
-    n, d = base + extra, 64
+    grid.  With prompt exclusion.  At d = 576 (9 bf16 windows, 5 fp8) the
+    remainder launch's prefetch ring (7 or 3 windows in flight) wraps and
+    takes its clamped tail."""
+    n = base + extra
     g = torch.Generator().manual_seed(B + extra)
     raw = torch.randn((n, d), generator=g)
     q = torch.randn((B, d), generator=g)
@@ -165,16 +169,17 @@ def test_topk_pool_past_whole_waves(oil, key_format, B, extra, base=262144):
     for b in range(B):
         if ex[b] >= 0:
             o[b, pr == int(ex[b])] = -np.inf
-    check_topk(s_.cpu().numpy(), i_.cpu().numpy(), o, 16)
+    check_topk(s_.cpu().numpy(), i_.cpu().numpy(), o, 16, eps=fp32_bound(d, key_format))
 
 
-@pytest.mark.parametrize("key_format,extra", [("fp8", 300), ("fp8", 100), ("bf16", 300)])
-def test_topk_pool_past_one_generation(oil, key_format, extra):
+@pytest.mark.parametrize("key_format,extra,d", [("fp8", 300, 64), ("fp8", 100, 64), ("bf16", 300, 64),
+                                                 ("fp8", 300, 576), ("bf16", 300, 576)])
+def test_topk_pool_past_one_generation(oil, key_format, extra, d):
     """131,072 rows are one generation of the fp8 scan's waves (two row blocks
     per wave) and half of one for bf16: 10 extra row blocks go to the
     remainder launch for fp8, 4 stay in the main grid; bf16 keeps all of
     them in its single partial generation."""
-    test_topk_pool_past_whole_waves(oil, key_format, 8, extra, base=131072)
+    test_topk_pool_past_whole_waves(oil, key_format, 8, extra, d, base=131072)
 
 
 @pytest.mark.parametrize("B", [65, 96, 128, 200, 256, 512])
@@ -210,6 +215,50 @@ def test_wide_batches_window_counts_fp8(oil, d, B):
     kinv = pool.scales[:n].cpu().numpy().astype(np.float64)
     qc, qinv = oracle.quantize_rows_fp8(q.numpy())
     check_topk(s.cpu().numpy(), i.cpu().numpy(), oracle.scores_fp8(codes, kinv, qc, qinv), 16)
+
+
+@pytest.mark.parametrize("d,B,key_format", [(8192, 2, "bf16"), (8192, 4, "bf16"), (12288, 2, "bf16"),
+                                              (12288, 4, "bf16"), (12288, 40, "bf16"), (8192, 2, "fp8"),
+                                              (8192, 4, "fp8"), (12288, 2, "fp8"), (12288, 40, "fp8")])
+def test_wide_rows_through_the_abi(oil, d, B, key_format):
+    """Row widths the C ABI accepts beyond the workloads: d = 8,192 with B = 2
+    and 4 (the GEMV's queries fill 32 and exactly 64 KiB of LDS), d = 12,288
+    (rows wider than one register pass of the normalising and quantizing
+    kernels; B = 2 still a GEMV at 48 KiB, B = 4 past 64 KiB falls back to the
+    MFMA scan, B = 40 two query tiles), bf16 and fp8 keys, with exclusion.
+    Stored rows are checked against the oracle's normalisation (bf16: within
+    one ulp; fp8: codes and scales bit-exact), scores at the fp32 bound too."""
+    n = 4000 + 37
+    wp = workloads.Pool(workloads.PoolSpec(n=n, d=d, vocab=5000, seed=d + B, n_clusters=16,
+                                           key_dtype="f32"))
+    raw = wp.raw_rows(0, n)
+    pool = oil.Pool(d, n, key_format=key_format)
+    pool.append(raw.cuda(), wp.tokens.cuda(), wp.traces.cuda(), wp.prompts.cuda())
+    q, src = workloads.queries(wp, workloads.QuerySpec(B=B, p_random=0.25, seed=d + B + 1))
+    q = q.float()
+    ex = torch.where(src >= 0, wp.prompts[src.clamp(min=0).long()], torch.full_like(src, -1))
+    s, i = pool.query_topk(q.cuda(), 16, exclude_prompt=ex.cuda())
+    torch.cuda.synchronize()
+    raw_np = raw.cpu().numpy()
+    if key_format == "fp8":
+        from tests._parity import untile_keys_fp8
+        codes = untile_keys_fp8(pool.keys.cpu().numpy(), n, d, n)
+        kc, kinv = oracle.quantize_rows_fp8(raw_np)
+        assert np.array_equal(codes, kc)
+        assert np.array_equal(pool.scales[:n].cpu().numpy().astype(np.float64), kinv)
+        qc, qinv = oracle.quantize_rows_fp8(q.numpy())
+        o = oracle.scores_fp8(kc, kinv, qc, qinv)
+        pr = wp.prompts.numpy()
+        for b in range(B):
+            if ex[b] >= 0:
+                o[b, pr == int(ex[b])] = -np.inf
+    else:
+        keys = _stored(pool, n)
+        ref = oracle.normalize_rows(raw_np)
+        diff = np.abs(keys.astype(np.int32) - ref.astype(np.int32))
+        assert diff.max() <= 1 and (diff > 0).mean() <= 1e-6
+        o = oracle_rows(keys, q.numpy(), wp.prompts.numpy(), ex.numpy())
+    check_topk(s.cpu().numpy(), i.cpu().numpy(), o, 16, eps=fp32_bound(d, key_format))
 
 
 def test_wide_batch_ragged_width_and_exclusion(oil):
