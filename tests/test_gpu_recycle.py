@@ -85,14 +85,19 @@ def _check_ring(rp, recs_list, R, d):
     return out, seq
 
 
-@pytest.mark.parametrize("R,batches,dtype", [
-    (5000, [(0, 16, 65), (1, 8, 33)], np.float32),       # no wrap
-    (300, [(2, 16, 65), (3, 16, 65), (4, 4, 17)], "bf16"),  # wraps around
-    (100, [(5, 32, 65)], np.float32),                    # one batch larger than the ring
-    (64, [(6, 70, 9), (7, 1, 1)], np.float32),           # 70 trees (two match groups); a root-only tree
+@pytest.mark.parametrize("R,batches,dtype,d", [
+    (5000, [(0, 16, 65), (1, 8, 33)], np.float32, 192),       # no wrap
+    (300, [(2, 16, 65), (3, 16, 65), (4, 4, 17)], "bf16", 192),  # wraps around
+    (100, [(5, 32, 65)], np.float32, 192),                    # one batch larger than the ring
+    (64, [(6, 70, 9), (7, 1, 1)], np.float32, 192),           # 70 trees (two match groups); a root-only tree
+    # key rows of 1,536 and 4,096 columns: the normalising kernel's two wider
+    # branches (eight values per thread; the looping pass)
+    (400, [(8, 8, 33), (9, 4, 17)], np.float32, 1536),
+    (400, [(10, 8, 33)], "bf16", 1536),
+    (300, [(11, 8, 33), (12, 4, 17)], np.float32, 4096),
+    (300, [(13, 8, 33)], "bf16", 4096),
 ])
-def test_insert_ring_bit_exact(oil, R, batches, dtype):
-    d = 192
+def test_insert_ring_bit_exact(oil, R, batches, dtype, d):
     rp = oil.RecyclePool(d, R)
     recs = []
     for seed, B, mx in batches:
