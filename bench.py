@@ -92,6 +92,21 @@ def _pcts(torch, ev):
             "mean": round(float(x.mean()), 4)}
 
 
+def _merge_rate(torch, fn, trees, K=50):
+    """Merges per second of fn() (one tree_merge call of `trees` trees), from
+    events around K back-to-back calls."""
+    fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(K):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    return {"merges_per_s": round(trees / (ms / 1e3), 1), "us_per_call": round(ms * 1e3, 2), "trees": trees}
+
+
 def _timed_events(torch, fn, steps):
     """Per-step GPU latency distribution of fn(t): an event at every step boundary."""
     steps = list(steps)
@@ -526,6 +541,22 @@ def other_workloads(args, oil, workloads, dev):
     out = {}
     K, W = 30, 3
 
+    # tiny pool: N = 4,096, d = 512, one query, k = 8, L = 8, 32 nodes: merges per second
+    cfg = workloads.TINY
+    ps, k, L, sb = cfg["pool"], cfg["k"], cfg["L"], cfg["sem_budget"]
+    wp = workloads.Pool(ps, device=dev)
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    pool.append(wp.raw_rows(0, ps.n), wp.tokens.to(dev), wp.traces.to(dev), wp.prompts.to(dev))
+    q, src = workloads.queries(wp, cfg["query"])
+    s_, i_ = pool.query_topk(q.contiguous(), k)
+    c_, l_ = pool.gather(i_, s_, oil.DepthRule.fixed(L), L)
+    anc = workloads.anchors(wp, src).to(dev)
+    tree = oil.merge_trees(anc, None, None, 0, c_, l_, sb, 1 + sb)
+    out["tiny"] = {"merge": _merge_rate(torch, lambda: oil.merge_trees(anc, None, None, 0, c_, l_, sb, 1 + sb,
+                                                                       out=tree), 1),
+                   "step": "merge of one tree: 8 chains of 8 under 32 nodes"}
+    del pool, wp
+
     # single-stream decode: N = 65,536, d = 4,096, one query per step, k = 16, L = 16, 64 nodes
     cfg = workloads.DECODE_64K
     ps, k, L, sb = cfg["pool"], cfg["k"], cfg["L"], cfg["sem_budget"]
@@ -552,9 +583,14 @@ def other_workloads(args, oil, workloads, dev):
     nt, sms = oil.scan_timer_stop()
     scan_s = sms / nt / 1e3
     gbs = (ps.n * ps.d * 2 + ps.d * 2) / scan_s / 1e9
+    s_, i_ = pool.query_topk(Q[W], k)
+    c_, l_ = pool.gather(i_, s_, rule, L)
+    tree = oil.merge_trees(A[W], None, None, 0, c_, l_, sb, 1 + sb)
     out["decode_64k"] = {"ms_per_step": round(ms, 4), "latency_ms": lat,
                          "scan_ms": round(scan_s * 1e3, 4), "scan_GBps": round(gbs, 1),
                          "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                         "merge": _merge_rate(torch, lambda: oil.merge_trees(A[W], None, None, 0, c_, l_, sb,
+                                                                             1 + sb, out=tree), 1),
                          "note": "512 MiB pool, twice the 256 MB Infinity Cache: read mostly from HBM",
                          "step": "query top-16 + gather 16 + merge (64 nodes), B = 1"}
     log(f"decode_64k: {out['decode_64k']['ms_per_step']} ms/step")
@@ -636,10 +672,75 @@ def other_workloads(args, oil, workloads, dev):
 
     _timed(torch, full, range(W))
     ms = _timed(torch, full, range(W, W + K))
+    q, anc, ctx, cl, ex = steps[W]
+    lt, ll = pool.lexical(ctx, cl, n_lex, L_lex, ex)
+    s_, i_ = pool.query_topk(q, k, exclude_prompt=ex)
+    c_, l_ = pool.gather(i_, s_, rule, L)
+    tree = oil.merge_trees(anc, lt, ll, lb, c_, l_, sb, mx)
     out["full_step_8192"] = {"ms_per_step": round(ms, 4), "trees_per_s": round(qsp.B / (ms / 1e3), 1),
                              "latency_ms": _timed_events(torch, full, range(W, W + K)),
+                             "merge": _merge_rate(torch, lambda: oil.merge_trees(anc, lt, ll, lb, c_, l_, sb, mx,
+                                                                                 out=tree), qsp.B),
                              "step": "lexical drafts + query top-32 + gather 12 + merge (48 + 16 nodes), B = 64"}
     log(f"full_step_8192: {ms:.3f} ms/step")
+    del pool, wp
+
+    # the paper's configuration at its largest store: N = 320,000, d = 4,096, one request per
+    # step: lexical drafts (3 of up to 32 tokens) + query top-8 + gather under D(s) = 48 / 8 / 0
+    # + merge (44 lexical + 16 reserved nodes, the top 3 lexical branches in the candidate set)
+    cfg = workloads.PAPER_320K
+    ps, qsp, k, L = cfg["pool"], cfg["query"], cfg["k"], cfg["L"]
+    n_lex, L_lex, lb, sb = cfg["n_lex"], cfg["L_lex"], cfg["lex_budget"], cfg["sem_budget"]
+    lr, lrl = cfg["lex_ret"], cfg["lex_ret_len"]
+    wp = workloads.Pool(ps, device=dev)
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    for s0 in range(0, ps.n, 65536):
+        m = min(65536, ps.n - s0)
+        pool.append(wp.raw_rows(s0, m), wp.tokens[s0:s0 + m].to(dev), wp.traces[s0:s0 + m].to(dev),
+                    wp.prompts[s0:s0 + m].to(dev))
+    KP = 200
+    q, src = workloads.queries(wp, workloads.QuerySpec(B=KP + W, noise=qsp.noise, p_random=qsp.p_random,
+                                                       seed=qsp.seed))
+    ctx, cl, ex = workloads.lexical_contexts(wp, src, ps.n)
+    anc = workloads.anchors(wp, src)
+    steps = [(q[t:t + 1].contiguous(), anc[t:t + 1].to(dev), ctx[t:t + 1].to(dev), cl[t:t + 1].to(dev),
+              ex[t:t + 1].to(dev)) for t in range(KP + W)]
+    rule = oil.DepthRule.paper()
+    mx = 1 + lb + sb
+    bufs = {}
+
+    def paper(t):
+        q1, a1, c1, l1, e1 = steps[t]
+        lt, ll = pool.lexical(c1, l1, n_lex, L_lex, e1, out=bufs.get("lex"))
+        bufs["lex"] = (lt, ll)
+        s_, i_ = pool.query_topk(q1, k, exclude_prompt=e1, out=bufs.get("q"))
+        bufs["q"] = (s_, i_)
+        c_, l_ = pool.gather(i_, s_, rule, L, out=bufs.get("g"))
+        bufs["g"] = (c_, l_)
+        bufs["t"] = oil.merge_trees(a1, lt, ll, lb, c_, l_, sb, mx, out=bufs.get("t"), lex_ret=lr,
+                                    lex_ret_len=lrl)
+
+    _timed(torch, paper, range(W))
+    ms = _timed(torch, paper, range(W, W + KP))
+    lat = _timed_events(torch, paper, range(W, W + KP))
+    oil.scan_timer_start(KP)
+    _timed(torch, paper, range(W, W + KP))
+    nt, sms = oil.scan_timer_stop()
+    scan_s = sms / nt / 1e3
+    gbs = (ps.n * ps.d * 2 + ps.d * 2) / scan_s / 1e9
+    out["paper_320k"] = {"ms_per_step": round(ms, 4), "latency_ms": lat, "steps": KP,
+                         "scan_ms": round(scan_s * 1e3, 4), "scan_GBps": round(gbs, 1),
+                         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                         "step": "lexical drafts (3 x 32) + query top-8 + gather (D(s) 48/8/0) + merge "
+                                 "(44 + 16 of 60 nodes), B = 1"}
+    q1, a1, c1, l1, e1 = steps[W]
+    paper(W)
+    lt, ll = bufs["lex"]
+    c_, l_ = bufs["g"]
+    out["paper_320k"]["merge"] = _merge_rate(
+        torch, lambda: oil.merge_trees(a1, lt, ll, lb, c_, l_, sb, mx, out=bufs["t"], lex_ret=lr, lex_ret_len=lrl),
+        1)
+    log(f"paper_320k: {ms:.3f} ms/step, p50 {lat['p50']} p99 {lat['p99']}")
     print(json.dumps({"workloads": out}), flush=True)
 
 

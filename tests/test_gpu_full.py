@@ -270,3 +270,80 @@ def test_batches_1m_full_size(oil):
                     assert not np.isin(gi[b][gi[b] >= 0], np.flatnonzero(prompts == int(ex[b]))).any()
         check_topk(gs[sample], gi[sample], orc.s, k, eps=fp32_bound(ps.d))
         _rescore_returned(wp, gs[::25], gi[::25], _bits(q[::25]))
+
+
+def test_paper_config_320k(oil):
+    """The paper's frozen configuration at its largest store: 320,000 positions
+    of width 4,096, one request per call (the B = 1 launches the benchmark
+    times), k = 8, theta = 0.8, D(s) = 48 / 8 / 0, the top 3 lexical branches
+    of up to 32 tokens under 60 - 16 = 44 nodes and B_ret = 16.  Eight sampled
+    requests: lexical drafts bit-exact against the oracle, retrieval by
+    T1-T3 (and the fp32 bound) against exact scores of every position, the
+    paper-rule gather and the merge (with the lexical branches in the
+    candidate set) bit-exact on the GPU's own inputs, end to end where the
+    top-k and the depth bands are unambiguous."""
+    cfg = workloads.PAPER_320K
+    ps, qs, k, L = cfg["pool"], cfg["query"], cfg["k"], cfg["L"]
+    n_lex, L_lex, lb, sb = cfg["n_lex"], cfg["L_lex"], cfg["lex_budget"], cfg["sem_budget"]
+    lr, lrl = cfg["lex_ret"], cfg["lex_ret_len"]
+    dev = torch.device("cuda")
+    wp = workloads.Pool(ps, device=dev)
+    nq = 8
+    q, src = workloads.queries(wp, workloads.QuerySpec(B=nq, noise=qs.noise, p_random=qs.p_random,
+                                                       seed=qs.seed))
+    orc = StreamedOracle(_bits(q), ps.n)
+    pool = oil.Pool(ps.d, ps.n, device=dev)
+    _fill(pool, wp, 0, ps.n, dev, [orc])
+    ctx, ctx_len, excl = workloads.lexical_contexts(wp, src, ps.n)
+    anchor = workloads.anchors(wp, src)
+    mx = 1 + lb + sb
+    rule, orule = oil.DepthRule.paper(), oracle.paper_rule()
+    tok, tr, pr = wp.tokens.cpu().numpy(), wp.traces.cpu().numpy(), wp.prompts.cpu().numpy()
+    gs, gi, glt, gll, gct, gcl, trees = [], [], [], [], [], [], []
+    for b in range(nq):                      # one request per call, as the benchmark runs them
+        sl = slice(b, b + 1)
+        lt, ll = pool.lexical(ctx[sl].to(dev), ctx_len[sl].to(dev), n_lex, L_lex, excl[sl].to(dev))
+        s, i = pool.query_topk(q[sl].contiguous(), k, exclude_prompt=excl[sl].to(dev))
+        ct, cl = pool.gather(i, s, rule, L)
+        tree = oil.merge_trees(anchor[sl].to(dev), lt, ll, lb, ct, cl, sb, mx, lex_ret=lr, lex_ret_len=lrl)
+        torch.cuda.synchronize()
+        gs.append(s.cpu().numpy()[0]), gi.append(i.cpu().numpy()[0])
+        glt.append(lt.cpu().numpy()[0]), gll.append(ll.cpu().numpy()[0])
+        gct.append(ct.cpu().numpy()[0]), gcl.append(cl.cpu().numpy()[0])
+        trees.append([a.cpu().numpy()[0] for a in tree])
+    gs, gi = np.stack(gs), np.stack(gi)
+    glt, gll, gct, gcl = np.stack(glt), np.stack(gll), np.stack(gct), np.stack(gcl)
+    # lexical drafts: bit-exact against the (uncapped) oracle
+    elt, ell = oracle.lexical_drafts(tok, tr, pr, ps.n, ctx.numpy(), ctx_len.numpy(), n_lex, L_lex,
+                                     excl.numpy())
+    assert np.array_equal(gll, ell) and np.array_equal(glt, elt)
+    # retrieval: exact scores of every position, self-exclusion applied
+    o = orc.s.copy()
+    for b in range(nq):
+        if excl[b] >= 0:
+            o[b, pr == int(excl[b])] = -np.inf
+    flags = check_topk(gs, gi, o, k, eps=fp32_bound(ps.d))
+    # gather (paper rule) and merge on the GPU's own inputs: bit-exact
+    ect, ecl = oracle.gather(tok, tr, ps.n, gi, gs, orule, L)
+    assert np.array_equal(gcl, ecl) and np.array_equal(gct, ect)
+    etree = oracle.tree_merge(anchor.numpy(), glt, gll, lb, ect, ecl, sb, mx, lex_ret=lr, lex_ret_len=lrl)
+    for b in range(nq):
+        for a, e in zip(trees[b], etree):
+            assert np.array_equal(a, e[b])
+    # the configuration is exercised: the 48-token band, lexical and
+    # retrieved nodes in the trees
+    assert (gcl > 8).any()
+    ns = np.stack([t[2] for t in trees])
+    assert (ns == 1).any() and (ns == 2).any()
+    print(f"paper config: chain lengths {sorted(set(gcl[gcl > 0].tolist()))}, lexical nodes per tree "
+          f"{(ns == 1).sum(1).tolist()}, retrieved {(ns == 2).sum(1).tolist()}, lexical branches bought "
+          f"from B_ret {(ns == 4).sum(1).tolist()}")
+    # end to end where the oracle's top-k and the bands are unambiguous
+    os_, oi = oracle.topk(o, k)
+    os32 = os_.astype(np.float32)
+    edges = [0.8, 0.82, 0.90]
+    for b in range(nq):
+        if flags[b][1] and away_from_edges(os32[b], edges):
+            assert gi[b].tolist() == oi[b].tolist()
+            c2, l2 = oracle.gather(tok, tr, ps.n, oi[b:b + 1], os32[b:b + 1], orule, L)
+            assert np.array_equal(gct[b], c2[0]) and np.array_equal(gcl[b], l2[0])

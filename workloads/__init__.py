@@ -69,6 +69,13 @@ STREAM_5120 = dict(pool=PoolSpec(n=2097152, d=5120, vocab=128256, seed=4, n_clus
 FULL_STEP_8192 = dict(pool=PoolSpec(n=524288, d=8192, vocab=128256, seed=5, n_clusters=256),
                       query=QuerySpec(B=64, noise=0.05, p_random=0.25, seed=105),
                       k=32, L=12, n_lex=4, L_lex=12, lex_budget=48, sem_budget=16)
+# The paper's frozen configuration at its largest store: 320,000 positions of
+# width 4,096 (2.6 GB of bf16 keys), one request per step, k = 8, theta = 0.8,
+# copy depth D(s) = 48 / 8 / 0 (chains up to 48 tokens), the top 3 lexical
+# branches of up to 32 tokens under 60 - 16 = 44 nodes, B_ret = 16.
+PAPER_320K = dict(pool=PoolSpec(n=320000, d=4096, vocab=128256, seed=6, n_clusters=256),
+                  query=QuerySpec(B=1, noise=0.05, p_random=0.25, seed=106),
+                  k=8, L=48, n_lex=3, L_lex=32, lex_budget=44, sem_budget=16, lex_ret=3, lex_ret_len=32)
 
 
 def _gen(seed: int, device) -> torch.Generator:
