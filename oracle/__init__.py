@@ -62,7 +62,8 @@ def _load():
         lib.orc_e4m3_round.restype = ctypes.c_uint8
         lib.orc_quantize_rows_fp8.argtypes = [P, i32, i64, i32, P, P]
         lib.orc_scores_fp8.argtypes = [P, P, i64, i32, P, P, i32, P]
-        lib.orc_lexical_drafts.argtypes = [P, P, P, i64, P, P, i32, i32, P, i32, i32, i32, i64, P, P, P]
+        lib.orc_lexical_drafts.argtypes = [P, P, P, i64, P, P, i32, i32, P, P, P, i32, i32, i32, i32, i64, P, P,
+                                           P]
         lib.orc_accept_walk.argtypes = [i32, i32, P, P, P, P, P, P, P]
         _lib = lib
     return _lib
@@ -241,13 +242,15 @@ def accept_walk(node_token, node_parent, n_nodes, target):
 
 
 def lexical_drafts(tokens, traces, prompts, n_valid, ctx, ctx_len, n_lex, L_lex, exclude_prompt=None,
-                   min_match=2, max_cand=1 << 62, with_capped=False):
+                   min_match=2, max_cand=1 << 62, with_capped=False, hist=None, hist_len=None):
     """Exact-suffix drafts: (tokens (B, n_lex, L_lex) -1 padded, lengths (B, n_lex)),
     plus, with ``with_capped``, the per-request flag (B,) marking where the
     candidate capacity may have changed the drafts.
 
     ``ctx`` is (B, C) right-aligned (most recent token last); the last
-    ``ctx_len[b]`` entries of row b are the request's context."""
+    ``ctx_len[b]`` entries of row b are the request's context.  ``hist`` (B, H),
+    optional: row b's first ``hist_len[b]`` entries are request b's own
+    committed tokens, oldest first, indexed as one more trace after the pool."""
     tok, tr, pr = _c(tokens, np.int32), _c(traces, np.int32), _c(prompts, np.int32)
     ctx = _c(ctx, np.int32)
     cl = _c(ctx_len, np.int32)
@@ -256,9 +259,15 @@ def lexical_drafts(tokens, traces, prompts, n_valid, ctx, ctx_len, n_lex, L_lex,
     ot = np.empty((B, n_lex, L_lex), np.int32)
     ol = np.empty((B, n_lex), np.int32)
     cap = np.empty((B,), np.int32)
+    if hist is not None:
+        hist = _c(hist, np.int32)
+        hist_len = _c(hist_len, np.int32)
+        H = hist.shape[1]
+    else:
+        H = 0
     _check(_load().orc_lexical_drafts(_ptr(tok), _ptr(tr), _ptr(pr), int(n_valid), _ptr(ctx), _ptr(cl),
-                                      C, B, _ptr(ex), n_lex, L_lex, min_match, int(max_cand), _ptr(ot),
-                                      _ptr(ol), _ptr(cap)),
+                                      C, B, _ptr(ex), _ptr(hist), _ptr(hist_len), H, n_lex, L_lex, min_match,
+                                      int(max_cand), _ptr(ot), _ptr(ol), _ptr(cap)),
            "lexical_drafts")
     return (ot, ol, cap) if with_capped else (ot, ol)
 

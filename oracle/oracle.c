@@ -506,6 +506,12 @@ int orc_accept_walk(int32_t B, int32_t max_nodes, const int32_t *node_token, con
 /*     candidates with m(p) >= m that are not yet held are ranked by how many  */
 /*     of those candidates give them (more first), then by their earliest     */
 /*     position, and taken in that order until n_lex are held.              */
+/* The request's own committed tokens (Sec. 4 (ii): the automaton indexes the */
+/* store and the current request's tokens; hist, optional): request b sees   */
+/* its hist_len[b] tokens as one more trace placed after the pool's last      */
+/* position (positions n_valid .., so they rank after every pool position on */
+/* ties), visible to no other request and never self-excluded; matches and    */
+/* continuations stay inside it like inside any trace.                        */
 /* Output: n_lex slots per request in pick order; unused slots -1 / length 0. */
 /* Parity pins: brute force, a library special case, relations (exclusion,    */
 /* back-off, capacity) and a hand-worked fixture.                              */
@@ -517,22 +523,43 @@ typedef struct {
     int64_t group; /* representative candidate (first in position order) */
 } orc_level_entry;
 
-static int32_t cont_len(const int32_t *traces, int64_t n_valid, int64_t p, int32_t L)
+/* One request's view of the indexed tokens: the pool's positions, then its */
+/* own history as one more trace. */
+typedef struct {
+    const int32_t *tokens, *traces, *prompts;
+    int64_t n_valid;     /* pool positions */
+    const int32_t *hist; /* the request's own committed tokens (or NULL) */
+    int64_t hl;          /* how many */
+} lex_view;
+
+static int32_t lv_tok(const lex_view *v, int64_t p)
 {
+    return p < v->n_valid ? v->tokens[p] : v->hist[p - v->n_valid];
+}
+
+static int lv_same_trace(const lex_view *v, int64_t p, int64_t q)
+{
+    if (p < v->n_valid && q < v->n_valid)
+        return v->traces[p] == v->traces[q];
+    return p >= v->n_valid && q >= v->n_valid;
+}
+
+static int32_t cont_len(const lex_view *v, int64_t p, int32_t L)
+{
+    int64_t end = v->n_valid + v->hl;
     int32_t len = 0;
-    while (len < L && p + 1 + len < n_valid && traces[p + 1 + len] == traces[p])
+    while (len < L && p + 1 + len < end && lv_same_trace(v, p + 1 + len, p))
         len++;
     return len;
 }
 
-static int same_cont(const int32_t *tokens, const int32_t *traces, int64_t n_valid, int64_t p, int64_t q,
-                     int32_t L)
+static int same_cont(const lex_view *v, int64_t p, int64_t q, int32_t L)
 {
-    int32_t a = cont_len(traces, n_valid, p, L), b = cont_len(traces, n_valid, q, L);
+    int32_t a = cont_len(v, p, L), b = cont_len(v, q, L);
     if (a != b)
         return 0;
     for (int32_t j = 1; j <= a; j++)
-        if (tokens[p + j] != tokens[q + j])
+        if (lv_tok(v, p + j) != lv_tok(v, q + j))
             return 0;
     return 1;
 }
@@ -553,13 +580,15 @@ static int level_cmp(const void *pa, const void *pb)
  * visit hold the same candidates, so they pick the same drafts). */
 int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32_t *prompts, int64_t n_valid,
                        const int32_t *ctx, const int32_t *ctx_len, int32_t C, int32_t B,
-                       const int32_t *exclude_prompt, int32_t n_lex, int32_t L_lex, int32_t min_match,
-                       int64_t max_cand, int32_t *out_tokens, int32_t *out_len, int32_t *out_capped)
+                       const int32_t *exclude_prompt, const int32_t *hist, const int32_t *hist_len, int32_t H,
+                       int32_t n_lex, int32_t L_lex, int32_t min_match, int64_t max_cand, int32_t *out_tokens,
+                       int32_t *out_len, int32_t *out_capped)
 {
     if (!tokens || !traces || !prompts || !ctx || !ctx_len || !out_tokens || !out_len || n_valid < 0 ||
-        C < 1 || B < 1 || n_lex < 1 || L_lex < 1 || min_match < 1 || max_cand < 1)
+        C < 1 || B < 1 || n_lex < 1 || L_lex < 1 || min_match < 1 || max_cand < 1 ||
+        (hist && (!hist_len || H < 1)))
         return ORC_EINVAL;
-    size_t cap = (size_t)(n_valid > 0 ? n_valid : 1);
+    size_t cap = (size_t)(n_valid > 0 ? n_valid : 1) + (size_t)(hist ? H : 0);
     int64_t *cand = (int64_t *)malloc(sizeof(int64_t) * cap);
     int32_t *mlen = (int32_t *)malloc(sizeof(int32_t) * cap);
     int64_t *group = (int64_t *)malloc(sizeof(int64_t) * cap);
@@ -584,16 +613,24 @@ int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32
             continue;
         const int32_t *cx = ctx + (int64_t)b * C + (C - cl); /* the cl most recent tokens */
         int32_t ex = exclude_prompt ? exclude_prompt[b] : -1;
+        lex_view view = {tokens, traces, prompts, n_valid, NULL, 0};
+        if (hist) {
+            int32_t hl = hist_len[b] < 0 ? 0 : (hist_len[b] > H ? H : hist_len[b]);
+            view.hist = hist + (int64_t)b * H;
+            view.hl = hl;
+        }
+        const lex_view *v = &view;
+        int64_t total = n_valid + view.hl;
         /* 1-2: candidates, in position order, and their match lengths */
         int64_t nc = 0;
         int32_t mtop = 0;
         for (int32_t m = 0; m <= C + 1; m++)
             n_at[m] = 0;
-        for (int64_t p = 0; p < n_valid; p++) {
+        for (int64_t p = 0; p < total; p++) {
             int32_t m = 0;
-            while (m < cl && p - m >= 0 && traces[p - m] == traces[p] && tokens[p - m] == cx[cl - 1 - m])
+            while (m < cl && p - m >= 0 && lv_same_trace(v, p - m, p) && lv_tok(v, p - m) == cx[cl - 1 - m])
                 m++;
-            if (m < min_match || (ex >= 0 && prompts[p] == ex) || cont_len(traces, n_valid, p, 1) == 0)
+            if (m < min_match || (p < n_valid && ex >= 0 && prompts[p] == ex) || cont_len(v, p, 1) == 0)
                 continue;
             cand[nc] = p;
             mlen[nc] = m;
@@ -634,7 +671,7 @@ int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32
         for (int64_t i = 0; i < nc; i++) {
             group[i] = i;
             for (int64_t j = 0; j < i; j++) {
-                if (group[j] == j && same_cont(tokens, traces, n_valid, cand[i], cand[j], L_lex)) {
+                if (group[j] == j && same_cont(v, cand[i], cand[j], L_lex)) {
                     group[i] = j;
                     break;
                 }
@@ -671,9 +708,9 @@ int orc_lexical_drafts(const int32_t *tokens, const int32_t *traces, const int32
             qsort(lev, (size_t)ne, sizeof(orc_level_entry), level_cmp);
             for (int64_t e = 0; e < ne && n_picked < n_lex; e++) {
                 int64_t p = lev[e].p;
-                int32_t len = cont_len(traces, n_valid, p, L_lex);
+                int32_t len = cont_len(v, p, L_lex);
                 for (int32_t j = 0; j < len; j++)
-                    ot[(int64_t)n_picked * L_lex + j] = tokens[p + 1 + j];
+                    ot[(int64_t)n_picked * L_lex + j] = lv_tok(v, p + 1 + j);
                 ol[n_picked] = len;
                 picked[n_picked++] = lev[e].group;
             }

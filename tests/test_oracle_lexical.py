@@ -6,7 +6,9 @@ by a different route (sets of occurrences per suffix length, dictionaries of
 continuations), a special case that reduces to numpy window matching plus
 ``collections.Counter``, and relations any correct implementation obeys
 (excluding a prompt equals deleting its trace; back-off stops once the
-longest level is full; the candidate capacity acts as a raised minimum key).
+longest level is full; the candidate capacity acts as a raised minimum key;
+a request's own committed tokens act as one more trace appended to the
+store, which only that request sees and no exclusion removes).
 """
 import collections
 import json
@@ -18,9 +20,21 @@ import pytest
 import oracle
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "lexical_sec3.json")
+GOLDEN_HIST = os.path.join(os.path.dirname(__file__), "golden", "lexical_history.json")
 
 
-def _run(pool, ctx_rows, n_lex, L_lex, C=None, exclude=None, min_match=2, max_cand=1 << 62):
+def _hist_rows(hist_rows, H=None, hist_len=None):
+    """(B, H) history buffer, -1 padded, and its lengths (default: each row's)."""
+    H = H or max(1, max(len(h) for h in hist_rows))
+    hist = np.full((len(hist_rows), H), -1, np.int32)
+    for b, h in enumerate(hist_rows):
+        hist[b, :len(h)] = h
+    hl = np.asarray(hist_len if hist_len is not None else [len(h) for h in hist_rows], np.int32)
+    return hist, hl
+
+
+def _run(pool, ctx_rows, n_lex, L_lex, C=None, exclude=None, min_match=2, max_cand=1 << 62, hist=None,
+         hist_len=None, H=None):
     tok, tr, pr = pool
     C = C or max(1, max(len(c) for c in ctx_rows))
     B = len(ctx_rows)
@@ -31,7 +45,11 @@ def _run(pool, ctx_rows, n_lex, L_lex, C=None, exclude=None, min_match=2, max_ca
             ctx[b, C - len(c):] = c
         cl[b] = len(c)
     ex = None if exclude is None else np.asarray(exclude, np.int32)
-    ot, ol = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, ex, min_match, max_cand)
+    hb = hl = None
+    if hist is not None:
+        hb, hl = _hist_rows(hist, H, hist_len)
+    ot, ol = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, ex, min_match, max_cand,
+                                   hist=hb, hist_len=hl)
     return [[[int(t) for t in ot[b, j, :ol[b, j]]] for j in range(n_lex) if ol[b, j] > 0] for b in range(B)]
 
 
@@ -257,3 +275,112 @@ def test_empty_inputs():
     assert _run(pool, [[]], 2, 2, C=4) == [[]]
     assert _run(pool, [[3]], 2, 2, C=4) == [[]]            # shorter than the minimum key
     assert _run(pool, [[2, 3]], 2, 2, C=4) == [[[4, 5]]]
+
+
+def test_golden_history():
+    g = json.load(open(GOLDEN_HIST))
+    pool = tuple(np.asarray(g["pool"][k], np.int32) for k in ("tokens", "traces", "prompts"))
+    for case in g["cases"]:
+        hl = [case["hist_len"]] if "hist_len" in case else None
+        got = _run(pool, [case["ctx"]], case["n_lex"], case["L_lex"], exclude=[case["exclude_prompt"]],
+                   min_match=case["min_match"], hist=[case["hist"]], hist_len=hl, H=g["H"])[0]
+        assert got == case["expect"], case["name"]
+
+
+def _append_trace(pool, h):
+    """The store with one more trace holding h, under a prompt no request excludes."""
+    tok, tr, pr = pool
+    if not len(h):
+        return pool
+    t_id = (int(tr.max()) + 1) if len(tr) else 0
+    p_id = (int(pr.max()) + 1) if len(pr) else 0
+    return (np.concatenate([tok, np.asarray(h, np.int32)]),
+            np.concatenate([tr, np.full(len(h), t_id, np.int32)]),
+            np.concatenate([pr, np.full(len(h), p_id, np.int32)]))
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_history_equals_an_appended_trace(seed):
+    """Each request of a batch, with a history of its own, gets what the
+    store with that history appended as one more never-excluded trace gives
+    it alone, and what the brute-force enumeration gives on that store: no
+    request sees another's history, matches and drafts stop at both ends of
+    it, and store positions come first on ties."""
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(0, 120))
+    vocab = int(rng.integers(2, 5))
+    pool = _random_pool(rng, n, vocab, int(rng.integers(3, 12))) if n else (np.zeros(0, np.int32),) * 3
+    tok, tr, pr = pool
+    B, H = 4, 24
+    hists, ctxs, exs = [], [], []
+    for b in range(B):
+        hl = int(rng.integers(0, H + 1))
+        h = rng.integers(0, vocab, hl).tolist()
+        cl = int(rng.integers(0, 8))
+        r = rng.random()
+        if r < 0.4 and hl >= cl:
+            ctx = h[hl - cl:]                       # the request's own tail
+        elif r < 0.7 and n > cl:
+            s0 = int(rng.integers(0, n - cl + 1))
+            ctx = tok[s0:s0 + cl].tolist()
+        else:
+            ctx = rng.integers(0, vocab, cl).tolist()
+        hists.append(h)
+        ctxs.append(ctx)
+        exs.append(int(rng.integers(-1, int(pr.max()) + 1)) if n else -1)
+    n_lex = int(rng.integers(1, 6))
+    L_lex = int(rng.integers(1, 5))
+    mm = int(rng.integers(1, 4))
+    cap = int(rng.choice([1, 2, 3, 5, 1 << 40]))
+    got = _run(pool, ctxs, n_lex, L_lex, C=8, exclude=exs, min_match=mm, max_cand=cap, hist=hists, H=H)
+    for b in range(B):
+        ext = _append_trace(pool, hists[b])
+        if len(ext[0]):
+            want = _run(ext, [ctxs[b]], n_lex, L_lex, C=8, exclude=[exs[b]], min_match=mm, max_cand=cap)[0]
+        else:
+            want = []
+        assert got[b] == want, (seed, b)
+        assert got[b] == brute_force(*ext, ctxs[b], n_lex, L_lex, exs[b], mm, cap), (seed, b)
+
+
+def test_history_matches_reach_across_the_store_boundary_nowhere():
+    """A suffix that exists only when the store's last trace and the
+    request's tokens are read as one sequence is no match, and a draft
+    taken at the store's last trace does not run into the request's tokens."""
+    pool = (np.asarray([3, 4, 5, 6], np.int32), np.zeros(4, np.int32), np.zeros(4, np.int32))
+    # [6, 1] straddles the boundary; [5, 6] ends the store with nothing after it
+    assert _run(pool, [[6, 1]], 2, 3, hist=[[1, 2, 9]]) == [[]]
+    assert _run(pool, [[5, 6]], 2, 3, hist=[[1, 2, 9]]) == [[]]
+    assert _run(pool, [[4, 5]], 2, 3, hist=[[1, 2, 9]]) == [[[6]]]
+    assert _run(pool, [[1, 2]], 2, 3, hist=[[1, 2, 9]]) == [[[9]]]
+
+
+def test_history_lengths_clamped():
+    """hist_len above H reads H tokens, below 0 none."""
+    pool = (np.asarray([1, 2, 3], np.int32), np.zeros(3, np.int32), np.zeros(3, np.int32))
+    h = [[7, 1, 2, 8, 8]]
+    assert _run(pool, [[1, 2]], 3, 2, hist=h, hist_len=[99]) == _run(pool, [[1, 2]], 3, 2, hist=h)
+    assert _run(pool, [[1, 2]], 3, 2, hist=h, hist_len=[-4]) == _run(pool, [[1, 2]], 3, 2)
+    assert _run(pool, [[1, 2]], 3, 2, hist=h) == [[[3], [8, 8]]]
+
+
+def test_history_alone_is_prompt_lookup():
+    """With an empty store and no back-off, one-token drafts are the tokens
+    that follow earlier occurrences of the context inside the request's own
+    tokens, most frequent first, ties to the earliest (numpy window matching
+    and a Counter)."""
+    rng = np.random.default_rng(5)
+    empty = (np.zeros(0, np.int32),) * 3
+    for trial in range(20):
+        h = rng.integers(0, 3, 200).astype(np.int32)
+        cl = int(rng.integers(2, 5))
+        ctx = h[len(h) - cl:].tolist()
+        win = np.lib.stride_tricks.sliding_window_view(h, cl)
+        ends = np.flatnonzero((win == np.asarray(ctx)).all(axis=1)) + cl - 1
+        nxt = [int(h[p + 1]) for p in ends if p + 1 < len(h)]
+        first = {}
+        for i, t in enumerate(nxt):
+            first.setdefault(t, i)
+        ranked = sorted(collections.Counter(nxt).items(), key=lambda kv: (-kv[1], first[kv[0]]))
+        got = _run(empty, [ctx], 3, 1, min_match=cl, hist=[h.tolist()])[0]
+        assert got == [[t] for t, _ in ranked[:3]]

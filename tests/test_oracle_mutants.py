@@ -27,12 +27,18 @@ MUTANTS = {
     "exclusion ignored": ("if (prompt && exclude && exclude[b] >= 0 && prompt[i] == exclude[b])", "if (0)"),
     "mask misses the node itself": ("            int32_t j = i, guard = 0;", "            int32_t j = node_parent[(int64_t)b * max_nodes + i], guard = 0;"),
     "bonus always from the root": ("        bonus[b] = target[o + cur];", "        bonus[b] = target[o];"),
-    "suffix match crosses traces": ("p - m >= 0 && traces[p - m] == traces[p] && tokens[p - m]", "p - m >= 0 && tokens[p - m]"),
-    "draft starts at the match": ("ot[(int64_t)n_picked * L_lex + j] = tokens[p + 1 + j];", "ot[(int64_t)n_picked * L_lex + j] = tokens[p + j];"),
+    "suffix match crosses traces": ("p - m >= 0 && lv_same_trace(v, p - m, p) && lv_tok", "p - m >= 0 && lv_tok"),
+    "draft starts at the match": ("ot[(int64_t)n_picked * L_lex + j] = lv_tok(v, p + 1 + j);", "ot[(int64_t)n_picked * L_lex + j] = lv_tok(v, p + j);"),
     "rarest continuation first": ("return a->count > b->count ? -1 : 1;", "return a->count < b->count ? -1 : 1;"),
     "lexical ties by latest position": ("return (a->p < b->p) ? -1 : (a->p > b->p);", "return (a->p > b->p) ? -1 : (a->p < b->p);"),
-    "lexical self-exclusion ignored": ("(ex >= 0 && prompts[p] == ex)", "(0)"),
-    "draft not clipped at trace end": ("p + 1 + len < n_valid && traces[p + 1 + len] == traces[p]", "p + 1 + len < n_valid"),
+    "lexical self-exclusion ignored": ("(p < n_valid && ex >= 0 && prompts[p] == ex)", "(0)"),
+    "draft not clipped at trace end": ("p + 1 + len < end && lv_same_trace(v, p + 1 + len, p)", "p + 1 + len < end"),
+    "history ignored": ("            view.hl = hl;", "            view.hl = 0;"),
+    "history joined to the store's last trace": ("    return p >= v->n_valid && q >= v->n_valid;", "    return 1;"),
+    "history removed by self-exclusion": ("(p < n_valid && ex >= 0 && prompts[p] == ex)", "(ex >= 0 && (p >= n_valid || prompts[p] == ex))"),
+    "every request sees the first history": ("view.hist = hist + (int64_t)b * H;", "view.hist = hist;"),
+    "history read one token past its length": ("            view.hl = hl;", "            view.hl = hl < H ? hl + 1 : hl;"),
+    "overlong history dropped instead of cut": ("(hist_len[b] > H ? H : hist_len[b])", "(hist_len[b] > H ? 0 : hist_len[b])"),
     "capacity ignored": ("if (n_ge + n_at[m] > max_cand)", "if (0)"),
     "held draft proposed again": ("if (picked[t] == g)", "if (picked[t] == -7)"),
     "accepted nodes recycled too": ("            if (accepted[n])\n                continue;", "            if (0)\n                continue;"),
