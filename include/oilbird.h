@@ -65,6 +65,8 @@ enum { OIL_F32 = 0, OIL_BF16 = 1 };
 #define OIL_LEX_MAX_N 16
 #define OIL_LEX_MAX_LEN 64
 #define OIL_LEX_MAX_CAND 4096
+/* Largest row of a request's own committed tokens the lexical source indexes. */
+#define OIL_LEX_MAX_HIST (1 << 20)
 
 /* Recycled pool: tokens per rollout (Sec. 4 (i b): up to six deep) and the
  * largest number of rollouts a lookup returns per request. */
@@ -215,8 +217,9 @@ int32_t oil_gather_continuations(const oil_pool *pool, const int32_t *idx, const
                                  int32_t *chain_tokens, int32_t *chain_len, void *stream);
 
 /* Workspace bytes oil_lexical_drafts needs for B requests with candidate
- * capacity max_cand (sized from the pool's capacity). */
-size_t oil_lexical_workspace_bytes(const oil_pool *pool, int32_t B, int32_t max_cand);
+ * capacity max_cand and history rows of H tokens (0: no history), sized from
+ * the pool's capacity; 0 for arguments outside the limits below. */
+size_t oil_lexical_workspace_bytes(const oil_pool *pool, int32_t B, int32_t max_cand, int32_t H);
 
 /* Exact-suffix lexical drafts over the pool's tokens: the lexical key of
  * Sec. 2 (the longest suffix of the context that recurs verbatim, backing off
@@ -238,13 +241,24 @@ size_t oil_lexical_workspace_bytes(const oil_pool *pool, int32_t B, int32_t max_
  *      to >= that length that are not yet held are ranked by how many of those
  *      candidates give them (more first), then by earliest position, and
  *      taken in that order until n_lex are held.
+ * The index also holds each request's own committed tokens (Sec. 4 (ii)),
+ * when hist is given, without appending them to the pool: request b sees its
+ * hl = min(max(hist_len[b], 0), H) tokens as one more trace at positions
+ * n_valid .. n_valid + hl - 1 (after every pool position, so the pool wins
+ * ties on earliest position), seen by no other request and removed by no
+ * exclusion; matches and drafts stay inside it as inside any trace.
  *   ctx        B x C int32, right-aligned (the most recent token last).
  *   ctx_len    B int32 (negative counts as 0).   C  1 .. OIL_LEX_MAX_CTX.
  *   exclude_prompt  B int32 or NULL; negative excludes nothing.  Requires a
  *              pool created with a prompt buffer when not NULL.
+ *   hist       B x H int32 or NULL: row b holds request b's committed tokens,
+ *              oldest first.   hist_len  B int32 (required with hist).
+ *   H          1 .. OIL_LEX_MAX_HIST with hist (ignored without), and
+ *              n_valid + H <= INT32_MAX.
  *   B 1 .. OIL_MAX_B.  n_lex 1 .. OIL_LEX_MAX_N.  L_lex 1 .. OIL_LEX_MAX_LEN.
  *   min_match  1 .. OIL_LEX_MAX_CTX.   max_cand  1 .. OIL_LEX_MAX_CAND.
- *   workspace  >= oil_lexical_workspace_bytes(pool, B, max_cand), 256-byte aligned.
+ *   workspace  >= oil_lexical_workspace_bytes(pool, B, max_cand, H), 256-byte
+ *              aligned.
  *   lex_tokens B x n_lex x L_lex int32 in pick order, -1 padded;
  *   lex_len    B x n_lex int32, 0 for unused slots.
  *   lex_capped B int32 or NULL: 1 where the capacity rule of step 3 may have
@@ -253,7 +267,8 @@ size_t oil_lexical_workspace_bytes(const oil_pool *pool, int32_t B, int32_t max_
  *              level holding candidates while fewer than n_lex drafts were
  *              held; 0 guarantees the drafts are exactly the uncapped key's. */
 int32_t oil_lexical_drafts(const oil_pool *pool, const int32_t *ctx, const int32_t *ctx_len, int32_t C,
-                           int32_t B, const int32_t *exclude_prompt, int32_t n_lex, int32_t L_lex,
+                           int32_t B, const int32_t *exclude_prompt, const int32_t *hist,
+                           const int32_t *hist_len, int32_t H, int32_t n_lex, int32_t L_lex,
                            int32_t min_match, int32_t max_cand, void *workspace,
                            size_t workspace_bytes, int32_t *lex_tokens, int32_t *lex_len,
                            int32_t *lex_capped, void *stream);

@@ -27,6 +27,7 @@ OIL_F32, OIL_BF16 = 0, 1
 MAX_K, MAX_B, MAX_NODES, MAX_BANDS = 64, 512, 256, 4
 MAX_B_FP8 = 512
 LEX_MAX_CTX, LEX_MAX_N, LEX_MAX_LEN, LEX_MAX_CAND = 32, 16, 64, 4096
+LEX_MAX_HIST = 1 << 20
 REC_DEPTH, REC_MAX_OUT = 6, 8
 
 _lib = None
@@ -93,7 +94,7 @@ def lib():
                                      i32, i32, i32, P, P, P, P, P]),
             "oil_status_string": (ctypes.c_char_p, [i32]),
             "oil_tree_mask": (i32, [i32, i32, P, P, P, P]),
-            "oil_lexical_workspace_bytes": (sz, [P, i32, i32]),
+            "oil_lexical_workspace_bytes": (sz, [P, i32, i32, i32]),
             "oil_recycle_key_bytes": (sz, [i32, i64]),
             "oil_recycle_create": (i32, [i32, i64, P, P, P, P, P, ctypes.POINTER(P)]),
             "oil_recycle_destroy": (i32, [P]),
@@ -101,7 +102,8 @@ def lib():
             "oil_recycle_insert": (i32, [P, i32, i32, P, P, P, P, P, P, P, i32, P, sz, P]),
             "oil_recycle_query_workspace_bytes": (sz, [P, i32]),
             "oil_recycle_query": (i32, [P, P, i32, P, i32, ctypes.c_float, i32, i32, P, sz, P, P, P, P]),
-            "oil_lexical_drafts": (i32, [P, P, P, i32, i32, P, i32, i32, i32, i32, P, sz, P, P, P, P]),
+            "oil_lexical_drafts": (i32, [P, P, P, i32, i32, P, P, P, i32, i32, i32, i32, i32, P, sz, P, P, P,
+                                         P]),
             "oil_accept_walk": (i32, [i32, i32, P, P, P, P, P, P, P, P]),
             "oil_read_stream": (i32, [P, sz, P, P]),
             "oil_scan_timer_start": (i32, [i32, i32]),
@@ -209,16 +211,22 @@ def pool_query_topk_noalloc(handle, queries, k, scores, idx, exclude_prompt=None
 QUERY_SCRATCH_BYTES = 32 << 20
 
 
-def lexical_workspace_bytes(handle, B, max_cand) -> int:
-    return lib().oil_lexical_workspace_bytes(handle, B, max_cand)
+def lexical_workspace_bytes(handle, B, max_cand, H=0) -> int:
+    return lib().oil_lexical_workspace_bytes(handle, B, max_cand, H)
 
 
 def lexical_drafts(handle, ctx, ctx_len, n_lex, L_lex, workspace, lex_tokens, lex_len,
-                   exclude_prompt=None, min_match=2, max_cand=LEX_MAX_CAND, stream=None, lex_capped=None):
+                   exclude_prompt=None, min_match=2, max_cand=LEX_MAX_CAND, stream=None, lex_capped=None,
+                   hist=None, hist_len=None):
+    """``hist`` (B, H) int32 device tensor or None: request b's own committed
+    tokens in its first ``hist_len[b]`` entries, indexed beside the pool."""
     B, C = ctx.shape
+    H = 0 if hist is None else hist.shape[1]
     _check("oil_lexical_drafts", lib().oil_lexical_drafts(
         handle, _ptr(_i32(ctx, "ctx")), _ptr(_i32(ctx_len, "ctx_len")), C, B,
-        _ptr(None if exclude_prompt is None else _i32(exclude_prompt, "exclude_prompt")), n_lex,
+        _ptr(None if exclude_prompt is None else _i32(exclude_prompt, "exclude_prompt")),
+        _ptr(None if hist is None else _i32(hist, "hist")),
+        _ptr(None if hist_len is None else _i32(hist_len, "hist_len")), H, n_lex,
         L_lex, min_match, max_cand, _ptr(workspace), workspace.numel() * workspace.element_size(),
         _ptr(_i32(lex_tokens, "lex_tokens")), _ptr(_i32(lex_len, "lex_len")),
         _ptr(None if lex_capped is None else _i32(lex_capped, "lex_capped")), _stream(stream)))
@@ -381,16 +389,19 @@ class Pool:
         return scores, idx
 
     def lexical(self, ctx, ctx_len, n_lex, L_lex, exclude_prompt=None, min_match=2,
-                max_cand=None, stream=None, out=None, capped=None):
+                max_cand=None, stream=None, out=None, capped=None, hist=None, hist_len=None):
         """Exact-suffix lexical drafts: (tokens (B, n_lex, L_lex), lengths (B, n_lex)).
-        ``capped``, a (B,) int32 device tensor or None, receives the capacity flags."""
+        ``capped``, a (B,) int32 device tensor or None, receives the capacity flags;
+        ``hist`` (B, H) / ``hist_len`` (B,), device int32 or None, the requests'
+        own committed tokens."""
         B = ctx.shape[0]
         max_cand = LEX_MAX_CAND if max_cand is None else max_cand
-        key = ("lex", B, max_cand)
+        H = 0 if hist is None else hist.shape[1]
+        key = ("lex", B, max_cand, H)
         if key not in self._ws:
-            nb = lexical_workspace_bytes(self.handle, B, max_cand)
+            nb = lexical_workspace_bytes(self.handle, B, max_cand, H)
             if nb == 0:
-                raise ValueError(f"unsupported lexical batch/capacity: B={B} max_cand={max_cand}")
+                raise ValueError(f"unsupported lexical batch/capacity/history: B={B} max_cand={max_cand} H={H}")
             self._ws[key] = torch.empty((nb,), dtype=torch.uint8, device=self.device)
         if out is None:
             lt = torch.empty((B, n_lex, L_lex), dtype=torch.int32, device=self.device)
@@ -398,7 +409,8 @@ class Pool:
         else:
             lt, ll = out
         lexical_drafts(self.handle, ctx, ctx_len, n_lex, L_lex, self._ws[key], lt, ll,
-                       exclude_prompt, min_match, max_cand, stream, lex_capped=capped)
+                       exclude_prompt, min_match, max_cand, stream, lex_capped=capped, hist=hist,
+                       hist_len=hist_len)
         return lt, ll
 
     def gather(self, idx, scores, rule: DepthRule, L, stream=None, out=None):

@@ -421,15 +421,17 @@ int32_t oil_gather_continuations(const oil_pool* pool, const int32_t* idx, const
                                          r, L, chain_tokens, chain_len, (hipStream_t)stream));
 }
 
-size_t oil_lexical_workspace_bytes(const oil_pool* pool, int32_t B, int32_t max_cand)
+size_t oil_lexical_workspace_bytes(const oil_pool* pool, int32_t B, int32_t max_cand, int32_t H)
 {
-    if (!pool || B < 1 || B > OIL_MAX_B || max_cand < 1 || max_cand > OIL_LEX_MAX_CAND)
+    if (!pool || B < 1 || B > OIL_MAX_B || max_cand < 1 || max_cand > OIL_LEX_MAX_CAND || H < 0 ||
+        H > OIL_LEX_MAX_HIST)
         return 0;
-    return oil::lexical_workspace_bytes(pool->capacity, B, max_cand);
+    return oil::lexical_workspace_bytes(pool->capacity, B, max_cand, H);
 }
 
 int32_t oil_lexical_drafts(const oil_pool* pool, const int32_t* ctx, const int32_t* ctx_len, int32_t C,
-                           int32_t B, const int32_t* exclude_prompt, int32_t n_lex, int32_t L_lex,
+                           int32_t B, const int32_t* exclude_prompt, const int32_t* hist,
+                           const int32_t* hist_len, int32_t H, int32_t n_lex, int32_t L_lex,
                            int32_t min_match, int32_t max_cand, void* workspace,
                            size_t workspace_bytes, int32_t* lex_tokens, int32_t* lex_len, int32_t* lex_capped,
                            void* stream)
@@ -439,16 +441,21 @@ int32_t oil_lexical_drafts(const oil_pool* pool, const int32_t* ctx, const int32
         return OIL_E_INVALID;
     if (exclude_prompt && !pool->prompts)
         return OIL_E_INVALID;
+    if (!hist)
+        H = 0;  // no history: H is ignored
+    else if (!hist_len || H < 1)
+        return OIL_E_INVALID;
     if (C > OIL_LEX_MAX_CTX || B > OIL_MAX_B || n_lex > OIL_LEX_MAX_N || L_lex > OIL_LEX_MAX_LEN ||
-        min_match > OIL_LEX_MAX_CTX || max_cand > OIL_LEX_MAX_CAND)
+        min_match > OIL_LEX_MAX_CTX || max_cand > OIL_LEX_MAX_CAND || H > OIL_LEX_MAX_HIST ||
+        pool->n_valid + (int64_t)H > (int64_t)INT32_MAX)
         return OIL_E_UNSUPPORTED;
-    if (!workspace || workspace_bytes < oil::lexical_workspace_bytes(pool->capacity, B, max_cand) ||
+    if (!workspace || workspace_bytes < oil::lexical_workspace_bytes(pool->capacity, B, max_cand, H) ||
         !aligned(workspace, kAlign))
         return OIL_E_WORKSPACE;
     return hip_status(oil::launch_lexical(pool->tokens, pool->traces, pool->prompts, pool->n_valid, ctx,
-                                          ctx_len, C, B, exclude_prompt, n_lex, L_lex, min_match,
-                                          max_cand, workspace, pool->capacity, lex_tokens, lex_len,
-                                          lex_capped, (hipStream_t)stream));
+                                          ctx_len, C, B, exclude_prompt, hist, hist_len, H, n_lex, L_lex,
+                                          min_match, max_cand, workspace, pool->capacity, lex_tokens,
+                                          lex_len, lex_capped, (hipStream_t)stream));
 }
 
 int32_t oil_tree_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,

@@ -94,12 +94,13 @@ hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tok
 
 hipError_t launch_tree_mask(int32_t B, int32_t max_nodes, const int32_t* node_parent,
                             const int32_t* n_nodes, uint32_t* mask, hipStream_t stream);
-size_t lexical_workspace_bytes(int64_t capacity, int32_t B, int32_t max_cand);
+size_t lexical_workspace_bytes(int64_t capacity, int32_t B, int32_t max_cand, int32_t Hh);
 hipError_t launch_lexical(const int32_t* tokens, const int32_t* traces, const int32_t* prompts,
                           int64_t n_valid, const int32_t* ctx, const int32_t* ctx_len, int32_t C,
-                          int32_t B, const int32_t* exclude, int32_t n_lex, int32_t L_lex,
-                          int32_t min_match, int32_t max_cand, void* workspace, int64_t capacity,
-                          int32_t* lex_tokens, int32_t* lex_len, int32_t* lex_capped, hipStream_t stream);
+                          int32_t B, const int32_t* exclude, const int32_t* hist, const int32_t* hist_len,
+                          int32_t Hh, int32_t n_lex, int32_t L_lex, int32_t min_match, int32_t max_cand,
+                          void* workspace, int64_t capacity, int32_t* lex_tokens, int32_t* lex_len,
+                          int32_t* lex_capped, hipStream_t stream);
 hipError_t launch_recycle_init(int64_t* head, hipStream_t stream);
 size_t recycle_insert_workspace_bytes(int32_t B, int32_t max_nodes);
 hipError_t launch_recycle_insert(int32_t B, int32_t max_nodes, const int32_t* node_token,

@@ -23,6 +23,11 @@
 //      the levels from m* down, adding each level's candidates to their
 //      group's count and earliest position and taking groups in (count desc,
 //      earliest asc) order with block-wide max reductions.
+// A request's own committed tokens (optional) are one more trace after the
+// pool: position n_valid + i is its i-th token.  They get chunks of their own
+// after the pool's, one workgroup per (chunk, request) in the histogram and
+// collect launches (lex_self_hist_kernel, lex_self_collect_kernel), so the
+// plan's scan and the position-ordered candidate list cover them unchanged.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -167,7 +172,7 @@ __global__ __launch_bounds__(kLexThreads) void lex_hist_kernel(
     const int32_t* __restrict__ tokens, const int32_t* __restrict__ traces,
     const int32_t* __restrict__ prompts, int64_t n_valid, const int32_t* __restrict__ ctx,
     const int32_t* __restrict__ ctx_len, int32_t C, int32_t B, const int32_t* __restrict__ exclude,
-    int32_t min_match, int32_t* __restrict__ H, int32_t n_chunks)
+    int32_t min_match, int32_t* __restrict__ H, int32_t n_tot)
 {
     __shared__ LexScanShared s;
     __shared__ int32_t hist[kLexGroup][kLexLevels];
@@ -210,8 +215,100 @@ __global__ __launch_bounds__(kLexThreads) void lex_hist_kernel(
     // chunk-major: H[b][c][m], one contiguous run of levels per request
     for (int e = t; e < G * kLexLevels; e += kLexThreads) {
         const int g = e / kLexLevels, m = e % kLexLevels;
-        H[((int64_t)(g0 + g) * n_chunks + c) * kLexHistLd + m] = hist[g][m];
+        H[((int64_t)(g0 + g) * n_tot + c) * kLexHistLd + m] = hist[g][m];
     }
+}
+
+// Request b's own committed tokens: the row, its clamped length, and its
+// context (rc[j] = j-th most recent token) staged for the walk back.
+struct LexSelfShared {
+    int32_t rc[OIL_LEX_CTX_MAX];
+    int32_t cl;
+};
+
+__device__ inline void lex_self_stage(LexSelfShared& s, const int32_t* __restrict__ ctx,
+                                      const int32_t* __restrict__ ctx_len, int32_t C, int b)
+{
+    const int t = threadIdx.x;
+    if (t < OIL_LEX_CTX_MAX)
+        s.rc[t] = t < C ? ctx[(int64_t)b * C + (C - 1 - t)] : -1;
+    if (t == 0) {
+        const int c = ctx_len[b];
+        s.cl = c < 0 ? 0 : (c > C ? C : c);
+    }
+    __syncthreads();
+}
+
+__device__ inline int32_t lex_self_len(const int32_t* __restrict__ hist_len, int32_t Hh, int b)
+{
+    const int32_t hl = hist_len[b];
+    return hl < 0 ? 0 : (hl > Hh ? Hh : hl);
+}
+
+// Match length of history index q (its token equal to the context's last),
+// or 0 when q is not a candidate (short match, nothing after it).  The walk
+// stays inside the row, which is one trace; no prompt excludes it.
+__device__ inline int lex_self_candidate(const LexSelfShared& s, const int32_t* __restrict__ row, int32_t hl,
+                                         int32_t q, int32_t min_match)
+{
+    const int cl = s.cl;
+    int m = 1;
+    for (int m0 = 1; m0 < cl; m0 += 16) {
+        int32_t tk[16];
+#pragma unroll
+        for (int u = 0; u < 16; u++) {
+            const int32_t i = q - m0 - u;
+            tk[u] = row[i >= 0 ? i : 0];  // clamped, unconditional
+        }
+#pragma unroll
+        for (int u = 0; u < 16; u++) {
+            const bool in = m0 + u < cl && q - m0 - u >= 0;
+            const int at = min(m0 + u, OIL_LEX_CTX_MAX - 1);
+            if (in && m == m0 + u && tk[u] == s.rc[at])
+                m++;
+        }
+        if (m < m0 + 16)
+            break;
+    }
+    return (m >= min_match && q + 1 < hl) ? m : 0;
+}
+
+// Histogram rows of the history chunks: one workgroup per (chunk, request),
+// written after the request's n_chunks pool rows.
+__global__ __launch_bounds__(kLexThreads) void lex_self_hist_kernel(
+    const int32_t* __restrict__ hist, const int32_t* __restrict__ hist_len, int32_t Hh,
+    const int32_t* __restrict__ ctx, const int32_t* __restrict__ ctx_len, int32_t C, int32_t min_match,
+    int32_t* __restrict__ H, int32_t n_chunks, int32_t n_tot)
+{
+    __shared__ LexSelfShared s;
+    __shared__ int32_t h[kLexLevels];
+    const int t = threadIdx.x, ch = blockIdx.x, b = blockIdx.y;
+    const int32_t hl = lex_self_len(hist_len, Hh, b);
+    const int32_t base = ch * kLexChunk;
+    const int32_t* row = hist + (int64_t)b * Hh;
+    if (t < kLexLevels)
+        h[t] = 0;
+    lex_self_stage(s, ctx, ctx_len, C, b);
+    if (s.cl >= min_match && base < hl) {
+        int32_t tk[kLexPerThread];
+#pragma unroll
+        for (int j = 0; j < kLexPerThread; j++) {
+            const int32_t q = base + j * kLexThreads + t;
+            tk[j] = row[q < hl ? q : hl - 1];
+        }
+        const int32_t last = s.rc[0];
+        for (int j = 0; j < kLexPerThread; j++) {
+            const int32_t q = base + j * kLexThreads + t;
+            if (q + 1 < hl && tk[j] == last) {
+                const int m = lex_self_candidate(s, row, hl, q, min_match);
+                if (m)
+                    atomicAdd(&h[m], 1);
+            }
+        }
+    }
+    __syncthreads();
+    if (t < kLexLevels)
+        H[((int64_t)b * n_tot + n_chunks + ch) * kLexHistLd + t] = h[t];
 }
 
 // Chunk c's histogram row, levels below `from` (and chunks past the end) as 0:
@@ -348,7 +445,7 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
     const int32_t* __restrict__ tokens, const int32_t* __restrict__ traces,
     const int32_t* __restrict__ prompts, int64_t n_valid, const int32_t* __restrict__ ctx,
     const int32_t* __restrict__ ctx_len, int32_t C, int32_t B, const int32_t* __restrict__ exclude,
-    int32_t min_match, const int32_t* __restrict__ plan, const int32_t* __restrict__ off, int32_t n_chunks,
+    int32_t min_match, const int32_t* __restrict__ plan, const int32_t* __restrict__ off, int32_t n_tot,
     int32_t max_cand, int32_t* __restrict__ cand_p, int32_t* __restrict__ cand_m)
 {
     __shared__ LexScanShared s;
@@ -370,7 +467,7 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
     int32_t lo_t = kLexLevels;
     bool busy = false;
     if (t < G) {
-        const int32_t* ob = off + (int64_t)(g0 + t) * (n_chunks + 1);
+        const int32_t* ob = off + (int64_t)(g0 + t) * (n_tot + 1);
         lo_t = plan[kPlan * (g0 + t) + 1];
         busy = ob[c + 1] > ob[c];
     }
@@ -435,7 +532,7 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
             const uint32_t r = list[e];
             const int q = (int)(r >> 12), g = (int)((r >> 6) & 63u), m = (int)(r & 63u);
             const uint32_t word = bm[g][q >> 5];
-            const int64_t at = (int64_t)off[(int64_t)(g0 + g) * (n_chunks + 1) + c] + wpre[g][q >> 5] +
+            const int64_t at = (int64_t)off[(int64_t)(g0 + g) * (n_tot + 1) + c] + wpre[g][q >> 5] +
                                __popc(word & ((1u << (q & 31)) - 1u));
             if (at < max_cand) {
                 cand_p[(int64_t)(g0 + g) * max_cand + at] = (int32_t)(base + q);
@@ -458,12 +555,79 @@ __global__ __launch_bounds__(kLexThreads) void lex_collect_kernel(
             if (!((word >> (q & 31)) & 1u))
                 continue;
             const int m = lex_candidate(s, g, p, n_valid, tokens, traces, prompts, min_match);
-            const int64_t at = (int64_t)off[(int64_t)(g0 + g) * (n_chunks + 1) + c] + wpre[g][q >> 5] +
+            const int64_t at = (int64_t)off[(int64_t)(g0 + g) * (n_tot + 1) + c] + wpre[g][q >> 5] +
                                __popc(word & ((1u << (q & 31)) - 1u));
             if (at < max_cand) {
                 cand_p[(int64_t)(g0 + g) * max_cand + at] = (int32_t)p;
                 cand_m[(int64_t)(g0 + g) * max_cand + at] = m;
             }
+        }
+    }
+}
+
+// The kept candidates of one history chunk of request b, in position order,
+// at the list offset the plan gave the chunk.
+__global__ __launch_bounds__(kLexThreads) void lex_self_collect_kernel(
+    const int32_t* __restrict__ hist, const int32_t* __restrict__ hist_len, int32_t Hh,
+    const int32_t* __restrict__ ctx, const int32_t* __restrict__ ctx_len, int32_t C, int32_t min_match,
+    const int32_t* __restrict__ plan, const int32_t* __restrict__ off, int32_t n_chunks, int32_t n_tot,
+    int64_t n_valid, int32_t max_cand, int32_t* __restrict__ cand_p, int32_t* __restrict__ cand_m)
+{
+    __shared__ LexSelfShared s;
+    __shared__ uint32_t bm[kLexWords];
+    __shared__ int32_t wpre[kLexWords];
+    const int t = threadIdx.x, ch = blockIdx.x, b = blockIdx.y, lane = t & (kWave - 1);
+    const int32_t* ob = off + (int64_t)b * (n_tot + 1) + n_chunks + ch;
+    const int32_t first = ob[0];
+    if (ob[1] == first)  // nothing kept here (or the capacity is full): uniform exit
+        return;
+    const int32_t lo = plan[kPlan * b + 1];
+    const int32_t hl = lex_self_len(hist_len, Hh, b);
+    const int32_t base = ch * kLexChunk;
+    const int32_t* row = hist + (int64_t)b * Hh;
+    for (int e = t; e < kLexWords; e += kLexThreads)
+        bm[e] = 0u;
+    lex_self_stage(s, ctx, ctx_len, C, b);  // its barrier also orders the clear
+    const int32_t last = s.rc[0];
+    uint8_t mj[kLexPerThread];
+#pragma unroll
+    for (int j = 0; j < kLexPerThread; j++) {
+        const int32_t q = base + j * kLexThreads + t;
+        mj[j] = 0;
+        if (q + 1 < hl && row[q] == last) {
+            const int m = lex_self_candidate(s, row, hl, q, min_match);
+            if (m && m >= lo) {
+                mj[j] = (uint8_t)m;
+                const int i = j * kLexThreads + t;
+                atomicOr(&bm[i >> 5], 1u << (i & 31));
+            }
+        }
+    }
+    __syncthreads();
+    if (t < kWave) {
+        // exclusive popcount prefix over the chunk's 128 words, two per lane
+        const int32_t a = __popc(bm[2 * lane]), c2 = __popc(bm[2 * lane + 1]);
+        int32_t incl = a + c2;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int32_t u = __shfl_up(incl, o, kWave);
+            if (lane >= o)
+                incl += u;
+        }
+        wpre[2 * lane] = incl - a - c2;
+        wpre[2 * lane + 1] = incl - c2;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kLexPerThread; j++) {
+        if (!mj[j])
+            continue;
+        const int i = j * kLexThreads + t;
+        const int64_t at =
+            (int64_t)first + wpre[i >> 5] + __popc(bm[i >> 5] & ((1u << (i & 31)) - 1u));
+        if (at < max_cand) {
+            cand_p[(int64_t)b * max_cand + at] = (int32_t)(n_valid + base + i);
+            cand_m[(int64_t)b * max_cand + at] = mj[j];
         }
     }
 }
@@ -500,8 +664,38 @@ __device__ inline uint32_t lex_draft(const int32_t* __restrict__ tokens, const i
     return h ? h : 1u;  // 0 marks an empty slot
 }
 
-// Do the drafts after p and q (both of length len >= 1) hold the same tokens?
-__device__ inline bool lex_same_draft(const int32_t* __restrict__ tokens, int64_t p, int64_t q, int len)
+// The same length and hash for a draft read from a flat run of `avail >= 1`
+// tokens (a request's own committed tokens after history index q).
+__device__ inline uint32_t lex_draft_flat(const int32_t* __restrict__ src, int32_t avail, int32_t L_lex,
+                                          int& len_out)
+{
+    const int len = avail < L_lex ? avail : L_lex;
+    uint32_t h = 0x811C9DC5u;
+    for (int j0 = 0; j0 < len; j0 += 16) {
+        int32_t tk[16];
+#pragma unroll
+        for (int u = 0; u < 16; u++)
+            tk[u] = src[min(j0 + u, len - 1)];  // in range: repeats the last token
+#pragma unroll
+        for (int u = 0; u < 16; u++)
+            if (j0 + u < len)
+                h = (h ^ (uint32_t)tk[u]) * 0x01000193u;
+    }
+    len_out = len;
+    h = mix32(h ^ ((uint32_t)len * 0x9E3779B9u));
+    return h ? h : 1u;
+}
+
+// Where the draft after candidate position p starts: the pool, or request
+// b's own tokens for p >= n_valid.
+__device__ inline const int32_t* lex_draft_src(const int32_t* __restrict__ tokens, int64_t n_valid,
+                                               const int32_t* __restrict__ hrow, int64_t p)
+{
+    return p < n_valid ? tokens + p + 1 : hrow + (p - n_valid) + 1;
+}
+
+// Do two drafts (both of length len >= 1) hold the same tokens?
+__device__ inline bool lex_same_draft(const int32_t* __restrict__ a, const int32_t* __restrict__ b, int len)
 {
     bool same = true;
     for (int j0 = 0; j0 < len && same; j0 += 16) {
@@ -509,7 +703,7 @@ __device__ inline bool lex_same_draft(const int32_t* __restrict__ tokens, int64_
 #pragma unroll
         for (int u = 0; u < 16; u++) {
             const int j = min(j0 + u, len - 1);  // in range: repeats the last token
-            blk &= tokens[p + 1 + j] == tokens[q + 1 + j];
+            blk &= a[j] == b[j];
         }
         same = blk;
     }
@@ -518,6 +712,7 @@ __device__ inline bool lex_same_draft(const int32_t* __restrict__ tokens, int64_
 
 __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
     const int32_t* __restrict__ tokens, const int32_t* __restrict__ traces, int64_t n_valid,
+    const int32_t* __restrict__ hist, const int32_t* __restrict__ hist_len, int32_t Hh,
     const int32_t* __restrict__ cand_p, const int32_t* __restrict__ cand_m, int32_t max_cand,
     const int32_t* __restrict__ plan, int32_t n_lex, int32_t L_lex, int32_t* __restrict__ lex_tokens,
     int32_t* __restrict__ lex_len, int32_t* __restrict__ lex_capped)
@@ -544,6 +739,8 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
     }
     const int32_t* cp = cand_p + (int64_t)b * max_cand;
     const int32_t* cm = cand_m + (int64_t)b * max_cand;
+    const int32_t* hrow = hist ? hist + (int64_t)b * Hh : tokens;  // read only for p >= n_valid
+    const int32_t hl = hist ? lex_self_len(hist_len, Hh, b) : 0;
     for (int e = t; e < kSelTable; e += kSelThreads) {
         tab_h[e] = 0u;
         tab_first[e] = 0x7FFFFFFF;
@@ -565,7 +762,9 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
         if (i < n) {
             p[r] = cp[i];
             m[r] = cm[i];
-            h[r] = lex_draft(tokens, traces, n_valid, p[r], L_lex, len[r]);
+            h[r] = p[r] < n_valid ? lex_draft(tokens, traces, n_valid, p[r], L_lex, len[r])
+                                  : lex_draft_flat(hrow + (p[r] - n_valid) + 1,
+                                                   hl - (int32_t)(p[r] - n_valid) - 1, L_lex, len[r]);
             lens[i] = (uint8_t)len[r];
             pos[i] = (int32_t)p[r];
         } else {
@@ -600,15 +799,16 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
         // the group of a draft is named by its earliest candidate; every
         // candidate with the same draft has the same hash, hence the same slot
         const int j = tab_first[slot[r]];
+        const int32_t* mine = lex_draft_src(tokens, n_valid, hrow, p[r]);
         if (j == i) {
             rep[r] = i;
-        } else if (lens[j] == len[r] && lex_same_draft(tokens, p[r], pos[j], len[r])) {
+        } else if (lens[j] == len[r] && lex_same_draft(mine, lex_draft_src(tokens, n_valid, hrow, pos[j]), len[r])) {
             rep[r] = j;
         } else {
             // a hash collision: the earliest candidate with the same draft
             rep[r] = i;
             for (int k = 0; k < i; k++) {
-                if (lens[k] == len[r] && lex_same_draft(tokens, p[r], pos[k], len[r])) {
+                if (lens[k] == len[r] && lex_same_draft(mine, lex_draft_src(tokens, n_valid, hrow, pos[k]), len[r])) {
                     rep[r] = k;
                     break;
                 }
@@ -659,8 +859,9 @@ __global__ __launch_bounds__(kSelThreads) void lex_select_kernel(
                 if (key[r] == best) {
                     held[r] = true;
                     int32_t* out = lex_tokens + ((int64_t)b * n_lex + n_held) * L_lex;
+                    const int32_t* src = lex_draft_src(tokens, n_valid, hrow, p[r]);
                     for (int e = 0; e < L_lex; e++)
-                        out[e] = e < len[r] ? tokens[p[r] + 1 + e] : -1;
+                        out[e] = e < len[r] ? src[e] : -1;
                     lex_len[(int64_t)b * n_lex + n_held] = len[r];
                 }
             }
@@ -686,9 +887,10 @@ struct LexWorkspace {
     size_t h_off, o_off, plan_off, p_off, m_off, total;
 };
 
-LexWorkspace lex_carve(int64_t capacity, int32_t B, int32_t max_cand)
+LexWorkspace lex_carve(int64_t capacity, int32_t B, int32_t max_cand, int32_t Hh)
 {
-    const size_t chunks = (size_t)(lex_chunks(capacity) > 0 ? lex_chunks(capacity) : 1);
+    const int64_t rows = (int64_t)lex_chunks(capacity) + lex_chunks(Hh);
+    const size_t chunks = (size_t)(rows > 0 ? rows : 1);
     LexWorkspace w;
     w.h_off = 0;
     w.o_off = align256(w.h_off + (size_t)B * chunks * kLexHistLd * sizeof(int32_t));
@@ -701,18 +903,21 @@ LexWorkspace lex_carve(int64_t capacity, int32_t B, int32_t max_cand)
 
 }  // namespace
 
-size_t lexical_workspace_bytes(int64_t capacity, int32_t B, int32_t max_cand)
+size_t lexical_workspace_bytes(int64_t capacity, int32_t B, int32_t max_cand, int32_t Hh)
 {
-    return lex_carve(capacity, B, max_cand).total;
+    return lex_carve(capacity, B, max_cand, Hh).total;
 }
 
 hipError_t launch_lexical(const int32_t* tokens, const int32_t* traces, const int32_t* prompts,
                           int64_t n_valid, const int32_t* ctx, const int32_t* ctx_len, int32_t C,
-                          int32_t B, const int32_t* exclude, int32_t n_lex, int32_t L_lex,
-                          int32_t min_match, int32_t max_cand, void* workspace, int64_t capacity,
-                          int32_t* lex_tokens, int32_t* lex_len, int32_t* lex_capped, hipStream_t stream)
+                          int32_t B, const int32_t* exclude, const int32_t* hist, const int32_t* hist_len,
+                          int32_t Hh, int32_t n_lex, int32_t L_lex, int32_t min_match, int32_t max_cand,
+                          void* workspace, int64_t capacity, int32_t* lex_tokens, int32_t* lex_len,
+                          int32_t* lex_capped, hipStream_t stream)
 {
-    const LexWorkspace w = lex_carve(capacity, B, max_cand);
+    if (!hist)
+        Hh = 0;
+    const LexWorkspace w = lex_carve(capacity, B, max_cand, Hh);
     char* ws = (char*)workspace;
     int32_t* H = (int32_t*)(ws + w.h_off);
     int32_t* off = (int32_t*)(ws + w.o_off);
@@ -720,29 +925,43 @@ hipError_t launch_lexical(const int32_t* tokens, const int32_t* traces, const in
     int32_t* cp = (int32_t*)(ws + w.p_off);
     int32_t* cm = (int32_t*)(ws + w.m_off);
     const int32_t n_chunks = lex_chunks(n_valid);
+    const int32_t n_self = lex_chunks(Hh);        // history chunks, per request
+    const int32_t n_tot = n_chunks + n_self;      // histogram rows per request
     const int groups = (B + kLexGroup - 1) / kLexGroup;
+    hipError_t e = hipSuccess;
     if (n_chunks > 0) {
         hipLaunchKernelGGL(lex_hist_kernel, dim3(n_chunks, groups), dim3(kLexThreads), 0, stream, tokens,
-                           traces, prompts, n_valid, ctx, ctx_len, C, B, exclude, min_match, H, n_chunks);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess)
+                           traces, prompts, n_valid, ctx, ctx_len, C, B, exclude, min_match, H, n_tot);
+        if ((e = hipGetLastError()) != hipSuccess)
             return e;
     }
-    hipLaunchKernelGGL(lex_plan_kernel, dim3(B), dim3(kLexThreads), 0, stream, H, n_chunks, min_match,
+    if (n_self > 0) {
+        hipLaunchKernelGGL(lex_self_hist_kernel, dim3(n_self, B), dim3(kLexThreads), 0, stream, hist, hist_len,
+                           Hh, ctx, ctx_len, C, min_match, H, n_chunks, n_tot);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    hipLaunchKernelGGL(lex_plan_kernel, dim3(B), dim3(kLexThreads), 0, stream, H, n_tot, min_match,
                        max_cand, off, plan);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
+    if ((e = hipGetLastError()) != hipSuccess)
         return e;
     if (n_chunks > 0) {
         hipLaunchKernelGGL(lex_collect_kernel, dim3(n_chunks, groups), dim3(kLexThreads), 0, stream, tokens,
                            traces, prompts, n_valid, ctx, ctx_len, C, B, exclude, min_match, plan, off,
-                           n_chunks, max_cand, cp, cm);
-        e = hipGetLastError();
-        if (e != hipSuccess)
+                           n_tot, max_cand, cp, cm);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    if (n_self > 0) {
+        hipLaunchKernelGGL(lex_self_collect_kernel, dim3(n_self, B), dim3(kLexThreads), 0, stream, hist,
+                           hist_len, Hh, ctx, ctx_len, C, min_match, plan, off, n_chunks, n_tot, n_valid,
+                           max_cand, cp, cm);
+        if ((e = hipGetLastError()) != hipSuccess)
             return e;
     }
     hipLaunchKernelGGL(lex_select_kernel, dim3(B), dim3(kSelThreads), 0, stream, tokens, traces, n_valid,
-                       cp, cm, max_cand, plan, n_lex, L_lex, lex_tokens, lex_len, lex_capped);
+                       hist, hist_len, Hh, cp, cm, max_cand, plan, n_lex, L_lex, lex_tokens, lex_len,
+                       lex_capped);
     return hipGetLastError();
 }
 

@@ -156,20 +156,24 @@ def test_lexical_validates(L):
     h = ctypes.c_void_p()
     P = f.aligned
     assert L.oil_pool_create(16, 10000, P, P, P, None, ctypes.byref(h)) == 0
-    assert L.oil_lexical_workspace_bytes(h, 0, 64) == 0
-    assert L.oil_lexical_workspace_bytes(h, 513, 64) == 0
-    assert L.oil_lexical_workspace_bytes(h, 4, 0) == 0
-    assert L.oil_lexical_workspace_bytes(h, 4, 4097) == 0
-    ws = L.oil_lexical_workspace_bytes(h, 4, 64)
+    assert L.oil_lexical_workspace_bytes(h, 0, 64, 0) == 0
+    assert L.oil_lexical_workspace_bytes(h, 513, 64, 0) == 0
+    assert L.oil_lexical_workspace_bytes(h, 4, 0, 0) == 0
+    assert L.oil_lexical_workspace_bytes(h, 4, 4097, 0) == 0
+    assert L.oil_lexical_workspace_bytes(h, 4, 64, -1) == 0
+    assert L.oil_lexical_workspace_bytes(h, 4, 64, (1 << 20) + 1) == 0
+    ws = L.oil_lexical_workspace_bytes(h, 4, 64, 0)
     assert ws > 0 and ws % 256 == 0
-    assert L.oil_lexical_workspace_bytes(h, 4, 4096) > ws
-    # (pool, ctx, ctx_len, C, B, exclude, n_lex, L_lex, min_match, max_cand, ws, ws_bytes, tok, len,
-    #  capped, stream)
-    ok = (h, P, P, 16, 4, None, 4, 12, 2, 64, P, ws, P, P, None, None)
+    assert L.oil_lexical_workspace_bytes(h, 4, 4096, 0) > ws
+    ws_h = L.oil_lexical_workspace_bytes(h, 4, 64, 5000)   # two history chunks per request
+    assert ws_h > ws and ws_h % 256 == 0
+    # (pool, ctx, ctx_len, C, B, exclude, hist, hist_len, H, n_lex, L_lex, min_match, max_cand, ws,
+    #  ws_bytes, tok, len, capped, stream)
+    ok = (h, P, P, 16, 4, None, None, None, 0, 4, 12, 2, 64, P, ws, P, P, None, None)
 
     def call(**kw):
-        names = ["pool", "ctx", "ctx_len", "C", "B", "exclude", "n_lex", "L_lex", "min_match",
-                 "max_cand", "ws", "ws_bytes", "tok", "len", "capped", "stream"]
+        names = ["pool", "ctx", "ctx_len", "C", "B", "exclude", "hist", "hist_len", "H", "n_lex", "L_lex",
+                 "min_match", "max_cand", "ws", "ws_bytes", "tok", "len", "capped", "stream"]
         a = dict(zip(names, ok))
         a.update(kw)
         return L.oil_lexical_drafts(*[a[n] for n in names])
@@ -191,6 +195,11 @@ def test_lexical_validates(L):
     assert call(ws_bytes=ws - 1) == -5
     assert call(ws=f.misaligned) == -5
     assert call(ws=None) == -5
+    assert call(hist=P, hist_len=None, H=100) == -1       # lengths required with a history
+    assert call(hist=P, hist_len=P, H=0) == -1
+    assert call(hist=P, hist_len=P, H=(1 << 20) + 1) == -3
+    assert call(hist=P, hist_len=P, H=5000) == -5          # the workspace must cover the history rows
+    assert call(hist=P, hist_len=P, H=5000, ws_bytes=ws_h - 1) == -5
     assert L.oil_pool_destroy(h) == 0
 
 

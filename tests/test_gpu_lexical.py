@@ -66,13 +66,16 @@ def _contexts(rng, tok, B, C, vocab):
     return ctx, cl
 
 
-def _compare(oil, pool, tok, tr, pr, ctx, cl, n_lex, L_lex, excl, mm, cap, with_flag=False):
+def _compare(oil, pool, tok, tr, pr, ctx, cl, n_lex, L_lex, excl, mm, cap, with_flag=False, hist=None,
+             hist_len=None):
     fl = torch.full((ctx.shape[0],), 7, dtype=torch.int32, device="cuda")
     lt, ll = pool.lexical(_cu(ctx), _cu(cl), n_lex, L_lex,
-                          None if excl is None else _cu(excl), mm, cap, capped=fl)
+                          None if excl is None else _cu(excl), mm, cap, capped=fl,
+                          hist=None if hist is None else _cu(hist),
+                          hist_len=None if hist is None else _cu(hist_len))
     torch.cuda.synchronize()
     et, el, ef = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, excl, mm, cap,
-                                       with_capped=True)
+                                       with_capped=True, hist=hist, hist_len=hist_len)
     assert np.array_equal(ll.cpu().numpy(), el)
     assert np.array_equal(lt.cpu().numpy(), et)
     assert np.array_equal(fl.cpu().numpy(), ef)
@@ -215,3 +218,142 @@ def test_full_step_8192_contexts(oil):
     b = pool.lexical(_cu(ctx.numpy()), _cu(cl.numpy()), cfg["n_lex"], cfg["L_lex"], _cu(ex.numpy()))
     torch.cuda.synchronize()
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def _histories(rng, B, H, vocab, tok=None):
+    """Request histories: ragged lengths (empty, short, the whole row, past
+    it, negative), tokens random (half of the rows over symbols the pool
+    lacks, so their contexts match only there) or copied out of the pool."""
+    hist = rng.integers(0, vocab, (B, H)).astype(np.int32)
+    hist[1::2] += vocab
+    hl = rng.integers(0, H + 1, B).astype(np.int32)
+    hl[0] = 0
+    if B > 1:
+        hl[1] = H
+    if B > 2:
+        hl[2] = H + 17                    # clamped to H
+    if B > 3:
+        hl[3] = -5                        # none
+    for b in range(B):
+        w = min(64, H)
+        if tok is not None and len(tok) > w and rng.random() < 0.3:
+            s0 = int(rng.integers(0, len(tok) - w))
+            hist[b, :w] = tok[s0:s0 + w]
+    return hist, hl
+
+
+def _own_tail_contexts(rng, ctx, cl, hist, hl, C):
+    """Every other request's context is the tail of its own history (the
+    usual case: the context is what the request just committed)."""
+    ctx, cl = ctx.copy(), cl.copy()
+    for b in range(ctx.shape[0]):
+        if b % 4 == 0:
+            continue
+        h = int(min(max(hl[b], 0), hist.shape[1]))
+        c = min(h, C, int(rng.integers(1, C + 1)))
+        if c >= 1:
+            ctx[b] = -1
+            ctx[b, C - c:] = hist[b, h - c:h]
+            cl[b] = c
+    return ctx, cl
+
+
+@pytest.mark.parametrize("seed,n,vocab,B,C,H", [
+    (20, 300, 3, 5, 8, 40),
+    (21, 10007, 3, 70, 16, 9000),     # three pool chunks, three history chunks, two request groups
+    (22, 4096, 2, 16, 32, 4096),      # exactly one chunk of each
+    (23, 20000, 4, 40, 12, 700),
+])
+def test_history_random_bit_exact(oil, seed, n, vocab, B, C, H):
+    """Each request's own committed tokens indexed beside the pool: drafts,
+    lengths and capacity flags equal the oracle's bit for bit."""
+    rng = np.random.default_rng(seed)
+    tok, tr, pr = _random_pool(rng, n, vocab, int(rng.integers(5, 60)), prompts_per_trace=2)
+    pool = _pool(oil, tok, tr, pr)
+    used_hist = 0
+    for trial in range(4):
+        ctx, cl = _contexts(rng, tok, B, C, vocab)
+        hist, hl = _histories(rng, B, H, vocab, tok)
+        ctx, cl = _own_tail_contexts(rng, ctx, cl, hist, hl, C)
+        excl = rng.integers(-1, int(pr.max()) + 1, B).astype(np.int32) if trial % 2 else None
+        n_lex = int(rng.integers(1, 17))
+        L_lex = int(rng.choice([1, 3, 12, 64]))
+        mm = int(rng.integers(1, 4))
+        cap = int(rng.choice([1, 7, 100, 4096]))
+        _compare(oil, pool, tok, tr, pr, ctx, cl, n_lex, L_lex, excl, mm, cap, hist=hist, hist_len=hl)
+        # the history must have changed some request's drafts
+        et, el = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, excl, mm, cap)
+        ht, hl_ = oracle.lexical_drafts(tok, tr, pr, len(tok), ctx, cl, n_lex, L_lex, excl, mm, cap,
+                                        hist=hist, hist_len=hl)
+        used_hist += int((~(ht == et).all(axis=(1, 2))).sum())
+    assert used_hist > 0
+
+
+def test_history_golden(oil):
+    g = json.load(open(os.path.join(GOLDEN, "lexical_history.json")))
+    tok, tr, pr = (np.asarray(g["pool"][k], np.int32) for k in ("tokens", "traces", "prompts"))
+    pool = _pool(oil, tok, tr, pr)
+    H = g["H"]
+    for case in g["cases"]:
+        hist = np.full((1, H), -1, np.int32)
+        hist[0, :len(case["hist"])] = case["hist"]
+        hl = np.asarray([case.get("hist_len", len(case["hist"]))], np.int32)
+        C = len(case["ctx"])
+        lt, ll = pool.lexical(_cu(np.asarray([case["ctx"]], np.int32)), _cu(np.asarray([C], np.int32)),
+                              case["n_lex"], case["L_lex"], _cu(np.asarray([case["exclude_prompt"]], np.int32)),
+                              case["min_match"], 4096, hist=_cu(hist), hist_len=_cu(hl))
+        torch.cuda.synchronize()
+        lt, ll = lt.cpu().numpy()[0], ll.cpu().numpy()[0]
+        got = [lt[j, :ll[j]].tolist() for j in range(case["n_lex"]) if ll[j] > 0]
+        assert got == case["expect"], case["name"]
+
+
+def test_history_with_an_empty_pool(oil):
+    """Nothing stored yet: the drafts come from the requests' own tokens only
+    (prompt lookup), across several history chunks."""
+    rng = np.random.default_rng(31)
+    empty = _pool(oil, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32), capacity=64)
+    z = np.zeros(0, np.int32)
+    B, C, H = 9, 8, 12000
+    hist, hl = _histories(rng, B, H, 3)
+    ctx, cl = _own_tail_contexts(rng, *_contexts(rng, z, B, C, 3), hist, hl, C)
+    el = _compare(oil, empty, z, z, z, ctx, cl, 6, 10, None, 2, 4096, hist=hist, hist_len=hl)
+    assert (el > 0).sum() > 5
+
+
+def test_history_after_a_full_capacity(oil):
+    """A capacity the pool's own candidates fill: the history's candidates,
+    later in position order, are cut, and the flag says so."""
+    rng = np.random.default_rng(32)
+    tok, tr, pr = _random_pool(rng, 30000, 2, 200)
+    pool = _pool(oil, tok, tr, pr)
+    B, C, H = 6, 6, 5000
+    hist, hl = _histories(rng, B, H, 2)
+    ctx, cl = _own_tail_contexts(rng, *_contexts(rng, tok, B, C, 2), hist, hl, C)
+    for cap in (1, 50, 4096):
+        _, ef = _compare(oil, pool, tok, tr, pr, ctx, cl, 8, 5, None, 2, cap, with_flag=True, hist=hist,
+                         hist_len=hl)
+        if cap == 1:
+            assert ef.sum() > 0
+
+
+def test_history_on_the_full_step_contexts(oil):
+    """The full-step workload's pool and contexts with a 16,384-token history
+    per request (the tokens of one earlier trace of the request's kind of
+    call plus fresh ones): drafts equal the oracle's."""
+    cfg = workloads.FULL_STEP_8192
+    ps, qs = cfg["pool"], cfg["query"]
+    wp = workloads.Pool(ps)
+    _, src = workloads.queries(wp, qs)
+    ctx, cl, ex = workloads.lexical_contexts(wp, src, ps.n)
+    tok, tr, pr = wp.tokens.numpy(), wp.traces.numpy(), wp.prompts.numpy()
+    B, H = ctx.shape[0], 16384
+    rng = np.random.default_rng(33)
+    hist = np.empty((B, H), np.int32)
+    for b in range(B):
+        s0 = int(rng.integers(0, len(tok) - H))
+        hist[b] = tok[s0:s0 + H]
+    hl = rng.integers(H // 2, H + 1, B).astype(np.int32)
+    pool = _pool(oil, tok, tr, pr)
+    _compare(oil, pool, tok, tr, pr, ctx.numpy(), cl.numpy(), cfg["n_lex"], cfg["L_lex"], ex.numpy(), 2, 4096,
+             hist=hist, hist_len=hl)
