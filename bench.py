@@ -330,6 +330,16 @@ def main():
     torch.cuda.synchronize()
     extras["lexical_us"] = round(1e3 * e0.elapsed_time(e1) / K, 2)
     extras["mean_lexical_drafts"] = round(float((lex_out[1] > 0).float().sum(1).mean()), 2)
+    # the same with each request's own 4,096-8,192 committed tokens indexed too
+    lhs, lhl = (t.to(dev) for t in workloads.request_history(wp, last_src, len(pool), lctx.cpu(), lcl.cpu(),
+                                                               8192))
+    pool.lexical(lctx, lcl, 4, 12, lex_ex, out=lex_out, hist=lhs, hist_len=lhl)
+    e0.record()
+    for _ in range(K):
+        pool.lexical(lctx, lcl, 4, 12, lex_ex, out=lex_out, hist=lhs, hist_len=lhl)
+    e1.record()
+    torch.cuda.synchronize()
+    extras["lexical_hist8192_us"] = round(1e3 * e0.elapsed_time(e1) / K, 2)
     # the rejected-branch recycled pool: a ring of 65,536 records (512 MiB of
     # keys at d = 4096), filled from the last step's verified trees with
     # synthetic per-node verifier states, then timed insert and lookup calls
@@ -683,21 +693,23 @@ def other_workloads(args, oil, workloads, dev):
         q, src = workloads.queries(wp, workloads.QuerySpec(B=qsp.B, noise=qsp.noise, p_random=qsp.p_random,
                                                            seed=qsp.seed + 11 * t))
         ctx, cl, ex = workloads.lexical_contexts(wp, src, ps.n)
-        steps.append((q.contiguous(), workloads.anchors(wp, src).to(dev), ctx.to(dev), cl.to(dev), ex.to(dev)))
+        hs, hl = workloads.request_history(wp, src, ps.n, ctx, cl, cfg["hist"], seed=t)
+        steps.append((q.contiguous(), workloads.anchors(wp, src).to(dev), ctx.to(dev), cl.to(dev), ex.to(dev),
+                      hs.to(dev), hl.to(dev)))
     rule = oil.DepthRule.fixed(L)
     mx = 1 + lb + sb
 
     def full(t):
-        q, anc, ctx, cl, ex = steps[t]
-        lt, ll = pool.lexical(ctx, cl, n_lex, L_lex, ex)
+        q, anc, ctx, cl, ex, hs, hl = steps[t]
+        lt, ll = pool.lexical(ctx, cl, n_lex, L_lex, ex, hist=hs, hist_len=hl)
         s_, i_ = pool.query_topk(q, k, exclude_prompt=ex)
         c_, l_ = pool.gather(i_, s_, rule, L)
         oil.merge_trees(anc, lt, ll, lb, c_, l_, sb, mx)
 
     _timed(torch, full, range(W))
     ms = _timed(torch, full, range(W, W + K))
-    q, anc, ctx, cl, ex = steps[W]
-    lt, ll = pool.lexical(ctx, cl, n_lex, L_lex, ex)
+    q, anc, ctx, cl, ex, hs, hl = steps[W]
+    lt, ll = pool.lexical(ctx, cl, n_lex, L_lex, ex, hist=hs, hist_len=hl)
     s_, i_ = pool.query_topk(q, k, exclude_prompt=ex)
     c_, l_ = pool.gather(i_, s_, rule, L)
     tree = oil.merge_trees(anc, lt, ll, lb, c_, l_, sb, mx)
@@ -705,7 +717,8 @@ def other_workloads(args, oil, workloads, dev):
                              "latency_ms": _timed_events(torch, full, range(W, W + K)),
                              "merge": _merge_rate(torch, lambda: oil.merge_trees(anc, lt, ll, lb, c_, l_, sb, mx,
                                                                                  out=tree), qsp.B),
-                             "step": "lexical drafts + query top-32 + gather 12 + merge (48 + 16 nodes), B = 64"}
+                             "step": "lexical drafts (pool + 4,096-8,192 own tokens per request) + query top-32 "
+                                     "+ gather 12 + merge (48 + 16 nodes), B = 64"}
     log(f"full_step_8192: {ms:.3f} ms/step")
     del pool, wp
 
@@ -726,16 +739,17 @@ def other_workloads(args, oil, workloads, dev):
     q, src = workloads.queries(wp, workloads.QuerySpec(B=KP + W, noise=qsp.noise, p_random=qsp.p_random,
                                                        seed=qsp.seed))
     ctx, cl, ex = workloads.lexical_contexts(wp, src, ps.n)
+    hs, hl = workloads.request_history(wp, src, ps.n, ctx, cl, cfg["hist"])
     anc = workloads.anchors(wp, src)
     steps = [(q[t:t + 1].contiguous(), anc[t:t + 1].to(dev), ctx[t:t + 1].to(dev), cl[t:t + 1].to(dev),
-              ex[t:t + 1].to(dev)) for t in range(KP + W)]
+              ex[t:t + 1].to(dev), hs[t:t + 1].to(dev), hl[t:t + 1].to(dev)) for t in range(KP + W)]
     rule = oil.DepthRule.paper()
     mx = 1 + lb + sb
     bufs = {}
 
     def paper(t):
-        q1, a1, c1, l1, e1 = steps[t]
-        lt, ll = pool.lexical(c1, l1, n_lex, L_lex, e1, out=bufs.get("lex"))
+        q1, a1, c1, l1, e1, h1, hl1 = steps[t]
+        lt, ll = pool.lexical(c1, l1, n_lex, L_lex, e1, out=bufs.get("lex"), hist=h1, hist_len=hl1)
         bufs["lex"] = (lt, ll)
         s_, i_ = pool.query_topk(q1, k, exclude_prompt=e1, out=bufs.get("q"))
         bufs["q"] = (s_, i_)
@@ -755,9 +769,9 @@ def other_workloads(args, oil, workloads, dev):
     out["paper_320k"] = {"ms_per_step": round(ms, 4), "latency_ms": lat, "steps": KP,
                          "scan_ms": round(scan_s * 1e3, 4), "scan_GBps": round(gbs, 1),
                          "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
-                         "step": "lexical drafts (3 x 32) + query top-8 + gather (D(s) 48/8/0) + merge "
-                                 "(44 + 16 of 60 nodes), B = 1"}
-    q1, a1, c1, l1, e1 = steps[W]
+                         "step": "lexical drafts (3 x 32; pool + 8,192-16,384 own tokens) + query top-8 "
+                                 "+ gather (D(s) 48/8/0) + merge (44 + 16 of 60 nodes), B = 1"}
+    q1, a1, c1, l1, e1, h1, hl1 = steps[W]
     paper(W)
     lt, ll = bufs["lex"]
     c_, l_ = bufs["g"]

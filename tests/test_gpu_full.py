@@ -175,8 +175,9 @@ def test_stream_5120_checkpoints(oil):
 
 def test_full_step_8192(oil):
     """N = 524,288, d = 8,192 bf16, B = 64, k = 32 chains of 12 merged with
-    4 exact-suffix lexical drafts per query (GPU lexical source) under 48 + 16
-    nodes: the whole draft step on the device."""
+    4 exact-suffix lexical drafts per query (GPU lexical source over the pool
+    and each request's own 4,096-8,192 committed tokens) under 48 + 16 nodes:
+    the whole draft step on the device."""
     cfg = workloads.FULL_STEP_8192
     ps, qs, k, L = cfg["pool"], cfg["query"], cfg["k"], cfg["L"]
     n_lex, L_lex, lb, sb = cfg["n_lex"], cfg["L_lex"], cfg["lex_budget"], cfg["sem_budget"]
@@ -189,9 +190,12 @@ def test_full_step_8192(oil):
     _fill(pool, wp, 0, ps.n, dev, [orc])
     # the lexical drafts come from the GPU lexical source and must equal the oracle's
     ctx, ctx_len, excl = workloads.lexical_contexts(wp, src, ps.n)
-    glt, gll = pool.lexical(ctx.to(dev), ctx_len.to(dev), n_lex, L_lex, excl.to(dev))
+    hist, hlen = workloads.request_history(wp, src, ps.n, ctx, ctx_len, cfg["hist"])
+    glt, gll = pool.lexical(ctx.to(dev), ctx_len.to(dev), n_lex, L_lex, excl.to(dev), hist=hist.to(dev),
+                            hist_len=hlen.to(dev))
     elt, ell = oracle.lexical_drafts(wp.tokens.numpy(), wp.traces.numpy(), wp.prompts.numpy(), ps.n,
-                                     ctx.numpy(), ctx_len.numpy(), n_lex, L_lex, excl.numpy())
+                                     ctx.numpy(), ctx_len.numpy(), n_lex, L_lex, excl.numpy(),
+                                     hist=hist.numpy(), hist_len=hlen.numpy())
     torch.cuda.synchronize()
     assert np.array_equal(gll.cpu().numpy(), ell) and np.array_equal(glt.cpu().numpy(), elt)
     lt, ll = glt.cpu(), gll.cpu()
@@ -276,7 +280,9 @@ def test_paper_config_320k(oil):
     """The paper's frozen configuration at its largest store: 320,000 positions
     of width 4,096, one request per call (the B = 1 launches the benchmark
     times), k = 8, theta = 0.8, D(s) = 48 / 8 / 0, the top 3 lexical branches
-    of up to 32 tokens under 60 - 16 = 44 nodes and B_ret = 16.  Eight sampled
+    of up to 32 tokens under 60 - 16 = 44 nodes and B_ret = 16, the lexical
+    source over the pool and the request's own 8,192-16,384 committed
+    tokens.  Eight sampled
     requests: lexical drafts bit-exact against the oracle, retrieval by
     T1-T3 (and the fp32 bound) against exact scores of every position, the
     paper-rule gather and the merge (with the lexical branches in the
@@ -295,6 +301,7 @@ def test_paper_config_320k(oil):
     pool = oil.Pool(ps.d, ps.n, device=dev)
     _fill(pool, wp, 0, ps.n, dev, [orc])
     ctx, ctx_len, excl = workloads.lexical_contexts(wp, src, ps.n)
+    hist, hlen = workloads.request_history(wp, src, ps.n, ctx, ctx_len, cfg["hist"])
     anchor = workloads.anchors(wp, src)
     mx = 1 + lb + sb
     rule, orule = oil.DepthRule.paper(), oracle.paper_rule()
@@ -302,7 +309,8 @@ def test_paper_config_320k(oil):
     gs, gi, glt, gll, gct, gcl, trees = [], [], [], [], [], [], []
     for b in range(nq):                      # one request per call, as the benchmark runs them
         sl = slice(b, b + 1)
-        lt, ll = pool.lexical(ctx[sl].to(dev), ctx_len[sl].to(dev), n_lex, L_lex, excl[sl].to(dev))
+        lt, ll = pool.lexical(ctx[sl].to(dev), ctx_len[sl].to(dev), n_lex, L_lex, excl[sl].to(dev),
+                              hist=hist[sl].to(dev), hist_len=hlen[sl].to(dev))
         s, i = pool.query_topk(q[sl].contiguous(), k, exclude_prompt=excl[sl].to(dev))
         ct, cl = pool.gather(i, s, rule, L)
         tree = oil.merge_trees(anchor[sl].to(dev), lt, ll, lb, ct, cl, sb, mx, lex_ret=lr, lex_ret_len=lrl)
@@ -315,7 +323,7 @@ def test_paper_config_320k(oil):
     glt, gll, gct, gcl = np.stack(glt), np.stack(gll), np.stack(gct), np.stack(gcl)
     # lexical drafts: bit-exact against the (uncapped) oracle
     elt, ell = oracle.lexical_drafts(tok, tr, pr, ps.n, ctx.numpy(), ctx_len.numpy(), n_lex, L_lex,
-                                     excl.numpy())
+                                     excl.numpy(), hist=hist.numpy(), hist_len=hlen.numpy())
     assert np.array_equal(gll, ell) and np.array_equal(glt, elt)
     # retrieval: exact scores of every position, self-exclusion applied
     o = orc.s.copy()

@@ -68,14 +68,16 @@ STREAM_5120 = dict(pool=PoolSpec(n=2097152, d=5120, vocab=128256, seed=4, n_clus
                    k=16, L=16, n_start=262144, append_min=1, append_max=8)
 FULL_STEP_8192 = dict(pool=PoolSpec(n=524288, d=8192, vocab=128256, seed=5, n_clusters=256),
                       query=QuerySpec(B=64, noise=0.05, p_random=0.25, seed=105),
-                      k=32, L=12, n_lex=4, L_lex=12, lex_budget=48, sem_budget=16)
+                      k=32, L=12, n_lex=4, L_lex=12, lex_budget=48, sem_budget=16, hist=8192)
 # The paper's frozen configuration at its largest store: 320,000 positions of
 # width 4,096 (2.6 GB of bf16 keys), one request per step, k = 8, theta = 0.8,
 # copy depth D(s) = 48 / 8 / 0 (chains up to 48 tokens), the top 3 lexical
-# branches of up to 32 tokens under 60 - 16 = 44 nodes, B_ret = 16.
+# branches of up to 32 tokens under 60 - 16 = 44 nodes, B_ret = 16; the
+# lexical source also indexes the request's own 8,192-16,384 committed tokens.
 PAPER_320K = dict(pool=PoolSpec(n=320000, d=4096, vocab=128256, seed=6, n_clusters=256),
                   query=QuerySpec(B=1, noise=0.05, p_random=0.25, seed=106),
-                  k=8, L=48, n_lex=3, L_lex=32, lex_budget=44, sem_budget=16, lex_ret=3, lex_ret_len=32)
+                  k=8, L=48, n_lex=3, L_lex=32, lex_budget=44, sem_budget=16, lex_ret=3, lex_ret_len=32,
+                  hist=16384)
 
 
 def _gen(seed: int, device) -> torch.Generator:
@@ -254,3 +256,51 @@ def lexical_contexts(pool: Pool, src: torch.Tensor, n_valid: int, C: int = 16, s
         ctx_len[b] = len(c)
         excl[b] = int(pr[i0])
     return torch.from_numpy(ctx), torch.from_numpy(ctx_len), torch.from_numpy(excl)
+
+
+def request_history(pool: Pool, src: torch.Tensor, n_valid: int, ctx: torch.Tensor, ctx_len: torch.Tensor,
+                    H: int, seed: int = 1):
+    """Each request's own committed tokens, oldest first, for the lexical
+    source's per-request index (Sec. 4 (ii)).
+
+    Row b ends with the current call: the source instance's tokens from its
+    first position up to the context window, then exactly the context's
+    cl tokens (so the context is the history's tail).  Before that come the
+    session's earlier calls: stored instances of uniformly drawn kinds of call,
+    each with MINTED positions re-drawn (a fresh instance of that call), cut at
+    the front to fill the row.  Lengths are uniform in [H/2, H].
+
+    Returns (hist (B, H) int32, -1 past each length; hist_len (B,) int32)."""
+    import numpy as np
+    tok = pool.tokens[:n_valid].numpy()
+    tr = pool.traces[:n_valid].numpy()
+    ctx, ctx_len = ctx.numpy(), ctx_len.numpy()
+    B, C = ctx.shape
+    n_inst = max(n_valid // TEMPLATE_LEN, 1)
+    inst_tok = tok[: n_inst * TEMPLATE_LEN].reshape(n_inst, TEMPLATE_LEN) if n_valid >= TEMPLATE_LEN else None
+    rng = np.random.default_rng(seed)
+    hist = np.full((B, H), -1, dtype=np.int32)
+    hlen = np.zeros((B,), dtype=np.int32)
+    for b in range(B):
+        hl = int(rng.integers(H // 2, H + 1))
+        cl = int(min(max(ctx_len[b], 0), C))
+        tail = ctx[b, C - cl:] if cl else np.zeros(0, np.int32)
+        i0 = int(src[b])
+        if cl and 0 <= i0 < n_valid:
+            first = int(np.searchsorted(tr, tr[i0], side="left"))
+            a = i0 + 1 if (i0 + 1 < n_valid and tr[i0 + 1] == tr[i0]) else i0
+            tail = np.concatenate([tok[first:max(a - cl + 1, first)], tail])
+        tail = tail[-hl:]
+        fill = hl - len(tail)
+        if fill > 0 and inst_tok is not None:
+            n_f = fill // TEMPLATE_LEN + 1
+            seg = inst_tok[rng.integers(0, n_inst, n_f)].copy()
+            at = rng.random((n_f, TEMPLATE_LEN)).argsort(axis=1)[:, :MINTED]
+            np.put_along_axis(seg, at, rng.integers(0, pool.spec.vocab, (n_f, MINTED)).astype(np.int32), axis=1)
+            filler = seg.reshape(-1)[-fill:]
+        else:
+            filler = rng.integers(0, pool.spec.vocab, max(fill, 0)).astype(np.int32)
+        row = np.concatenate([filler, tail]).astype(np.int32)
+        hist[b, :len(row)] = row
+        hlen[b] = len(row)
+    return torch.from_numpy(hist), torch.from_numpy(hlen)
