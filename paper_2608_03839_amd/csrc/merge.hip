@@ -1,117 +1,55 @@
 // Root-first merge of draft chains into one tree per query (Sec. 4 (iii),
 // Eq. 4; BuildLexical then MergeFromRoot in Algorithm 1).
 //
-// One wave per tree.  The tree's input chains are first copied into LDS with
-// coalesced loads; the tree itself lives in registers: node slot j belongs to
-// lane j % 64, register j / 64 (up to 256 slots).  Each token of a chain is
-// one wave-wide step: every lane tests its slots for "child of the current
-// node carrying this token" (two compares, two ballots, one scalar AND) and
-// the result names the match (siblings never repeat a token, so there is at
-// most one).  A match is walked for free; otherwise the next slot is bought
-// if the phase's budget remains, else the rest of the chain is dropped.
+// The sequential definition inserts chains one after another: walk the
+// existing nodes while the tokens match, then buy one node per token while
+// the phase's budget lasts, and drop the rest of a chain once it is spent.
 // Lexical drafts go first under their allocation (BuildLexical).  The fixed
 // reservation then takes Algorithm 1's candidate set C in its order: the
 // retrieved chains, the top n_lex_ret lexical drafts cut to L_lex_ret tokens
 // (a draft the allocation cut short buys its rest here; source 4), and the
 // recycled-pool rollouts.
+//
+// One 256-thread workgroup per tree computes the same tree without a
+// sequential walk.  Within a phase, the nodes chain c buys are its prefixes
+// of lengths E(c)+1 .. len(c) that no earlier chain holds, where E(c) is the
+// longest common prefix with an earlier chain (capped at what that chain put
+// in the tree); the budget then keeps the first of these in chain order (once
+// it is spent no later chain buys anything, so every chain before the one it
+// runs out in is in the tree whole).  So: all pairwise common prefixes at
+// once (a thread per chain pair, LDS max), an exclusive scan of the new-node
+// counts per phase (node ids in creation order), and for each chain's first
+// new node the parent, which the earliest chain holding the prefix E(c)
+// created (LDS min over the same pairs).
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace oil {
 
-constexpr int kSlotsPerLane = OIL_NODES_MAX / 64;
+constexpr int kMergeThreads = 256;
+constexpr int kMergeChains = 64 + 64 + 64 + OIL_REC_OUT_MAX;  // n_lex + k + n_lex_ret + n_rec at most
 
-// Insert one chain (token m in lane m's `mine`, len <= 64) from the root.
-// Unused slots hold parent -1, and the current node is never -1, so a slot
-// matches only if it is a live child of the current node.  The walk follows
-// existing nodes while they match; from the first token that matches no
-// child on, every token is a new node (a node just bought has no children),
-// bought while the budget lasts.
-__device__ __forceinline__ void insert_chain(int32_t (&ntok)[kSlotsPerLane], int32_t (&npar)[kSlotsPerLane],
-                                             int32_t (&nsrc)[kSlotsPerLane], int& count, int& spent,
-                                             int budget, int src, int32_t mine, int len)
-{
-    const int lane = threadIdx.x;
-    int cur = 0, m = 0;
-    for (; m < len; m++) {
-        const int32_t t = __builtin_amdgcn_readlane(mine, m);
-        int found = -1;
-#pragma unroll
-        for (int q = 0; q < kSlotsPerLane; q++) {
-            if (q * 64 >= count)
-                break;
-            // two ballots ANDed on the scalar unit: cheaper than one ballot of a
-            // combined predicate, which the compiler materialises in a register
-            const uint64_t msk = __ballot(npar[q] == cur) & __ballot(ntok[q] == t);
-            if (msk) {
-                found = q * 64 + __ffsll((unsigned long long)msk) - 1;
-                break;
-            }
-        }
-        if (found < 0)
-            break;
-        cur = found;
-    }
-    for (; m < len && spent < budget; m++) {
-        const int32_t t = __builtin_amdgcn_readlane(mine, m);
-        const int j = count++;
-        spent++;
-        if (lane == (j & 63)) {
-            const int q = j >> 6;
-#pragma unroll
-            for (int qq = 0; qq < kSlotsPerLane; qq++)
-                if (qq == q) {
-                    ntok[qq] = t;
-                    npar[qq] = cur;
-                    nsrc[qq] = src;
-                }
-        }
-        cur = j;
-    }
-}
-
-// Insert n chains of one source, stored in LDS with stride Lc (lengths in
-// lens[], clamped to Lc and to Lmax), in order.  The next chain's tokens are
-// read from LDS while the current one is inserted.
-__device__ __forceinline__ void insert_source(int32_t (&ntok)[kSlotsPerLane], int32_t (&npar)[kSlotsPerLane],
-                                              int32_t (&nsrc)[kSlotsPerLane], int& count, int& spent,
-                                              int budget, int src, const int32_t* chains, const int32_t* lens,
-                                              int n, int Lc, int Lmax = 64)
-{
-    const int lane = threadIdx.x;
-    if (n <= 0)
-        return;
-    const int32_t len_r = lane < n ? min(min(lens[lane], Lc), Lmax) : 0;  // n <= 64
-    int32_t mine = lane < Lc ? chains[lane] : -1;
-    for (int c = 0; c < n; c++) {
-        const int len = __builtin_amdgcn_readlane(len_r, c);
-        const int32_t next = (c + 1 < n && lane < Lc) ? chains[(c + 1) * Lc + lane] : -1;
-        insert_chain(ntok, npar, nsrc, count, spent, budget, src, mine, len);
-        mine = next;
-    }
-}
-
-// Copy the tree's six input arrays from global memory to LDS with one wave:
-// their elements are taken as one concatenated index range, eight loads per
-// lane in flight at clamped (always valid) addresses, then the stores.  An
-// empty array (which may be NULL) owns no index.
+// Copy the tree's six input arrays from global memory to LDS: their elements
+// are taken as one concatenated index range, four loads per thread in flight
+// at clamped (always valid) addresses, then the stores.  An empty array
+// (which may be NULL) owns no index.
 __device__ __forceinline__ void stage_lds(const int32_t* const (&src)[6], int32_t* const (&dst)[6],
                                           const int (&n)[6])
 {
-    constexpr int kU = 8;
-    const int lane = threadIdx.x;
+    constexpr int kU = 4;
+    const int t = threadIdx.x;
     int end[6], total = 0;
 #pragma unroll
     for (int a = 0; a < 6; a++) {
         total += n[a];
         end[a] = total;
     }
-    for (int i0 = 0; i0 < total; i0 += 64 * kU) {
+    for (int i0 = 0; i0 < total; i0 += kMergeThreads * kU) {
         int32_t v[kU];
         int32_t* to[kU];
 #pragma unroll
         for (int u = 0; u < kU; u++) {
-            const int i = min(i0 + u * 64 + lane, total - 1);
+            const int i = min(i0 + u * kMergeThreads + t, total - 1);
             int a = 0, base = 0;
 #pragma unroll
             for (int q = 0; q < 5; q++)
@@ -124,12 +62,58 @@ __device__ __forceinline__ void stage_lds(const int32_t* const (&src)[6], int32_
         }
 #pragma unroll
         for (int u = 0; u < kU; u++)
-            if (i0 + u * 64 + lane < total)
+            if (i0 + u * kMergeThreads + t < total)
                 *to[u] = v[u];
     }
 }
 
-__global__ __launch_bounds__(64) void merge_kernel(
+// Common prefix length of two chains held in LDS.
+__device__ __forceinline__ int chain_lcp(const int32_t* a, const int32_t* b, int n)
+{
+    int m = 0;
+    while (m < n && a[m] == b[m])
+        m++;
+    return m;
+}
+
+// Exclusive scan of the new-node counts of chains [c0, c1) (at most 4 per
+// lane of wave 0) and the nodes each buys from `budget`; returns the total
+// bought, to every lane of wave 0.
+__device__ __forceinline__ int phase_scan(const int32_t* c_len, const int32_t* c_E, int32_t* c_base,
+                                          int32_t* c_buy, int c0, int c1, int budget, int id0)
+{
+    const int lane = threadIdx.x;  // wave 0 only
+    constexpr int kPer = 4;
+    int n[kPer], sum = 0;
+#pragma unroll
+    for (int u = 0; u < kPer; u++) {
+        const int c = c0 + lane * kPer + u;
+        n[u] = c < c1 ? max(c_len[c] - c_E[c], 0) : 0;
+        sum += n[u];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int v = __shfl_up(incl, o, kWave);
+        if (lane >= o)
+            incl += v;
+    }
+    int r = incl - sum;  // new nodes of the chains before this lane's first
+#pragma unroll
+    for (int u = 0; u < kPer; u++) {
+        const int c = c0 + lane * kPer + u;
+        if (c < c1) {
+            const int buy = min(max(budget - r, 0), n[u]);
+            c_buy[c] = buy;
+            c_base[c] = id0 + r;
+        }
+        r += n[u];
+    }
+    const int total = __shfl(incl, kWave - 1, kWave);
+    return min(total, budget);
+}
+
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     const int32_t* __restrict__ anchor, const int32_t* __restrict__ lex_tokens,
     const int32_t* __restrict__ lex_len, int32_t n_lex, int32_t L_lex, int32_t lex_budget, int32_t n_lex_ret,
     int32_t L_lex_ret, const int32_t* __restrict__ sem_tokens, const int32_t* __restrict__ sem_len, int32_t k,
@@ -138,7 +122,7 @@ __global__ __launch_bounds__(64) void merge_kernel(
     int32_t L_rec, int32_t sem_budget, int32_t max_nodes, int32_t* __restrict__ node_token,
     int32_t* __restrict__ node_parent, int8_t* __restrict__ node_source, int32_t* __restrict__ n_nodes)
 {
-    // LDS: lexical chains, retrieved chains, rollouts, then the three length arrays
+    // LDS: lexical chains, retrieved chains, rollouts, the three length arrays, then the chain table
     extern __shared__ int32_t sm[];
     int32_t* lex_s = sm;
     int32_t* sem_s = lex_s + n_lex * L_lex;
@@ -146,7 +130,12 @@ __global__ __launch_bounds__(64) void merge_kernel(
     int32_t* llen_s = rec_s + n_rec * L_rec;
     int32_t* slen_s = llen_s + n_lex;
     int32_t* rlen_s = slen_s + k;
-    const int b = blockIdx.x, lane = threadIdx.x;
+    __shared__ int32_t c_off[kMergeChains], c_len[kMergeChains], c_E[kMergeChains], c_base[kMergeChains],
+        c_buy[kMergeChains], c_av[kMergeChains], c_star[kMergeChains];
+    __shared__ int32_t s_total[2];
+    const int b = blockIdx.x, t = threadIdx.x;
+    const int NC1 = n_lex;                            // phase 1: the lexical allocation
+    const int NC = n_lex + k + n_lex_ret + n_rec;     // phase 2: C under the reservation
     {
         const int32_t* const src[6] = {lex_tokens + (int64_t)b * n_lex * L_lex, sem_tokens + (int64_t)b * k * L,
                                        rec_tokens + (int64_t)b * n_rec * L_rec, lex_len + (int64_t)b * n_lex,
@@ -156,37 +145,117 @@ __global__ __launch_bounds__(64) void merge_kernel(
         stage_lds(src, dst, n);
     }
     __syncthreads();
-
-    int32_t ntok[kSlotsPerLane], npar[kSlotsPerLane], nsrc[kSlotsPerLane];
-#pragma unroll
-    for (int q = 0; q < kSlotsPerLane; q++) {
-        ntok[q] = -1;
-        npar[q] = -1;
-        nsrc[q] = -1;
+    // the chain table, in insertion order
+    for (int c = t; c < NC; c += kMergeThreads) {
+        int off, len;
+        if (c < n_lex) {
+            off = c * L_lex;
+            len = min(max(llen_s[c], 0), L_lex);
+        } else if (c < n_lex + k) {
+            const int i = c - n_lex;
+            off = (int)(sem_s - sm) + i * L;
+            len = min(max(slen_s[i], 0), L);
+        } else if (c < n_lex + k + n_lex_ret) {
+            const int i = c - n_lex - k;
+            off = i * L_lex;
+            len = min(min(max(llen_s[i], 0), L_lex), L_lex_ret);
+        } else {
+            const int i = c - n_lex - k - n_lex_ret;
+            off = (int)(rec_s - sm) + i * L_rec;
+            len = min(max(rlen_s[i], 0), L_rec);
+        }
+        c_off[c] = off;
+        c_len[c] = len;
+        c_E[c] = 0;
+        c_star[c] = 0x7FFFFFFF;
     }
-    if (lane == 0) {
-        ntok[0] = anchor[b];
-        nsrc[0] = 0;
-    }
-    int count = 1;
-    int spent = 0;
-    insert_source(ntok, npar, nsrc, count, spent, lex_budget, 1, lex_s, llen_s, n_lex, L_lex);
-    spent = 0;
-    insert_source(ntok, npar, nsrc, count, spent, sem_budget, 2, sem_s, slen_s, k, L);
-    // the top lexical branches, then the recycled-pool rollouts, inside the same reservation
-    insert_source(ntok, npar, nsrc, count, spent, sem_budget, 4, lex_s, llen_s, n_lex_ret, L_lex, L_lex_ret);
-    insert_source(ntok, npar, nsrc, count, spent, sem_budget, 3, rec_s, rlen_s, n_rec, L_rec);
-#pragma unroll
-    for (int q = 0; q < kSlotsPerLane; q++) {
-        const int slot = q * 64 + lane;
-        if (slot < max_nodes) {
-            const int64_t o = (int64_t)b * max_nodes + slot;
-            node_token[o] = ntok[q];
-            node_parent[o] = npar[q];
-            node_source[o] = (int8_t)nsrc[q];
+    __syncthreads();
+    // phase 1: E(c) over earlier lexical drafts, every one of them in the tree whole
+    for (int p = t; p < NC1 * NC1; p += kMergeThreads) {
+        const int c = p / NC1, e = p % NC1;
+        if (e < c) {
+            const int v = chain_lcp(sm + c_off[e], sm + c_off[c], min(c_len[e], c_len[c]));
+            if (v)
+                atomicMax(&c_E[c], v);
         }
     }
-    if (lane == 0)
+    __syncthreads();
+    if (t < kWave)
+        s_total[0] = phase_scan(c_len, c_E, c_base, c_buy, 0, NC1, lex_budget, 1);  // same value on every lane
+    __syncthreads();
+    // what each lexical draft left in the tree (a draft that bought nothing
+    // left nothing an earlier draft had not)
+    for (int c = t; c < NC1; c += kMergeThreads)
+        c_av[c] = c_buy[c] > 0 ? c_E[c] + c_buy[c] : 0;
+    __syncthreads();
+    // phase 2: E(c) over the lexical tree and the earlier chains of C
+    const int NC2 = NC - NC1;
+    for (int p = t; p < NC2 * NC; p += kMergeThreads) {
+        const int c = NC1 + p / NC, e = p % NC;
+        if (e < c) {
+            const int cap = e < NC1 ? c_av[e] : c_len[e];
+            const int v = chain_lcp(sm + c_off[e], sm + c_off[c], min(cap, c_len[c]));
+            if (v)
+                atomicMax(&c_E[c], v);
+        }
+    }
+    __syncthreads();
+    if (t < kWave) {
+        const int tot = phase_scan(c_len, c_E, c_base, c_buy, NC1, NC, sem_budget, 1 + s_total[0]);
+        if (t == 0)
+            s_total[1] = tot;
+    }
+    __syncthreads();
+    for (int c = NC1 + t; c < NC; c += kMergeThreads)
+        c_av[c] = c_len[c];  // every chain of C before the last one that buys is in the tree whole
+    __syncthreads();
+    // the creator of each buying chain's attachment node: the earliest chain
+    // that holds the chain's first E(c) tokens
+    for (int p = t; p < NC * NC; p += kMergeThreads) {
+        const int c = p / NC, e = p % NC;
+        if (e < c && c_buy[c] > 0 && c_E[c] > 0) {
+            const int Ec = c_E[c];
+            const int cap = min(c_av[e], c_len[c]);
+            if (cap >= Ec && chain_lcp(sm + c_off[e], sm + c_off[c], Ec) == Ec)
+                atomicMin(&c_star[c], e);
+        }
+    }
+    __syncthreads();
+    // the nodes: chain c's j-th bought node is its token E(c) + j, id base(c) + j
+    const int count = 1 + s_total[0] + s_total[1];
+    for (int p = t; p < NC * 64; p += kMergeThreads) {
+        const int c = p >> 6, j = p & 63;
+        if (j >= c_buy[c])
+            continue;
+        const int Ec = c_E[c], id = c_base[c] + j;
+        int parent;
+        if (j > 0) {
+            parent = id - 1;
+        } else if (Ec == 0) {
+            parent = 0;
+        } else {
+            const int s = c_star[c];
+            parent = c_base[s] + (Ec - 1 - c_E[s]);
+        }
+        const int src = c < n_lex ? 1 : (c < n_lex + k ? 2 : (c < n_lex + k + n_lex_ret ? 4 : 3));
+        const int64_t o = (int64_t)b * max_nodes + id;
+        node_token[o] = sm[c_off[c] + Ec + j];
+        node_parent[o] = parent;
+        node_source[o] = (int8_t)src;
+    }
+    for (int slot = t; slot < max_nodes; slot += kMergeThreads) {
+        const int64_t o = (int64_t)b * max_nodes + slot;
+        if (slot == 0) {
+            node_token[o] = anchor[b];
+            node_parent[o] = -1;
+            node_source[o] = 0;
+        } else if (slot >= count) {
+            node_token[o] = -1;
+            node_parent[o] = -1;
+            node_source[o] = -1;
+        }
+    }
+    if (t == 0)
         n_nodes[b] = count;
 }
 
@@ -203,7 +272,7 @@ hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tok
                         int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                         int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, hipStream_t stream)
 {
-    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(64), merge_lds_bytes(n_lex, L_lex, k, L, n_rec, L_rec),
+    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(kMergeThreads), merge_lds_bytes(n_lex, L_lex, k, L, n_rec, L_rec),
                        stream, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget, n_lex_ret, L_lex_ret,
                        sem_tokens, sem_len, k,
                        L, rec_tokens, rec_len, n_rec, L_rec, sem_budget, max_nodes, node_token, node_parent,
