@@ -155,7 +155,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-fp8", action="store_true",
                     help="skip the fp8 key-pool variant (reported beside the headline, not as it)")
-    ap.add_argument("--cpu-sample-queries", type=int, default=8)
+    ap.add_argument("--cpu-sample-queries", type=int, default=16)
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the step benchmark: retrieval calls on the same pool for "
                          "B in 1..512, one JSON line with the scan's GB/s and MFMA TFLOP/s per B")

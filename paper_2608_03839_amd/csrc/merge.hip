@@ -67,13 +67,44 @@ __device__ __forceinline__ void stage_lds(const int32_t* const (&src)[6], int32_
     }
 }
 
-// Common prefix length of two chains held in LDS.
+// Common prefix length of two chains held in LDS, compared eight tokens per
+// round (the loads of a round issued together, at clamped indexes).
 __device__ __forceinline__ int chain_lcp(const int32_t* a, const int32_t* b, int n)
 {
     int m = 0;
-    while (m < n && a[m] == b[m])
-        m++;
+    for (int m0 = 0; m0 < n; m0 += 8) {
+        int32_t x[8], y[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+            const int i = min(m0 + u, n - 1);
+            x[u] = a[i];
+            y[u] = b[i];
+        }
+        int run = 0;
+        bool go = true;
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+            go = go && m0 + u < n && x[u] == y[u];
+            run += go ? 1 : 0;
+        }
+        m += run;
+        if (run < 8)
+            break;
+    }
     return m;
+}
+
+// Chain pair number p (0 .. NC(NC-1)/2 - 1) -> (c, e), e < c, in the
+// triangular order p = c(c-1)/2 + e.
+__device__ __forceinline__ void pair_of(int p, int& c, int& e)
+{
+    int cc = (int)((1.0f + sqrtf(1.0f + 8.0f * (float)p)) * 0.5f);
+    while (cc * (cc - 1) / 2 > p)
+        cc--;
+    while ((cc + 1) * cc / 2 <= p)
+        cc++;
+    c = cc;
+    e = p - cc * (cc - 1) / 2;
 }
 
 // Exclusive scan of the new-node counts of chains [c0, c1) (at most 4 per
@@ -130,6 +161,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     int32_t* llen_s = rec_s + n_rec * L_rec;
     int32_t* slen_s = llen_s + n_lex;
     int32_t* rlen_s = slen_s + k;
+    uint8_t* lcp8 = (uint8_t*)(rlen_s + n_rec);  // common prefix of each chain pair
     __shared__ int32_t c_off[kMergeChains], c_len[kMergeChains], c_E[kMergeChains], c_base[kMergeChains],
         c_buy[kMergeChains], c_av[kMergeChains], c_star[kMergeChains];
     __shared__ int32_t s_total[2];
@@ -170,13 +202,22 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
         c_star[c] = 0x7FFFFFFF;
     }
     __syncthreads();
+    // every common prefix, once: lcp8[c(c-1)/2 + e] for e < c
+    const int NP = NC * (NC - 1) / 2;
+    for (int p = t; p < NP; p += kMergeThreads) {
+        int c, e;
+        pair_of(p, c, e);
+        const int n = min(c_len[e], c_len[c]);
+        lcp8[p] = (uint8_t)(n > 0 ? chain_lcp(sm + c_off[e], sm + c_off[c], n) : 0);
+    }
+    __syncthreads();
     // phase 1: E(c) over earlier lexical drafts, every one of them in the tree whole
-    for (int p = t; p < NC1 * NC1; p += kMergeThreads) {
-        const int c = p / NC1, e = p % NC1;
-        if (e < c) {
-            const int v = chain_lcp(sm + c_off[e], sm + c_off[c], min(c_len[e], c_len[c]));
-            if (v)
-                atomicMax(&c_E[c], v);
+    for (int p = t; p < NC1 * (NC1 - 1) / 2; p += kMergeThreads) {
+        const int v = lcp8[p];
+        if (v) {
+            int c, e;
+            pair_of(p, c, e);
+            atomicMax(&c_E[c], v);
         }
     }
     __syncthreads();
@@ -187,17 +228,16 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     // left nothing an earlier draft had not)
     for (int c = t; c < NC1; c += kMergeThreads)
         c_av[c] = c_buy[c] > 0 ? c_E[c] + c_buy[c] : 0;
+    for (int c = NC1 + t; c < NC; c += kMergeThreads)
+        c_av[c] = c_len[c];  // every chain of C before the last one that buys is in the tree whole
     __syncthreads();
     // phase 2: E(c) over the lexical tree and the earlier chains of C
-    const int NC2 = NC - NC1;
-    for (int p = t; p < NC2 * NC; p += kMergeThreads) {
-        const int c = NC1 + p / NC, e = p % NC;
-        if (e < c) {
-            const int cap = e < NC1 ? c_av[e] : c_len[e];
-            const int v = chain_lcp(sm + c_off[e], sm + c_off[c], min(cap, c_len[c]));
-            if (v)
-                atomicMax(&c_E[c], v);
-        }
+    for (int p = NC1 * (NC1 - 1) / 2 + t; p < NP; p += kMergeThreads) {
+        int c, e;
+        pair_of(p, c, e);
+        const int v = min((int)lcp8[p], c_av[e]);
+        if (v)
+            atomicMax(&c_E[c], v);
     }
     __syncthreads();
     if (t < kWave) {
@@ -206,19 +246,14 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
             s_total[1] = tot;
     }
     __syncthreads();
-    for (int c = NC1 + t; c < NC; c += kMergeThreads)
-        c_av[c] = c_len[c];  // every chain of C before the last one that buys is in the tree whole
-    __syncthreads();
     // the creator of each buying chain's attachment node: the earliest chain
     // that holds the chain's first E(c) tokens
-    for (int p = t; p < NC * NC; p += kMergeThreads) {
-        const int c = p / NC, e = p % NC;
-        if (e < c && c_buy[c] > 0 && c_E[c] > 0) {
-            const int Ec = c_E[c];
-            const int cap = min(c_av[e], c_len[c]);
-            if (cap >= Ec && chain_lcp(sm + c_off[e], sm + c_off[c], Ec) == Ec)
-                atomicMin(&c_star[c], e);
-        }
+    for (int p = t; p < NP; p += kMergeThreads) {
+        int c, e;
+        pair_of(p, c, e);
+        const int Ec = c_E[c];
+        if (c_buy[c] > 0 && Ec > 0 && lcp8[p] >= Ec && c_av[e] >= Ec)
+            atomicMin(&c_star[c], e);
     }
     __syncthreads();
     // the nodes: chain c's j-th bought node is its token E(c) + j, id base(c) + j
@@ -259,10 +294,13 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
         n_nodes[b] = count;
 }
 
-size_t merge_lds_bytes(int32_t n_lex, int32_t L_lex, int32_t k, int32_t L, int32_t n_rec, int32_t L_rec)
+size_t merge_lds_bytes(int32_t n_lex, int32_t L_lex, int32_t k, int32_t L, int32_t n_rec, int32_t L_rec,
+                       int32_t n_lex_ret)
 {
+    const size_t nc = (size_t)n_lex + k + n_lex_ret + n_rec;
     return ((size_t)n_lex * L_lex + (size_t)k * L + (size_t)n_rec * L_rec + n_lex + k + n_rec) *
-           sizeof(int32_t);
+               sizeof(int32_t) +
+           nc * (nc - 1) / 2;
 }
 
 hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tokens,
@@ -272,7 +310,7 @@ hipError_t launch_merge(int32_t B, const int32_t* anchor, const int32_t* lex_tok
                         int32_t sem_budget, int32_t max_nodes, int32_t* node_token,
                         int32_t* node_parent, int8_t* node_source, int32_t* n_nodes, hipStream_t stream)
 {
-    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(kMergeThreads), merge_lds_bytes(n_lex, L_lex, k, L, n_rec, L_rec),
+    hipLaunchKernelGGL(merge_kernel, dim3(B), dim3(kMergeThreads), merge_lds_bytes(n_lex, L_lex, k, L, n_rec, L_rec, n_lex_ret),
                        stream, anchor, lex_tokens, lex_len, n_lex, L_lex, lex_budget, n_lex_ret, L_lex_ret,
                        sem_tokens, sem_len, k,
                        L, rec_tokens, rec_len, n_rec, L_rec, sem_budget, max_nodes, node_token, node_parent,
