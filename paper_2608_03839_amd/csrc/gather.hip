@@ -5,7 +5,9 @@
 // maximum, not a filter) is a wave max-reduction; each lane then reads its
 // copy depth from the band table, walks x_{i+2}, ..., x_{i+1+depth} while the
 // trace id stays that of i and the position stays inside the pool, and drops
-// the chain if fewer than two tokens came out.
+// the chain if fewer than two tokens came out.  The walk reads 16 positions
+// per round with independent loads at clamped addresses (the trace id of i
+// with the first round), so a chain costs one memory round trip per 16 tokens.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -41,12 +43,25 @@ __global__ __launch_bounds__(64) void gather_kernel(
     depth = depth < L ? depth : L;
     int32_t got = 0;
     if (depth > 0) {
-        const int32_t tr = traces[i];
-        for (int32_t m = 1; m <= depth; m++) {
-            const int64_t p = (int64_t)i + 1 + m;
-            if (p >= n_valid || traces[p] != tr)
-                break;
-            out[got++] = tokens[p];
+        int32_t tr = 0;
+        bool open = true;
+        for (int32_t m0 = 1; m0 <= depth && open; m0 += 16) {
+            int32_t tk[16], tv[16];
+            if (m0 == 1)
+                tr = traces[i];
+#pragma unroll
+            for (int u = 0; u < 16; u++) {
+                const int64_t p = (int64_t)i + 1 + m0 + u;
+                const int64_t pc = p < n_valid ? p : n_valid - 1;
+                tk[u] = tokens[pc];
+                tv[u] = traces[pc];
+            }
+#pragma unroll
+            for (int u = 0; u < 16; u++) {
+                open = open && m0 + u <= depth && (int64_t)i + 1 + m0 + u < n_valid && tv[u] == tr;
+                if (open)
+                    out[got++] = tk[u];
+            }
         }
     }
     if (got < 2)
