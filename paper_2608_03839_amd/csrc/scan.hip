@@ -39,6 +39,9 @@
 // query's exclusion id get the "no position" bit pattern.
 #include <hip/hip_ext.h>
 
+#include <numeric>
+#include <utility>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -80,16 +83,10 @@
 #ifndef OIL_TAIL_PF2
 #define OIL_TAIL_PF2 3
 #endif
-// Row blocks per workgroup of the wide scan (B > 64) with 1, 2 and 4 query
-// tiles per wave.
-#ifndef OIL_WIDE_MT1
-#define OIL_WIDE_MT1 4
-#endif
-#ifndef OIL_WIDE_MT2
-#define OIL_WIDE_MT2 4
-#endif
-#ifndef OIL_WIDE_MT4
-#define OIL_WIDE_MT4 4
+// Cache policy of the wide scan's key copies: 2 = nt (streaming, as the
+// narrow scans' nontemporal key loads).
+#ifndef OIL_WIDE_KEY_CPOL
+#define OIL_WIDE_KEY_CPOL 2
 #endif
 
 namespace oil {
@@ -379,21 +376,37 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 
 // ----------------------------------------------------------------- MFMA, wide batches (64 < B <= 512)
 // Past ~300 queries the contraction is MFMA-bound, so keys must be fetched
-// once and reused by every query tile.  A block owns MT row blocks; its four
-// waves split the query tiles (NTW tiles each).  Each 64-column window of the
-// block's keys (MT tiles of 4 KiB) is copied into LDS once with gfx950's
-// 16-byte global->LDS loads (the four waves share the copies), through a
-// three-window ring with one barrier per window; every wave reads its A
-// operands from LDS (lane l's 16 bytes sit at 16 l: conflict-free) and its
-// own query fragments from L2.  Per (row block, query tile) the MFMA sequence
-// is the same as in scan_mfma_kernel (windows in order, sub-steps in order).
-// With at most 2 query tiles per wave and 4 row blocks the register budget is
-// capped for two waves per SIMD (the accumulators then fit beside the rest).
+// once and reused by every query tile.  A block owns MT row blocks; its WAVES
+// waves split the query tiles (NTW tiles each).  Each key window of the block
+// (MT tiles of 4 KiB) lands in LDS once, in an R-window ring, shared by every
+// wave: either with 16-byte buffer loads straight to LDS (each wave copies
+// 4 MT / WAVES of the block's 1 KiB chunks), or (KREG) through registers:
+// 16-byte nontemporal loads two windows ahead, then 16-byte LDS stores.
+// Every wave reads its A operands from LDS (lane l's 16 bytes sit at 16 l:
+// conflict-free) and its own query fragments from L2 into registers, NB - 1
+// windows ahead.  Per (row block, query tile) the MFMA sequence is the same
+// as in scan_mfma_kernel (windows in order, sub-steps in order), so scores
+// are bit-identical to the narrow scan's and the rescore's.
+//
+// Schedule of window w (NG MFMA groups: four bf16 sub-steps, or two fp8
+// pairs).  The A operands of group g + 1 are read from LDS while group g's
+// MFMAs run; the fragments of window w + NB - 1 are requested between the
+// MFMAs of the first NG - 1 groups (one load every few MFMAs: a burst of
+// loads ahead of the MFMAs would hold up their issue).  Before the last group
+// each wave makes sure its part of window w + 1 is in LDS (direct copies:
+// wait for the copies issued R - 2 windows earlier; KREG: wait for the LDS
+// stores made in this stage's first group), and the waves meet at one
+// barrier: window w + 1 is then in LDS, and every wave has finished reading
+// window w - 1, whose slot receives the copies of window w + R - 1, issued
+// between the last group's MFMAs.  The first A operands of window w + 1 are
+// read right after the barrier, so the last group's MFMAs hide the LDS
+// latency.  Loads past the last window repeat the last window (clamped index:
+// uniform wait counts; the repeats land in a free slot or hit in cache).
+//
 // A workgroup barrier without the memory fence __syncthreads() carries: that
-// fence would wait for every outstanding global-to-LDS copy, the ones meant to
-// stay in flight included.  The caller waits (vmcnt) for the copies the next
-// stage reads before calling this; the scheduling barriers keep LDS accesses
-// on their side of it.
+// fence would wait for every outstanding copy to LDS, the ones meant to stay
+// in flight included.  The scheduling barriers keep LDS accesses on their
+// side of it.
 __device__ __forceinline__ void block_barrier()
 {
     __builtin_amdgcn_sched_barrier(0);
@@ -401,8 +414,11 @@ __device__ __forceinline__ void block_barrier()
     __builtin_amdgcn_sched_barrier(0);
 }
 
+// Waves per SIMD the wide scan's registers allow: two with at most 4 row
+// blocks and 2 query tiles (bf16) or 1 tile (fp8, whose pairs hold twice the
+// A operands).
 #ifndef OIL_WIDE_WPE
-#define OIL_WIDE_WPE(MT, NTW) ((MT) <= 4 && (NTW) <= 2 ? 2 : 1)
+#define OIL_WIDE_WPE(MT, NTW, FMT) ((MT) <= 4 && (NTW) <= ((FMT) == kKeyBf16 ? 2 : 1) ? 2 : 1)
 #endif
 
 template <int N>
@@ -414,17 +430,52 @@ __device__ __forceinline__ void wait_vmcnt_at_most()
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <int MT, int NTW, int FMT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OIL_WIDE_WPE(MT, NTW)))) void
+// f(std::integral_constant<int, 0>{}), ..., f(std::integral_constant<int, N - 1>{}), in order.
+template <int... I, class F>
+__device__ __forceinline__ void unrolled_impl(std::integer_sequence<int, I...>, F&& f)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void unrolled(F&& f)
+{
+    unrolled_impl(std::make_integer_sequence<int, N>{}, f);
+}
+
+template <int MT, int NTW, int R, int NB, int WAVES, int WPE, int KREG, int FMT>
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(WPE))) void
 scan_mfma_wide_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
     const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
     const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld,
     const float* __restrict__ kscale, const float* __restrict__ qscale)
 {
-    // three windows of the block's MT key tiles, as three separate LDS objects
-    // so that the slot each access uses is known at compile time
-    __shared__ bf16x8 ring0[MT][4][64], ring1[MT][4][64], ring2[MT][4][64];
+    constexpr int NG = FMT == kKeyBf16 ? 4 : 2;  // MFMA groups per window
+    constexpr int CG = 4 / NG;                   // 1 KiB operand chunks per group
+    constexpr int NM = MT * NTW;                 // MFMAs per group
+    constexpr int NQ = NTW * 4;                  // fragment loads per window
+    constexpr int CPW = 4 * MT / WAVES;          // 1 KiB key copies per wave and window
+    static_assert(CPW * WAVES == 4 * MT && (NB == 2 || NB == 3), "copy split / fragment sets");
+    // loads a wave may have in flight once the copies of window w + 1 are in
+    // (see the schedule above)
+    constexpr int kInFlight = (R - 3) * (NQ + CPW) + NQ;
+    static_assert(R >= 4 && R <= 6 && kInFlight <= 63, "ring depth / vmcnt range");
+    // stages per trip: ring slot and fragment set return to their start
+    constexpr int U0 = R * NB / std::gcd(R, NB);
+    constexpr int U = KREG && U0 % 2 ? 2 * U0 : U0;  // KREG: staging sets alternate too
+    // R windows of the block's MT key tiles, as separate LDS objects so that
+    // the slot each access uses is known at compile time (unused ones vanish)
+    __shared__ bf16x8 ring0[MT][4][64], ring1[MT][4][64], ring2[MT][4][64], ring3[MT][4][64],
+        ring4[MT][4][64], ring5[MT][4][64];
+    auto slot = [&](auto s_t) -> bf16x8 (&)[MT][4][64] {
+        constexpr int s = decltype(s_t)::value;
+        if constexpr (s == 0) return ring0;
+        else if constexpr (s == 1) return ring1;
+        else if constexpr (s == 2) return ring2;
+        else if constexpr (s == 3) return ring3;
+        else if constexpr (s == 4) return ring4;
+        else return ring5;
+    };
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
     const int h = lane >> 5, r = lane & 31;
@@ -436,20 +487,42 @@ scan_mfma_wide_kernel(
     // loads take a scalar base and one shared 32-bit lane offset.
     const uint32_t loff = (uint32_t)lane * 16;
 
-    // this wave's share of the block's key copies: (mt, s) pairs with (4 mt + s) % 4 == wave
-    const char* src[MT];
+    // this wave's share of the block's key copies: jobs j = wave + WAVES c
+    // (c < CPW), job j being 1 KiB chunk j % 4 of tile j / 4
+    const char* src[CPW];
+    uint32_t dst[CPW];  // byte offset of the job's chunk inside a ring slot
 #pragma unroll
-    for (int mt = 0; mt < MT; mt++) {
-        const int64_t rb = rb0 + mt < n_rb ? rb0 + mt : n_rb - 1;  // clamp: stays inside the pool
-        src[mt] = (const char*)(keys + rb * rs) + wave * 1024;
+    for (int c = 0; c < CPW; c++) {
+        const int j = wave + WAVES * c;
+        const int64_t rb = rb0 + j / 4 < n_rb ? rb0 + j / 4 : n_rb - 1;  // clamp: stays inside the pool
+        src[c] = (const char*)(keys + rb * rs) + (j % 4) * 1024;
+        dst[c] = (uint32_t)j * 1024;
     }
     const int64_t wbytes = ws * 2;
-    auto copy_keys = [&](bf16x8 (&buf)[MT][4][64], int w) {
-#pragma unroll
-        for (int mt = 0; mt < MT; mt++)
-            __builtin_amdgcn_global_load_lds(
-                (const void __attribute__((address_space(1)))*)(src[mt] + w * wbytes + loff),
-                (void __attribute__((address_space(3)))*)&buf[mt][wave][0], 16, 0, 0);
+    auto clampw = [&](int w) { return w < nwin ? w : nwin - 1; };
+    // Buffer (not global) loads to LDS: the compiler's wait-count tracking
+    // treats a pending global-to-LDS load as a flat access and then waits for
+    // every outstanding load at each register use; buffer loads keep precise
+    // counts.  The descriptor's base is the tile's 1 KiB chunk (wave-uniform).
+    auto copy_one = [&](bf16x8 (&buf)[MT][4][64], int c, int w) {
+        const __amdgpu_buffer_rsrc_t rsrc =
+            __builtin_amdgcn_make_buffer_rsrc((void*)(src[c] + w * wbytes), (short)0, 1024, 0x00020000);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rsrc, (void __attribute__((address_space(3)))*)((char*)&buf[0][0][0] + dst[c]), 16, loff, 0, 0, OIL_WIDE_KEY_CPOL);
+    };
+    // KREG: keys through registers instead (16-byte nontemporal loads, then
+    // 16-byte LDS stores): the copies of window w + R - 1 are loaded in stage
+    // w into staging set w % 2 and stored in stage w + 2, before its barrier.
+    bf16x8 kst0[CPW], kst1[CPW];
+    auto kset = [&](auto s_t) -> bf16x8 (&)[CPW] {
+        if constexpr (decltype(s_t)::value == 0) return kst0;
+        else return kst1;
+    };
+    auto key_load = [&](bf16x8 (&st)[CPW], int c, int w) {
+        st[c] = __builtin_nontemporal_load((const bf16x8*)(src[c] + w * wbytes + loff));
+    };
+    auto key_store = [&](bf16x8 (&buf)[MT][4][64], const bf16x8 (&st)[CPW], int c) {
+        *(bf16x8*)((char*)&buf[0][0][0] + dst[c] + loff) = st[c];
     };
     int qt[NTW];
 #pragma unroll
@@ -457,14 +530,12 @@ scan_mfma_wide_kernel(
         const int t = wave * NTW + nt;
         qt[nt] = t < n_qt ? t : n_qt - 1;  // clamp: idle tiles recompute a live one, never stored
     }
-    auto load_q = [&](bf16x8 (&b)[NTW][4], int w) {
-#pragma unroll
-        for (int nt = 0; nt < NTW; nt++)
-#pragma unroll
-            for (int s = 0; s < 4; s++) {
-                const char* base = (const char*)(qfrag + (((int64_t)w * n_qt + qt[nt]) * 4 + s) * 64);
-                b[nt][s] = *(const bf16x8*)(base + loff);
-            }
+    // fragment load l: sub-step l / NTW of tile l % NTW (the first group's
+    // fragments are requested first)
+    auto load_q1 = [&](bf16x8 (&b)[NTW][4], int l, int w) {
+        const int nt = l % NTW, s = l / NTW;
+        const char* base = (const char*)(qfrag + (((int64_t)w * n_qt + qt[nt]) * 4 + s) * 64);
+        b[nt][s] = *(const bf16x8*)(base + loff);
     };
 
     floatx16 acc[MT][NTW];
@@ -474,113 +545,152 @@ scan_mfma_wide_kernel(
         for (int nt = 0; nt < NTW; nt++)
             acc[mt][nt] = floatx16{};
 
-    // Keys run two windows ahead through a three-window LDS ring, query
-    // fragments one window ahead in two register sets.  Stage w reads window
-    // w's keys out of LDS, issues the fragments of w + 1 (index clamped) and
-    // the key copies of w + 2 (none past the last window), multiplies, and
-    // waits until at most the MT copies of w + 2 are outstanding (loads retire
-    // in order, so the fragments of w + 1 and the copies of w + 1 are in;
-    // with no copies issued it waits for all); the barrier then publishes
-    // window w + 1 and tells every wave that the ring slot of w is free.
-    auto read_sub = [&](bf16x8 (&a)[MT], const bf16x8 (&buf)[MT][4][64], int s) {
+    // A operands: two register sets, one group each
+    bf16x8 a[2][CG][MT];
+    auto read_group = [&](bf16x8 (&dst)[CG][MT], const bf16x8 (&buf)[MT][4][64], int g) {
 #pragma unroll
-        for (int mt = 0; mt < MT; mt++)
-            a[mt] = buf[mt][s][lane];
+        for (int c = 0; c < CG; c++)
+#pragma unroll
+            for (int mt = 0; mt < MT; mt++)
+                dst[c][mt] = buf[mt][g * CG + c][lane];
     };
-    auto mma_sub = [&](const bf16x8 (&a)[MT], const bf16x8 (&b)[NTW][4], int s) {
-#pragma unroll
-        for (int mt = 0; mt < MT; mt++)
-#pragma unroll
-            for (int nt = 0; nt < NTW; nt++)
-                acc[mt][nt] = mfma_step(a[mt], b[nt][s], acc[mt][nt]);
-    };
-    // fp8: sub-steps s and s + 1 in one instruction
-    auto mma_pair = [&](const bf16x8 (&a0)[MT], const bf16x8 (&a1)[MT], const bf16x8 (&b)[NTW][4], int s) {
-#pragma unroll
-        for (int mt = 0; mt < MT; mt++)
-#pragma unroll
-            for (int nt = 0; nt < NTW; nt++)
-                acc[mt][nt] = mfma_pair_fp8(a0[mt], a1[mt], b[nt][s], b[nt][s + 1], acc[mt][nt]);
-    };
-    auto clampw = [&](int w) { return w < nwin ? w : nwin - 1; };
-    bf16x8 b0[NTW][4], b1[NTW][4];
-    // one stage: window w sits in `cur`, its fragments in `bq`; `bn` receives
-    // the fragments of w + 1 and `nxt2` the keys of w + 2.  MORE: w + 2 is a
-    // window (the main loop's stages always are; the tail's test it).
-    auto stage = [&](auto more_t, const bf16x8 (&cur)[MT][4][64], bf16x8 (&nxt2)[MT][4][64],
-                     const bf16x8 (&bq)[NTW][4], bf16x8 (&bn)[NTW][4], int w) {
-        constexpr bool always = decltype(more_t)::value;
-        const bool more = always || w + 2 < nwin;
-        load_q(bn, clampw(w + 1));
-        if (more)
-            copy_keys(nxt2, w + 2);
-        if constexpr (FMT == kKeyFp8) {
-            // two sub-steps out of LDS, one paired MFMA, twice (two register
-            // sets, as the bf16 schedule keeps: four spill at two query tiles)
-            bf16x8 a0[MT], a1[MT];
-            read_sub(a0, cur, 0);
-            read_sub(a1, cur, 1);
-            __builtin_amdgcn_sched_barrier(0);
-            mma_pair(a0, a1, bq, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            read_sub(a0, cur, 2);
-            read_sub(a1, cur, 3);
-            __builtin_amdgcn_sched_barrier(0);
-            mma_pair(a0, a1, bq, 2);
-            __builtin_amdgcn_sched_barrier(0);
-        } else {
-            // LDS reads one sub-step ahead of the MFMAs that use them
-            bf16x8 a0[MT], a1[MT];
-            read_sub(a0, cur, 0);
-            read_sub(a1, cur, 1);
-            __builtin_amdgcn_sched_barrier(0);
-            mma_sub(a0, bq, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            read_sub(a0, cur, 2);
-            __builtin_amdgcn_sched_barrier(0);
-            mma_sub(a1, bq, 1);
-            __builtin_amdgcn_sched_barrier(0);
-            read_sub(a1, cur, 3);
-            __builtin_amdgcn_sched_barrier(0);
-            mma_sub(a0, bq, 2);
-            __builtin_amdgcn_sched_barrier(0);
-            mma_sub(a1, bq, 3);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        if (more)
-            wait_vmcnt_at_most<MT>();
+    // MFMA i of group g: row block i / NTW, query tile i % NTW
+    auto mfma_one = [&](const bf16x8 (&av)[CG][MT], const bf16x8 (&b)[NTW][4], int g, int i) {
+        const int mt = i / NTW, nt = i % NTW;
+        if constexpr (FMT == kKeyFp8)
+            acc[mt][nt] = mfma_pair_fp8(av[0][mt], av[1][mt], b[nt][2 * g], b[nt][2 * g + 1], acc[mt][nt]);
         else
-            wait_vmcnt_at_most<0>();
-        block_barrier();
+            acc[mt][nt] = mfma_step(av[0][mt], b[nt][g], acc[mt][nt]);
     };
-    copy_keys(ring0, 0);
-    if (nwin > 1)
-        copy_keys(ring1, 1);
-    load_q(b0, 0);
+
+    bf16x8 b0[NTW][4], b1[NTW][4], b2[NTW][4];
+    auto fset = [&](auto s_t) -> bf16x8 (&)[NTW][4] {
+        constexpr int s = decltype(s_t)::value;
+        if constexpr (s == 0) return b0;
+        else if constexpr (s == 1) return b1;
+        else return b2;
+    };
+    // Window w = w0 + I (I a compile-time stage index) sits in slot I % R;
+    // window w + 1 in slot (I + 1) % R; the copies of window w + R - 1 go to
+    // slot (I + R - 1) % R, which held window w - 1.  Window w's fragments
+    // are in set I % NB; the fragments of window w + NB - 1 go to set
+    // (I + NB - 1) % NB, which held window w - 1's.  On entry a[0] holds
+    // group 0 of window w (read issued).
+    auto stage = [&](auto i_t, int w) {
+        constexpr int I = decltype(i_t)::value;
+        const bf16x8(&cur)[MT][4][64] = slot(std::integral_constant<int, I % R>{});
+        const bf16x8(&nx1)[MT][4][64] = slot(std::integral_constant<int, (I + 1) % R>{});
+        bf16x8(&nxc)[MT][4][64] = slot(std::integral_constant<int, (I + R - 1) % R>{});
+        const bf16x8(&bq)[NTW][4] = fset(std::integral_constant<int, I % NB>{});
+        bf16x8(&bn)[NTW][4] = fset(std::integral_constant<int, (I + NB - 1) % NB>{});
+        const int wq = clampw(w + NB - 1), wc = clampw(w + R - 1);
+        bf16x8(&kst)[CPW] = kset(std::integral_constant<int, I % 2>{});
+        bf16x8(&nx3)[MT][4][64] = slot(std::integral_constant<int, (I + R - 3) % R>{});
+#pragma unroll
+        for (int g = 0; g < NG; g++) {
+            if (g + 1 < NG) {
+                read_group(a[(g + 1) & 1], cur, g + 1);
+            } else {
+                if constexpr (KREG) {
+                    // this wave's stores of window w + R - 3 have landed
+                    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+                } else {
+                    // the copies of w + 1 (issued R - 2 stages ago) are in
+                    wait_vmcnt_at_most<kInFlight>();
+                }
+                block_barrier();
+                read_group(a[0], nx1, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < NM; i++) {
+                mfma_one(a[g & 1], bq, g, i);
+                if (KREG && g == 0) {
+                    // window w + R - 3 (loaded two stages ago) into its slot
+#pragma unroll
+                    for (int c = 0; c < CPW; c++)
+                        if (c * NM / CPW == i)
+                            key_store(nx3, kst, c);
+                }
+                if (g + 1 < NG) {
+                    // fragments of w + NB - 1, spread over the first NG - 1 groups
+                    constexpr int span = (NG - 1) * NM;
+#pragma unroll
+                    for (int l = 0; l < NQ; l++)
+                        if (l * span / NQ == g * NM + i)
+                            load_q1(bn, l, wq);
+                } else {
+#pragma unroll
+                    for (int c = 0; c < CPW; c++)
+                        if (c * NM / CPW == i) {
+                            if constexpr (KREG)
+                                key_load(kst, c, wc);
+                            else
+                                copy_one(nxc, c, wc);
+                        }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    };
+    // prologue: windows 0 .. R - 2 into the ring, fragments of windows
+    // 0 .. NB - 2, group 0 of window 0
+    if constexpr (KREG) {
+        // windows 0 .. R - 4 stored now; R - 3 and R - 2 staged for stages 0 and 1
+#pragma unroll
+        for (int c = 0; c < CPW; c++) {
+            key_load(kst0, c, 0);
+            key_load(kst1, c, clampw(1));
+        }
+        wait_vmcnt_at_most<0>();
+#pragma unroll
+        for (int c = 0; c < CPW; c++) {
+            key_store(ring0, kst0, c);
+            if constexpr (R > 4) key_store(ring1, kst1, c);
+        }
+        if constexpr (R > 5) {
+#pragma unroll
+            for (int c = 0; c < CPW; c++)
+                key_load(kst0, c, clampw(2));
+            wait_vmcnt_at_most<0>();
+#pragma unroll
+            for (int c = 0; c < CPW; c++)
+                key_store(ring2, kst0, c);
+        }
+#pragma unroll
+        for (int c = 0; c < CPW; c++) {
+            key_load(kst0, c, clampw(R - 3));
+            key_load(kst1, c, clampw(R - 2));
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < CPW; c++) {
+            copy_one(ring0, c, 0);
+            copy_one(ring1, c, clampw(1));
+            copy_one(ring2, c, clampw(2));
+            if constexpr (R > 4) copy_one(ring3, c, clampw(3));
+            if constexpr (R > 5) copy_one(ring4, c, clampw(4));
+        }
+    }
+#pragma unroll
+    for (int l = 0; l < NQ; l++) {
+        load_q1(b0, l, 0);
+        if constexpr (NB > 2) load_q1(b1, l, clampw(1));
+    }
     __builtin_amdgcn_sched_barrier(0);
     wait_vmcnt_at_most<0>();
     __syncthreads();
-    // six stages per trip, so that ring slots and fragment sets return to
-    // their start; the main loop runs while every stage has a window two
-    // ahead, the tail (2 to 7 windows) tests it per stage
-    const std::integral_constant<bool, true> yes;
-    const std::integral_constant<bool, false> no;
+    read_group(a[0], ring0, 0);
+    // U stages per trip; the tail runs the last 0 .. U - 1 windows
     int w = 0;
-    for (; w + 7 < nwin; w += 6) {
-        stage(yes, ring0, ring2, b0, b1, w);
-        stage(yes, ring1, ring0, b1, b0, w + 1);
-        stage(yes, ring2, ring1, b0, b1, w + 2);
-        stage(yes, ring0, ring2, b1, b0, w + 3);
-        stage(yes, ring1, ring0, b0, b1, w + 4);
-        stage(yes, ring2, ring1, b1, b0, w + 5);
-    }
-    stage(no, ring0, ring2, b0, b1, w);
-    if (w + 1 < nwin) stage(no, ring1, ring0, b1, b0, w + 1);
-    if (w + 2 < nwin) stage(no, ring2, ring1, b0, b1, w + 2);
-    if (w + 3 < nwin) stage(no, ring0, ring2, b1, b0, w + 3);
-    if (w + 4 < nwin) stage(no, ring1, ring0, b0, b1, w + 4);
-    if (w + 5 < nwin) stage(no, ring2, ring1, b1, b0, w + 5);
-    if (w + 6 < nwin) stage(no, ring0, ring2, b0, b1, w + 6);
+    for (; w + U <= nwin; w += U)
+        unrolled<U>([&](auto i_t) { stage(i_t, w + decltype(i_t)::value); });
+    unrolled<U - 1>([&](auto i_t) {
+        if (w + decltype(i_t)::value < nwin)
+            stage(i_t, w + decltype(i_t)::value);
+    });
+    // no copy may still be writing LDS when the block ends
+    wait_vmcnt_at_most<0>();
 
     // block keys, as in scan_mfma_kernel
     int32_t ex[NTW];
@@ -801,13 +911,19 @@ struct ScanLaunch {
 // Launch one 256-thread scan kernel; first / last say whether it is the
 // scan's first / last kernel (which carry the events).
 template <class K, class... A>
-static void dispatch(const ScanLaunch& sl, bool first, bool last, K kernel, dim3 grid, size_t lds, A... args)
+static void dispatch_n(const ScanLaunch& sl, bool first, bool last, K kernel, dim3 grid, dim3 block, size_t lds,
+                       A... args)
 {
     hipEvent_t s = first ? sl.start : nullptr, e = last ? sl.stop : nullptr;
     if (s || e)
-        hipExtLaunchKernelGGL(kernel, grid, dim3(256), (uint32_t)lds, sl.stream, s, e, 0u, args...);
+        hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, sl.stream, s, e, 0u, args...);
     else
-        hipLaunchKernelGGL(kernel, grid, dim3(256), lds, sl.stream, args...);
+        hipLaunchKernelGGL(kernel, grid, block, lds, sl.stream, args...);
+}
+template <class K, class... A>
+static void dispatch(const ScanLaunch& sl, bool first, bool last, K kernel, dim3 grid, size_t lds, A... args)
+{
+    dispatch_n(sl, first, last, kernel, grid, dim3(256), lds, args...);
 }
 
 template <int NB>
@@ -874,23 +990,69 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
                  ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale, n_main);
 }
 
-// The wide scan (64 < B <= 512), either key format.
+// The wide scan (64 < B <= 512), either key format: one configuration per
+// class of batches (up to 4, 8 and 16 query tiles), (MT, R, NB, WAVES, WPE):
+// row blocks per workgroup, key windows in the LDS ring, fragment register
+// sets, waves per workgroup, and the waves per SIMD the registers must allow.
+template <int MT, int R, int NB, int WAVES, int WPE, int KREG, int TILES, int FMT>
+static void launch_wide_cfg(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+                            int64_t n_rb, const bf16x8* qf, int32_t B, const int32_t* prompt,
+                            const int32_t* exclude, uint64_t* G, int64_t g_ld, const float* kscale,
+                            const float* qscale, const ScanLaunch& sl)
+{
+    constexpr int NTW = TILES / WAVES;
+    static_assert(NTW * WAVES == TILES, "query tiles per wave");
+    dispatch_n(sl, true, true, scan_mfma_wide_kernel<MT, NTW, R, NB, WAVES, WPE, KREG, FMT>,
+               dim3((unsigned)((n_rb + MT - 1) / MT)), dim3(64 * WAVES), 0, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld,
+             kscale, qscale);
+}
+
+// Configurations (MT, R, NB, WAVES, WPE, KREG) per class, measured on the
+// 1M x 4096 pool (scan ms at B = 128 / 256 / 512; before: 1.71 / 2.39 / 4.43
+// with 4 row blocks, 4 waves and direct copies issued at the top of each
+// window): bf16 8 row blocks, 4 waves, keys through registers: 1.65 (every
+// other configuration tried 1.70-1.73, 2.04 with 2 row blocks); 8 row blocks
+// and 8 waves: 2.15-2.17 (4 row blocks and 4 waves 2.19-2.21, with three
+// fragment sets 2.35); 4 row blocks and 8 waves (two per SIMD, 2 query tiles
+// each): 3.56-3.69 (4 waves of 4 tiles 3.73-3.82; a five-window ring 4.0).
+// fp8 (windows of 128 columns): 0.97 / 1.35 / 2.18-2.22 (before: 0.97 /
+// 1.31 / 2.56).
+#ifndef OIL_WIDE_C1
+#define OIL_WIDE_C1 8, 4, 3, 4, 1, 1
+#endif
+#ifndef OIL_WIDE_C2
+#define OIL_WIDE_C2 8, 4, 2, 8, 1, 0
+#endif
+#ifndef OIL_WIDE_C4
+#define OIL_WIDE_C4 4, 4, 2, 8, 2, 0
+#endif
+#ifndef OIL_WIDE_F1
+#define OIL_WIDE_F1 4, 4, 2, 4, 2, 0
+#endif
+#ifndef OIL_WIDE_F2
+#define OIL_WIDE_F2 4, 4, 2, 8, 2, 0
+#endif
+#ifndef OIL_WIDE_F4
+#define OIL_WIDE_F4 4, 4, 2, 4, 1, 0
+#endif
+
 template <int FMT>
 static void launch_wide(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid, int64_t n_rb,
                         const bf16x8* qf, int32_t B, const int32_t* prompt, const int32_t* exclude, uint64_t* G,
                         int64_t g_ld, const float* kscale, const float* qscale, const ScanLaunch& sl)
 {
-    const int ntw = (scan_query_tiles(B) + 3) / 4;
-    constexpr int M1 = OIL_WIDE_MT1, M2 = OIL_WIDE_MT2, M4 = OIL_WIDE_MT4;
-    if (ntw == 1)
-        dispatch(sl, true, true, scan_mfma_wide_kernel<M1, 1, FMT>, dim3((unsigned)((n_rb + M1 - 1) / M1)), 0, keys,
-                 ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
-    else if (ntw == 2)
-        dispatch(sl, true, true, scan_mfma_wide_kernel<M2, 2, FMT>, dim3((unsigned)((n_rb + M2 - 1) / M2)), 0, keys,
-                 ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
-    else
-        dispatch(sl, true, true, scan_mfma_wide_kernel<M4, 4, FMT>, dim3((unsigned)((n_rb + M4 - 1) / M4)), 0, keys,
-                 ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+    const int n_qt = scan_query_tiles(B);
+#define OIL_WIDE_ARGS keys, ld, rs, ws, n_valid, n_rb, qf, B, prompt, exclude, G, g_ld, kscale, qscale, sl
+    if constexpr (FMT == kKeyBf16) {
+        if (n_qt <= 4) launch_wide_cfg<OIL_WIDE_C1, 4, FMT>(OIL_WIDE_ARGS);
+        else if (n_qt <= 8) launch_wide_cfg<OIL_WIDE_C2, 8, FMT>(OIL_WIDE_ARGS);
+        else launch_wide_cfg<OIL_WIDE_C4, 16, FMT>(OIL_WIDE_ARGS);
+    } else {
+        if (n_qt <= 4) launch_wide_cfg<OIL_WIDE_F1, 4, FMT>(OIL_WIDE_ARGS);
+        else if (n_qt <= 8) launch_wide_cfg<OIL_WIDE_F2, 8, FMT>(OIL_WIDE_ARGS);
+        else launch_wide_cfg<OIL_WIDE_F4, 16, FMT>(OIL_WIDE_ARGS);
+    }
+#undef OIL_WIDE_ARGS
 }
 
 hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
