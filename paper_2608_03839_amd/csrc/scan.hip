@@ -317,9 +317,11 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     // Accumulator layout of a 32x32 MFMA tile: lane l, element 4 i + j holds
     // row 8 i + 4 (l / 32) + j (a key) and column l % 32 (a query).  Each
     // (query, row block) keeps its best (score, position) key.  The keys of
-    // the block's 4 MT row blocks are gathered in LDS and stored row by row
-    // (consecutive threads, consecutive row blocks of one query): whole
-    // cache lines instead of one scattered 8-byte store per query.
+    // the block's 4 MT row blocks are gathered in LDS and stored by the whole
+    // block, row by row (consecutive threads, consecutive row blocks of one
+    // query: 4 MT keys per query row) instead of one scattered 8-byte store
+    // per query (~30 us more at 1M x 4096, B = 32) or one segment per wave
+    // (6 us more).
     __shared__ uint64_t gk[4][NT * 32][MT + 1];  // per wave; +1: rows land in different banks
     int32_t ex[NT];
     float qs[NT];
@@ -361,16 +363,15 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
                 gk[wave][nt * 32 + r][mt] = best;
         }
     }
-    // the wave's own LDS rows: no barrier, only the wave's LDS writes must land
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-    __builtin_amdgcn_wave_barrier();
+    __syncthreads();
     const int nq = B < NT * 32 ? B : NT * 32;
+    constexpr int KPB = 4 * MT;  // the block's keys per query
 #pragma unroll
-    for (int c0 = 0; c0 < NT * 32 * MT; c0 += 64) {
-        const int c = c0 + lane;
-        const int q = c / MT, j = c % MT;
-        if (q < nq && rb0 + j < n_rb)
-            G[q * g_ld + rb0 + j] = gk[wave][q][j];
+    for (int c0 = 0; c0 < NT * 32 * KPB; c0 += 256) {
+        const int c = c0 + (int)threadIdx.x;
+        const int q = c / KPB, j = c % KPB;
+        if (q < nq && rbb + j < n_rb)
+            G[q * g_ld + rbb + j] = gk[j / MT][q][j % MT];
     }
 }
 
