@@ -189,18 +189,21 @@ def test_topk_wide_batches(oil, B):
 
 
 @pytest.mark.parametrize("d,B", [(64, 100), (128, 300), (256, 100), (320, 129), (384, 200), (448, 512),
-                                 (640, 256), (704, 128), (768, 300), (832, 257)])
+                                 (640, 256), (704, 128), (768, 300), (768, 100), (832, 257), (832, 65),
+                                 (1600, 128), (1600, 200)])
 def test_wide_batches_window_counts(oil, d, B):
-    """The wide scan's three-slot ring over 1 to 13 key windows: main loop
-    trips of six windows plus a tail of two to seven (or the tail alone), with
-    one, two and four query tiles per wave."""
+    """The wide scan's four-slot ring over 1 to 25 key windows: main-loop
+    trips of 12 windows (B <= 128: keys through registers, three fragment
+    sets) or 4 (B > 128), plus a tail of the rest (or the tail alone), for
+    each class of batch."""
     _query_case(oil, 3000 + d, d, B, 16, seed=60 + d)
 
 
-@pytest.mark.parametrize("d,B", [(128, 100), (640, 200), (768, 130), (1408, 300), (1536, 512)])
+@pytest.mark.parametrize("d,B", [(128, 100), (640, 100), (1408, 120), (640, 200), (768, 130), (1408, 300),
+                                 (1536, 512)])
 def test_wide_batches_window_counts_fp8(oil, d, B):
     """The same ring on fp8 keys (128-column windows): 1, 5, 6, 11 and 12
-    windows, one to four query tiles per wave."""
+    windows for each class of batch."""
     wp = workloads.Pool(workloads.PoolSpec(n=2500 + d, d=d, vocab=5000, seed=90 + d, n_clusters=16))
     n = wp.spec.n
     pool = oil.Pool(d, n, key_format="fp8")
