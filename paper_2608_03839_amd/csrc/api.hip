@@ -51,8 +51,8 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 int32_t hip_status(hipError_t e) { return e == hipSuccess ? OIL_OK : OIL_E_HIP; }
 
 struct QueryWorkspace {
-    size_t q_off, sc_off, g_off, ca_off, cb_off, total;
-    int64_t g_ld;
+    size_t q_off, sc_off, g_off, ca_off, cb_off, fs_off, total;
+    int64_t g_ld, fs_ld;  // fs_ld = 0: no full-score array (MFMA scans)
 };
 
 QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
@@ -67,12 +67,17 @@ QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
     w.g_ld = oil::topk_block_ld(p->capacity);
     const size_t g_bytes = (size_t)B * (size_t)w.g_ld * sizeof(uint64_t);
     const size_t c_bytes = oil::topk_cand_bytes(B, k, p->capacity);
+    // the GEMV scan (bf16, B <= 4) writes every score instead of being rescored
+    const bool gemv = p->fmt != oil::kKeyFp8 && !oil::scan_uses_mfma(B, p->ld);
+    w.fs_ld = gemv ? (int64_t)round_up((size_t)p->capacity, 64) : 0;
+    const size_t fs_bytes = (size_t)B * (size_t)w.fs_ld * sizeof(float);
     w.q_off = 0;
     w.sc_off = round_up(w.q_off + q_bytes, kAlign);
     w.g_off = round_up(w.sc_off + sc_bytes, kAlign);
     w.ca_off = round_up(w.g_off + g_bytes, kAlign);
     w.cb_off = round_up(w.ca_off + c_bytes, kAlign);
-    w.total = round_up(w.cb_off + c_bytes, kAlign);
+    w.fs_off = round_up(w.cb_off + c_bytes, kAlign);
+    w.total = round_up(w.fs_off + fs_bytes, kAlign);
     return w;
 }
 
@@ -105,6 +110,7 @@ int32_t query_topk_enqueue(const oil_pool* pool, const void* queries, int32_t q_
     uint64_t* G = (uint64_t*)(ws + w.g_off);
     uint64_t* ca = (uint64_t*)(ws + w.ca_off);
     uint64_t* cb = (uint64_t*)(ws + w.cb_off);
+    float* FS = w.fs_ld ? (float*)(ws + w.fs_off) : nullptr;
     const int64_t n_valid = pool->n_valid;
 
     const bool fp8 = pool->fmt == oil::kKeyFp8;
@@ -125,7 +131,8 @@ int32_t query_topk_enqueue(const oil_pool* pool, const void* queries, int32_t q_
         hipEvent_t ev0, ev1;
         timer_slot(&ev0, &ev1);
         e = oil::launch_scan(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, pool->prompts,
-                             exclude_prompt, G, w.g_ld, st, pool->fmt, pool->kscale, qscale, ev0, ev1);
+                             exclude_prompt, G, w.g_ld, st, pool->fmt, pool->kscale, qscale, ev0, ev1, FS,
+                             w.fs_ld);
         if (g_timer.ev && e == hipSuccess && n_valid > 0) {
             g_timer.seen++;
             if (ev0)
@@ -135,11 +142,11 @@ int32_t query_topk_enqueue(const oil_pool* pool, const void* queries, int32_t q_
     const uint64_t* chosen = nullptr;
     if (e == hipSuccess)
         e = oil::launch_topk_blocks(G, w.g_ld, n_valid, B, k, ca, cb, &chosen, st);
-    if (e == hipSuccess)
+    if (e == hipSuccess && !FS)
         e = oil::launch_rescore(pool->keys, pool->ld, pool->rs, pool->ws, n_valid, qbuf, B, chosen, k,
                                 pool->prompts, exclude_prompt, SC, st, pool->fmt, pool->kscale, qscale);
     if (e == hipSuccess)
-        e = oil::launch_topk_final(chosen, B, k, SC, n_valid, scores, idx, st);
+        e = oil::launch_topk_final(chosen, B, k, SC, n_valid, scores, idx, st, FS, w.fs_ld);
     return hip_status(e);
 }
 

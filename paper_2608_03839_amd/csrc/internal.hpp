@@ -51,7 +51,8 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
                        const void* qbuf, int32_t B, const int32_t* prompt, const int32_t* exclude,
                        uint64_t* G, int64_t g_ld, hipStream_t stream, int fmt = kKeyBf16,
                        const float* kscale = nullptr, const float* qscale = nullptr,
-                       hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+                       hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, float* full_scores = nullptr,
+                       int64_t fs_ld = 0);
 hipError_t launch_rescore(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                           const void* qbuf, int32_t B, const uint64_t* blocks, int32_t k,
                           const int32_t* prompt, const int32_t* exclude, float* SC,
@@ -72,8 +73,12 @@ size_t topk_cand_bytes(int32_t B, int32_t k, int64_t capacity);
 hipError_t launch_topk_blocks(const uint64_t* G, int64_t g_ld, int64_t n_valid, int32_t B, int32_t k,
                               uint64_t* cand_a, uint64_t* cand_b, const uint64_t** chosen,
                               hipStream_t stream);
+// SC: the rescored scores (k * 32 per query), or, with full_scores set (the
+// GEMV scan's every score, fs_ld per query), the chosen blocks' rows read
+// from there.
 hipError_t launch_topk_final(const uint64_t* chosen, int32_t B, int32_t k, const float* SC,
-                             int64_t n_valid, float* out_s, int32_t* out_i, hipStream_t stream);
+                             int64_t n_valid, float* out_s, int32_t* out_i, hipStream_t stream,
+                             const float* full_scores = nullptr, int64_t fs_ld = 0);
 
 // Plain streaming read of n16 16-byte words (measurement aid); XOR of the
 // words folded into *sink.

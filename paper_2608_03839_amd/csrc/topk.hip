@@ -15,7 +15,8 @@
 //      until one list of k remains; up to 4096 block keys, one workgroup
 //      takes them all);
 //   2. the rescore kernels (scan.hip) recompute the 32 scores of each chosen
-//      block, bit-identical to the scan's;
+//      block, bit-identical to the scan's (for the GEMV scan's batches, which
+//      write every score, the final step reads them instead);
 //   3. select the k largest of those k * 32 keys, ranked and written in order.
 // Selection inside a workgroup is a radix select over 8-bit digits of the
 // 64-bit keys (LDS histogram with wave-aggregated increments; it stops as
@@ -175,7 +176,7 @@ __global__ __launch_bounds__(kSelThreads) void topk_merge_kernel(
 template <int VPT>
 __global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
     const uint64_t* __restrict__ blocks, int k, const float* __restrict__ SC, int64_t n_valid,
-    float* __restrict__ out_s, int32_t* __restrict__ out_i)
+    float* __restrict__ out_s, int32_t* __restrict__ out_i, const float* __restrict__ FS, int64_t fs_ld)
 {
     __shared__ SelShared sh;
     __shared__ int64_t first_row[OIL_TOPK_MAX];
@@ -195,7 +196,7 @@ __global__ __launch_bounds__(kSelThreads) void topk_final_kernel(
         if (g < k && first_row[g] >= 0) {
             const int64_t row = first_row[g] + slot % kRowBlock;
             if (row < n_valid)
-                v[j] = rank_key(sc[slot], (uint32_t)row);
+                v[j] = rank_key(FS ? FS[b * fs_ld + row] : sc[slot], (uint32_t)row);
         }
     }
     block_select(v, k, sh);
@@ -274,14 +275,15 @@ hipError_t launch_topk_blocks(const uint64_t* G, int64_t g_ld, int64_t n_valid, 
 }
 
 hipError_t launch_topk_final(const uint64_t* chosen, int32_t B, int32_t k, const float* SC,
-                             int64_t n_valid, float* out_s, int32_t* out_i, hipStream_t stream)
+                             int64_t n_valid, float* out_s, int32_t* out_i, hipStream_t stream,
+                             const float* full_scores, int64_t fs_ld)
 {
     if (k * kRowBlock <= kSelThreads * 4)
         hipLaunchKernelGGL(topk_final_kernel<4>, dim3(B), dim3(kSelThreads), 0, stream, chosen, k, SC,
-                           n_valid, out_s, out_i);
+                           n_valid, out_s, out_i, full_scores, fs_ld);
     else
         hipLaunchKernelGGL(topk_final_kernel<kFinalVpt>, dim3(B), dim3(kSelThreads), 0, stream, chosen, k, SC,
-                           n_valid, out_s, out_i);
+                           n_valid, out_s, out_i, full_scores, fs_ld);
     return hipGetLastError();
 }
 
