@@ -762,12 +762,13 @@ __global__ __launch_bounds__(64) void rescore_mfma_kernel(
     const int h = lane >> 5, r = lane & 31;
     float* out = SC + ((int64_t)qb * k + slot) * kRowBlock;
     const uint64_t bk = blocks[(int64_t)qb * k + slot];
-    if (bk == 0) {
+    const int64_t rb = key_pos(bk) / kRowBlock;
+    // no block (or, defensively, one past the pool: nothing is read there)
+    if (bk == 0 || rb * kRowBlock >= n_valid) {
         if (lane < kRowBlock)
             out[lane] = __uint_as_float(kNoScoreBits);
         return;
     }
-    const int64_t rb = key_pos(bk) / kRowBlock;
     const int t = qb >> 5, n = qb & 31;
     const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
     const int64_t ws8 = ws / 8;
