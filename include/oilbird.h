@@ -151,7 +151,7 @@ int32_t oil_pool_append(oil_pool *pool, const void *keys, int32_t key_dtype, con
 
 /* Workspace bytes oil_pool_query_topk needs for B queries and k neighbours
  * (sized from the pool's capacity, so it stays valid as the pool grows; with
- * bf16 keys and B <= 4 it includes every score, B x capacity float32). */
+ * bf16 keys and B <= 4 it includes room for up to 2 MiB of scores). */
 size_t oil_query_workspace_bytes(const oil_pool *pool, int32_t B, int32_t k);
 
 /* Retrieval (Algorithm 1 retrieve step, Eq. 2): normalise each query row as

@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "../../include/oilbird.h"
@@ -43,6 +44,9 @@ static __device__ __align__(256) unsigned char scratch[OIL_QUERY_SCRATCH_BYTES];
 namespace {
 
 constexpr size_t kAlign = 256;
+// Most scores the GEMV scan writes per call (2 MiB): past it the writes cost
+// the scan more than rescoring the chosen blocks.
+constexpr int64_t kFullScoresMax = 1 << 19;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -67,9 +71,12 @@ QueryWorkspace carve(const oil_pool* p, int32_t B, int32_t k)
     w.g_ld = oil::topk_block_ld(p->capacity);
     const size_t g_bytes = (size_t)B * (size_t)w.g_ld * sizeof(uint64_t);
     const size_t c_bytes = oil::topk_cand_bytes(B, k, p->capacity);
-    // the GEMV scan (bf16, B <= 4) writes every score instead of being rescored
+    // the GEMV scan (bf16, B <= 4) writes every score instead of being
+    // rescored while B * n_valid <= kFullScoresMax (fs_ld per query, the
+    // positions a call may hold for that)
     const bool gemv = p->fmt != oil::kKeyFp8 && !oil::scan_uses_mfma(B, p->ld);
-    w.fs_ld = gemv ? (int64_t)round_up((size_t)p->capacity, 64) : 0;
+    const int64_t fs_max = (kFullScoresMax / B) / 64 * 64;
+    w.fs_ld = gemv ? std::min((int64_t)round_up((size_t)p->capacity, 64), fs_max) : 0;
     const size_t fs_bytes = (size_t)B * (size_t)w.fs_ld * sizeof(float);
     w.q_off = 0;
     w.sc_off = round_up(w.q_off + q_bytes, kAlign);
@@ -110,8 +117,8 @@ int32_t query_topk_enqueue(const oil_pool* pool, const void* queries, int32_t q_
     uint64_t* G = (uint64_t*)(ws + w.g_off);
     uint64_t* ca = (uint64_t*)(ws + w.ca_off);
     uint64_t* cb = (uint64_t*)(ws + w.cb_off);
-    float* FS = w.fs_ld ? (float*)(ws + w.fs_off) : nullptr;
     const int64_t n_valid = pool->n_valid;
+    float* FS = (w.fs_ld && n_valid <= w.fs_ld) ? (float*)(ws + w.fs_off) : nullptr;
 
     const bool fp8 = pool->fmt == oil::kKeyFp8;
     const bool mfma = fp8 || oil::scan_uses_mfma(B, pool->ld);
