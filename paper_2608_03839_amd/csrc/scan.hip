@@ -14,7 +14,7 @@
 // window the chip reads one contiguous region at a time, the access pattern
 // of a plain copy.
 //
-// Two kernels, chosen by the query batch:
+// Kernels, chosen by the query batch:
 //  * scan_gemv (B <= 4): a matrix-vector product on the vector ALU
 //    (v_dot2 bf16 -> fp32).  Lane l accumulates row l % 32 of the tile over
 //    half of each window's columns; one xor-32 exchange completes the row.
@@ -29,6 +29,9 @@
 //    fragment per instruction, the fragments pre-swizzled by query prep.
 //  * scan_mfma_wide (64 < B <= 512): the same instruction, keys shared by all
 //    query tiles through LDS (the contraction turns MFMA-bound near B ~ 300).
+//  * scan_tail (remainder of the B <= 64 scan): the few row blocks past its
+//    last whole generation of waves, one workgroup each, through a deep LDS
+//    ring.
 //
 // The first two run a software pipeline: a ring of PF + 1 register stages,
 // window w + PF requested before window w is consumed.  Loads are
@@ -87,6 +90,11 @@
 #endif
 #ifndef OIL_TAIL_PF2
 #define OIL_TAIL_PF2 3
+#endif
+// Remainders of up to one row block per compute unit past the B <= 64
+// scan's whole generations of waves go to scan_tail_kernel (0: never).
+#ifndef OIL_TAIL_LDS
+#define OIL_TAIL_LDS 1
 #endif
 // Cache policy of the wide scan's key copies: 2 = nt (streaming, as the
 // narrow scans' nontemporal key loads).
@@ -748,6 +756,176 @@ scan_mfma_wide_kernel(
     }
 }
 
+// ----------------------------------------------------------------- remainder of the B <= 64 scan
+// Row blocks past the last whole generation of scan_mfma_kernel's waves are
+// too few to keep HBM busy: each one's walk over the windows is bound by
+// load latency, not bandwidth.  Here one workgroup takes one such row block:
+// four copy waves stream its 4 KiB tiles into an LDS ring of TS chunks of TC
+// windows (copy wave v moves the 1 KiB operand chunk v of every window, with
+// buffer loads straight to LDS), so up to TS * TC windows are in flight, and
+// NT compute waves, one per query tile, run the row block's MFMA sequence:
+// the instructions of scan_mfma_kernel in the same order (windows in order,
+// sub-steps in order), so every score is bit-identical to the main grid's
+// and the rescore's.  The two kinds of waves run separate loops that meet at
+// the same two barriers per chunk (chunk i in LDS; chunk i consumed, its slot
+// free for chunk i + TS).  Query fragments go to registers TP windows ahead.
+#ifndef OIL_TAIL_TC
+#define OIL_TAIL_TC 8
+#endif
+#ifndef OIL_TAIL_TS
+#define OIL_TAIL_TS 4
+#endif
+template <int NT, int FMT>
+__global__ __launch_bounds__(64 * (NT + 4)) void scan_tail_kernel(
+    const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+    const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
+    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld,
+    const float* __restrict__ kscale, const float* __restrict__ qscale, int64_t rb_base)
+{
+    constexpr int TC = OIL_TAIL_TC, TS = OIL_TAIL_TS;
+    constexpr int TP = TC - 1;  // fragment prefetch distance (windows); set of window w: w % TC
+    static_assert(TC >= 2 && TS >= 2 && (TS - 1) * TC <= 63, "vmcnt range");
+    __shared__ bf16x8 ring[TS][TC][4][64];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
+    const int h = lane >> 5, r = lane & 31;
+    const int64_t rb = rb_base + blockIdx.x;
+    const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
+    const int nch = (nwin + TC - 1) / TC;
+    auto clampw = [&](int w) { return w < nwin ? w : nwin - 1; };
+
+    if (wave >= NT) {
+        // copy wave v: operand chunk v (1 KiB) of every window
+        const int v = wave - NT;
+        const char* src = (const char*)(keys + rb * rs) + v * 1024;
+        const int64_t wbytes = ws * 2;
+        const uint32_t loff = (uint32_t)lane * 16;
+        auto issue = [&](int ch) {
+            bf16x8(&buf)[TC][4][64] = ring[ch % TS];
+#pragma unroll
+            for (int c = 0; c < TC; c++) {
+                const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+                    (void*)(src + clampw(ch * TC + c) * wbytes), (short)0, 1024, 0x00020000);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rsrc, (void __attribute__((address_space(3)))*)&buf[c][v][0], 16, loff, 0, 0,
+                    OIL_WIDE_KEY_CPOL);
+            }
+        };
+        for (int ch = 0; ch < TS && ch < nch; ch++)
+            issue(ch);
+        for (int i = 0; i < nch; i++) {
+            // this wave's copies of chunk i have landed: the copies of at
+            // most TS - 1 later chunks may still be in flight
+            const int later = nch - 1 - i < TS - 1 ? nch - 1 - i : TS - 1;
+            unrolled<TS>([&](auto n_t) {
+                constexpr int n = decltype(n_t)::value;
+                if (later == n)
+                    wait_vmcnt_at_most<n * TC>();
+            });
+            block_barrier();  // chunk i is in LDS
+            block_barrier();  // chunk i has been read
+            if (i + TS < nch)
+                issue(i + TS);
+        }
+        return;
+    }
+
+    // compute wave nt: query tile nt
+    const int nt = wave;
+    const bf16x8* qf = qfrag + (int64_t)nt * 4 * 64 + lane;
+    auto load_frag = [&](bf16x8 (&b)[4], int w) {
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+            b[s] = qf[(((int64_t)w * NT) * 4 + s) * 64];
+    };
+    bf16x8 fb[TC][4];
+#pragma unroll
+    for (int p = 0; p < TP; p++)
+        load_frag(fb[p], clampw(p));
+    floatx16 acc = floatx16{};
+    // A operands: two register sets; window c's in set c % 2, read while
+    // window c - 1's MFMAs run (a chunk's first window: after its barrier)
+    bf16x8 a0[4], a1[4];
+    auto aset = [&](auto k_t) -> bf16x8(&)[4] {
+        if constexpr (decltype(k_t)::value == 0) return a0;
+        else return a1;
+    };
+    auto read_a = [&](bf16x8 (&a)[4], const bf16x8(&buf)[TC][4][64], int c) {
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+            a[s] = buf[c][s][lane];
+    };
+    // window c of chunk i: the fragments of window w + TP requested, the A
+    // operands of window c + 1 read, then window c's MFMAs (the scheduling
+    // barriers keep each window's loads and MFMAs in that order)
+    auto window = [&](const bf16x8(&buf)[TC][4][64], auto c_t, int w) {
+        constexpr int c = decltype(c_t)::value;
+        load_frag(fb[(c + TP) % TC], clampw(w + TP));
+        if constexpr (c + 1 < TC)
+            read_a(aset(std::integral_constant<int, (c + 1) % 2>{}), buf, c + 1);
+        __builtin_amdgcn_sched_barrier(0x0006);
+        const bf16x8(&a)[4] = aset(std::integral_constant<int, c % 2>{});
+        if constexpr (FMT == kKeyFp8) {
+            acc = mfma_pair_fp8(a[0], a[1], fb[c][0], fb[c][1], acc);
+            acc = mfma_pair_fp8(a[2], a[3], fb[c][2], fb[c][3], acc);
+        } else {
+#pragma unroll
+            for (int s = 0; s < 4; s++)
+                acc = mfma_step(a[s], fb[c][s], acc);
+        }
+        __builtin_amdgcn_sched_barrier(0x0006);
+    };
+    const int nfull = nwin / TC;
+    for (int i = 0; i < nfull; i++) {
+        block_barrier();  // chunk i is in LDS
+        const bf16x8(&buf)[TC][4][64] = ring[i % TS];
+        read_a(a0, buf, 0);
+        unrolled<TC>([&](auto c_t) { window(buf, c_t, i * TC + decltype(c_t)::value); });
+        block_barrier();  // chunk i has been read
+    }
+    if (nfull < nch) {  // the last, partial chunk
+        block_barrier();
+        const bf16x8(&buf)[TC][4][64] = ring[nfull % TS];
+        read_a(a0, buf, 0);
+        unrolled<TC>([&](auto c_t) {
+            const int w = nfull * TC + decltype(c_t)::value;
+            if (w < nwin)
+                window(buf, c_t, w);
+        });
+        block_barrier();
+    }
+
+    // block keys, as in scan_mfma_kernel
+    const int qb = nt * 32 + r;
+    const bool qlive = qb < B;
+    const int32_t ex = (exclude && qlive) ? exclude[qb] : -1;
+    const float qs = (FMT == kKeyBf16 || !qlive) ? 1.f : qscale[qb];
+    int32_t pr[16];
+    float ks[16];
+    if (exclude)
+        tile_rows_load(pr, prompt, rb * kRowBlock, h, n_valid);
+    if constexpr (FMT == kKeyFp8)
+        tile_rows_load(ks, kscale, rb * kRowBlock, h, n_valid);
+    uint64_t best = 0;
+#pragma unroll
+    for (int e = 0; e < 16; e++) {
+        const int64_t row = rb * kRowBlock + (e / 4) * 8 + h * 4 + e % 4;
+        if (row < n_valid) {
+            float v = acc[e];
+            if constexpr (FMT == kKeyFp8)
+                v = v * (ks[e] * qs);  // powers of two: exact
+            if (ex >= 0 && pr[e] == ex)
+                v = __uint_as_float(kNoScoreBits);
+            const uint64_t key = rank_key(v, (uint32_t)row);
+            best = key > best ? key : best;
+        }
+    }
+    const uint64_t other = __shfl_xor(best, 32, kWave);
+    best = other > best ? other : best;
+    if (qlive && h == 0)
+        G[qb * g_ld + rb] = best;
+}
+
 // ----------------------------------------------------------------- rescore the chosen blocks
 // One wave per (chosen block slot, query).  The block comes from its best key
 // (0: no block, the slot's scores are "no position").  Scores land in
@@ -984,12 +1162,22 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
     // (262,144 x 5,120, B = 16) the remainder's waves start only when the
     // generation ends: 2 / 7 / 15 row blocks cost the main grid 16 / 37 /
     // 87 us, the second launch 28 / 41 / 41 us.
+    // scan_tail_kernel (one workgroup per row block, a deep LDS ring) takes
+    // such a remainder when it holds at most one row block per compute unit:
+    // about 12 us at 1M x 4096 (B = 32) whatever the count.  Past two or more
+    // generations, fewer than 16 row blocks stay in the main grid (measured
+    // there: about 2 us for 8-15 of them).
     constexpr int64_t kTailMin = 16, kTailMinOneGen = 8;
     int64_t n_main = n_rb, n_tail = 0;
+    bool lds_tail = false;
     if (n_rb > gen) {
         const int64_t rem = n_rb % gen;
         const int64_t tail_min = n_rb < 2 * gen ? kTailMinOneGen : kTailMin;
-        if (rem >= tail_min && rem <= gen / 4) {
+        if (OIL_TAIL_LDS && rem >= (n_rb < 2 * gen ? 1 : kTailMin) && rem <= device_cus()) {
+            n_main = n_rb - rem;
+            n_tail = rem;
+            lds_tail = true;
+        } else if (rem >= tail_min && rem <= gen / 4) {
             n_main = n_rb - rem;
             n_tail = rem;
         }
@@ -997,7 +1185,10 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
     dispatch(sl, true, n_tail == 0, scan_mfma_kernel<MT, NT, PF, FMT>,
              dim3((unsigned)((n_main + 4 * MT - 1) / (4 * MT))), 0, keys, ld, rs, ws, n_valid, qf, B, prompt,
              exclude, G, g_ld, kscale, qscale, (int64_t)0);
-    if (n_tail > 0)
+    if (lds_tail)
+        dispatch_n(sl, false, true, scan_tail_kernel<NT, FMT>, dim3((unsigned)n_tail), dim3(64 * (NT + 4)), 0,
+                   keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale, n_main);
+    else if (n_tail > 0)
         dispatch(sl, false, true, scan_mfma_kernel<1, NT, TPF, FMT>, dim3((unsigned)((n_tail + 3) / 4)), 0, keys,
                  ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale, n_main);
 }

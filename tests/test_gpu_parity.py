@@ -137,13 +137,11 @@ def test_topk_runs_of_neighbours(oil, key_format, B, k):
                                                    ("bf16", 16, 400, 64), ("bf16", 16, 400, 576),
                                                    ("bf16", 40, 1000, 576), ("fp8", 8, 777, 576)])
 def test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=262144):
-    """Pools a little past a whole number of scan waves (262,144 rows plus up
-    to a few thousand): from 16 row blocks on (8 when the main grid is a
-    single generation of waves), the rows beyond go to the scan's remainder
-    launch (one row block per wave, deeper prefetch); fewer stay in the main
-    grid.  With prompt exclusion.  At d = 576 (9 bf16 windows, 5 fp8) the
-    remainder launch's prefetch ring (7 or 3 windows in flight) wraps and
-    takes its clamped tail."""
+    """Pools a little past a whole number of generations of scan waves
+    (262,144 rows plus up to a few thousand): the row blocks beyond, up to one
+    per compute unit, go to the remainder kernel (one workgroup per row block,
+    an LDS ring of 8-window chunks); with prompt exclusion.  At d = 576 (9
+    bf16 windows, 5 fp8) its last chunk is partial (1 or 5 windows)."""
     n = base + extra
     g = torch.Generator().manual_seed(B + extra)
     raw = torch.randn((n, d), generator=g)
@@ -176,10 +174,29 @@ def test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=262144):
                                                  ("fp8", 300, 576), ("bf16", 300, 576)])
 def test_topk_pool_past_one_generation(oil, key_format, extra, d):
     """131,072 rows are one generation of the fp8 scan's waves (two row blocks
-    per wave) and half of one for bf16: 10 extra row blocks go to the
-    remainder launch for fp8, 4 stay in the main grid; bf16 keeps all of
-    them in its single partial generation."""
+    per wave) and half of one for bf16: the 10 or 4 extra row blocks go to the
+    remainder kernel for fp8; bf16 keeps all of them in its single partial
+    generation."""
     test_topk_pool_past_whole_waves(oil, key_format, 8, extra, d, base=131072)
+
+
+@pytest.mark.parametrize("key_format,B,extra,d,base", [("bf16", 40, 1000, 2112, 131072),
+                                                        ("fp8", 8, 1000, 4352, 131072),
+                                                        ("bf16", 16, 1000, 2112, 262144)])
+def test_topk_remainder_ring_wraps(oil, key_format, B, extra, d, base):
+    """Remainders on rows wider than the remainder kernel's LDS ring (32
+    windows): 33 bf16 windows (four whole chunks, then one window) and 34 fp8
+    windows (four whole chunks, then two), one and two query tiles; the ring's
+    slots are reused and the last chunk is partial."""
+    test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
+
+
+@pytest.mark.parametrize("key_format,B", [("bf16", 16), ("fp8", 40)])
+def test_topk_large_remainder(oil, key_format, B):
+    """More remainder row blocks than compute units (375, past one generation
+    of bf16 waves or two of fp8 two-tile waves): they go to the
+    register-prefetch remainder launch (one row block per wave) instead."""
+    test_topk_pool_past_whole_waves(oil, key_format, B, 12000, 64)
 
 
 @pytest.mark.parametrize("B", [65, 96, 128, 200, 256, 512])
