@@ -394,7 +394,9 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 // ----------------------------------------------------------------- MFMA, wide batches (64 < B <= 512)
 // Past ~300 queries the contraction is MFMA-bound, so keys must be fetched
 // once and reused by every query tile.  A block owns MT row blocks; its WAVES
-// waves split the query tiles (NTW tiles each).  Each key window of the block
+// waves split the query tiles (NTW tiles each) and, in groups of RS, the row
+// blocks (MT / RS each: more waves share a key window without more
+// accumulation registers per wave).  Each key window of the block
 // (MT tiles of 4 KiB) lands in LDS once, in an R-window ring, shared by every
 // wave: either with 16-byte buffer loads straight to LDS (each wave copies
 // 4 MT / WAVES of the block's 1 KiB chunks), or (KREG) through registers:
@@ -459,7 +461,7 @@ __device__ __forceinline__ void unrolled(F&& f)
     unrolled_impl(std::make_integer_sequence<int, N>{}, f);
 }
 
-template <int MT, int NTW, int R, int NB, int WAVES, int WPE, int KREG, int FMT>
+template <int MT, int NTW, int R, int NB, int WAVES, int WPE, int KREG, int FMT, int RS>
 __global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(WPE))) void
 scan_mfma_wide_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
@@ -469,7 +471,9 @@ scan_mfma_wide_kernel(
 {
     constexpr int NG = FMT == kKeyBf16 ? 4 : 2;  // MFMA groups per window
     constexpr int CG = 4 / NG;                   // 1 KiB operand chunks per group
-    constexpr int NM = MT * NTW;                 // MFMAs per group
+    constexpr int MTW = MT / RS;                 // row blocks per wave (RS waves share a tile group)
+    static_assert(MTW * RS == MT && WAVES % RS == 0, "row split");
+    constexpr int NM = MTW * NTW;                // MFMAs per group
     constexpr int NQ = NTW * 4;                  // fragment loads per window
     constexpr int CPW = 4 * MT / WAVES;          // 1 KiB key copies per wave and window
     static_assert(CPW * WAVES == 4 * MT && (NB == 2 || NB == 3), "copy split / fragment sets");
@@ -496,6 +500,7 @@ scan_mfma_wide_kernel(
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
     const int h = lane >> 5, r = lane & 31;
+    const int rp = wave % RS, tg = wave / RS;  // the wave's row part and tile group
     const int64_t rb0 = (int64_t)blockIdx.x * MT;
     const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
     const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
@@ -544,7 +549,7 @@ scan_mfma_wide_kernel(
     int qt[NTW];
 #pragma unroll
     for (int nt = 0; nt < NTW; nt++) {
-        const int t = wave * NTW + nt;
+        const int t = tg * NTW + nt;
         qt[nt] = t < n_qt ? t : n_qt - 1;  // clamp: idle tiles recompute a live one, never stored
     }
     // fragment load l: sub-step l / NTW of tile l % NTW (the first group's
@@ -555,24 +560,24 @@ scan_mfma_wide_kernel(
         b[nt][s] = *(const bf16x8*)(base + loff);
     };
 
-    floatx16 acc[MT][NTW];
+    floatx16 acc[MTW][NTW];
 #pragma unroll
-    for (int mt = 0; mt < MT; mt++)
+    for (int mt = 0; mt < MTW; mt++)
 #pragma unroll
         for (int nt = 0; nt < NTW; nt++)
             acc[mt][nt] = floatx16{};
 
     // A operands: two register sets, one group each
-    bf16x8 a[2][CG][MT];
-    auto read_group = [&](bf16x8 (&dst)[CG][MT], const bf16x8 (&buf)[MT][4][64], int g) {
+    bf16x8 a[2][CG][MTW];
+    auto read_group = [&](bf16x8 (&dst)[CG][MTW], const bf16x8 (&buf)[MT][4][64], int g) {
 #pragma unroll
         for (int c = 0; c < CG; c++)
 #pragma unroll
-            for (int mt = 0; mt < MT; mt++)
-                dst[c][mt] = buf[mt][g * CG + c][lane];
+            for (int mt = 0; mt < MTW; mt++)
+                dst[c][mt] = buf[rp * MTW + mt][g * CG + c][lane];
     };
     // MFMA i of group g: row block i / NTW, query tile i % NTW
-    auto mfma_one = [&](const bf16x8 (&av)[CG][MT], const bf16x8 (&b)[NTW][4], int g, int i) {
+    auto mfma_one = [&](const bf16x8 (&av)[CG][MTW], const bf16x8 (&b)[NTW][4], int g, int i) {
         const int mt = i / NTW, nt = i % NTW;
         if constexpr (FMT == kKeyFp8)
             acc[mt][nt] = mfma_pair_fp8(av[0][mt], av[1][mt], b[nt][2 * g], b[nt][2 * g + 1], acc[mt][nt]);
@@ -714,13 +719,13 @@ scan_mfma_wide_kernel(
     float qs[NTW];
 #pragma unroll
     for (int nt = 0; nt < NTW; nt++) {
-        const int qb = (wave * NTW + nt) * 32 + r;
+        const int qb = (tg * NTW + nt) * 32 + r;
         ex[nt] = (exclude && qb < B) ? exclude[qb] : -1;
         qs[nt] = (FMT == kKeyBf16 || qb >= B) ? 1.f : qscale[qb];
     }
 #pragma unroll
-    for (int mt = 0; mt < MT; mt++) {
-        const int64_t rb = rb0 + mt;
+    for (int mt = 0; mt < MTW; mt++) {
+        const int64_t rb = rb0 + rp * MTW + mt;
         int32_t pr[16];
         float ks[16];
         if (exclude)
@@ -729,7 +734,7 @@ scan_mfma_wide_kernel(
             tile_rows_load(ks, kscale, rb * kRowBlock, h, n_valid);
 #pragma unroll
         for (int nt = 0; nt < NTW; nt++) {
-            const int qb = (wave * NTW + nt) * 32 + r;
+            const int qb = (tg * NTW + nt) * 32 + r;
             // the tile moves out of the accumulation registers here, one tile at a time
             floatx16 t = acc[mt][nt];
             asm volatile("" : "+v"(t));
@@ -1194,49 +1199,53 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
 }
 
 // The wide scan (64 < B <= 512), either key format: one configuration per
-// class of batches (up to 4, 8 and 16 query tiles), (MT, R, NB, WAVES, WPE):
-// row blocks per workgroup, key windows in the LDS ring, fragment register
-// sets, waves per workgroup, and the waves per SIMD the registers must allow.
-template <int MT, int R, int NB, int WAVES, int WPE, int KREG, int TILES, int FMT>
+// class of batches (up to 4, 8 and 16 query tiles), (MT, R, NB, WAVES, WPE,
+// KREG, RS): row blocks per workgroup, key windows in the LDS ring, fragment
+// register sets, waves per workgroup, the waves per SIMD the registers must
+// allow, keys through registers, and the waves that split a tile's row blocks.
+template <int MT, int R, int NB, int WAVES, int WPE, int KREG, int RS, int TILES, int FMT>
 static void launch_wide_cfg(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                             int64_t n_rb, const bf16x8* qf, int32_t B, const int32_t* prompt,
                             const int32_t* exclude, uint64_t* G, int64_t g_ld, const float* kscale,
                             const float* qscale, const ScanLaunch& sl)
 {
-    constexpr int NTW = TILES / WAVES;
-    static_assert(NTW * WAVES == TILES, "query tiles per wave");
-    dispatch_n(sl, true, true, scan_mfma_wide_kernel<MT, NTW, R, NB, WAVES, WPE, KREG, FMT>,
+    constexpr int NTW = TILES * RS / WAVES;
+    static_assert(NTW * WAVES == TILES * RS, "query tiles per wave");
+    dispatch_n(sl, true, true, scan_mfma_wide_kernel<MT, NTW, R, NB, WAVES, WPE, KREG, FMT, RS>,
                dim3((unsigned)((n_rb + MT - 1) / MT)), dim3(64 * WAVES), 0, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld,
              kscale, qscale);
 }
 
-// Configurations (MT, R, NB, WAVES, WPE, KREG) per class, measured on the
-// 1M x 4096 pool (scan ms at B = 128 / 256 / 512; before: 1.71 / 2.39 / 4.43
-// with 4 row blocks, 4 waves and direct copies issued at the top of each
-// window): bf16 8 row blocks, 4 waves, keys through registers: 1.65 (every
-// other configuration tried 1.70-1.73, 2.04 with 2 row blocks); 8 row blocks
-// and 8 waves: 2.15-2.17 (4 row blocks and 4 waves 2.19-2.21, with three
-// fragment sets 2.35); 4 row blocks and 8 waves (two per SIMD, 2 query tiles
-// each): 3.56-3.69 (4 waves of 4 tiles 3.73-3.82; a five-window ring 4.0).
-// fp8 (windows of 128 columns): 0.97 / 1.35 / 2.18-2.22 (before: 0.97 /
-// 1.31 / 2.56).
+// Configurations (MT, R, NB, WAVES, WPE, KREG, RS) per class, measured on
+// the 1M x 4096 pool (scan ms at B = 128 / 256 / 512; before: 1.71 / 2.39 /
+// 4.43 with 4 row blocks, 4 waves and direct copies issued at the top of each
+// window): bf16 8 row blocks, 8 waves (two per SIMD), each 4 row blocks of
+// one tile: 1.49-1.51 (4 waves of 8 row blocks, keys through registers,
+// 1.58-1.65; a five-window ring 1.52; keys through registers 1.54; 4 row
+// splits 1.62; 4 row blocks 1.77); 8 row blocks and 8 waves of 8 row blocks
+// each: 2.05-2.17 (row split 2.05-2.06; 4 row blocks and 4 waves 2.19-2.21,
+// with three fragment sets 2.35); 4 row blocks and 8 waves (two per SIMD, 2
+// query tiles each): 3.56-3.69 (4 waves of 4 tiles 3.73-3.82; a five-window
+// ring 4.0; row splits need more than 256 registers).  fp8 (windows of 128
+// columns): 0.88 / 1.29-1.35 / 2.18-2.22 (before: 0.97 / 1.31 / 2.56; 4 row
+// blocks of 4 waves at B <= 128: 0.95).
 #ifndef OIL_WIDE_C1
-#define OIL_WIDE_C1 8, 4, 3, 4, 1, 1
+#define OIL_WIDE_C1 8, 4, 2, 8, 2, 0, 2
 #endif
 #ifndef OIL_WIDE_C2
-#define OIL_WIDE_C2 8, 4, 2, 8, 1, 0
+#define OIL_WIDE_C2 8, 4, 2, 8, 1, 0, 1
 #endif
 #ifndef OIL_WIDE_C4
-#define OIL_WIDE_C4 4, 4, 2, 8, 2, 0
+#define OIL_WIDE_C4 4, 4, 2, 8, 2, 0, 1
 #endif
 #ifndef OIL_WIDE_F1
-#define OIL_WIDE_F1 4, 4, 2, 4, 2, 0
+#define OIL_WIDE_F1 8, 4, 2, 8, 2, 0, 2
 #endif
 #ifndef OIL_WIDE_F2
-#define OIL_WIDE_F2 4, 4, 2, 8, 2, 0
+#define OIL_WIDE_F2 4, 4, 2, 8, 2, 0, 1
 #endif
 #ifndef OIL_WIDE_F4
-#define OIL_WIDE_F4 4, 4, 2, 4, 1, 0
+#define OIL_WIDE_F4 4, 4, 2, 4, 1, 0, 1
 #endif
 
 template <int FMT>
