@@ -398,10 +398,9 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 // blocks (MT / RS each: more waves share a key window without more
 // accumulation registers per wave).  Each key window of the block
 // (MT tiles of 4 KiB) lands in LDS once, in an R-window ring, shared by every
-// wave: either with 16-byte buffer loads straight to LDS (each wave copies
-// 4 MT / WAVES of the block's 1 KiB chunks), or (KREG) through registers:
-// 16-byte nontemporal loads two windows ahead, then 16-byte LDS stores.
-// Every wave reads its A operands from LDS (lane l's 16 bytes sit at 16 l:
+// wave, with 16-byte buffer loads straight to LDS (each wave copies 4 MT /
+// WAVES of the block's 1 KiB chunks; loading the keys through registers and
+// storing them to LDS measured slower).  Every wave reads its A operands from LDS (lane l's 16 bytes sit at 16 l:
 // conflict-free) and its own query fragments from L2 into registers, NB - 1
 // windows ahead.  Per (row block, query tile) the MFMA sequence is the same
 // as in scan_mfma_kernel (windows in order, sub-steps in order), so scores
@@ -412,9 +411,8 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 // MFMAs run; the fragments of window w + NB - 1 are requested between the
 // MFMAs of the first NG - 1 groups (one load every few MFMAs: a burst of
 // loads ahead of the MFMAs would hold up their issue).  Before the last group
-// each wave makes sure its part of window w + 1 is in LDS (direct copies:
-// wait for the copies issued R - 2 windows earlier; KREG: wait for the LDS
-// stores made in this stage's first group), and the waves meet at one
+// each wave makes sure its part of window w + 1 is in LDS (it waits for the
+// copies it issued R - 2 windows earlier), and the waves meet at one
 // barrier: window w + 1 is then in LDS, and every wave has finished reading
 // window w - 1, whose slot receives the copies of window w + R - 1, issued
 // between the last group's MFMAs.  The first A operands of window w + 1 are
@@ -461,7 +459,7 @@ __device__ __forceinline__ void unrolled(F&& f)
     unrolled_impl(std::make_integer_sequence<int, N>{}, f);
 }
 
-template <int MT, int NTW, int R, int NB, int WAVES, int WPE, int KREG, int FMT, int RS>
+template <int MT, int NTW, int R, int NB, int WAVES, int WPE, int FMT, int RS>
 __global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(WPE))) void
 scan_mfma_wide_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
@@ -482,8 +480,7 @@ scan_mfma_wide_kernel(
     constexpr int kInFlight = (R - 3) * (NQ + CPW) + NQ;
     static_assert(R >= 4 && R <= 6 && kInFlight <= 63, "ring depth / vmcnt range");
     // stages per trip: ring slot and fragment set return to their start
-    constexpr int U0 = R * NB / std::gcd(R, NB);
-    constexpr int U = KREG && U0 % 2 ? 2 * U0 : U0;  // KREG: staging sets alternate too
+    constexpr int U = R * NB / std::gcd(R, NB);
     // R windows of the block's MT key tiles, as separate LDS objects so that
     // the slot each access uses is known at compile time (unused ones vanish)
     __shared__ bf16x8 ring0[MT][4][64], ring1[MT][4][64], ring2[MT][4][64], ring3[MT][4][64],
@@ -531,20 +528,6 @@ scan_mfma_wide_kernel(
             __builtin_amdgcn_make_buffer_rsrc((void*)(src[c] + w * wbytes), (short)0, 1024, 0x00020000);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             rsrc, (void __attribute__((address_space(3)))*)((char*)&buf[0][0][0] + dst[c]), 16, loff, 0, 0, OIL_WIDE_KEY_CPOL);
-    };
-    // KREG: keys through registers instead (16-byte nontemporal loads, then
-    // 16-byte LDS stores): the copies of window w + R - 1 are loaded in stage
-    // w into staging set w % 2 and stored in stage w + 2, before its barrier.
-    bf16x8 kst0[CPW], kst1[CPW];
-    auto kset = [&](auto s_t) -> bf16x8 (&)[CPW] {
-        if constexpr (decltype(s_t)::value == 0) return kst0;
-        else return kst1;
-    };
-    auto key_load = [&](bf16x8 (&st)[CPW], int c, int w) {
-        st[c] = __builtin_nontemporal_load((const bf16x8*)(src[c] + w * wbytes + loff));
-    };
-    auto key_store = [&](bf16x8 (&buf)[MT][4][64], const bf16x8 (&st)[CPW], int c) {
-        *(bf16x8*)((char*)&buf[0][0][0] + dst[c] + loff) = st[c];
     };
     int qt[NTW];
 #pragma unroll
@@ -606,20 +589,13 @@ scan_mfma_wide_kernel(
         const bf16x8(&bq)[NTW][4] = fset(std::integral_constant<int, I % NB>{});
         bf16x8(&bn)[NTW][4] = fset(std::integral_constant<int, (I + NB - 1) % NB>{});
         const int wq = clampw(w + NB - 1), wc = clampw(w + R - 1);
-        bf16x8(&kst)[CPW] = kset(std::integral_constant<int, I % 2>{});
-        bf16x8(&nx3)[MT][4][64] = slot(std::integral_constant<int, (I + R - 3) % R>{});
 #pragma unroll
         for (int g = 0; g < NG; g++) {
             if (g + 1 < NG) {
                 read_group(a[(g + 1) & 1], cur, g + 1);
             } else {
-                if constexpr (KREG) {
-                    // this wave's stores of window w + R - 3 have landed
-                    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-                } else {
-                    // the copies of w + 1 (issued R - 2 stages ago) are in
-                    wait_vmcnt_at_most<kInFlight>();
-                }
+                // the copies of w + 1 (issued R - 2 stages ago) are in
+                wait_vmcnt_at_most<kInFlight>();
                 block_barrier();
                 read_group(a[0], nx1, 0);
             }
@@ -627,13 +603,6 @@ scan_mfma_wide_kernel(
 #pragma unroll
             for (int i = 0; i < NM; i++) {
                 mfma_one(a[g & 1], bq, g, i);
-                if (KREG && g == 0) {
-                    // window w + R - 3 (loaded two stages ago) into its slot
-#pragma unroll
-                    for (int c = 0; c < CPW; c++)
-                        if (c * NM / CPW == i)
-                            key_store(nx3, kst, c);
-                }
                 if (g + 1 < NG) {
                     // fragments of w + NB - 1, spread over the first NG - 1 groups
                     constexpr int span = (NG - 1) * NM;
@@ -644,12 +613,8 @@ scan_mfma_wide_kernel(
                 } else {
 #pragma unroll
                     for (int c = 0; c < CPW; c++)
-                        if (c * NM / CPW == i) {
-                            if constexpr (KREG)
-                                key_load(kst, c, wc);
-                            else
-                                copy_one(nxc, c, wc);
-                        }
+                        if (c * NM / CPW == i)
+                            copy_one(nxc, c, wc);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -657,42 +622,13 @@ scan_mfma_wide_kernel(
     };
     // prologue: windows 0 .. R - 2 into the ring, fragments of windows
     // 0 .. NB - 2, group 0 of window 0
-    if constexpr (KREG) {
-        // windows 0 .. R - 4 stored now; R - 3 and R - 2 staged for stages 0 and 1
 #pragma unroll
-        for (int c = 0; c < CPW; c++) {
-            key_load(kst0, c, 0);
-            key_load(kst1, c, clampw(1));
-        }
-        wait_vmcnt_at_most<0>();
-#pragma unroll
-        for (int c = 0; c < CPW; c++) {
-            key_store(ring0, kst0, c);
-            if constexpr (R > 4) key_store(ring1, kst1, c);
-        }
-        if constexpr (R > 5) {
-#pragma unroll
-            for (int c = 0; c < CPW; c++)
-                key_load(kst0, c, clampw(2));
-            wait_vmcnt_at_most<0>();
-#pragma unroll
-            for (int c = 0; c < CPW; c++)
-                key_store(ring2, kst0, c);
-        }
-#pragma unroll
-        for (int c = 0; c < CPW; c++) {
-            key_load(kst0, c, clampw(R - 3));
-            key_load(kst1, c, clampw(R - 2));
-        }
-    } else {
-#pragma unroll
-        for (int c = 0; c < CPW; c++) {
-            copy_one(ring0, c, 0);
-            copy_one(ring1, c, clampw(1));
-            copy_one(ring2, c, clampw(2));
-            if constexpr (R > 4) copy_one(ring3, c, clampw(3));
-            if constexpr (R > 5) copy_one(ring4, c, clampw(4));
-        }
+    for (int c = 0; c < CPW; c++) {
+        copy_one(ring0, c, 0);
+        copy_one(ring1, c, clampw(1));
+        copy_one(ring2, c, clampw(2));
+        if constexpr (R > 4) copy_one(ring3, c, clampw(3));
+        if constexpr (R > 5) copy_one(ring4, c, clampw(4));
     }
 #pragma unroll
     for (int l = 0; l < NQ; l++) {
@@ -1200,10 +1136,10 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
 
 // The wide scan (64 < B <= 512), either key format: one configuration per
 // class of batches (up to 4, 8 and 16 query tiles), (MT, R, NB, WAVES, WPE,
-// KREG, RS): row blocks per workgroup, key windows in the LDS ring, fragment
+// RS): row blocks per workgroup, key windows in the LDS ring, fragment
 // register sets, waves per workgroup, the waves per SIMD the registers must
-// allow, keys through registers, and the waves that split a tile's row blocks.
-template <int MT, int R, int NB, int WAVES, int WPE, int KREG, int RS, int TILES, int FMT>
+// allow, and the waves that split a tile's row blocks.
+template <int MT, int R, int NB, int WAVES, int WPE, int RS, int TILES, int FMT>
 static void launch_wide_cfg(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
                             int64_t n_rb, const bf16x8* qf, int32_t B, const int32_t* prompt,
                             const int32_t* exclude, uint64_t* G, int64_t g_ld, const float* kscale,
@@ -1211,12 +1147,12 @@ static void launch_wide_cfg(const uint16_t* keys, int32_t ld, int64_t rs, int64_
 {
     constexpr int NTW = TILES * RS / WAVES;
     static_assert(NTW * WAVES == TILES * RS, "query tiles per wave");
-    dispatch_n(sl, true, true, scan_mfma_wide_kernel<MT, NTW, R, NB, WAVES, WPE, KREG, FMT, RS>,
+    dispatch_n(sl, true, true, scan_mfma_wide_kernel<MT, NTW, R, NB, WAVES, WPE, FMT, RS>,
                dim3((unsigned)((n_rb + MT - 1) / MT)), dim3(64 * WAVES), 0, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld,
              kscale, qscale);
 }
 
-// Configurations (MT, R, NB, WAVES, WPE, KREG, RS) per class, measured on
+// Configurations (MT, R, NB, WAVES, WPE, RS) per class, measured on
 // the 1M x 4096 pool (scan ms at B = 128 / 256 / 512; before: 1.71 / 2.39 /
 // 4.43 with 4 row blocks, 4 waves and direct copies issued at the top of each
 // window): bf16 8 row blocks, 8 waves (two per SIMD), each 4 row blocks of
@@ -1230,22 +1166,22 @@ static void launch_wide_cfg(const uint16_t* keys, int32_t ld, int64_t rs, int64_
 // columns): 0.88 / 1.29-1.35 / 2.18-2.22 (before: 0.97 / 1.31 / 2.56; 4 row
 // blocks of 4 waves at B <= 128: 0.95).
 #ifndef OIL_WIDE_C1
-#define OIL_WIDE_C1 8, 4, 2, 8, 2, 0, 2
+#define OIL_WIDE_C1 8, 4, 2, 8, 2, 2
 #endif
 #ifndef OIL_WIDE_C2
-#define OIL_WIDE_C2 8, 4, 2, 8, 1, 0, 1
+#define OIL_WIDE_C2 8, 4, 2, 8, 1, 1
 #endif
 #ifndef OIL_WIDE_C4
-#define OIL_WIDE_C4 4, 4, 2, 8, 2, 0, 1
+#define OIL_WIDE_C4 4, 4, 2, 8, 2, 1
 #endif
 #ifndef OIL_WIDE_F1
-#define OIL_WIDE_F1 8, 4, 2, 8, 2, 0, 2
+#define OIL_WIDE_F1 8, 4, 2, 8, 2, 2
 #endif
 #ifndef OIL_WIDE_F2
-#define OIL_WIDE_F2 4, 4, 2, 8, 2, 0, 1
+#define OIL_WIDE_F2 4, 4, 2, 8, 2, 1
 #endif
 #ifndef OIL_WIDE_F4
-#define OIL_WIDE_F4 4, 4, 2, 4, 1, 0, 1
+#define OIL_WIDE_F4 4, 4, 2, 4, 1, 1
 #endif
 
 template <int FMT>
