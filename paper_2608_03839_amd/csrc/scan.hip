@@ -459,7 +459,7 @@ __device__ __forceinline__ void unrolled(F&& f)
     unrolled_impl(std::make_integer_sequence<int, N>{}, f);
 }
 
-template <int MT, int NTW, int R, int NB, int WAVES, int WPE, int FMT, int RS>
+template <int MT, int NTW, int R, int NB, int WAVES, int WPE, int FMT, int RS, int SKIP>
 __global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(WPE))) void
 scan_mfma_wide_kernel(
     const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
@@ -560,12 +560,21 @@ scan_mfma_wide_kernel(
                 dst[c][mt] = buf[rp * MTW + mt][g * CG + c][lane];
     };
     // MFMA i of group g: row block i / NTW, query tile i % NTW
+    // SKIP (batches that leave the class's last tiles empty): those tiles
+    // skip their MFMAs (a scalar branch each, which costs full batches up to
+    // 5%, hence a separate instantiation)
+    bool tlive[NTW];
+#pragma unroll
+    for (int nt = 0; nt < NTW; nt++)
+        tlive[nt] = tg * NTW + nt < n_qt;  // wave-uniform
     auto mfma_one = [&](const bf16x8 (&av)[CG][MTW], const bf16x8 (&b)[NTW][4], int g, int i) {
         const int mt = i / NTW, nt = i % NTW;
-        if constexpr (FMT == kKeyFp8)
-            acc[mt][nt] = mfma_pair_fp8(av[0][mt], av[1][mt], b[nt][2 * g], b[nt][2 * g + 1], acc[mt][nt]);
-        else
-            acc[mt][nt] = mfma_step(av[0][mt], b[nt][g], acc[mt][nt]);
+        if (!SKIP || tlive[nt]) {
+            if constexpr (FMT == kKeyFp8)
+                acc[mt][nt] = mfma_pair_fp8(av[0][mt], av[1][mt], b[nt][2 * g], b[nt][2 * g + 1], acc[mt][nt]);
+            else
+                acc[mt][nt] = mfma_step(av[0][mt], b[nt][g], acc[mt][nt]);
+        }
     };
 
     bf16x8 b0[NTW][4], b1[NTW][4], b2[NTW][4];
@@ -581,7 +590,7 @@ scan_mfma_wide_kernel(
     // are in set I % NB; the fragments of window w + NB - 1 go to set
     // (I + NB - 1) % NB, which held window w - 1's.  On entry a[0] holds
     // group 0 of window w (read issued).
-    auto stage = [&](auto i_t, int w) {
+    auto stage = [&](auto i_t, int w) __attribute__((always_inline)) {
         constexpr int I = decltype(i_t)::value;
         const bf16x8(&cur)[MT][4][64] = slot(std::integral_constant<int, I % R>{});
         const bf16x8(&nx1)[MT][4][64] = slot(std::integral_constant<int, (I + 1) % R>{});
@@ -1147,9 +1156,14 @@ static void launch_wide_cfg(const uint16_t* keys, int32_t ld, int64_t rs, int64_
 {
     constexpr int NTW = TILES * RS / WAVES;
     static_assert(NTW * WAVES == TILES * RS, "query tiles per wave");
-    dispatch_n(sl, true, true, scan_mfma_wide_kernel<MT, NTW, R, NB, WAVES, WPE, FMT, RS>,
-               dim3((unsigned)((n_rb + MT - 1) / MT)), dim3(64 * WAVES), 0, keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld,
-             kscale, qscale);
+    const dim3 grid((unsigned)((n_rb + MT - 1) / MT)), block(64 * WAVES);
+    // a batch that fills the class's tiles runs without the skip branches
+    if (scan_query_tiles(B) == TILES)
+        dispatch_n(sl, true, true, scan_mfma_wide_kernel<MT, NTW, R, NB, WAVES, WPE, FMT, RS, 0>, grid, block, 0, keys,
+                   ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
+    else
+        dispatch_n(sl, true, true, scan_mfma_wide_kernel<MT, NTW, R, NB, WAVES, WPE, FMT, RS, 1>, grid, block, 0, keys,
+                   ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale);
 }
 
 // Configurations (MT, R, NB, WAVES, WPE, RS) per class, measured on
