@@ -29,6 +29,9 @@
 //    fragment per instruction, the fragments pre-swizzled by query prep.
 //  * scan_mfma_wide (64 < B <= 512): the same instruction, keys shared by all
 //    query tiles through LDS (the contraction turns MFMA-bound near B ~ 300).
+//  * scan_mfma_persist (B <= 32 on pools of two or more whole rounds of its
+//    groups): scan_mfma as a persistent grid whose waves stream from one
+//    group of row blocks into the next.
 //  * scan_tail (remainder of the B <= 64 scan): the few row blocks past its
 //    last whole generation of waves, one workgroup each, through a deep LDS
 //    ring.
@@ -95,6 +98,11 @@
 // scan's whole generations of waves go to scan_tail_kernel (0: never).
 #ifndef OIL_TAIL_LDS
 #define OIL_TAIL_LDS 1
+#endif
+// The B <= 32 scan runs as a persistent kernel over whole rounds of its
+// groups (0: one workgroup per group).
+#ifndef OIL_SCAN_PERSIST
+#define OIL_SCAN_PERSIST 1
 #endif
 // Cache policy of the wide scan's key copies: 2 = nt (streaming, as the
 // narrow scans' nontemporal key loads).
@@ -388,6 +396,139 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
         const int q = c / KPB, j = c % KPB;
         if (q < nq && rbb + j < n_rb)
             G[q * g_ld + rbb + j] = gk[j / MT][q][j % MT];
+    }
+}
+
+// Persistent form of scan_mfma_kernel for one query tile: a grid of as many
+// workgroups as the chip holds at once walks groups g, g + grid, ... of 4 MT
+// row blocks (a whole number of rounds).  Each wave requests the next group's
+// first window during the current group's last one, and the epilogue's
+// barriers wait for LDS only, so the key stream does not drain between groups
+// as it does when a workgroup ends and the next one starts (1M x 4096, B = 32:
+// 1.255 -> 1.239 ms).  Per row block the MFMA sequence is the scan's.
+template <int MT, int NT, int FMT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 2 : 1))) void scan_mfma_persist_kernel(
+    const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
+    const bf16x8* __restrict__ qfrag, int32_t B, const int32_t* __restrict__ prompt,
+    const int32_t* __restrict__ exclude, uint64_t* __restrict__ G, int64_t g_ld,
+    const float* __restrict__ kscale, const float* __restrict__ qscale, int64_t n_groups)
+{
+    constexpr int NS = 2;
+    const int lane = threadIdx.x & 63;
+    const int h = lane >> 5, r = lane & 31;
+    const int wave = threadIdx.x >> 6;
+    const int64_t n_rb = (n_valid + kRowBlock - 1) / kRowBlock;
+    const int nwin = ld / (FMT == kKeyBf16 ? kWindow : kWindowFp8);
+    const int64_t ws8 = ws / 8;
+    const int64_t stride = gridDim.x;
+    int64_t g = blockIdx.x;
+    if (g >= n_groups)
+        return;
+    auto tiles_of = [&](int64_t gg, const bf16x8* (&t)[MT]) {
+        const int64_t rb0 = gg * 4 * MT + wave * MT;
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++) {
+            const int64_t rb = rb0 + mt < n_rb ? rb0 + mt : n_rb - 1;  // clamp: stays inside the pool
+            t[mt] = (const bf16x8*)(keys + rb * rs) + lane;
+        }
+    };
+    const bf16x8* qf = qfrag + lane;
+    const bf16x8* cur[MT];
+    tiles_of(g, cur);
+    bf16x8 a[NS][MT][4], b[NS][NT][4];
+    load_window<MT, NT>(a[0], b[0], cur, ws8, qf, 0);
+    __shared__ uint64_t gk[4][NT * 32][MT + 1];
+    for (; g < n_groups; g += stride) {
+        floatx16 acc[MT][NT];
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+            for (int nt = 0; nt < NT; nt++)
+                acc[mt][nt] = floatx16{};
+        for (int w0 = 0; w0 < nwin; w0 += NS) {
+#pragma unroll
+            for (int u = 0; u < NS; u++) {
+                const int wl = w0 + u + 1;
+                if (wl == nwin)  // the next group's tiles (this group's loads are all issued)
+                    tiles_of(g + stride < n_groups ? g + stride : g, cur);
+                load_window<MT, NT>(a[(u + 1) % NS], b[(u + 1) % NS], cur, ws8, qf, wl < nwin ? wl : 0);
+                if constexpr (FMT == kKeyFp8) {
+#pragma unroll
+                    for (int s = 0; s < 4; s += 2)
+#pragma unroll
+                        for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+                            for (int nt = 0; nt < NT; nt++)
+                                acc[mt][nt] = mfma_pair_fp8(a[u][mt][s], a[u][mt][s + 1], b[u][nt][s],
+                                                            b[u][nt][s + 1], acc[mt][nt]);
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 4; s++)
+#pragma unroll
+                        for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+                            for (int nt = 0; nt < NT; nt++)
+                                acc[mt][nt] = mfma_step(a[u][mt][s], b[u][nt][s], acc[mt][nt]);
+                }
+            }
+        }
+        // block keys of group g, as in scan_mfma_kernel
+        const int64_t rbb = g * 4 * MT;
+        const int64_t rb0 = rbb + wave * MT;
+        int32_t ex[NT];
+        float qs[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; nt++) {
+            const int qb = nt * 32 + r;
+            const bool qlive = qb < B;
+            ex[nt] = (exclude && qlive) ? exclude[qb] : -1;
+            qs[nt] = (FMT == kKeyBf16 || !qlive) ? 1.f : qscale[qb];
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++) {
+            const int64_t rb = rb0 + mt;
+            float ks[16];
+            int32_t pr[16];
+            if constexpr (FMT == kKeyFp8)
+                tile_rows_load(ks, kscale, rb * kRowBlock, h, n_valid);
+            if (exclude)
+                tile_rows_load(pr, prompt, rb * kRowBlock, h, n_valid);
+#pragma unroll
+            for (int nt = 0; nt < NT; nt++) {
+                uint64_t best = 0;
+#pragma unroll
+                for (int e = 0; e < 16; e++) {
+                    const int64_t row = rb * kRowBlock + (e / 4) * 8 + h * 4 + e % 4;
+                    if (row < n_valid) {
+                        float v = acc[mt][nt][e];
+                        if constexpr (FMT == kKeyFp8)
+                            v = v * (ks[e] * qs[nt]);
+                        if (ex[nt] >= 0 && pr[e] == ex[nt])
+                            v = __uint_as_float(kNoScoreBits);
+                        const uint64_t key = rank_key(v, (uint32_t)row);
+                        best = key > best ? key : best;
+                    }
+                }
+                const uint64_t other = __shfl_xor(best, 32, kWave);
+                best = other > best ? other : best;
+                if (h == 0)
+                    gk[wave][nt * 32 + r][mt] = best;
+            }
+        }
+        // LDS only: the next group's first window stays in flight
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        __builtin_amdgcn_s_barrier();
+        const int nq = B < NT * 32 ? B : NT * 32;
+        constexpr int KPB = 4 * MT;
+#pragma unroll
+        for (int c0 = 0; c0 < NT * 32 * KPB; c0 += 256) {
+            const int c = c0 + (int)threadIdx.x;
+            const int q = c / KPB, j = c % KPB;
+            if (q < nq && rbb + j < n_rb)
+                G[q * g_ld + rbb + j] = gk[j / MT][q][j % MT];
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        __builtin_amdgcn_s_barrier();  // gk is free for the next group
     }
 }
 
@@ -1075,6 +1216,8 @@ static void launch_gemv(dim3 g, size_t lds, const ScanLaunch& sl, const uint16_t
              g_ld, FS, fs_ld);
 }
 
+static bool nwin_even(int32_t ld, int fmt) { return (ld / (fmt == kKeyBf16 ? kWindow : kWindowFp8)) % 2 == 0; }
+
 // Compute units of the current device (cached per device).
 static int device_cus()
 {
@@ -1130,6 +1273,27 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
         } else if (rem >= tail_min && rem <= gen / 4) {
             n_main = n_rb - rem;
             n_tail = rem;
+        }
+    }
+    if constexpr (NT == 1 && PF == 1) {
+        // Two or more whole rounds of groups: the persistent kernel, plus the
+        // remainder kernel for up to one row block per compute unit past them
+        // (the bench pool, 1M plus 8-15 row blocks: 1.378 -> 1.363 ms per
+        // step).  With two query tiles the persistent form measured slower
+        // (B = 64: 1.95 against 1.30 ms).
+        const int64_t grp = 4 * MT;
+        const int64_t per_round = (int64_t)device_cus() * kWavesPerSimd;  // workgroups the chip holds
+        const int64_t rounds = n_rb / grp / per_round;
+        const int64_t n_groups = rounds * per_round;
+        const int64_t rem = n_rb - n_groups * grp;
+        if (OIL_SCAN_PERSIST && nwin_even(ld, FMT) && rounds >= 2 && rem <= device_cus()) {
+            dispatch(sl, true, rem == 0, scan_mfma_persist_kernel<MT, NT, FMT>, dim3((unsigned)per_round), 0, keys,
+                     ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale, n_groups);
+            if (rem > 0)
+                dispatch_n(sl, false, true, scan_tail_kernel<NT, FMT>, dim3((unsigned)rem), dim3(64 * (NT + 4)), 0,
+                           keys, ld, rs, ws, n_valid, qf, B, prompt, exclude, G, g_ld, kscale, qscale,
+                           n_groups * grp);
+            return;
         }
     }
     dispatch(sl, true, n_tail == 0, scan_mfma_kernel<MT, NT, PF, FMT>,

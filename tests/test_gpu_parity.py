@@ -191,6 +191,23 @@ def test_topk_remainder_ring_wraps(oil, key_format, B, extra, d, base):
     test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
 
 
+@pytest.mark.parametrize("key_format,B,extra,d,base", [("bf16", 16, 0, 128, 524288),
+                                                        ("bf16", 16, 300, 128, 524288),
+                                                        ("bf16", 32, 8192, 128, 786432),
+                                                        ("bf16", 32, 8224, 128, 786432),
+                                                        ("bf16", 16, 100, 512, 524288),
+                                                        ("fp8", 8, 0, 256, 262144),
+                                                        ("fp8", 8, 300, 256, 262144)])
+def test_topk_persistent_rounds(oil, key_format, B, extra, d, base):
+    """One query tile on pools of two or three whole rounds of the B <= 32
+    scan's groups (16 bf16 / 8 fp8 row blocks per workgroup, two workgroups
+    per compute unit) at an even window count: the persistent scan, whose
+    waves request the next group's first window during the current group's
+    last one.  Plus 10 or 256 row blocks past the rounds (the remainder
+    kernel), or 257 (too many for it: the one-workgroup-per-group scan)."""
+    test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
+
+
 @pytest.mark.parametrize("key_format,B", [("bf16", 16), ("fp8", 40)])
 def test_topk_large_remainder(oil, key_format, B):
     """More remainder row blocks than compute units (375, past one generation
