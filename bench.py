@@ -478,7 +478,7 @@ def main():
                "scan_ms": round(s8 * 1e3, 4), "achieved": round(b8 / s8 / 1e9, 1), "unit_roofline": "GB/s",
                "frac": round(b8 / s8 / 1e9 / HBM_PEAK_GBS, 4), "bytes_per_launch": int(b8),
                "traffic": read_traffic(b8, PROFILE_TRAFFIC_FP8),
-               "kernel": "scan_mfma_persist_kernel<2,1,fp8> + scan_tail_kernel<1,fp8>",
+               "kernel": "scan_mfma_kernel<2,1,1,fp8>",
                "keys": "OCP FP8 E4M3, power-of-two scale per row (4 GiB at 1M x 4096)"}
         log(f"fp8 pool: {K} steps in {(f1 - f0) * 1e3:.1f} ms; scan {s8 * 1e3:.4f} ms avg")
         del pool8

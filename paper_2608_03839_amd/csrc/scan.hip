@@ -29,9 +29,9 @@
 //    fragment per instruction, the fragments pre-swizzled by query prep.
 //  * scan_mfma_wide (64 < B <= 512): the same instruction, keys shared by all
 //    query tiles through LDS (the contraction turns MFMA-bound near B ~ 300).
-//  * scan_mfma_persist (B <= 32 on pools of two or more whole rounds of its
-//    groups): scan_mfma as a persistent grid whose waves stream from one
-//    group of row blocks into the next.
+//  * scan_mfma_persist (bf16 keys, B <= 32, pools of two or more whole
+//    rounds of its groups): scan_mfma as a persistent grid whose waves
+//    stream from one group of row blocks into the next.
 //  * scan_tail (remainder of the B <= 64 scan): the few row blocks past its
 //    last whole generation of waves, one workgroup each, through a deep LDS
 //    ring.
@@ -99,10 +99,13 @@
 #ifndef OIL_TAIL_LDS
 #define OIL_TAIL_LDS 1
 #endif
-// The B <= 32 scan runs as a persistent kernel over whole rounds of its
-// groups (0: one workgroup per group).
+// The bf16 B <= 32 scan runs as a persistent kernel over whole rounds of its
+// groups (0: one workgroup per group; PERSIST_FP8: fp8 keys too).
 #ifndef OIL_SCAN_PERSIST
 #define OIL_SCAN_PERSIST 1
+#endif
+#ifndef OIL_SCAN_PERSIST_FP8
+#define OIL_SCAN_PERSIST_FP8 0
 #endif
 // Cache policy of the wide scan's key copies: 2 = nt (streaming, as the
 // narrow scans' nontemporal key loads).
@@ -1275,12 +1278,14 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
             n_tail = rem;
         }
     }
-    if constexpr (NT == 1 && PF == 1) {
+    if constexpr (NT == 1 && PF == 1 && (FMT == kKeyBf16 || OIL_SCAN_PERSIST_FP8)) {
         // Two or more whole rounds of groups: the persistent kernel, plus the
         // remainder kernel for up to one row block per compute unit past them
         // (the bench pool, 1M plus 8-15 row blocks: 1.378 -> 1.363 ms per
         // step).  With two query tiles the persistent form measured slower
-        // (B = 64: 1.95 against 1.30 ms).
+        // (B = 64: 1.95 against 1.30 ms); with fp8 keys it gains at exactly 1M
+        // (B = 32: 0.675 -> 0.665 ms) but loses on the bench pool, whose
+        // remainder then costs a launch (0.7315 -> 0.7363 ms per step).
         const int64_t grp = 4 * MT;
         const int64_t per_round = (int64_t)device_cus() * kWavesPerSimd;  // workgroups the chip holds
         const int64_t rounds = n_rb / grp / per_round;

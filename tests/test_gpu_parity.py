@@ -200,11 +200,12 @@ def test_topk_remainder_ring_wraps(oil, key_format, B, extra, d, base):
                                                         ("fp8", 8, 300, 256, 262144)])
 def test_topk_persistent_rounds(oil, key_format, B, extra, d, base):
     """One query tile on pools of two or three whole rounds of the B <= 32
-    scan's groups (16 bf16 / 8 fp8 row blocks per workgroup, two workgroups
-    per compute unit) at an even window count: the persistent scan, whose
+    scan's groups (16 bf16 row blocks per workgroup, two workgroups per
+    compute unit) at an even window count: the persistent bf16 scan, whose
     waves request the next group's first window during the current group's
     last one.  Plus 10 or 256 row blocks past the rounds (the remainder
-    kernel), or 257 (too many for it: the one-workgroup-per-group scan)."""
+    kernel), or 257 (too many for it: the one-workgroup-per-group scan).
+    fp8 keys at the same shapes keep the one-workgroup-per-group scan."""
     test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
 
 
