@@ -104,6 +104,9 @@
 #ifndef OIL_SCAN_PERSIST
 #define OIL_SCAN_PERSIST 1
 #endif
+#ifndef OIL_SCAN_PERSIST_PART
+#define OIL_SCAN_PERSIST_PART 1
+#endif
 #ifndef OIL_SCAN_PERSIST_FP8
 #define OIL_SCAN_PERSIST_FP8 0
 #endif
@@ -1279,8 +1282,9 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
         }
     }
     if constexpr (NT == 1 && PF == 1 && (FMT == kKeyBf16 || OIL_SCAN_PERSIST_FP8)) {
-        // Two or more whole rounds of groups: the persistent kernel, plus the
-        // remainder kernel for up to one row block per compute unit past them
+        // Two or more whole rounds of groups (and a last round at least half
+        // full): the persistent kernel, plus the remainder kernel for up to one
+        // row block per compute unit past its groups
         // (the bench pool, 1M plus 8-15 row blocks: 1.378 -> 1.363 ms per
         // step).  With two query tiles the persistent form measured slower
         // (B = 64: 1.95 against 1.30 ms); with fp8 keys it gains at exactly 1M
@@ -1288,8 +1292,11 @@ static void launch_narrow(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
         // remainder then costs a launch (0.7315 -> 0.7363 ms per step).
         const int64_t grp = 4 * MT;
         const int64_t per_round = (int64_t)device_cus() * kWavesPerSimd;  // workgroups the chip holds
-        const int64_t rounds = n_rb / grp / per_round;
-        const int64_t n_groups = rounds * per_round;
+        const int64_t full = n_rb / grp, rounds = full / per_round, part = full % per_round;
+        // whole rounds, or all whole groups when the last round is at least half full
+        int64_t n_groups = rounds * per_round;
+        if (OIL_SCAN_PERSIST_PART && 2 * part >= per_round)
+            n_groups = full;
         const int64_t rem = n_rb - n_groups * grp;
         if (OIL_SCAN_PERSIST && nwin_even(ld, FMT) && rounds >= 2 && rem <= device_cus()) {
             dispatch(sl, true, rem == 0, scan_mfma_persist_kernel<MT, NT, FMT>, dim3((unsigned)per_round), 0, keys,

@@ -196,6 +196,8 @@ def test_topk_remainder_ring_wraps(oil, key_format, B, extra, d, base):
                                                         ("bf16", 32, 8192, 128, 786432),
                                                         ("bf16", 32, 8224, 128, 786432),
                                                         ("bf16", 16, 100, 512, 524288),
+                                                        ("bf16", 16, 153760, 128, 524288),
+                                                        ("bf16", 16, 51360, 128, 524288),
                                                         ("fp8", 8, 0, 256, 262144),
                                                         ("fp8", 8, 300, 256, 262144)])
 def test_topk_persistent_rounds(oil, key_format, B, extra, d, base):
@@ -204,8 +206,11 @@ def test_topk_persistent_rounds(oil, key_format, B, extra, d, base):
     compute unit) at an even window count: the persistent bf16 scan, whose
     waves request the next group's first window during the current group's
     last one.  Plus 10 or 256 row blocks past the rounds (the remainder
-    kernel), or 257 (too many for it: the one-workgroup-per-group scan).
-    fp8 keys at the same shapes keep the one-workgroup-per-group scan."""
+    kernel), or 257 (too many for it: the one-workgroup-per-group scan); or a
+    last round of 300 groups plus 5 row blocks (at least half full: the
+    persistent scan takes every whole group, the remainder kernel the rest),
+    or of 100 groups plus 5 (the one-workgroup-per-group scan).  fp8 keys at
+    the same shapes keep the one-workgroup-per-group scan."""
     test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
 
 
