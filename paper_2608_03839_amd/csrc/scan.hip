@@ -430,19 +430,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 2
     int64_t g = blockIdx.x;
     if (g >= n_groups)
         return;
-    auto tiles_of = [&](int64_t gg, const bf16x8* (&t)[MT]) {
+    // tiles as offsets from the pool's base (16-byte units), so every load
+    // keeps the global address space (pointers carried across the group
+    // switch would become flat accesses, which also count as LDS accesses)
+    const bf16x8* kv = (const bf16x8*)keys;
+    auto tiles_of = [&](int64_t gg, int64_t (&t)[MT]) {
         const int64_t rb0 = gg * 4 * MT + wave * MT;
 #pragma unroll
         for (int mt = 0; mt < MT; mt++) {
             const int64_t rb = rb0 + mt < n_rb ? rb0 + mt : n_rb - 1;  // clamp: stays inside the pool
-            t[mt] = (const bf16x8*)(keys + rb * rs) + lane;
+            t[mt] = rb * rs / 8 + lane;
         }
     };
-    const bf16x8* qf = qfrag + lane;
-    const bf16x8* cur[MT];
+    auto load = [&](bf16x8 (&av)[MT][4], bf16x8 (&bv)[NT][4], const int64_t (&t)[MT], int w) {
+#pragma unroll
+        for (int mt = 0; mt < MT; mt++)
+#pragma unroll
+            for (int s = 0; s < 4; s++)
+                av[mt][s] = __builtin_nontemporal_load(kv + t[mt] + w * ws8 + s * 64);
+#pragma unroll
+        for (int nt = 0; nt < NT; nt++)
+#pragma unroll
+            for (int s = 0; s < 4; s++)
+                bv[nt][s] = qfrag[(((int64_t)w * NT + nt) * 4 + s) * 64 + lane];
+    };
+    int64_t cur[MT];
     tiles_of(g, cur);
     bf16x8 a[NS][MT][4], b[NS][NT][4];
-    load_window<MT, NT>(a[0], b[0], cur, ws8, qf, 0);
+    load(a[0], b[0], cur, 0);
     __shared__ uint64_t gk[4][NT * 32][MT + 1];
     for (; g < n_groups; g += stride) {
         floatx16 acc[MT][NT];
@@ -457,7 +472,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 2
                 const int wl = w0 + u + 1;
                 if (wl == nwin)  // the next group's tiles (this group's loads are all issued)
                     tiles_of(g + stride < n_groups ? g + stride : g, cur);
-                load_window<MT, NT>(a[(u + 1) % NS], b[(u + 1) % NS], cur, ws8, qf, wl < nwin ? wl : 0);
+                load(a[(u + 1) % NS], b[(u + 1) % NS], cur, wl < nwin ? wl : 0);
                 if constexpr (FMT == kKeyFp8) {
 #pragma unroll
                     for (int s = 0; s < 4; s += 2)
