@@ -29,12 +29,16 @@ namespace oil {
 constexpr int kMergeThreads = 256;
 constexpr int kMergeChains = 64 + 64 + 64 + OIL_REC_OUT_MAX;  // n_lex + k + n_lex_ret + n_rec at most
 
-// Copy the tree's six input arrays from global memory to LDS: their elements
-// are taken as one concatenated index range, four loads per thread in flight
-// at clamped (always valid) addresses, then the stores.  An empty array
-// (which may be NULL) owns no index.
-__device__ __forceinline__ void stage_lds(const int32_t* const (&src)[6], int32_t* const (&dst)[6],
-                                          const int (&n)[6])
+// Copy the tree's six input arrays from global memory to LDS, where they sit
+// back to back from dst in the same order: their elements are taken as one
+// concatenated index range, four loads per thread in flight at clamped
+// (always valid) addresses, then the stores.  An empty array (which may be
+// NULL) owns no index.  The source of an index is picked by a chain of
+// selects between the six pointers (not by indexing an array of them), so
+// the loads stay global loads and the stores LDS stores.
+__device__ __forceinline__ void stage_lds(const int32_t* s0, const int32_t* s1, const int32_t* s2,
+                                          const int32_t* s3, const int32_t* s4, const int32_t* s5,
+                                          int32_t* dst, const int (&n)[6])
 {
     constexpr int kU = 4;
     const int t = threadIdx.x;
@@ -46,24 +50,21 @@ __device__ __forceinline__ void stage_lds(const int32_t* const (&src)[6], int32_
     }
     for (int i0 = 0; i0 < total; i0 += kMergeThreads * kU) {
         int32_t v[kU];
-        int32_t* to[kU];
 #pragma unroll
         for (int u = 0; u < kU; u++) {
             const int i = min(i0 + u * kMergeThreads + t, total - 1);
-            int a = 0, base = 0;
-#pragma unroll
-            for (int q = 0; q < 5; q++)
-                if (i >= end[q]) {
-                    a = q + 1;
-                    base = end[q];
-                }
-            v[u] = src[a][i - base];
-            to[u] = dst[a] + (i - base);
+            const int32_t* p = i < end[0]   ? s0 + i
+                               : i < end[1] ? s1 + (i - end[0])
+                               : i < end[2] ? s2 + (i - end[1])
+                               : i < end[3] ? s3 + (i - end[2])
+                               : i < end[4] ? s4 + (i - end[3])
+                                            : s5 + (i - end[4]);
+            v[u] = *p;
         }
 #pragma unroll
         for (int u = 0; u < kU; u++)
             if (i0 + u * kMergeThreads + t < total)
-                *to[u] = v[u];
+                dst[i0 + u * kMergeThreads + t] = v[u];
     }
 }
 
@@ -169,12 +170,10 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     const int NC1 = n_lex;                            // phase 1: the lexical allocation
     const int NC = n_lex + k + n_lex_ret + n_rec;     // phase 2: C under the reservation
     {
-        const int32_t* const src[6] = {lex_tokens + (int64_t)b * n_lex * L_lex, sem_tokens + (int64_t)b * k * L,
-                                       rec_tokens + (int64_t)b * n_rec * L_rec, lex_len + (int64_t)b * n_lex,
-                                       sem_len + (int64_t)b * k, rec_len + (int64_t)b * n_rec};
-        int32_t* const dst[6] = {lex_s, sem_s, rec_s, llen_s, slen_s, rlen_s};
         const int n[6] = {n_lex * L_lex, k * L, n_rec * L_rec, n_lex, k, n_rec};
-        stage_lds(src, dst, n);
+        stage_lds(lex_tokens + (int64_t)b * n_lex * L_lex, sem_tokens + (int64_t)b * k * L,
+                  rec_tokens + (int64_t)b * n_rec * L_rec, lex_len + (int64_t)b * n_lex, sem_len + (int64_t)b * k,
+                  rec_len + (int64_t)b * n_rec, sm, n);  // lex_s .. rlen_s, back to back from sm
     }
     __syncthreads();
     // the chain table, in insertion order
