@@ -74,9 +74,10 @@ def read_ceiling(torch, oil, buf, dev, reps=5):
     """A plain streaming read of the same key buffer (the library's read-stream
     kernel, non-temporal 16-byte loads): the practical HBM read ceiling.  It
     reads the largest prefix that splits into 512 equal stretches of whole
-    4 KiB stripes (all but a few MB of the buffer): with uneven stretches the
-    same kernel reads 4-5% slower."""
-    unit = 512 * 4096
+    512 KiB blocks (8 GiB of the 8.62 GB 1M x 4096 buffer): with uneven
+    stretches the same kernel reads 4-5% slower, and with stretches of whole
+    4 KiB stripes that do not start on 512 KiB boundaries 1-3% slower."""
+    unit = 512 * 512 * 1024
     n = buf.numel() * buf.element_size() // unit * unit
     buf = buf.view(-1).view(torch.uint8)[:n]
     sink = torch.zeros(1, dtype=torch.int64, device=dev)

@@ -79,7 +79,7 @@ enum { OIL_F32 = 0, OIL_BF16 = 1 };
 int32_t oil_key_stride(int32_t dim);
 
 /* Bytes the caller must provide for `capacity` keys of width `dim`:
- * oil_key_stride(dim) * (capacity rounded up to 32) * 2.
+ * oil_key_stride(dim) * R * 32 * 2, R the row blocks per window below.
  *
  * Key buffer layout (bf16 elements).  Rows are grouped in blocks of 32 and
  * the padded columns in windows of 64; each (row block, window) pair is one
@@ -87,8 +87,10 @@ int32_t oil_key_stride(int32_t dim);
  * by window: all row blocks of window 0, then of window 1, and so on.  While
  * the scan's wavefronts walk their row blocks window by window, the chip
  * reads one contiguous region at a time, and every 16-byte per-lane load
- * covers 1 KiB contiguous.  With R = capacity rounded up to 32, divided by
- * 32, row i and column j live at
+ * covers 1 KiB contiguous.  R, the row blocks per window, is capacity / 32
+ * rounded up, and past 1,024 rounded up to a multiple of 128 (every window
+ * then starts on a 512 KiB boundary, which the scan reads measurably faster).
+ * Row i and column j live at
  *     ((j / 64) * R + i / 32) * 2048 + (s * 64 + lane) * 8 + (j % 8),
  *     s = (j % 32) / 8,  lane = i % 32 + 32 * ((j % 64) / 32).
  */
@@ -128,7 +130,8 @@ int32_t oil_pool_size(const oil_pool *pool, int64_t *n_valid);
  * (OIL_MAX_B_FP8 = OIL_MAX_B per call). */
 size_t oil_pool_key_bytes_fp8(int32_t dim, int64_t capacity);
 
-/* key_buf: oil_pool_key_bytes_fp8(dim, capacity) bytes, 256-byte aligned;
+/* key_buf: oil_pool_key_bytes_fp8(dim, capacity) bytes (the padded width
+ * times R * 32, R as for the bf16 pool), 256-byte aligned;
  * scale_buf: capacity float32 (the inverse scale of each stored row); other
  * buffers as for oil_pool_create. */
 int32_t oil_pool_create_fp8(int32_t dim, int64_t capacity, void *key_buf, float *scale_buf,

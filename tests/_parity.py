@@ -36,10 +36,14 @@ def untile_keys(buf_bits, n, dim, capacity):
 
     Layout: 4 KiB tiles of 32 rows x 64 columns ordered (sub-step s,
     lane = row % 32 + 32 * half, element e), stored window-major: tile
-    (row block rb, window w) at (w * R + rb) * 2048, R = ceil(capacity / 32)."""
+    (row block rb, window w) at (w * R + rb) * 2048, R the row blocks per
+    window (ceil(capacity / 32), padded for large pools): the whole buffer
+    holds ld / 64 windows of R tiles."""
     ld = (dim + 63) // 64 * 64
-    R = (capacity + 31) // 32
-    t = np.asarray(buf_bits)[: R * 32 * ld].reshape(ld // 64, R, 4, 2, 32, 8)
+    buf = np.asarray(buf_bits)
+    R = buf.size // (32 * ld)
+    assert R * 32 * ld == buf.size and R * 32 >= capacity
+    t = buf.reshape(ld // 64, R, 4, 2, 32, 8)
     rows = t.transpose(1, 4, 0, 3, 2, 5).reshape(R * 32, ld)
     return np.ascontiguousarray(rows[:n, :dim])
 
@@ -52,8 +56,10 @@ def untile_keys_fp8(buf, n, dim, capacity):
     (p * 2 + hh) * 16 + ((col % 16) // 8) * 8 + e inside the window, stored
     window-major like the bf16 tiles."""
     ld = (dim + 127) // 128 * 128
-    R = (capacity + 31) // 32
-    t = np.asarray(buf)[: R * 32 * ld].reshape(ld // 128, R, 4, 2, 32, 2, 8)
+    buf = np.asarray(buf)
+    R = buf.size // (32 * ld)
+    assert R * 32 * ld == buf.size and R * 32 >= capacity
+    t = buf.reshape(ld // 128, R, 4, 2, 32, 2, 8)
     # axes: window, row block, p, lane half, row in block, hh, e
     # column in window = p * 32 + hh * 16 + half * 8 + e
     rows = t.transpose(1, 4, 0, 2, 5, 3, 6).reshape(R * 32, ld)

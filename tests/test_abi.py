@@ -39,6 +39,11 @@ def test_stride_and_sizes(L):
     assert L.oil_pool_key_bytes(4096, 10) == 4096 * 32 * 2      # rows round up to 32
     assert L.oil_pool_key_bytes(100, 33) == 128 * 64 * 2
     assert L.oil_pool_key_bytes(0, 10) == 0
+    # past 1,024 row blocks a window's row blocks round up to a multiple of 128
+    assert L.oil_pool_key_bytes(64, 1024 * 32) == 64 * 1024 * 32 * 2
+    assert L.oil_pool_key_bytes(64, 1024 * 32 + 1) == 64 * 1152 * 32 * 2
+    assert L.oil_pool_key_bytes(4096, 1048576 + 480) == 4096 * 32896 * 32 * 2
+    assert L.oil_pool_key_bytes_fp8(4096, 1048576 + 480) == 4096 * 32896 * 32
 
 
 class _FakeBufs:
