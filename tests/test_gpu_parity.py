@@ -191,6 +191,18 @@ def test_topk_remainder_ring_wraps(oil, key_format, B, extra, d, base):
     test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
 
 
+@pytest.mark.parametrize("key_format,B,extra,d,base", [("bf16", 8, 1, 192, 32768),
+                                                        ("bf16", 40, 1, 192, 32768),
+                                                        ("fp8", 8, 1, 256, 32768),
+                                                        ("bf16", 8, 4064, 192, 32768)])
+def test_topk_padded_windows(oil, key_format, B, extra, d, base):
+    """Pools just past 1,024 row blocks, where each window's row blocks are
+    padded to a multiple of 128 (1,025 and 1,151 row blocks, both stored as
+    1,152 per window), filled to capacity: the last rows sit next to the
+    padding, and the planted near-copies include the pool's last row."""
+    test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
+
+
 @pytest.mark.parametrize("key_format,B,extra,d,base", [("bf16", 16, 0, 128, 524288),
                                                         ("bf16", 16, 300, 128, 524288),
                                                         ("bf16", 32, 8192, 128, 786432),
