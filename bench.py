@@ -515,7 +515,8 @@ def sweep(args, oil, workloads, dev, cfg):
     wp = workloads.Pool(ps, device=dev)
     K, W = max(args.steps // 10, 5), 2
     out = {"pool_rows": N, "dim": d, "k": k,
-           "kernels": "bf16: B<=4 scan_gemv, B<=64 scan_mfma, B>64 scan_mfma_wide; fp8: B<=64 scan_mfma, B>64 scan_mfma_wide"}
+           "kernels": "bf16: B<=64 scan_mfma (B<=4: scan_gemv on pools of at most 2^19 scores per call, "
+                      "not this one), B>64 scan_mfma_wide; fp8: B<=64 scan_mfma, B>64 scan_mfma_wide"}
     fmts = [("bf16", 2, MFMA_BF16_PEAK_TFLOPS)] + ([] if args.no_fp8 else [("fp8", 1, MFMA_FP8_PEAK_TFLOPS)])
     # every pool allocated and filled before any is measured: a key buffer
     # allocated where a freed one was (after the caching allocator returns it)

@@ -41,6 +41,9 @@ hipError_t launch_normalize_rows(const void* raw, int dtype, int32_t d, int64_t 
                                  const int32_t* trace_in, const int32_t* prompt_in, int32_t* tok_out,
                                  int32_t* trace_out, int32_t* prompt_out, hipStream_t stream);
 
+// Whether B queries of padded width ld fit the GEMV scan (B <= 4, queries in
+// 64 KiB of LDS).  It runs only where it also writes every score (no rescore);
+// elsewhere the MFMA scan takes those batches.
 int scan_uses_mfma(int32_t B, int32_t ld);
 int scan_query_tiles(int32_t B);
 // fmt: kKeyBf16, or kKeyFp8 (ld = fp8 row width, a multiple of

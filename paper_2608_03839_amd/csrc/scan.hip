@@ -18,13 +18,15 @@
 //  * scan_gemv (B <= 4): a matrix-vector product on the vector ALU
 //    (v_dot2 bf16 -> fp32).  Lane l accumulates row l % 32 of the tile over
 //    half of each window's columns; one xor-32 exchange completes the row.
-//    Queries sit in LDS, read as broadcasts.  On small pools (B * N at most
-//    2^19 scores) it also writes every score: the final selection reads the
-//    chosen blocks' scores from there, and no rescore runs.  On larger pools
-//    those writes, interleaved with the key stream, would cost the scan more
-//    than the rescore (1M positions: +25 us at B = 1, +73 us at B = 4,
-//    against a ~12 us rescore).
-//  * scan_mfma (4 < B <= 64): the batch makes the scan a dense contraction;
+//    Queries sit in LDS, read as broadcasts.  It runs on small pools only (B *
+//    N at most 2^19 scores), where it also writes every score: the final
+//    selection reads the chosen blocks' scores from there, and no rescore
+//    runs.  On larger pools those writes, interleaved with the key stream,
+//    would cost the scan more than a rescore (1M positions: +25 us at B = 1,
+//    +73 us at B = 4), and the MFMA scan, its 32-query tile mostly empty,
+//    reads the pool faster than the GEMV without them (1.208 / 1.207 ms at
+//    B = 1 / 4 against 1.232 / 1.250), so it takes those batches.
+//  * scan_mfma (B <= 64): the batch makes the scan a dense contraction;
 //    v_mfma_f32_32x32x16_bf16 multiplies a 32-key tile by a 32-query tile
 //    fragment per instruction, the fragments pre-swizzled by query prep.
 //  * scan_mfma_wide (64 < B <= 512): the same instruction, keys shared by all
@@ -75,11 +77,6 @@
 #endif
 #ifndef OIL_FP8_PF
 #define OIL_FP8_PF 1
-#endif
-// Windows in flight per wave of the GEMV rescore (B <= 4: few waves, each
-// walking every window of one block, so latency-bound).
-#ifndef OIL_RESCORE_GEMV_PF
-#define OIL_RESCORE_GEMV_PF 7
 #endif
 // Prefetch depth (windows in flight per wave) of the MFMA rescore.  At 1M x
 // 4096, B = k = 32 (1024 waves, one per SIMD): depth 0 73 us, 1 45, 2 46, 3 47.5.
@@ -1128,71 +1125,6 @@ __global__ __launch_bounds__(64) void rescore_mfma_kernel(
     }
 }
 
-// GEMV path: the scan's per-query order (windows, then sub-steps, v_dot2 in
-// element order, then the xor-32 exchange), query read from global memory.
-template <int PF>
-__global__ __launch_bounds__(64) void rescore_gemv_kernel(
-    const uint16_t* __restrict__ keys, int32_t ld, int64_t rs, int64_t ws, int64_t n_valid,
-    const uint16_t* __restrict__ q, const uint64_t* __restrict__ blocks, int k,
-    const int32_t* __restrict__ prompt, const int32_t* __restrict__ exclude, float* __restrict__ SC)
-{
-    constexpr int NS = PF + 1;
-    const int slot = blockIdx.x, qb = blockIdx.y, lane = threadIdx.x;
-    const int h = lane >> 5, r = lane & 31;
-    float* out = SC + ((int64_t)qb * k + slot) * kRowBlock;
-    const uint64_t bk = blocks[(int64_t)qb * k + slot];
-    const int64_t rb = key_pos(bk) / kRowBlock;
-    // no block (or, defensively, one past the pool: nothing is read there)
-    if (bk == 0 || rb * kRowBlock >= n_valid) {
-        if (lane < kRowBlock)
-            out[lane] = __uint_as_float(kNoScoreBits);
-        return;
-    }
-    const int nwin = ld / kWindow;
-    const int64_t ws8 = ws / 8;
-    const bf16x8* tile = (const bf16x8*)(keys + rb * rs) + lane;
-    const uint16_t* qrow = q + (int64_t)qb * ld;
-    float acc = 0.f;
-    // the block's key tiles and the query's matching columns, both in the
-    // prefetch ring (the query read from global memory each window would put
-    // an L2 round trip on every step)
-    bf16x8 a[NS][4], b[NS][4];
-    auto load = [&](int stage, int w) {
-#pragma unroll
-        for (int s = 0; s < 4; s++) {
-            a[stage][s] = __builtin_nontemporal_load(tile + w * ws8 + s * 64);
-            b[stage][s] = *(const bf16x8*)(qrow + w * kWindow + 32 * h + 8 * s);
-        }
-    };
-#pragma unroll
-    for (int p = 0; p < PF; p++)
-        load(p, p < nwin ? p : nwin - 1);
-    const int nloop = (nwin + NS - 1) / NS * NS;
-    for (int w0 = 0; w0 < nloop; w0 += NS) {
-#pragma unroll
-        for (int u = 0; u < NS; u++) {
-            const int wl = w0 + u + PF < nwin ? w0 + u + PF : nwin - 1;
-            load((u + PF) % NS, wl);
-            if (w0 + u < nwin) {
-#pragma unroll
-                for (int s = 0; s < 4; s++)
-                    acc = dot8_bf16(a[u][s], b[u][s], acc);
-            }
-        }
-    }
-    const float full = acc + __shfl_xor(acc, 32, kWave);
-    if (h != 0)
-        return;
-    const int64_t row = rb * kRowBlock + r;
-    const int32_t ex = exclude ? exclude[qb] : -1;
-    float v = full;
-    if (row >= n_valid)
-        v = __uint_as_float(kNoScoreBits);
-    else if (ex >= 0)
-        v = masked_score(v, row, ex, prompt);
-    out[r] = v;
-}
-
 // ----------------------------------------------------------------- launchers
 // The GEMV keeps all queries of the call in LDS (at most 64 KiB).
 int scan_uses_mfma(int32_t B, int32_t ld) { return B > 4 || (int64_t)B * ld * 2 > 65536; }
@@ -1431,7 +1363,7 @@ hipError_t launch_scan(const uint16_t* keys, int32_t ld, int64_t rs, int64_t ws,
                                                              G, g_ld, kscale, qscale, sl);
         return hipGetLastError();
     }
-    if (!scan_uses_mfma(B, ld)) {
+    if (!scan_uses_mfma(B, ld) && FS) {  // the GEMV scan only where it writes every score
         const dim3 g((unsigned)((n_rb + 3) / 4));
         const size_t lds = (size_t)B * ld * sizeof(uint16_t);
         const uint16_t* q = (const uint16_t*)qbuf;
@@ -1469,9 +1401,6 @@ hipError_t launch_rescore(const uint16_t* keys, int32_t ld, int64_t rs, int64_t 
         hipLaunchKernelGGL((rescore_mfma_kernel<OIL_RESCORE_PF, kKeyFp8>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
                            (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC, kscale,
                            qscale);
-    else if (!scan_uses_mfma(B, ld))
-        hipLaunchKernelGGL((rescore_gemv_kernel<OIL_RESCORE_GEMV_PF>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
-                           (const uint16_t*)qbuf, blocks, k, prompt, exclude, SC);
     else
         hipLaunchKernelGGL((rescore_mfma_kernel<OIL_RESCORE_PF, kKeyBf16>), g, dim3(64), 0, stream, keys, ld, rs, ws, n_valid,
                            (const bf16x8*)qbuf, scan_query_tiles(B), blocks, k, prompt, exclude, SC, nullptr,

@@ -14,7 +14,7 @@
 //      per workgroup, then merges of up to 4096 candidates per workgroup,
 //      until one list of k remains; up to 4096 block keys, one workgroup
 //      takes them all);
-//   2. the rescore kernels (scan.hip) recompute the 32 scores of each chosen
+//   2. the rescore kernel (scan.hip) recomputes the 32 scores of each chosen
 //      block, bit-identical to the scan's (for the GEMV scan's batches, which
 //      write every score, the final step reads them instead);
 //   3. select the k largest of those k * 32 keys, ranked and written in order.

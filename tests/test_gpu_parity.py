@@ -191,6 +191,18 @@ def test_topk_remainder_ring_wraps(oil, key_format, B, extra, d, base):
     test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
 
 
+@pytest.mark.parametrize("key_format,B,extra,d,base", [("bf16", 1, 80000, 128, 524288),
+                                                        ("bf16", 2, 300, 128, 524288),
+                                                        ("bf16", 4, 0, 192, 262144)])
+def test_topk_small_batches_on_large_pools(oil, key_format, B, extra, d, base):
+    """B <= 4 on pools of more than 2^19 / B positions, where the GEMV scan
+    would not write every score: the MFMA scan takes them (one query tile,
+    the rest of its 32 columns empty), then the MFMA rescore.  604,288 rows
+    at B = 1 (the one-workgroup-per-group scan past two rounds), 524,588 at
+    B = 2 (the persistent scan plus 10 remainder row blocks), 262,144 at B = 4."""
+    test_topk_pool_past_whole_waves(oil, key_format, B, extra, d, base=base)
+
+
 @pytest.mark.parametrize("key_format,B,extra,d,base", [("bf16", 8, 1, 192, 32768),
                                                         ("bf16", 40, 1, 192, 32768),
                                                         ("fp8", 8, 1, 256, 32768),
