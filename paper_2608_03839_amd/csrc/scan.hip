@@ -348,7 +348,9 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     // block, row by row (consecutive threads, consecutive row blocks of one
     // query: 4 MT keys per query row) instead of one scattered 8-byte store
     // per query (~30 us more at 1M x 4096, B = 32) or one segment per wave
-    // (6 us more).
+    // (6 us more).  The stores are non-temporal (streamed past the caches the
+    // key stream uses): at 1M x 4096, B = 32 the persistent scan takes
+    // 1,215 us against 1,224 with plain stores.
     __shared__ uint64_t gk[4][NT * 32][MT + 1];  // per wave; +1: rows land in different banks
     int32_t ex[NT];
     float qs[NT];
@@ -398,7 +400,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
         const int c = c0 + (int)threadIdx.x;
         const int q = c / KPB, j = c % KPB;
         if (q < nq && rbb + j < n_rb)
-            G[q * g_ld + rbb + j] = gk[j / MT][q][j % MT];
+            __builtin_nontemporal_store(gk[j / MT][q][j % MT], &G[q * g_ld + rbb + j]);
     }
 }
 
@@ -543,7 +545,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 2
             const int c = c0 + (int)threadIdx.x;
             const int q = c / KPB, j = c % KPB;
             if (q < nq && rbb + j < n_rb)
-                G[q * g_ld + rbb + j] = gk[j / MT][q][j % MT];
+                __builtin_nontemporal_store(gk[j / MT][q][j % MT], &G[q * g_ld + rbb + j]);
         }
         __builtin_amdgcn_s_waitcnt(0xc07f);
         __builtin_amdgcn_s_barrier();  // gk is free for the next group
@@ -858,8 +860,16 @@ scan_mfma_wide_kernel(
             }
             const uint64_t other = __shfl_xor(best, 32, kWave);
             best = other > best ? other : best;
-            if (qb < B && h == 0 && rb * kRowBlock < n_valid)
-                G[qb * g_ld + rb] = best;
+            // streamed past the caches up to four query tiles (B = 128: 1.498
+            // -> 1.460 ms); plain stores at 8 and 16 tiles, whose block keys
+            // are 2-4x as many (B = 256 / 512: 2.11 / 3.63 ms against 2.18 /
+            // 3.87 streamed)
+            if (qb < B && h == 0 && rb * kRowBlock < n_valid) {
+                if constexpr (NTW * WAVES / RS <= 4)
+                    __builtin_nontemporal_store(best, &G[qb * g_ld + rb]);
+                else
+                    G[qb * g_ld + rb] = best;
+            }
             __builtin_amdgcn_sched_barrier(0);  // one tile at a time: bounds the live registers
         }
     }
@@ -1032,7 +1042,7 @@ __global__ __launch_bounds__(64 * (NT + 4)) void scan_tail_kernel(
     const uint64_t other = __shfl_xor(best, 32, kWave);
     best = other > best ? other : best;
     if (qlive && h == 0)
-        G[qb * g_ld + rb] = best;
+        __builtin_nontemporal_store(best, &G[qb * g_ld + rb]);
 }
 
 // ----------------------------------------------------------------- rescore the chosen blocks
